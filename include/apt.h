@@ -1,0 +1,159 @@
+/*
+ * apt.h - C ABI of the WpAq bipolar-INT bit-plane integer GEMM for AMD gfx950.
+ *
+ * The library computes C = A * W^T for signed p-bit weight codes W [N][K] and
+ * signed q-bit activation codes A [M][K] (1 <= p, q <= 8), the arbitrary
+ * precision integer matrix multiply of APT-LLM (arXiv 2508.19087, Sec. III),
+ * plus an optional fp16 per-token x per-channel scale epilogue.
+ *
+ * Number format (Sec. III-A, the bipolar-INT value equation): an n-bit word
+ * u = u^(n-1) ... u^(0) has the value (u)_D = sum_i (2 u^(i) - 1) 2^i, so each
+ * bit stands for -1 or +1.  A signed n-bit code x becomes the bipolar word by
+ * flipping its sign bit, u = (x mod 2^n) XOR 2^(n-1), and then (u)_D = 2x + 1
+ * (Sec. III-A, the signed-to-bipolar correspondence).  The conversion is exact;
+ * a quantiser's scale s becomes s/2 in bipolar form (Sec. III-A, the rewrite of
+ * the linear quantisation formula), so the scales passed to apt_gemm are the
+ * bipolar ones.
+ *
+ * The integer result is C[m][n] = sum_{k<K} (uA[m][k])_D * (uW[n][k])_D, which
+ * Sec. III-B obtains as sum_{i,j} 2^(i+j) Y^(i,j) over the 1-bit plane products.
+ *
+ * Conventions shared by every call:
+ *   - Pointers marked "device" are device pointers owned by the caller (for
+ *     example torch tensors' data_ptr()).  The library never allocates or frees
+ *     memory on these paths.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Calls that take a stream validate their arguments on the host, enqueue
+ *     their kernels on that stream and return without synchronising.
+ *   - No call launches anything when validation fails.
+ *   - The library holds no mutable global state; calls are thread-safe.
+ *   - Codes outside the signed b-bit range are reduced modulo 2^b (only the low
+ *     b bits of each int8 code are used).
+ *
+ * Packed bit-plane layout (Sec. IV-A: decompose into n 1-bit matrices, pack
+ * bits into 32-bit unsigned words, concatenate the planes):
+ *   K_pad = ceil(K / 128) * 128, NC = K_pad / 128 chunks per row.
+ *   The buffer holds R * NC * b * 4 little-endian uint32 words:
+ *       word index  ((r * NC + c) * b + i) * 4 + w,   0 <= w < 4,
+ *   and bit e (LSB = 0) of that word is bit i of the bipolar word u[r][k] with
+ *       k = 128 c + 32 w + e.
+ *   Bits with k >= K are zero.  The planes of one row are concatenated per
+ *   128-element chunk (b planes x 16 bytes, contiguous), so a row's chunk is one
+ *   contiguous b*16-byte transfer.  Buffers must be 16-byte aligned.
+ *
+ * Row sums: rowsum[r] = sum_{k<K} (u[r][k])_D, the sum of the bipolar values of
+ * row r (= sum of 2x+1).  apt_gemm routes that contract 8-bit operands on the
+ * matrix cores use them for the exact affine correction of the operand offset.
+ */
+#ifndef APT_H
+#define APT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  APT_OK = 0,
+  APT_ERR_INVALID_ARG = 1, /* bad size, bit width, pointer, alignment or combination */
+  APT_ERR_UNSUPPORTED = 2, /* the int32 result cannot hold K (2^p-1) (2^q-1), or the config is not buildable */
+  APT_ERR_HIP = 3,         /* the HIP runtime reported an error on launch */
+  APT_ERR_WORKSPACE = 4    /* the workspace is missing or too small */
+} apt_status_t;
+
+/* GEMM routes.  All compute the same int32 result. */
+enum {
+  APT_ROUTE_AUTO = 0,       /* let apt_select_config decide */
+  APT_ROUTE_XOR = 1,        /* XOR + popcount on packed words, cross-lane reduction (Sec. III-B, 1-bit XOR form) */
+  APT_ROUTE_PM1_MFMA = 2,   /* every (i, j) plane pair as +-1 int8 operands on the int8 matrix cores */
+  APT_ROUTE_INT8_MFMA = 3   /* planes reassembled in LDS into one int8 operand, one int8 MFMA per element pair */
+};
+
+/* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950
+ * terms).  Fields a route does not use are ignored.
+ *   route      APT_ROUTE_*
+ *   bm, bn     output tile per workgroup (MFMA routes: bm in {64,128,256}, bn in {64,128,256})
+ *   bk         K elements staged per pipeline step (MFMA routes: 128)
+ *   waves_m, waves_n   wave grid inside a workgroup (MFMA routes)
+ *   k_split    reserved, must be 0 or 1
+ *   lds_stages LDS buffers (MFMA routes: 2)
+ *   mt         XOR route: activation rows per workgroup (1, 2, 4 or 8)
+ */
+typedef struct {
+  int32_t route;
+  int32_t bm, bn, bk;
+  int32_t waves_m, waves_n;
+  int32_t k_split;
+  int32_t lds_stages;
+  int32_t mt;
+  int32_t reserved[3];
+} apt_config_t;
+
+/* Bytes of a packed buffer for `rows` rows of K codes at `bits` bits
+ * (rows * ceil(K/128) * bits * 16).  Returns 0 for rows < 1, K < 1 or bits
+ * outside [1, 8]. */
+size_t apt_packed_bytes(int rows, int K, int bits);
+
+/* Converts signed p-bit weight codes to bipolar-INT and packs the bit-planes
+ * (Sec. III-A conversion; Sec. IV-A steps 1-3).
+ *   w_codes   device, int8 [N][K] row-major, signed p-bit codes
+ *   w_packed  device, apt_packed_bytes(N, K, p) bytes, 16-byte aligned, fully written
+ *   w_rowsum  device, int32 [N] or NULL; receives the row sums defined above
+ * Errors: APT_ERR_INVALID_ARG for N < 1, K < 1, p outside [1, 8], NULL codes or
+ * packed pointer, or a misaligned packed pointer; APT_ERR_HIP on launch failure. */
+apt_status_t apt_pack_weights(const int8_t* w_codes, int N, int K, int p,
+                              void* w_packed, int32_t* w_rowsum, void* stream);
+
+/* The same conversion and packing for signed q-bit activation codes
+ * a_codes [M][K] (device, int8).  "Quantize" is the lossless re-quantisation of
+ * signed INT codes into bipolar-INT (Sec. III-A); the codes themselves come
+ * from the caller.  Arguments and errors as apt_pack_weights. */
+apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, int q,
+                                           void* a_packed, int32_t* a_rowsum, void* stream);
+
+/* Host-only.  Chooses the route and tile shape for (M, N, K, p, q) from the
+ * table measured on MI355X, falling back to the nearest entry (Sec. V-B,
+ * lookup table and approximate matching).  The choice never changes results.
+ * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8] or out == NULL. */
+apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out);
+
+/* Workspace bytes apt_gemm needs for this problem and config (cfg NULL = the
+ * selected one).  Every route currently needs 0. */
+size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_config_t* cfg);
+
+/* C = A * W^T on packed operands, with the fused recombination of Sec. III-B
+ * and the optional scale epilogue.
+ *   a_packed  device, packed q-bit activations [M][K] (apt_quantize_pack_activations)
+ *   w_packed  device, packed p-bit weights [N][K] (apt_pack_weights)
+ *   a_rowsum, w_rowsum  device int32 [M] / [N] from the packers; required by
+ *             the MFMA routes, ignored by APT_ROUTE_XOR (may be NULL there)
+ *   c_int32   device int32 [M][N] row-major, or NULL
+ *   a_scale   device fp16 bits [M], per-token bipolar scale, or NULL
+ *   w_scale   device fp16 bits [N], per-channel bipolar scale, or NULL
+ *   c_fp16    device fp16 bits [M][N] row-major, or NULL;
+ *             c_fp16[m][n] = fp16_rne(float(C) * float(a_scale[m]) * float(w_scale[n]))
+ *   cfg       NULL = apt_select_config, else a config to force
+ *   workspace, workspace_bytes  device scratch (see apt_gemm_workspace_bytes)
+ * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8], NULL or
+ * misaligned packed pointers, both outputs NULL, c_fp16 without both scales, a
+ * route needing row sums without them, or an invalid cfg;
+ * APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31; APT_ERR_WORKSPACE when the
+ * workspace is too small; APT_ERR_HIP on launch failure. */
+apt_status_t apt_gemm(int M, int N, int K, int p, int q,
+                      const void* a_packed, const void* w_packed,
+                      const int32_t* a_rowsum, const int32_t* w_rowsum,
+                      int32_t* c_int32,
+                      const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
+                      const apt_config_t* cfg,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* apt_status_string(apt_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APT_H */

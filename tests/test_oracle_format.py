@@ -1,0 +1,108 @@
+"""Pins of the oracle's bipolar-INT conversion, decoding and packed layout
+against what APT-LLM (arXiv 2508.19087) Sec. III-A / IV-A fix, independent of
+the oracle's own formulas."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as ref
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def all_codes(bits):
+    return np.arange(-(1 << (bits - 1)), 1 << (bits - 1), dtype=np.int64).astype(np.int8)
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+def test_roundtrip_every_code(bits):
+    """Lossless signed <-> bipolar round trip over every code (Sec. III-A):
+    value = 2x + 1, word = x + 2^(b-1), image = all odd integers in range,
+    inverse recovers x, complementing every bit negates the value."""
+    x = all_codes(bits)
+    u = ref.convert(x, bits)
+    v = ref.decode(u, bits)
+    xi = x.astype(np.int64)
+    assert np.array_equal(v, 2 * xi + 1)
+    assert np.array_equal(u.astype(np.int64), xi + (1 << (bits - 1)))
+    top = (1 << bits) - 1
+    assert sorted(v.tolist()) == list(range(-top, top + 1, 2))
+    assert np.array_equal((v.astype(np.int64) - 1) // 2, xi)
+    comp = (~u) & np.uint8(top)
+    assert np.array_equal(ref.decode(comp, bits), -v)
+
+
+def test_golden_code_table():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "bipolar_codes.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(rows) == 14
+    for bits, code, word, value in rows:
+        bits, code, value = int(bits), int(code), int(value)
+        u = ref.convert(np.array([code], np.int8), bits)
+        assert format(int(u[0]), "0%db" % bits) == word
+        assert int(ref.decode(u, bits)[0]) == value
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+def test_out_of_range_codes_use_low_bits(bits):
+    """Codes outside the signed range are reduced modulo 2^b."""
+    x = np.arange(-128, 128, dtype=np.int64).astype(np.int8)
+    low = (x.astype(np.int64) & ((1 << bits) - 1))
+    wrapped = np.where(low >= (1 << (bits - 1)), low - (1 << bits), low)
+    assert np.array_equal(ref.values(x, bits), 2 * wrapped + 1)
+
+
+def test_bad_bits_rejected():
+    with pytest.raises(ValueError):
+        ref.convert(np.zeros(3, np.int8), 0)
+    with pytest.raises(ValueError):
+        ref.decode(np.zeros(3, np.uint8), 9)
+
+
+def test_golden_packed_layout():
+    lines = {l.split()[0]: l.split()[1:] for l in open(os.path.join(GOLDEN, "packed_layout_w2.txt"))
+             if l.strip() and not l.startswith("#")}
+    R, K, bits = int(lines["R"][0]), int(lines["K"][0]), int(lines["bits"][0])
+    u = (np.arange(K) % 4).astype(np.uint8).reshape(R, K)
+    want = np.array([int(w, 16) for w in lines["words"]], dtype=np.uint32)
+    got = ref.pack(u, bits)
+    assert np.array_equal(got, want)
+    back, stray = ref.unpack(got, R, K, bits)
+    assert stray == 0 and np.array_equal(back, u)
+
+
+def _pack_by_dict(u, bits):
+    """Independent statement of the layout: a map from (row, k, plane) to the
+    (word, bit) it occupies, filled element by element."""
+    R, K = u.shape
+    nc = (K + 127) // 128
+    words = {}
+    for r in range(R):
+        for k in range(K):
+            for i in range(bits):
+                if (int(u[r, k]) >> i) & 1:
+                    idx = ((r * nc + k // 128) * bits + i) * 4 + (k % 128) // 32
+                    words[idx] = words.get(idx, 0) | (1 << (k % 32))
+    out = np.zeros(R * nc * bits * 4, dtype=np.uint32)
+    for idx, val in words.items():
+        out[idx] = val
+    return out
+
+
+@pytest.mark.parametrize("R,K,bits", [(1, 1, 1), (3, 31, 2), (2, 33, 3), (2, 129, 4), (1, 300, 8),
+                                      (4, 128, 5), (2, 257, 7)])
+def test_pack_unpack(R, K, bits):
+    g = np.random.default_rng(R * 1000 + K * 10 + bits)
+    u = g.integers(0, 1 << bits, size=(R, K)).astype(np.uint8)
+    packed = ref.pack(u, bits)
+    assert packed.size == ref.packed_words(R, K, bits)
+    assert np.array_equal(packed, _pack_by_dict(u, bits))
+    back, stray = ref.unpack(packed, R, K, bits)
+    assert stray == 0 and np.array_equal(back, u)
+    if K % 128:
+        bad = packed.copy()
+        nc = (K + 127) // 128
+        last = ((0 * nc + nc - 1) * bits + 0) * 4 + 3
+        bad[last] |= np.uint32(1 << 31)
+        assert ref.unpack(bad, R, K, bits)[1] == 1
