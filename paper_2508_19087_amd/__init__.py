@@ -1,0 +1,15 @@
+"""WpAq bipolar-INT bit-plane integer GEMM for AMD MI355X (gfx950).
+
+An MI355X-native implementation of the arbitrary-precision integer matrix
+multiply of APT-LLM (arXiv 2508.19087): signed-INT codes are converted to
+bipolar-INT, split into bit-planes packed in HBM, and multiplied exactly into
+an int32 result with an optional fp16 scale epilogue.  The computation lives in
+hand-written HIP kernels behind the C ABI of include/apt.h (libapt.so); this
+package is its Python binding.
+"""
+from .apt import (APT_ERR_HIP, APT_ERR_INVALID_ARG, APT_ERR_UNSUPPORTED, APT_ERR_WORKSPACE,  # noqa: F401
+                  APT_OK, APT_ROUTE_AUTO, APT_ROUTE_INT8_MFMA, APT_ROUTE_PM1_MFMA, APT_ROUTE_XOR,
+                  ROUTE_NAMES, AptError, Packed, apt_config_t, apt_gemm, apt_gemm_workspace_bytes,
+                  apt_pack_weights, apt_packed_bytes, apt_quantize_pack_activations,
+                  apt_select_config, gemm, header_functions, lib, pack, select_config,
+                  status_string)

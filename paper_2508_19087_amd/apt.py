@@ -1,0 +1,197 @@
+"""Python binding of libapt.so (include/apt.h): argument marshalling only.
+
+Every function named ``apt_*`` calls the C entry point of the same name with
+plain integers and device pointers.  The torch helpers below (``pack``,
+``gemm``, ...) only allocate outputs with torch and pass ``data_ptr()`` and the
+current HIP stream; every step of the computation runs in the library's
+kernels.  Importing this module fails loudly when the library is not built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from dataclasses import dataclass
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libapt.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "apt.h")
+
+APT_OK = 0
+APT_ERR_INVALID_ARG = 1
+APT_ERR_UNSUPPORTED = 2
+APT_ERR_HIP = 3
+APT_ERR_WORKSPACE = 4
+
+APT_ROUTE_AUTO = 0
+APT_ROUTE_XOR = 1
+APT_ROUTE_PM1_MFMA = 2
+APT_ROUTE_INT8_MFMA = 3
+ROUTE_NAMES = {APT_ROUTE_XOR: "xor_popcount", APT_ROUTE_PM1_MFMA: "pm1_planes_mfma",
+               APT_ROUTE_INT8_MFMA: "reassembled_int8_mfma"}
+
+
+class apt_config_t(ctypes.Structure):
+    _fields_ = [("route", ctypes.c_int32), ("bm", ctypes.c_int32), ("bn", ctypes.c_int32),
+                ("bk", ctypes.c_int32), ("waves_m", ctypes.c_int32), ("waves_n", ctypes.c_int32),
+                ("k_split", ctypes.c_int32), ("lds_stages", ctypes.c_int32), ("mt", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 3)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
+
+    @classmethod
+    def make(cls, route, bm=0, bn=0, bk=0, waves_m=0, waves_n=0, k_split=0, lds_stages=0, mt=0):
+        c = cls()
+        c.route, c.bm, c.bn, c.bk = route, bm, bn, bk
+        c.waves_m, c.waves_n, c.k_split, c.lds_stages, c.mt = waves_m, waves_n, k_split, lds_stages, mt
+        return c
+
+
+class AptError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, status_string(status), status))
+
+
+_vp = ctypes.c_void_p
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libapt.so is not built (run __graft_entry__.build() or "
+                              "python paper_2508_19087_amd/build.py): %s" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        L.apt_packed_bytes.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.apt_packed_bytes.restype = ctypes.c_size_t
+        for name in ("apt_pack_weights", "apt_quantize_pack_activations"):
+            f = getattr(L, name)
+            f.argtypes = [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp]
+            f.restype = ctypes.c_int
+        L.apt_select_config.argtypes = [ctypes.c_int] * 5 + [ctypes.POINTER(apt_config_t)]
+        L.apt_select_config.restype = ctypes.c_int
+        L.apt_gemm_workspace_bytes.argtypes = [ctypes.c_int] * 5 + [ctypes.POINTER(apt_config_t)]
+        L.apt_gemm_workspace_bytes.restype = ctypes.c_size_t
+        L.apt_gemm.argtypes = ([ctypes.c_int] * 5 + [_vp] * 8 + [ctypes.POINTER(apt_config_t)] +
+                               [_vp, ctypes.c_size_t, _vp])
+        L.apt_gemm.restype = ctypes.c_int
+        L.apt_status_string.argtypes = [ctypes.c_int]
+        L.apt_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions include/apt.h declares."""
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(apt_[a-z0-9_]+)\s*\(", text)))
+
+
+# ---- C entry points, same names -------------------------------------------------
+
+def apt_packed_bytes(rows: int, K: int, bits: int) -> int:
+    return int(lib().apt_packed_bytes(rows, K, bits))
+
+
+def apt_pack_weights(w_codes, N, K, p, w_packed, w_rowsum, stream) -> int:
+    return lib().apt_pack_weights(w_codes, N, K, p, w_packed, w_rowsum, stream)
+
+
+def apt_quantize_pack_activations(a_codes, M, K, q, a_packed, a_rowsum, stream) -> int:
+    return lib().apt_quantize_pack_activations(a_codes, M, K, q, a_packed, a_rowsum, stream)
+
+
+def apt_select_config(M, N, K, p, q):
+    """(status, apt_config_t)."""
+    c = apt_config_t()
+    st = lib().apt_select_config(M, N, K, p, q, ctypes.byref(c))
+    return st, c
+
+
+def apt_gemm_workspace_bytes(M, N, K, p, q, cfg=None) -> int:
+    return int(lib().apt_gemm_workspace_bytes(M, N, K, p, q, ctypes.byref(cfg) if cfg else None))
+
+
+def apt_gemm(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale, w_scale,
+             c_fp16, cfg, workspace, workspace_bytes, stream) -> int:
+    return lib().apt_gemm(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32,
+                          a_scale, w_scale, c_fp16, ctypes.byref(cfg) if cfg is not None else None,
+                          workspace, workspace_bytes, stream)
+
+
+def status_string(status: int) -> str:
+    return lib().apt_status_string(status).decode()
+
+
+def check(status: int, where: str):
+    if status != APT_OK:
+        raise AptError(status, where)
+
+
+# ---- torch helpers (allocation + pointers only) -------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+@dataclass
+class Packed:
+    """A packed bit-plane operand on the device: uint8 buffer + int32 row sums."""
+    data: "object"
+    rowsum: "object"
+    rows: int
+    K: int
+    bits: int
+
+
+def pack(codes, bits: int, activations: bool = False, stream=None) -> Packed:
+    """Packs int8 codes [rows][K] (a CUDA tensor) into bit-planes on the device."""
+    torch = _torch()
+    assert codes.is_cuda and codes.dtype == torch.int8 and codes.dim() == 2
+    codes = codes.contiguous()
+    rows, K = codes.shape
+    nbytes = apt_packed_bytes(rows, K, bits)
+    if nbytes == 0:
+        raise AptError(APT_ERR_INVALID_ARG, "apt_packed_bytes")
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=codes.device)
+    rs = torch.empty(rows, dtype=torch.int32, device=codes.device)
+    fn = apt_quantize_pack_activations if activations else apt_pack_weights
+    check(fn(codes.data_ptr(), rows, K, bits, buf.data_ptr(), rs.data_ptr(), _stream_ptr(stream)),
+          fn.__name__)
+    return Packed(buf, rs, rows, K, bits)
+
+
+def gemm(a: Packed, w: Packed, out_int32: bool = True, a_scale=None, w_scale=None,
+         out_fp16: bool = False, cfg: apt_config_t | None = None, stream=None):
+    """C = A W^T on packed operands.  Returns (c_int32 or None, c_fp16 or None)."""
+    torch = _torch()
+    assert a.K == w.K
+    M, N, K = a.rows, w.rows, a.K
+    dev = a.data.device
+    c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
+    c16 = torch.empty((M, N), dtype=torch.float16, device=dev) if out_fp16 else None
+    check(apt_gemm(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
+                   _ptr(a.rowsum), _ptr(w.rowsum), _ptr(c32), _ptr(a_scale), _ptr(w_scale),
+                   _ptr(c16), cfg, None, 0, _stream_ptr(stream)), "apt_gemm")
+    return c32, c16
+
+
+def select_config(M, N, K, p, q) -> apt_config_t:
+    st, c = apt_select_config(M, N, K, p, q)
+    check(st, "apt_select_config")
+    return c

@@ -1,0 +1,133 @@
+// api.hip - the extern "C" entry points declared in include/apt.h: argument
+// validation, config resolution and kernel launch on the caller's stream.
+// Validation always runs before any HIP call, so a rejected call touches
+// neither the device nor the runtime.
+#include <string.h>
+
+#include "apt_internal.h"
+
+namespace {
+
+bool bits_ok(int b) { return b >= 1 && b <= 8; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// K (2^p - 1)(2^q - 1) bounds |C|; it must stay below 2^31.
+bool fits_int32(int K, int p, int q) {
+  const int64_t bound = (int64_t)K * ((1 << p) - 1) * ((1 << q) - 1);
+  return bound < ((int64_t)1 << 31);
+}
+
+apt_status_t hip_status(hipError_t e) { return e == hipSuccess ? APT_OK : APT_ERR_HIP; }
+
+apt_status_t pack_common(const int8_t* codes, int rows, int K, int bits, void* packed,
+                         int32_t* rowsum, void* stream) {
+  if (rows < 1 || K < 1 || !bits_ok(bits) || codes == nullptr || packed == nullptr ||
+      !aligned16(packed))
+    return APT_ERR_INVALID_ARG;
+  return hip_status(apt::launch_pack(codes, rows, K, bits, static_cast<uint32_t*>(packed), rowsum,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+// Checks a config against the problem; returns APT_OK or the status to report.
+apt_status_t check_config(const apt_config_t& c, int M, int p, int q, bool have_rowsums) {
+  if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
+  switch (c.route) {
+    case APT_ROUTE_XOR:
+      if (!apt::xor_config_ok(c)) return APT_ERR_INVALID_ARG;
+      if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
+      return APT_OK;
+    case APT_ROUTE_INT8_MFMA:
+      if (!apt::int8_config_ok(c)) return APT_ERR_INVALID_ARG;
+      if (!have_rowsums) return APT_ERR_INVALID_ARG;
+      return APT_OK;
+    case APT_ROUTE_PM1_MFMA:
+      if (p > 7 || q > 7) return APT_ERR_UNSUPPORTED;
+      if (!apt::pm1_config_ok(c, p, q)) return APT_ERR_INVALID_ARG;
+      return APT_OK;
+    default:
+      return APT_ERR_INVALID_ARG;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t apt_packed_bytes(int rows, int K, int bits) {
+  if (rows < 1 || K < 1 || !bits_ok(bits)) return 0;
+  return (size_t)rows * (size_t)apt::num_chunks(K) * (size_t)bits * apt::kWordsPerPlane * 4;
+}
+
+apt_status_t apt_pack_weights(const int8_t* w_codes, int N, int K, int p, void* w_packed,
+                              int32_t* w_rowsum, void* stream) {
+  return pack_common(w_codes, N, K, p, w_packed, w_rowsum, stream);
+}
+
+apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, int q,
+                                           void* a_packed, int32_t* a_rowsum, void* stream) {
+  return pack_common(a_codes, M, K, q, a_packed, a_rowsum, stream);
+}
+
+apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out) {
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q) || out == nullptr)
+    return APT_ERR_INVALID_ARG;
+  *out = apt::select_config(M, N, K, p, q);
+  return APT_OK;
+}
+
+size_t apt_gemm_workspace_bytes(int, int, int, int, int, const apt_config_t*) { return 0; }
+
+apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, const void* w_packed,
+                      const int32_t* a_rowsum, const int32_t* w_rowsum, int32_t* c_int32,
+                      const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
+                      const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return APT_ERR_INVALID_ARG;
+  if (a_packed == nullptr || w_packed == nullptr || !aligned16(a_packed) || !aligned16(w_packed))
+    return APT_ERR_INVALID_ARG;
+  if (c_int32 == nullptr && c_fp16 == nullptr) return APT_ERR_INVALID_ARG;
+  if (c_fp16 != nullptr && (a_scale == nullptr || w_scale == nullptr)) return APT_ERR_INVALID_ARG;
+  if (!fits_int32(K, p, q)) return APT_ERR_UNSUPPORTED;
+
+  apt_config_t c;
+  if (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
+    c = apt::select_config(M, N, K, p, q);
+  else
+    c = *cfg;
+  const bool have_rowsums = a_rowsum != nullptr && w_rowsum != nullptr;
+  apt_status_t st = check_config(c, M, p, q, have_rowsums);
+  if (st != APT_OK) return st;
+
+  apt::GemmArgs g;
+  g.M = M; g.N = N; g.K = K; g.p = p; g.q = q;
+  g.a_packed = static_cast<const uint32_t*>(a_packed);
+  g.w_packed = static_cast<const uint32_t*>(w_packed);
+  g.a_rowsum = a_rowsum;
+  g.w_rowsum = w_rowsum;
+  g.c_int32 = c_int32;
+  g.a_scale = reinterpret_cast<const __half*>(a_scale);
+  g.w_scale = reinterpret_cast<const __half*>(w_scale);
+  g.c_fp16 = reinterpret_cast<__half*>(c_fp16);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (c.route) {
+    case APT_ROUTE_XOR: return hip_status(apt::launch_gemm_xor(g, c, s));
+    case APT_ROUTE_INT8_MFMA: return hip_status(apt::launch_gemm_int8(g, c, s));
+    case APT_ROUTE_PM1_MFMA: return hip_status(apt::launch_gemm_pm1(g, c, s));
+  }
+  return APT_ERR_INVALID_ARG;
+}
+
+const char* apt_status_string(apt_status_t status) {
+  switch (status) {
+    case APT_OK: return "ok";
+    case APT_ERR_INVALID_ARG: return "invalid argument";
+    case APT_ERR_UNSUPPORTED: return "unsupported problem or configuration";
+    case APT_ERR_HIP: return "HIP runtime error";
+    case APT_ERR_WORKSPACE: return "workspace missing or too small";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,52 @@
+// apt_internal.h - definitions shared by the gfx950 kernels and the C ABI of
+// the WpAq bipolar-INT GEMM library.  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+#include "../../include/apt.h"
+
+namespace apt {
+
+// Packed layout (fixed in apt.h): 128 elements per chunk, 4 uint32 words per
+// plane per chunk, planes of one chunk contiguous.
+constexpr int kChunk = 128;
+constexpr int kWordsPerPlane = 4;
+
+inline int num_chunks(int K) { return (K + kChunk - 1) / kChunk; }
+
+// Launch of the converter + bit-plane packer (pack.hip).
+hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t* packed,
+                       int32_t* rowsum, hipStream_t stream);
+
+// Arguments every GEMM route receives (device pointers; validated by the ABI).
+struct GemmArgs {
+  int M, N, K, p, q;
+  const uint32_t* a_packed;
+  const uint32_t* w_packed;
+  const int32_t* a_rowsum;
+  const int32_t* w_rowsum;
+  int32_t* c_int32;
+  const __half* a_scale;
+  const __half* w_scale;
+  __half* c_fp16;
+};
+
+// XOR + popcount route (gemm_xor.hip).  Any shape.
+hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
+bool xor_config_ok(const apt_config_t& cfg);
+
+// Reassembled int8 MFMA route (gemm_mfma.hip).
+hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
+bool int8_config_ok(const apt_config_t& cfg);
+
+// Plane-pair +-1 MFMA route (gemm_pm1.hip).
+hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
+bool pm1_config_ok(const apt_config_t& cfg, int p, int q);
+
+// Host-side selector (select.cpp).
+apt_config_t select_config(int M, int N, int K, int p, int q);
+
+}  // namespace apt

@@ -1,0 +1,83 @@
+// reassemble.h - bit-plane words -> int8 MFMA operand bytes on gfx950.
+//
+// The packed format stores b bit-planes of a row (APT-LLM, arXiv 2508.19087,
+// Sec. IV-A).  The int8 MFMA routes rebuild the b-bit bipolar word of every
+// element from its planes before the multiply: because
+//     sum_{i,j} 2^(i+j) W_i A_j = (sum_i 2^i W_i)(sum_j 2^j A_j),
+// recombining the planes before the product gives the same sum as the
+// paper's recovery after the 1-bit products (Sec. III-B), with one int8
+// multiply-accumulate per element pair instead of p*q 1-bit ones.
+//
+// One 32-bit word per plane covers 32 elements; they become 8 output dwords
+// (32 bytes).  Output dword t, byte j holds the element at bit 8j + t of the
+// word.  The same order is used for every bit width and for both operands, and
+// a dot product is unchanged by a permutation of k applied to both sides, so
+// the order never shows in the result.
+//
+// The rebuild is a 3-level merge tree: pairs of planes -> 2-bit fields
+// (elements at even / odd bit positions), pairs of those -> nibbles, then
+// nibbles -> bytes.  Each merge is a shift plus a bit-field select
+// (v_bfi_b32).  With b <= 4 the top level only splits nibbles into bytes.
+// Missing planes (i >= b) are zero and fold away at compile time.
+#pragma once
+
+#include <stdint.h>
+
+namespace apt {
+
+__device__ __forceinline__ uint32_t bsel(uint32_t mask, uint32_t a, uint32_t b) {
+  return (a & mask) | (b & ~mask);
+}
+
+// Bytes of the unsigned b-bit words u (B <= 7), or of u XOR 0x80 = the signed
+// code (B == 8), for the 32 elements of plane words pw[0..B-1].
+template <int B>
+__device__ __forceinline__ void reassemble_word(const uint32_t* pw, uint32_t out[8]) {
+  if (B == 1) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) out[t] = (pw[0] >> t) & 0x01010101u;
+    return;
+  }
+  auto PL = [&](int i) -> uint32_t { return i < B ? pw[i] : 0u; };
+  // level 1: 2-bit fields; e: elements at bits 2f, o: elements at bits 2f+1
+  const uint32_t m1 = 0x55555555u;
+  uint32_t e01 = bsel(m1, PL(0), PL(1) << 1), o01 = bsel(m1, PL(0) >> 1, PL(1));
+  uint32_t e23 = bsel(m1, PL(2), PL(3) << 1), o23 = bsel(m1, PL(2) >> 1, PL(3));
+  // level 2: nibbles; ee: elements 4f, eo: 4f+2, oe: 4f+1, oo: 4f+3
+  const uint32_t m2 = 0x33333333u;
+  uint32_t ee = bsel(m2, e01, e23 << 2), eo = bsel(m2, e01 >> 2, e23);
+  uint32_t oe = bsel(m2, o01, o23 << 2), oo = bsel(m2, o01 >> 2, o23);
+  const uint32_t m3 = 0x0F0F0F0Fu;
+  if (B <= 4) {
+    // level 3: nibble 2j -> byte j (element 8j + s), nibble 2j+1 -> element 8j + 4 + s
+    out[0] = ee & m3;         out[4] = (ee >> 4) & m3;
+    out[1] = oe & m3;         out[5] = (oe >> 4) & m3;
+    out[2] = eo & m3;         out[6] = (eo >> 4) & m3;
+    out[3] = oo & m3;         out[7] = (oo >> 4) & m3;
+  } else {
+    uint32_t e45 = bsel(m1, PL(4), PL(5) << 1), o45 = bsel(m1, PL(4) >> 1, PL(5));
+    uint32_t e67 = bsel(m1, PL(6), PL(7) << 1), o67 = bsel(m1, PL(6) >> 1, PL(7));
+    uint32_t ee2 = bsel(m2, e45, e67 << 2), eo2 = bsel(m2, e45 >> 2, e67);
+    uint32_t oe2 = bsel(m2, o45, o67 << 2), oo2 = bsel(m2, o45 >> 2, o67);
+    out[0] = bsel(m3, ee, ee2 << 4);  out[4] = bsel(m3, ee >> 4, ee2);
+    out[1] = bsel(m3, oe, oe2 << 4);  out[5] = bsel(m3, oe >> 4, oe2);
+    out[2] = bsel(m3, eo, eo2 << 4);  out[6] = bsel(m3, eo >> 4, eo2);
+    out[3] = bsel(m3, oo, oo2 << 4);  out[7] = bsel(m3, oo >> 4, oo2);
+    if (B == 8) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) out[t] ^= 0x80808080u;
+    }
+  }
+}
+
+// Operand offset of the reassembled byte y: bipolar value v = 2 y + c.
+//   B <= 7: y = u,        v = 2u - (2^B - 1)  ->  c = 1 - 2^B
+//   B == 8: y = u - 128,  v = 2u - 255        ->  c = 1
+template <int B>
+__host__ __device__ constexpr int operand_offset() { return B == 8 ? 1 : 1 - (1 << B); }
+
+// Operand byte of a padding element (all plane bits zero).
+template <int B>
+__host__ __device__ constexpr int operand_pad() { return B == 8 ? -128 : 0; }
+
+}  // namespace apt

@@ -1,0 +1,110 @@
+"""Host-side checks of the C ABI (no kernel launches): every declared symbol is
+exported, sizes and selector outputs are as documented, and invalid arguments
+are rejected with the documented status before anything reaches the GPU."""
+import ctypes
+
+import pytest
+
+import paper_2508_19087_amd as apt
+import synth
+
+
+def test_exports_every_declared_symbol():
+    names = apt.header_functions()
+    assert set(names) == {"apt_packed_bytes", "apt_pack_weights", "apt_quantize_pack_activations",
+                          "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
+                          "apt_status_string"}
+    L = apt.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("rows,K,bits,want", [
+    (1, 1, 1, 16), (1, 128, 1, 16), (1, 129, 1, 32), (3, 4096, 2, 3 * 32 * 2 * 16),
+    (11008, 4096, 4, 11008 * 32 * 4 * 16), (2, 11008, 8, 2 * 86 * 8 * 16),
+    (0, 5, 1, 0), (5, 0, 1, 0), (5, 5, 0, 0), (5, 5, 9, 0)])
+def test_packed_bytes(rows, K, bits, want):
+    assert apt.apt_packed_bytes(rows, K, bits) == want
+
+
+def test_status_strings():
+    for s in range(5):
+        assert apt.status_string(s)
+    assert apt.status_string(99) == "unknown status"
+
+
+def _shapes():
+    out = [(16, 512, 512, 1, 2), (2048, 11008, 4096, 4, 4)]
+    for M in (1, 4, 8):
+        out += [(M, 4096, 4096, 2, 2), (M, 11008, 4096, 2, 2)]
+    for p, q in synth.SWEEP_BITS:
+        out.append((512, 4096, 11008, p, q))
+    for name, (N, K) in synth.LAYER_SHAPES.items():
+        for M in (1, 1024):
+            out.append((M, N, K, 2, 4))
+    return out
+
+
+@pytest.mark.parametrize("shape", _shapes())
+def test_select_config_valid(shape):
+    st, c = apt.apt_select_config(*shape)
+    assert st == apt.APT_OK
+    assert c.route in (apt.APT_ROUTE_XOR, apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_PM1_MFMA)
+    if shape[0] <= 8:
+        assert c.route == apt.APT_ROUTE_XOR
+    assert apt.apt_gemm_workspace_bytes(*shape, c) == 0
+
+
+def test_select_config_rejects():
+    assert apt.apt_select_config(0, 1, 1, 1, 1)[0] == apt.APT_ERR_INVALID_ARG
+    assert apt.apt_select_config(1, 1, 1, 9, 1)[0] == apt.APT_ERR_INVALID_ARG
+    L = apt.lib()
+    assert L.apt_select_config(1, 1, 1, 1, 1, None) == apt.APT_ERR_INVALID_ARG
+
+
+# Fake, never-dereferenced device addresses: every call below must be rejected
+# by host validation before any HIP call.
+A, W, C = 0x7F0000000000, 0x7F0000100000, 0x7F0000200000
+RA, RW, S = 0x7F0000300000, 0x7F0000400000, 0x7F0000500000
+
+
+def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=None, c16=None,
+         cfg=None):
+    return apt.apt_gemm(M, N, K, p, q, a, w, ra, rw, c32, sa, sw, c16, cfg, None, 0, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(M=0), apt.APT_ERR_INVALID_ARG), (dict(N=-1), apt.APT_ERR_INVALID_ARG),
+    (dict(K=0), apt.APT_ERR_INVALID_ARG), (dict(p=0), apt.APT_ERR_INVALID_ARG),
+    (dict(q=9), apt.APT_ERR_INVALID_ARG), (dict(a=None), apt.APT_ERR_INVALID_ARG),
+    (dict(w=None), apt.APT_ERR_INVALID_ARG), (dict(a=A + 4), apt.APT_ERR_INVALID_ARG),
+    (dict(w=W + 8), apt.APT_ERR_INVALID_ARG), (dict(c32=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c16=C, sa=S), apt.APT_ERR_INVALID_ARG), (dict(c16=C, sw=S), apt.APT_ERR_INVALID_ARG),
+    (dict(K=33026, p=8, q=8), apt.APT_ERR_UNSUPPORTED),
+    (dict(K=1 << 30, p=2, q=2), apt.APT_ERR_UNSUPPORTED),
+    (dict(cfg=apt.apt_config_t.make(7)), apt.APT_ERR_INVALID_ARG),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 96, 128, 128, 2, 2)),
+     apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ra=None),
+     apt.APT_ERR_INVALID_ARG),
+    (dict(p=8, cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)), apt.APT_ERR_UNSUPPORTED),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, k_split=2)), apt.APT_ERR_UNSUPPORTED),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=3)), apt.APT_ERR_INVALID_ARG),
+])
+def test_gemm_validation(kw, want):
+    assert gemm(**kw) == want
+
+
+@pytest.mark.parametrize("kw", [dict(rows=0), dict(K=0), dict(bits=0), dict(bits=9),
+                                dict(codes=None), dict(packed=None), dict(packed=A + 4)])
+def test_pack_validation(kw):
+    args = dict(codes=A, rows=4, K=64, bits=3, packed=W, rowsum=None)
+    args.update(kw)
+    for fn in (apt.apt_pack_weights, apt.apt_quantize_pack_activations):
+        st = fn(args["codes"], args["rows"], args["K"], args["bits"], args["packed"],
+                args["rowsum"], None)
+        assert st == apt.APT_ERR_INVALID_ARG
+
+
+def test_config_struct_layout():
+    assert ctypes.sizeof(apt.apt_config_t) == 12 * 4

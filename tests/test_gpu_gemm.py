@@ -1,0 +1,100 @@
+"""GPU parity of every GEMM route against the oracle: bit-exact int32 over
+all 64 (p, q) pairs, ragged shapes, config invariance, repeat determinism and
+the fp16 scale epilogue."""
+import itertools
+
+import numpy as np
+import pytest
+
+import paper_2508_19087_amd as apt
+import synth
+from gpu_util import (assert_fp16_ok, assert_int32_equal, forced_configs, oracle_full,
+                      pack_problem, run)
+
+pytestmark = pytest.mark.gpu
+PQ = list(itertools.product(range(1, 9), range(1, 9)))
+
+
+@pytest.mark.parametrize("p,q", PQ)
+def test_all_bit_widths_every_route(p, q):
+    g = synth.rng(1000, p, q)
+    for M, N, K in [(17, 33, 257), (70, 130, 300)]:
+        prob = synth.random_problem(g, M, N, K, p, q)
+        want = oracle_full(prob)
+        packed = pack_problem(prob)
+        for name, cfg in forced_configs(p, q):
+            got, _ = run(prob, cfg=cfg, packed=packed)
+            assert_int32_equal(got, want, "%s p=%d q=%d %dx%dx%d" % (name, p, q, M, N, K))
+
+
+SHAPES = [(1, 1, 1), (1, 7, 31), (2, 5, 32), (3, 64, 33), (4, 3, 127), (5, 129, 128), (8, 256, 129),
+          (9, 100, 1), (16, 512, 512), (17, 65, 4096), (64, 64, 64), (65, 257, 385),
+          (128, 128, 256), (129, 255, 1000), (300, 513, 640)]
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+@pytest.mark.parametrize("p,q", [(1, 2), (2, 2), (4, 4), (3, 8), (8, 8), (2, 4)])
+def test_ragged_shapes(M, N, K, p, q):
+    prob = synth.random_problem(synth.rng(2000, M, N, K, p, q), M, N, K, p, q)
+    want = oracle_full(prob)
+    packed = pack_problem(prob)
+    got, _ = run(prob, packed=packed)  # selected config
+    assert_int32_equal(got, want, "auto")
+    for name, cfg in forced_configs(p, q):
+        got, _ = run(prob, cfg=cfg, packed=packed)
+        assert_int32_equal(got, want, name)
+
+
+def test_extreme_values_all_ones_and_zeros():
+    """Worst-case magnitudes: all-ones / all-zeros bipolar words at p = q = 8."""
+    for M, N, K in [(3, 5, 1000), (70, 80, 4100)]:
+        a = np.full((M, K), 127, np.int8)
+        w = np.full((N, K), 127, np.int8)
+        w[1::2] = -128
+        prob = synth.Problem("extreme", M, N, K, 8, 8, w, a)
+        want = oracle_full(prob)
+        assert want[0, 0] == K * 255 * 255 and want[0, 1] == -K * 255 * 255
+        packed = pack_problem(prob)
+        for name, cfg in [("auto", None)] + forced_configs(8, 8):
+            got, _ = run(prob, cfg=cfg, packed=packed)
+            assert_int32_equal(got, want, name)
+
+
+def test_max_k_p8_q8():
+    """Largest K whose worst case fits int32 at p = q = 8 (33025)."""
+    K = 33025
+    a = np.full((2, K), 127, np.int8)
+    w = np.full((3, K), 127, np.int8)
+    w[1] = -128
+    prob = synth.Problem("maxk", 2, 3, K, 8, 8, w, a)
+    want = oracle_full(prob)
+    packed = pack_problem(prob)
+    for name, cfg in [("auto", None)] + forced_configs(8, 8):
+        got, _ = run(prob, cfg=cfg, packed=packed)
+        assert_int32_equal(got, want, name)
+
+
+def test_deterministic_repeats():
+    """20 launches of each route give bit-identical outputs (an LDS race would
+    show up as run-to-run differences)."""
+    prob = synth.random_problem(synth.rng(3000), 300, 700, 1500, 4, 4)
+    want = oracle_full(prob)
+    packed = pack_problem(prob)
+    for name, cfg in forced_configs(4, 4):
+        for _ in range(20):
+            got, _ = run(prob, cfg=cfg, packed=packed)
+            assert_int32_equal(got, want, name)
+
+
+@pytest.mark.parametrize("M,N,K,p,q", [(1, 300, 640, 2, 2), (8, 129, 4096, 2, 4),
+                                       (100, 200, 1000, 4, 4), (33, 70, 129, 8, 8)])
+def test_fp16_epilogue(M, N, K, p, q):
+    prob = synth.random_problem(synth.rng(4000, M, N, K), M, N, K, p, q, with_scales=True)
+    want = oracle_full(prob)
+    packed = pack_problem(prob)
+    for name, cfg in [("auto", None)] + forced_configs(p, q):
+        c32, c16 = run(prob, cfg=cfg, fp16=True, packed=packed)
+        assert_int32_equal(c32, want, name)
+        assert_fp16_ok(c16, want, prob, name)
+        _, c16b = run(prob, cfg=cfg, int32=False, fp16=True, packed=packed)
+        assert np.array_equal(c16b.view(np.uint16), c16.view(np.uint16))
