@@ -1,0 +1,293 @@
+"""Benchmark of the WpAq bipolar-INT GEMM hot path on one MI355X.
+
+One step is one pass of the whole path over one batch of synthetic input:
+  decode  (M = 1):    pack the W2A2 token's activations, then the two 7B-class
+                      decode GEMMs (N=4096 and N=11008, K=4096) with int32 and
+                      fp16-epilogue outputs;
+  prefill (M = 2048): pack the W4A4 activations, then the 2048 x 11008 x 4096
+                      GEMM with int32 output.
+Weights are packed once before timing (they are static).  Every call goes
+through the C ABI with the config chosen by the library's selector.
+
+Printed JSON line: whole-step effective TOPS (2 M N K summed over the three
+GEMMs), the roofline of the dominant kernel (the prefill GEMM, int8 MFMA
+bound) timed with HIP events on its own stream, the HBM-bound decode GEMM
+measured separately with cold weights, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective TOPS and % of int8-MFMA/HBM roofline for WpAq GEMM, M=1 & M=2048"
+PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA, 5.0 POP/s
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, 8 TB/s
+MALL_BYTES = 256 << 20      # Infinity Cache; cold-weight runs rotate through > 2x this
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2508_19087_amd/csrc/gemm_int8.h", "paper_2508_19087_amd/csrc/reassemble.h",
+                  "paper_2508_19087_amd/csrc/gemm_xor.h", "paper_2508_19087_amd/csrc/select.hip"]
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Workload:
+    """Device buffers of one bench step, built through the library's own calls."""
+
+    def __init__(self):
+        import numpy as np
+        import torch
+
+        import paper_2508_19087_amd as apt
+        import synth
+        self.apt, self.torch, self.np = apt, torch, np
+        self.stream = torch.cuda.current_stream()
+        self.sp = self.stream.cuda_stream
+        self.dec = [synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]
+        self.pre = synth.w4a4_prefill()
+        dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+        self.items = []
+        for prob, fp16 in [(self.dec[0], True), (self.dec[1], True), (self.pre, False)]:
+            it = {"prob": prob, "fp16": fp16}
+            w = apt.pack(dev(prob.w_codes), prob.p)  # weights: packed once
+            it["w"] = w
+            it["a_codes"] = dev(prob.a_codes)
+            it["a_buf"] = torch.empty(apt.apt_packed_bytes(prob.M, prob.K, prob.q), dtype=torch.uint8,
+                                      device="cuda")
+            it["a_rs"] = torch.empty(prob.M, dtype=torch.int32, device="cuda")
+            it["c32"] = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+            wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, None)
+            it["ws"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            it["ws_bytes"] = wsb
+            if fp16:
+                it["sa"], it["sw"] = dev(prob.a_scale), dev(prob.w_scale)
+                it["c16"] = torch.empty((prob.M, prob.N), dtype=torch.float16, device="cuda")
+            self.items.append(it)
+        self.ops = sum(it["prob"].ops for it in self.items)
+        torch.cuda.synchronize()
+
+    def pack_act(self, it):
+        p = it["prob"]
+        st = self.apt.apt_quantize_pack_activations(it["a_codes"].data_ptr(), p.M, p.K, p.q,
+                                                    it["a_buf"].data_ptr(), it["a_rs"].data_ptr(),
+                                                    self.sp)
+        self.apt.check(st, "apt_quantize_pack_activations")
+
+    def gemm(self, it, w=None):
+        p = it["prob"]
+        w = w if w is not None else it["w"]
+        fp16 = it["fp16"]
+        st = self.apt.apt_gemm(p.M, p.N, p.K, p.p, p.q, it["a_buf"].data_ptr(), w.data.data_ptr(),
+                               it["a_rs"].data_ptr(), w.rowsum.data_ptr(), it["c32"].data_ptr(),
+                               it["sa"].data_ptr() if fp16 else None,
+                               it["sw"].data_ptr() if fp16 else None,
+                               it["c16"].data_ptr() if fp16 else None, None,
+                               it["ws"].data_ptr(), it["ws_bytes"], self.sp)
+        self.apt.check(st, "apt_gemm")
+
+    def step(self, ev=None):
+        for i, it in enumerate(self.items):
+            self.pack_act(it)
+            if ev is not None and i == 2:
+                ev[0].record(self.stream)
+            self.gemm(it)
+            if ev is not None and i == 2:
+                ev[1].record(self.stream)
+
+
+def decode_cold(wl, reps: int = 3):
+    """The M=1 decode GEMMs with cold weights: rotate through enough packed
+    weight copies (> 2x the Infinity Cache) that every launch reads HBM."""
+    torch, apt = wl.torch, wl.apt
+    out = {}
+    for it in wl.items[:2]:
+        p = it["prob"]
+        wbytes = it["w"].data.numel()
+        copies = max(8, int(2 * MALL_BYTES // wbytes) + 1)
+        ws = []
+        for _ in range(copies):
+            ws.append(apt.Packed(it["w"].data.clone(), it["w"].rowsum.clone(), p.N, p.K, p.p))
+        wl.pack_act(it)
+        torch.cuda.synchronize()
+        times = []
+        for r in range(reps):
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in ws]
+            for w, (e0, e1) in zip(ws, evs):
+                e0.record(wl.stream)
+                wl.gemm(it, w)
+                e1.record(wl.stream)
+            torch.cuda.synchronize()
+            if r > 0:
+                times += [e0.elapsed_time(e1) for e0, e1 in evs]
+        t = sorted(times)[len(times) // 2] * 1e-3
+        bytes_alg = (p.N * p.K * p.p + p.M * p.K * p.q) / 8 + p.M * p.N * (4 + 2) + 2 * (p.M + p.N)
+        out["m1_n%d_k%d" % (p.N, p.K)] = {
+            "median_us": round(t * 1e6, 3), "algorithmic_bytes": int(bytes_alg),
+            "achieved_GBs": round(bytes_alg / t / 1e9, 1), "peak_GBs": PEAK_HBM_GBS,
+            "frac": round(bytes_alg / t / 1e9 / PEAK_HBM_GBS, 4), "weight_copies": copies,
+            "effective_TOPS": round(p.ops / t / 1e12, 4)}
+        del ws
+    # practical ceiling: a plain device copy of the larger weight matrix, cold
+    big = wl.items[1]["w"].data
+    n = big.numel()
+    copies = max(8, int(2 * MALL_BYTES // n) + 1)
+    srcs = [big.clone() for _ in range(copies)]
+    dst = torch.empty_like(big)
+    times = []
+    for r in range(reps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in srcs]
+        for s, (e0, e1) in zip(srcs, evs):
+            e0.record(wl.stream)
+            dst.copy_(s)
+            e1.record(wl.stream)
+        torch.cuda.synchronize()
+        if r > 0:
+            times += [e0.elapsed_time(e1) for e0, e1 in evs]
+    t = sorted(times)[len(times) // 2] * 1e-3
+    out["copy_ceiling_same_bytes"] = {"bytes_read": n, "median_us": round(t * 1e6, 3),
+                                      "read_GBs": round(n / t / 1e9, 1)}
+    return out
+
+
+def stored_traffic():
+    """HBM traffic of the prefill GEMM from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel sources."""
+    path = os.path.join(PROFILES, "gemm_int8_w4a4_2048x11008x4096_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except Exception:
+        return None
+    if d.get("kernel_hash") != kernel_hash():
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(target_s: float = 12.0):
+    """The oracle on a bounded sample of the step: both M=1 decode GEMMs in
+    full plus the first R rows of the prefill GEMM, conversion and decoding of
+    the operands included.  Rate in effective TOPS."""
+    import numpy as np
+
+    import synth
+    from oracle import oracle as ref
+    dec = [synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]
+    pre = synth.w4a4_prefill()
+
+    def run(rows):
+        ops = 0
+        t0 = time.perf_counter()
+        for p in dec:
+            C = ref.gemm(p.a_codes, p.w_codes, p.p, p.q)
+            ref.epilogue(C, p.a_scale, p.w_scale)
+            ops += p.ops
+        va = ref.values(pre.a_codes[:rows], pre.q)
+        vw = ref.values(pre.w_codes, pre.p)
+        ref.matmul(va, vw)
+        ops += 2 * rows * pre.N * pre.K
+        return ops, time.perf_counter() - t0
+
+    # calibrate: the fixed part (decode GEMMs, weight decoding) and the cost
+    # of one prefill row, then size the sample to the target time
+    t0 = time.perf_counter()
+    for p in dec:
+        ref.gemm(p.a_codes, p.w_codes, p.p, p.q)
+    vw = ref.values(pre.w_codes, pre.p)
+    t1 = time.perf_counter()
+    va = ref.values(pre.a_codes[:64], pre.q)
+    ref.matmul(va, vw)
+    t2 = time.perf_counter()
+    per_row = (t2 - t1) / 64
+    rows = int(min(pre.M, max(16, (target_s - (t1 - t0)) / per_row)))
+    del vw, va
+    ops, t = run(rows)
+    return {"value": round(ops / t / 1e12, 6), "unit": "TOPS", "cores": ref.num_threads(),
+            "kind": "oracle", "seconds": round(t, 2),
+            "sample": ("both M=1 W2A2 decode GEMMs in full (with fp16 epilogue) + rows 0..%d of the "
+                       "2048x11008x4096 W4A4 GEMM, bipolar conversion and decoding included; "
+                       "%.3g effective ops" % (rows - 1, ops))}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode-cold", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(no sharding or collectives); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    log("bench: building workload")
+    wl = Workload()
+    for _ in range(args.warmup):
+        wl.step()
+    torch.cuda.synchronize()
+    log("bench: timing %d steps" % args.steps)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e in evs:
+        wl.step(e)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    step_s = (t1 - t0) / args.steps
+    gemm_s = sum(e0.elapsed_time(e1) for e0, e1 in evs) / len(evs) * 1e-3
+    pre = wl.pre
+    achieved = pre.ops / gemm_s / 1e12
+    traffic = stored_traffic()
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": traffic,
+                "kernel": "gemm_int8_kernel W4A4 M=2048 N=11008 K=4096",
+                "avg_launch_us": round(gemm_s * 1e6, 2)}
+    cfg = wl.apt.select_config(pre.M, pre.N, pre.K, pre.p, pre.q).as_dict()
+    result = {
+        "metric": METRIC, "value": round(wl.ops / step_s / 1e12, 3), "unit": "TOPS",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(step_s * 1e3, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+        "config": {"workload": "W2A2 decode M=1 (N=4096 and N=11008, K=4096, int32 + fp16 epilogue) "
+                               "+ W4A4 prefill M=2048 N=11008 K=4096 (int32); activations packed "
+                               "every step, weights packed once",
+                   "prefill_config": cfg},
+        "roofline": roofline,
+    }
+    if not args.no_decode_cold:
+        log("bench: decode GEMMs with cold weights")
+        result["decode_cold"] = decode_cold(wl)
+    if not args.no_cpu_baseline:
+        log("bench: CPU oracle baseline")
+        result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -32,14 +32,17 @@
  *
  * Packed bit-plane layout (Sec. IV-A: decompose into n 1-bit matrices, pack
  * bits into 32-bit unsigned words, concatenate the planes):
- *   K_pad = ceil(K / 128) * 128, NC = K_pad / 128 chunks per row.
- *   The buffer holds R * NC * b * 4 little-endian uint32 words:
- *       word index  ((r * NC + c) * b + i) * 4 + w,   0 <= w < 4,
+ *   K_pad = ceil(K / 128) * 128, NC = K_pad / 128 chunks per row;
+ *   rows are grouped by 8, R_pad = ceil(R / 8) * 8.
+ *   The buffer holds R_pad * NC * b * 4 little-endian uint32 words:
+ *       word index  ((g * NC + c) * b + i) * 32 + s * 4 + w,
+ *       g = r / 8, s = r mod 8, 0 <= w < 4,
  *   and bit e (LSB = 0) of that word is bit i of the bipolar word u[r][k] with
  *       k = 128 c + 32 w + e.
- *   Bits with k >= K are zero.  The planes of one row are concatenated per
- *   128-element chunk (b planes x 16 bytes, contiguous), so a row's chunk is one
- *   contiguous b*16-byte transfer.  Buffers must be 16-byte aligned.
+ *   Bits with k >= K, and all bits of rows r >= R, are zero.  A 128-byte line
+ *   holds one plane of one chunk for 8 consecutive rows, and all b planes of
+ *   a chunk of those rows are one contiguous b*128-byte block, so a tile of
+ *   rows moves with whole-line transfers.  Buffers must be 16-byte aligned.
  *
  * Row sums: rowsum[r] = sum_{k<K} (u[r][k])_D, the sum of the bipolar values of
  * row r (= sum of 2x+1).  apt_gemm routes that contract 8-bit operands on the
@@ -92,8 +95,8 @@ typedef struct {
 } apt_config_t;
 
 /* Bytes of a packed buffer for `rows` rows of K codes at `bits` bits
- * (rows * ceil(K/128) * bits * 16).  Returns 0 for rows < 1, K < 1 or bits
- * outside [1, 8]. */
+ * (ceil(rows/8) * 8 * ceil(K/128) * bits * 16).  Returns 0 for rows < 1,
+ * K < 1 or bits outside [1, 8]. */
 size_t apt_packed_bytes(int rows, int K, int bits);
 
 /* Converts signed p-bit weight codes to bipolar-INT and packs the bit-planes
@@ -119,8 +122,11 @@ apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, 
  * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8] or out == NULL. */
 apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out);
 
-/* Workspace bytes apt_gemm needs for this problem and config (cfg NULL = the
- * selected one).  Every route currently needs 0. */
+/* Device workspace bytes apt_gemm needs for this problem and config (cfg
+ * NULL or route AUTO = the selected one): the reassembled int8 MFMA route
+ * expands the activations once per call into int8 MFMA fragments,
+ * ceil(M/32)*32 * K_pad' bytes with K_pad' = K_pad rounded up to a multiple of
+ * 256; the other routes need 0.  Returns 0 for invalid sizes. */
 size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_config_t* cfg);
 
 /* C = A * W^T on packed operands, with the fused recombination of Sec. III-B
@@ -135,12 +141,15 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
  *   c_fp16    device fp16 bits [M][N] row-major, or NULL;
  *             c_fp16[m][n] = fp16_rne(float(C) * float(a_scale[m]) * float(w_scale[n]))
  *   cfg       NULL = apt_select_config, else a config to force
- *   workspace, workspace_bytes  device scratch (see apt_gemm_workspace_bytes)
+ *   workspace, workspace_bytes  device scratch of at least
+ *             apt_gemm_workspace_bytes(...) bytes, 16-byte aligned (NULL when 0);
+ *             its contents are overwritten; calls that share a workspace must
+ *             not overlap in time
  * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8], NULL or
  * misaligned packed pointers, both outputs NULL, c_fp16 without both scales, a
- * route needing row sums without them, or an invalid cfg;
- * APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31; APT_ERR_WORKSPACE when the
- * workspace is too small; APT_ERR_HIP on launch failure. */
+ * route needing row sums without them, a misaligned workspace, or an invalid
+ * cfg; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31; APT_ERR_WORKSPACE
+ * when the workspace is missing or too small; APT_ERR_HIP on launch failure. */
 apt_status_t apt_gemm(int M, int N, int K, int p, int q,
                       const void* a_packed, const void* w_packed,
                       const int32_t* a_rowsum, const int32_t* w_rowsum,

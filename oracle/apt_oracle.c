@@ -18,7 +18,8 @@
  *   - apt_oracle_rowsum:   the sum of decoded values of each row;
  *   - apt_oracle_pack / apt_oracle_unpack: the packed bit-plane layout of
  *                          Sec. IV-A as fixed by the library header (planes of
- *                          32-bit words, concatenated per 128-element chunk).
+ *                          32-bit words, concatenated per 128-element chunk of
+ *                          8-row groups).
  * No bit tricks, no planes, no popcounts on the multiply path.  The fp16 scale
  * epilogue is evaluated in float64 by the Python side of the oracle.
  *
@@ -107,19 +108,24 @@ int apt_oracle_rowsum(const int32_t* v, int R, int K, int32_t* out) {
   return 0;
 }
 
-/* Word index of (row r, chunk c, plane i, word w) in the packed layout. */
+/* Word index of (row r, chunk c, plane i, word w) in the packed layout: rows
+ * in groups of 8, then chunk, then plane, then row within the group, then
+ * word. */
 static int64_t packed_word_index(int r, int c, int i, int w, int nchunks, int bits) {
-  return (((int64_t)r * nchunks + c) * bits + i) * 4 + w;
+  int64_t group = r / 8, slot = r % 8;
+  return ((group * nchunks + c) * bits + i) * 32 + slot * 4 + w;
 }
 
 /* Reference packing of bipolar words u [R][K] into the documented layout:
  * plane i of element k of row r is bit (k mod 32) of word
- * ((r*NC + k/128)*bits + i)*4 + (k mod 128)/32.  Every other bit is zero.
- * `packed` must hold R*NC*bits*4 words. */
+ * packed_word_index(r, k/128, i, (k mod 128)/32).  Every other bit, including
+ * all bits of the padding rows R..R_pad-1, is zero.  `packed` must hold
+ * ceil(R/8)*8*NC*bits*4 words. */
 int apt_oracle_pack(const uint8_t* u, int R, int K, int bits, uint32_t* packed) {
   if (bits < 1 || bits > 8 || R < 1 || K < 1) return -1;
   int nchunks = (K + 127) / 128;
-  int64_t total = (int64_t)R * nchunks * bits * 4;
+  int64_t rpad = ((int64_t)R + 7) / 8 * 8;
+  int64_t total = rpad * nchunks * bits * 4;
   for (int64_t t = 0; t < total; ++t) packed[t] = 0u;
   for (int r = 0; r < R; ++r) {
     for (int k = 0; k < K; ++k) {
@@ -134,13 +140,14 @@ int apt_oracle_pack(const uint8_t* u, int R, int K, int bits, uint32_t* packed) 
 }
 
 /* Reads bipolar words u [R][K] back out of a packed buffer.  Returns the
- * number of set bits found at positions k >= K (must be 0), or -1 on bad
- * arguments. */
+ * number of padding elements (k >= K, or rows R..R_pad-1) with a set bit
+ * (must be 0), or -1 on bad arguments. */
 int64_t apt_oracle_unpack(const uint32_t* packed, int R, int K, int bits, uint8_t* u) {
   if (bits < 1 || bits > 8 || R < 1 || K < 1) return -1;
   int nchunks = (K + 127) / 128;
+  int rpad = (R + 7) / 8 * 8;
   int64_t stray = 0;
-  for (int r = 0; r < R; ++r) {
+  for (int r = 0; r < rpad; ++r) {
     for (int k = 0; k < nchunks * 128; ++k) {
       int c = k / 128, w = (k % 128) / 32, e = k % 32;
       unsigned value = 0;
@@ -148,7 +155,7 @@ int64_t apt_oracle_unpack(const uint32_t* packed, int R, int K, int bits, uint8_
         uint32_t bit = (packed[packed_word_index(r, c, i, w, nchunks, bits)] >> e) & 1u;
         value |= bit << i;
       }
-      if (k < K)
+      if (k < K && r < R)
         u[(int64_t)r * K + k] = (uint8_t)value;
       else
         stray += (value != 0);

@@ -134,7 +134,7 @@ def rowsum(v: np.ndarray) -> np.ndarray:
 
 
 def packed_words(rows: int, K: int, bits: int) -> int:
-    return rows * ((K + 127) // 128) * bits * 4
+    return (rows + 7) // 8 * 8 * ((K + 127) // 128) * bits * 4
 
 
 def pack(u: np.ndarray, bits: int) -> np.ndarray:

@@ -177,17 +177,24 @@ def pack(codes, bits: int, activations: bool = False, stream=None) -> Packed:
 
 
 def gemm(a: Packed, w: Packed, out_int32: bool = True, a_scale=None, w_scale=None,
-         out_fp16: bool = False, cfg: apt_config_t | None = None, stream=None):
-    """C = A W^T on packed operands.  Returns (c_int32 or None, c_fp16 or None)."""
+         out_fp16: bool = False, cfg: apt_config_t | None = None, stream=None, workspace=None):
+    """C = A W^T on packed operands.  Returns (c_int32 or None, c_fp16 or None).
+    A workspace of apt_gemm_workspace_bytes is allocated with torch unless one
+    is passed."""
     torch = _torch()
     assert a.K == w.K
     M, N, K = a.rows, w.rows, a.K
     dev = a.data.device
     c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
     c16 = torch.empty((M, N), dtype=torch.float16, device=dev) if out_fp16 else None
+    ws_bytes = apt_gemm_workspace_bytes(M, N, K, w.bits, a.bits, cfg)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(apt_gemm(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
                    _ptr(a.rowsum), _ptr(w.rowsum), _ptr(c32), _ptr(a_scale), _ptr(w_scale),
-                   _ptr(c16), cfg, None, 0, _stream_ptr(stream)), "apt_gemm")
+                   _ptr(c16), cfg, ws_ptr, ws_len, _stream_ptr(stream)), "apt_gemm")
     return c32, c16
 
 

@@ -55,7 +55,8 @@ extern "C" {
 
 size_t apt_packed_bytes(int rows, int K, int bits) {
   if (rows < 1 || K < 1 || !bits_ok(bits)) return 0;
-  return (size_t)rows * (size_t)apt::num_chunks(K) * (size_t)bits * apt::kWordsPerPlane * 4;
+  return (size_t)apt::padded_rows(rows) * (size_t)apt::num_chunks(K) * (size_t)bits *
+         apt::kWordsPerPlane * 4;
 }
 
 apt_status_t apt_pack_weights(const int8_t* w_codes, int N, int K, int p, void* w_packed,
@@ -75,15 +76,19 @@ apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* 
   return APT_OK;
 }
 
-size_t apt_gemm_workspace_bytes(int, int, int, int, int, const apt_config_t*) { return 0; }
+size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_config_t* cfg) {
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return 0;
+  const apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
+                             ? apt::select_config(M, N, K, p, q)
+                             : *cfg;
+  return c.route == APT_ROUTE_INT8_MFMA ? apt::int8_workspace_bytes(M, K) : 0;
+}
 
 apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, const void* w_packed,
                       const int32_t* a_rowsum, const int32_t* w_rowsum, int32_t* c_int32,
                       const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
                       const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
                       void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return APT_ERR_INVALID_ARG;
   if (a_packed == nullptr || w_packed == nullptr || !aligned16(a_packed) || !aligned16(w_packed))
     return APT_ERR_INVALID_ARG;
@@ -99,6 +104,11 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, c
   const bool have_rowsums = a_rowsum != nullptr && w_rowsum != nullptr;
   apt_status_t st = check_config(c, M, p, q, have_rowsums);
   if (st != APT_OK) return st;
+  if (c.route == APT_ROUTE_INT8_MFMA) {
+    if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, K))
+      return APT_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return APT_ERR_INVALID_ARG;
+  }
 
   apt::GemmArgs g;
   g.M = M; g.N = N; g.K = K; g.p = p; g.q = q;
@@ -113,7 +123,7 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, c
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (c.route) {
     case APT_ROUTE_XOR: return hip_status(apt::launch_gemm_xor(g, c, s));
-    case APT_ROUTE_INT8_MFMA: return hip_status(apt::launch_gemm_int8(g, c, s));
+    case APT_ROUTE_INT8_MFMA: return hip_status(apt::launch_gemm_int8(g, c, workspace, s));
     case APT_ROUTE_PM1_MFMA: return hip_status(apt::launch_gemm_pm1(g, c, s));
   }
   return APT_ERR_INVALID_ARG;

@@ -11,11 +11,21 @@
 namespace apt {
 
 // Packed layout (fixed in apt.h): 128 elements per chunk, 4 uint32 words per
-// plane per chunk, planes of one chunk contiguous.
+// plane per chunk; rows in groups of 8, and for each group and chunk the b
+// planes follow each other, each plane holding the 8 rows' 4 words.
 constexpr int kChunk = 128;
 constexpr int kWordsPerPlane = 4;
+constexpr int kRowGroup = 8;
+constexpr int kPlaneStride = kRowGroup * kWordsPerPlane;  // words from plane i to plane i+1
 
 inline int num_chunks(int K) { return (K + kChunk - 1) / kChunk; }
+inline int padded_rows(int R) { return (R + kRowGroup - 1) / kRowGroup * kRowGroup; }
+
+// Word offset of the 4 words of plane i, chunk c, row r.
+__host__ __device__ __forceinline__ int64_t plane_words(int r, int c, int i, int nchunks, int bits) {
+  return ((int64_t)(r / kRowGroup) * nchunks + c) * bits * kPlaneStride + i * kPlaneStride +
+         (r % kRowGroup) * kWordsPerPlane;
+}
 
 // Launch of the converter + bit-plane packer (pack.hip).
 hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t* packed,
@@ -38,9 +48,12 @@ struct GemmArgs {
 hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
 bool xor_config_ok(const apt_config_t& cfg);
 
-// Reassembled int8 MFMA route (gemm_mfma.hip).
-hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
+// Reassembled int8 MFMA route (gemm_int8.hip).  The workspace holds the
+// activations expanded into MFMA fragments (int8_workspace_bytes).
+hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
+                            hipStream_t stream);
 bool int8_config_ok(const apt_config_t& cfg);
+size_t int8_workspace_bytes(int M, int K);
 
 // Plane-pair +-1 MFMA route (gemm_pm1.hip).
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);

@@ -1,16 +1,27 @@
 // gemm_int8.h - the reassembled-int8 MFMA route of the WpAq bipolar-INT
 // GEMM for gfx950 (APT-LLM, arXiv 2508.19087, Sec. III-B and IV-B).
 //
-// Each workgroup owns one BM x BN output tile and every bit-plane pair of it,
-// as the paper's recovery-oriented scheduling does (Sec. IV-B).  K advances
-// one 128-element chunk per pipeline step:
-//   1. global -> registers: the packed planes of the tile's A rows (q planes)
-//      and W rows (p planes), prefetched one step ahead;
-//   2. registers -> LDS: each row's planes are merged back into one byte per
-//      element (reassemble.h) and written to a double-buffered LDS tile;
-//   3. LDS -> MFMA: v_mfma_i32_32x32x32_i8 over the reassembled bytes.
-// Recombination therefore happens before the multiply; the paper's Sec. III-B
-// sum over plane products is the same number by distributivity.
+// The bit-planes of each operand are merged back into one byte per element
+// before the multiply (reassemble.h), so one v_mfma_i32_32x32x32_i8 covers
+// every plane pair of an element pair; the paper's Sec. III-B sum over plane
+// products is the same number by distributivity.
+//
+// Two kernels:
+//   expand_a_kernel  once per call, the activations' planes are reassembled
+//                    into operand bytes laid out as ready-made MFMA fragments
+//                    (a workspace buffer), so the main kernel loads them with
+//                    whole-line 1 KB reads straight into registers;
+//   gemm_int8_kernel each workgroup owns one BM x BN output tile and every
+//                    plane pair of it, as the paper's recovery-oriented
+//                    scheduling does (Sec. IV-B).  K advances one 128-element
+//                    chunk per pipeline step: the weight planes of the tile
+//                    are fetched two chunks ahead, reassembled into a
+//                    double-buffered LDS tile while the matrix cores work on
+//                    the previous chunk, and the activation fragments of the
+//                    next chunk are fetched k-step by k-step behind the MFMAs.
+// Only the weights pass through LDS: staging both operands there would need
+// as many LDS bytes per chunk as the MFMAs take cycles, and LDS would bound
+// the kernel.
 //
 // Operand bytes are y = u (b <= 7) or u - 128 (b == 8) with bipolar value
 // v = 2y + c.  Expanding sum_k v_a v_w over the real K gives the epilogue
@@ -28,173 +39,295 @@ namespace apt {
 namespace int8 {
 
 constexpr int kWave = 64;
-constexpr int kRowBytes = kChunk + 16;  // padded LDS row: 128 operand bytes + 16
+constexpr int kRowBytes = kChunk + 16;          // padded LDS row: 128 operand bytes + 16
+constexpr int kStepBytes = 32;                  // K bytes per MFMA k-step
+constexpr int kSteps = kChunk / kStepBytes;     // k-steps per chunk
+constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes x 16 bytes
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
+// All-zero plane words: the weight planes of a chunk past the end (the main
+// loop always runs an even number of chunks) are read from here, which makes
+// them padding elements.  Large enough for any in-group offset of 8 planes.
+static __device__ __attribute__((aligned(16))) uint32_t kZeroPlanes[512] = {};
+
 struct Int8Params {
   GemmArgs g;
-  int nchunks;
+  int nchunks;        // NC, chunks of K
+  int nsteps;         // k-steps in the activation fragment buffer (even chunk count x 4)
   int tiles_n;
+  int mblocks;        // 32-row blocks of the activation fragment buffer
+  const v4i* a_frag;  // activation fragments (workspace)
 };
 
-// Staging of one operand: ROWS rows of a tile, each split into SPLIT items of
-// 128/SPLIT elements (4/SPLIT words per plane).
+// Bytes of the activation fragment buffer for M rows and K.
+inline size_t a_frag_bytes(int M, int K) {
+  const int nce = (num_chunks(K) + 1) & ~1;
+  return (size_t)((M + 31) / 32) * 32 * nce * kChunk;
+}
+
+// ---- activation expansion ---------------------------------------------------
+// Fragment (mb, ks) holds k-step ks of rows 32 mb .. 32 mb + 31 in MFMA operand
+// order: lane l (vector index ((mb * nsteps + ks) * 64 + l)) carries 16 bytes of
+// row 32 mb + l mod 32, namely bytes 16 (l / 32) .. 16 (l / 32) + 15 of the
+// k-step's 32 reassembled bytes.  Rows past M and chunks past the last one are
+// expanded from all-zero planes (padding elements).
+template <int Q>
+__global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restrict__ a_packed, int M,
+                                                       int nchunks, int nsteps, int mblocks,
+                                                       v4i* __restrict__ out) {
+  const int rows = mblocks * 32;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)rows * (nsteps / kSteps)) return;
+  const int row = (int)(t % rows);
+  const int chunk = (int)(t / rows);
+  uint32_t pw[kWordsPerPlane][Q];
+  if (row < M && chunk < nchunks) {
+    const uint32_t* src = a_packed + plane_words(row, chunk, 0, nchunks, Q);
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      uint4 v = *reinterpret_cast<const uint4*>(src + j * kPlaneStride);
+      pw[0][j] = v.x; pw[1][j] = v.y; pw[2][j] = v.z; pw[3][j] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < kWordsPerPlane; ++w)
+#pragma unroll
+      for (int j = 0; j < Q; ++j) pw[w][j] = 0u;
+  }
+  const int mb = row / 32, l = row % 32;
+#pragma unroll
+  for (int w = 0; w < kWordsPerPlane; ++w) {
+    uint32_t o[8];
+    reassemble_word<Q>(pw[w], o);
+    v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w) * kFragVecs;
+    f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+  }
+}
+
+// ---- weight staging -----------------------------------------------------------
+// ROWS weight rows of a tile, each split into SPLIT items of 128/SPLIT elements
+// (4/SPLIT words per plane).  Rows past the matrix edge are clamped to its last
+// row: their products only reach outputs that are never stored, and the code
+// stays branch-free so the scheduler can interleave it with the MFMAs.
 template <int B, int ROWS, int SPLIT, int T>
 struct Stage {
   static constexpr int kWpi = kWordsPerPlane / SPLIT;
   static constexpr int kItems = ROWS * SPLIT / T;
-  static_assert(ROWS * SPLIT % T == 0, "items must divide evenly");
+  static_assert(ROWS * SPLIT % T == 0 && kItems >= 1, "items must divide evenly");
   uint32_t raw[kItems][B][kWpi];
 
+  // Loads chunk `chunk` of the item rows; a chunk at or past the end reads the
+  // zero planes, i.e. padding elements.
   __device__ __forceinline__ void load(const uint32_t* __restrict__ packed, int row0, int rows,
                                        int nchunks, int chunk, int tid) {
+    const bool real = chunk < nchunks;
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
       const int item = tid + T * it;
-      const int r = row0 + item / SPLIT;
+      const int r = min(row0 + item / SPLIT, rows - 1);
       const int sub = item % SPLIT;
-      if (r < rows) {
-        const uint32_t* src = packed + (((int64_t)r * nchunks + chunk) * B) * kWordsPerPlane + sub * kWpi;
+      const uint32_t* src = real ? packed + plane_words(r, chunk, 0, nchunks, B) + sub * kWpi
+                                 : kZeroPlanes + (r % kRowGroup) * kWordsPerPlane + sub * kWpi;
 #pragma unroll
-        for (int i = 0; i < B; ++i) {
-          if (kWpi == 4) {
-            uint4 v = *reinterpret_cast<const uint4*>(src + i * kWordsPerPlane);
-            raw[it][i][0] = v.x; raw[it][i][1] = v.y; raw[it][i][2] = v.z; raw[it][i][3] = v.w;
-          } else if (kWpi == 2) {
-            uint2 v = *reinterpret_cast<const uint2*>(src + i * kWordsPerPlane);
-            raw[it][i][0] = v.x; raw[it][i][1] = v.y;
-          } else {
-            raw[it][i][0] = src[i * kWordsPerPlane];
-          }
+      for (int i = 0; i < B; ++i) {
+        if (kWpi == 4) {
+          uint4 v = *reinterpret_cast<const uint4*>(src + i * kPlaneStride);
+          raw[it][i][0] = v.x; raw[it][i][1] = v.y; raw[it][i][2] = v.z; raw[it][i][3] = v.w;
+        } else if (kWpi == 2) {
+          uint2 v = *reinterpret_cast<const uint2*>(src + i * kPlaneStride);
+          raw[it][i][0] = v.x; raw[it][i][1] = v.y;
+        } else {
+          raw[it][i][0] = src[i * kPlaneStride];
         }
-      } else {
-#pragma unroll
-        for (int i = 0; i < B; ++i)
-#pragma unroll
-          for (int w = 0; w < kWpi; ++w) raw[it][i][w] = 0u;
       }
     }
+  }
+
+  // Reassembles word u (0 <= u < kWords) of this thread's items into LDS.
+  static constexpr int kWords = kItems * kWpi;
+  __device__ __forceinline__ void store_word(uint8_t* lds_tile, int tid, int u) const {
+    const int it = u / kWpi, w = u % kWpi;
+    const int item = tid + T * it;
+    const int r = item / SPLIT;
+    const int sub = item % SPLIT;
+    uint32_t pw[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
+    uint32_t o[8];
+    reassemble_word<B>(pw, o);
+    uint4* d4 = reinterpret_cast<uint4*>(lds_tile + r * kRowBytes + (sub * kWpi + w) * kStepBytes);
+    d4[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    d4[1] = make_uint4(o[4], o[5], o[6], o[7]);
   }
 
   __device__ __forceinline__ void store(uint8_t* lds_tile, int tid) const {
 #pragma unroll
-    for (int it = 0; it < kItems; ++it) {
-      const int item = tid + T * it;
-      const int r = item / SPLIT;
-      const int sub = item % SPLIT;
-      uint8_t* dst = lds_tile + r * kRowBytes + sub * kWpi * 32;
-#pragma unroll
-      for (int w = 0; w < kWpi; ++w) {
-        uint32_t pw[B];
-#pragma unroll
-        for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
-        uint32_t o[8];
-        reassemble_word<B>(pw, o);
-        uint4* d4 = reinterpret_cast<uint4*>(dst + w * 32);
-        d4[0] = make_uint4(o[0], o[1], o[2], o[3]);
-        d4[1] = make_uint4(o[4], o[5], o[6], o[7]);
-      }
-    }
+    for (int u = 0; u < kWords; ++u) store_word(lds_tile, tid, u);
   }
 };
 
-template <int P, int Q, int BM, int BN, int WM, int WN, int SPLIT>
+__host__ __device__ constexpr int offset_of(int b) { return b == 8 ? 1 : 1 - (1 << b); }
+__host__ __device__ constexpr int pad_of(int b) { return b == 8 ? -128 : 0; }
+
+// ---- main kernel --------------------------------------------------------------
+// The MFMA takes the weight fragment as its first operand, so the accumulator
+// of lane l holds D[n][m] for m = l mod 32 and four consecutive n: each lane
+// stores 16 contiguous output bytes.
+template <int P, int BM, int BN, int WM, int WN, int SPLIT>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm) {
   constexpr int T = WM * WN * kWave;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
-  constexpr int FM = WTM / 32, FN = WTN / 32;  // 32x32 MFMA tiles per wave
-  constexpr int kStageBytes = (BM + BN) * kRowBytes;
+  constexpr int FM = WTM / 32, FN = WTN / 32;  // 32x32 fragments per wave
+  constexpr int kStageBytes = BN * kRowBytes;
   static_assert(FM >= 1 && FN >= 1, "wave tile too small");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
 
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
+  const int NCE = (NC + 1) & ~1;  // even chunk count; a last odd chunk is all padding
   const int tid = threadIdx.x;
   const int lane = tid % kWave;
   const int wave = tid / kWave;
   const int wm = wave / WN, wn = wave % WN;
 
-  const int tile = blockIdx.x;
+  // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
+  // run of tiles (consecutive tiles share their activation rows) so that its
+  // L2 keeps the shared operand.
+  const int ntiles = gridDim.x;
+  int tile = blockIdx.x;
+  if (ntiles % 8 == 0) tile = (blockIdx.x % 8) * (ntiles / 8) + blockIdx.x / 8;
   const int tm = tile / prm.tiles_n, tn = tile % prm.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  Stage<Q, BM, SPLIT, T> sa;
-  Stage<P, BN, SPLIT, T> sw;
+  using SW = Stage<P, BN, SPLIT, T>;
+  SW rw0, rw1;
+  uint8_t* buf0 = lds;
+  uint8_t* buf1 = lds + kStageBytes;
 
-  v16i acc[FM][FN];
+  v16i acc[FN][FM];
 #pragma unroll
-  for (int a = 0; a < FM; ++a)
+  for (int b = 0; b < FN; ++b)
 #pragma unroll
-    for (int b = 0; b < FN; ++b)
+    for (int a = 0; a < FM; ++a)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0;
+      for (int v = 0; v < 16; ++v) acc[b][a][v] = 0;
 
-  sa.load(g.a_packed, m0, g.M, NC, 0, tid);
-  sw.load(g.w_packed, n0, g.N, NC, 0, tid);
-  sa.store(lds, tid);
-  sw.store(lds + BM * kRowBytes, tid);
-  __syncthreads();
+  // Activation fragments of this wave: 32-row blocks clamped to the buffer.
+  const v4i* a_ptr[FM];
+#pragma unroll
+  for (int a = 0; a < FM; ++a) {
+    const int mb = min((m0 + wm * WTM) / 32 + a, prm.mblocks - 1);
+    a_ptr[a] = prm.a_frag + (int64_t)mb * prm.nsteps * kFragVecs + lane;
+  }
+  v4i afr[kSteps][FM];
 
   const int lrow = lane % 32;
   const int lk = (lane / 32) * 16;
-  for (int c = 0; c < NC; ++c) {
-    const bool more = c + 1 < NC;
-    if (more) {
-      sa.load(g.a_packed, m0, g.M, NC, c + 1, tid);
-      sw.load(g.w_packed, n0, g.N, NC, c + 1, tid);
-    }
-    const uint8_t* st = lds + (c & 1) * kStageBytes;
-    const uint8_t* a_t = st + (wm * WTM + lrow) * kRowBytes + lk;
-    const uint8_t* w_t = st + (BM + wn * WTN + lrow) * kRowBytes + lk;
+
+  // One pipeline phase: the MFMAs of chunk c from LDS buffer `cst`, k-step by
+  // k-step.  During k-step ks the weight fragments of ks+1 are read, one slice
+  // of the next chunk's weight reassembly goes to LDS buffer `sst`, and the
+  // activation fragment registers of ks are refilled with chunk c+1.  A
+  // scheduling fence closes every k-step.
+  auto phase = [&](const uint8_t* cst, uint8_t* sst, const SW& rw, int c) {
+    const uint8_t* w_t = cst + (wn * WTN + lrow) * kRowBytes + lk;
+    const int next_step = min(c + 1, NCE - 1) * kSteps;
+    v4i wf[2][FN];
 #pragma unroll
-    for (int ks = 0; ks < kChunk / 32; ++ks) {
-      v4i af[FM], bf[FN];
+    for (int b = 0; b < FN; ++b) wf[0][b] = *reinterpret_cast<const v4i*>(w_t + b * 32 * kRowBytes);
 #pragma unroll
-      for (int a = 0; a < FM; ++a)
-        af[a] = *reinterpret_cast<const v4i*>(a_t + a * 32 * kRowBytes + ks * 32);
-#pragma unroll
-      for (int b = 0; b < FN; ++b)
-        bf[b] = *reinterpret_cast<const v4i*>(w_t + b * 32 * kRowBytes + ks * 32);
-#pragma unroll
-      for (int a = 0; a < FM; ++a)
+    for (int ks = 0; ks < kSteps; ++ks) {
+      const int cur = ks & 1, nxt = cur ^ 1;
+      if (ks + 1 < kSteps) {
 #pragma unroll
         for (int b = 0; b < FN; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[a], bf[b], acc[a][b], 0, 0, 0);
+          wf[nxt][b] = *reinterpret_cast<const v4i*>(w_t + b * 32 * kRowBytes + (ks + 1) * kStepBytes);
+      }
+#pragma unroll
+      for (int u = ks * SW::kWords / kSteps; u < (ks + 1) * SW::kWords / kSteps; ++u)
+        rw.store_word(sst, tid, u);
+#pragma unroll
+      for (int b = 0; b < FN; ++b)
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+          acc[b][a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[cur][b], afr[ks][a], acc[b][a], 0, 0, 0);
+#pragma unroll
+      for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)(next_step + ks) * kFragVecs];
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (more) {
-      uint8_t* nx = lds + ((c + 1) & 1) * kStageBytes;
-      sa.store(nx, tid);
-      sw.store(nx + BM * kRowBytes, tid);
-    }
+  };
+
+  // Prologue: weight chunk 0 into LDS buffer 0, chunk 1 in registers,
+  // activation fragments of chunk 0 in registers.
+  rw0.load(g.w_packed, n0, g.N, NC, 0, tid);
+  rw1.load(g.w_packed, n0, g.N, NC, 1, tid);
+#pragma unroll
+  for (int ks = 0; ks < kSteps; ++ks)
+#pragma unroll
+    for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)ks * kFragVecs];
+  rw0.store(buf0, tid);
+  __syncthreads();
+
+  // Two chunks per trip.  While the MFMAs of chunk c run, weight chunk c+1
+  // (already in registers) is reassembled into the other LDS buffer and
+  // weight chunk c+2 is fetched into the register set just consumed.
+  for (int c = 0; c < NCE; c += 2) {
+    rw0.load(g.w_packed, n0, g.N, NC, c + 2, tid);
+    phase(buf0, buf1, rw1, c);
+    __syncthreads();
+    rw1.load(g.w_packed, n0, g.N, NC, c + 3, tid);
+    phase(buf1, buf0, rw0, c + 1);
     __syncthreads();
   }
 
-  // Epilogue: affine correction, optional fp16 scaling, stores.
-  constexpr int ca = operand_offset<Q>(), cw = operand_offset<P>();
+  // Epilogue: affine correction, optional fp16 scaling, 16-byte stores.
+  const int q = g.q;
+  const uint32_t ca = (uint32_t)(q == 8 ? 1 : 1 - (1 << q)), cw = (uint32_t)offset_of(P);
   const uint32_t pad_term =
-      4u * (uint32_t)(NC * kChunk - g.K) * (uint32_t)(operand_pad<Q>() * operand_pad<P>());
-  const uint32_t const_term = (uint32_t)(ca * cw) * (uint32_t)g.K + pad_term;
+      4u * (uint32_t)(NCE * kChunk - g.K) * (uint32_t)((q == 8 ? -128 : 0) * pad_of(P));
+  const uint32_t const_term = ca * cw * (uint32_t)g.K + pad_term;
+  const bool vec_ok = (g.N % 4) == 0;
 #pragma unroll
-  for (int b = 0; b < FN; ++b) {
-    const int n = n0 + wn * WTN + b * 32 + lrow;
-    if (n >= g.N) continue;
-    const uint32_t wterm = (uint32_t)ca * (uint32_t)g.w_rowsum[n];
-    const float sw_f = g.c_fp16 ? __half2float(g.w_scale[n]) : 0.f;
+  for (int a = 0; a < FM; ++a) {
+    const int m = m0 + wm * WTM + a * 32 + lrow;
+    if (m >= g.M) continue;
+    const uint32_t aterm = cw * (uint32_t)g.a_rowsum[m] - const_term;
+    const float sa = g.c_fp16 ? __half2float(g.a_scale[m]) : 0.f;
 #pragma unroll
-    for (int a = 0; a < FM; ++a) {
+    for (int b = 0; b < FN; ++b) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * WTM + a * 32 + (v / 4) * 8 + (lane / 32) * 4 + (v % 4);
-        if (m < g.M) {
-          const uint32_t d = (uint32_t)acc[a][b][v];
-          const uint32_t cval = 4u * d + (uint32_t)cw * (uint32_t)g.a_rowsum[m] + wterm - const_term;
-          const int64_t o = (int64_t)m * g.N + n;
-          if (g.c_int32) g.c_int32[o] = (int32_t)cval;
-          if (g.c_fp16) {
-            float f = (float)(int32_t)cval * __half2float(g.a_scale[m]);
-            g.c_fp16[o] = __float2half_rn(f * sw_f);
+      for (int gi = 0; gi < 4; ++gi) {
+        const int n4 = n0 + wn * WTN + b * 32 + gi * 8 + (lane / 32) * 4;
+        if (n4 >= g.N) continue;
+        int32_t cv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = min(n4 + j, g.N - 1);
+          cv[j] = (int32_t)(4u * (uint32_t)acc[b][a][gi * 4 + j] + aterm + ca * (uint32_t)g.w_rowsum[n]);
+        }
+        const int64_t o = (int64_t)m * g.N + n4;
+        const bool full = vec_ok && n4 + 3 < g.N;
+        if (g.c_int32) {
+          if (full) {
+            *reinterpret_cast<int4*>(g.c_int32 + o) = make_int4(cv[0], cv[1], cv[2], cv[3]);
+          } else {
+            for (int j = 0; j < 4 && n4 + j < g.N; ++j) g.c_int32[o + j] = cv[j];
+          }
+        }
+        if (g.c_fp16) {
+          __half h[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int n = min(n4 + j, g.N - 1);
+            h[j] = __float2half_rn((float)cv[j] * sa * __half2float(g.w_scale[n]));
+          }
+          if (full) {
+            *reinterpret_cast<uint2*>(g.c_fp16 + o) = *reinterpret_cast<const uint2*>(h);
+          } else {
+            for (int j = 0; j < 4 && n4 + j < g.N; ++j) g.c_fp16[o + j] = h[j];
           }
         }
       }
@@ -206,20 +339,21 @@ struct TileShape {
   int bm, bn, wm, wn, split;
 };
 constexpr TileShape kShapes[] = {
+    {256, 256, 4, 2, 2},
+    {256, 256, 2, 4, 2},
+    {256, 128, 4, 2, 4},
     {128, 128, 2, 2, 2},
-    {256, 128, 2, 2, 2},
-    {256, 256, 2, 2, 1},
 };
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
-template <int P, int Q, int S>
+template <int P, int S>
 hipError_t launch_shape(const Int8Params& prm0, hipStream_t stream) {
   constexpr TileShape sh = kShapes[S];
   Int8Params prm = prm0;
   prm.tiles_n = (prm.g.N + sh.bn - 1) / sh.bn;
   const int tiles_m = (prm.g.M + sh.bm - 1) / sh.bm;
-  const size_t lds = 2 * (size_t)(sh.bm + sh.bn) * kRowBytes;
-  auto kern = gemm_int8_kernel<P, Q, sh.bm, sh.bn, sh.wm, sh.wn, sh.split>;
+  const size_t lds = 2 * (size_t)sh.bn * kRowBytes;
+  auto kern = gemm_int8_kernel<P, sh.bm, sh.bn, sh.wm, sh.wn, sh.split>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -227,20 +361,24 @@ hipError_t launch_shape(const Int8Params& prm0, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int P, int Q>
-inline hipError_t launch_pq(int shape, const Int8Params& prm, hipStream_t stream) {
+template <int P>
+inline hipError_t launch_p_shape(int shape, const Int8Params& prm, hipStream_t stream) {
   switch (shape) {
-    case 0: return launch_shape<P, Q, 0>(prm, stream);
-    case 1: return launch_shape<P, Q, 1>(prm, stream);
-    case 2: return launch_shape<P, Q, 2>(prm, stream);
+    case 0: return launch_shape<P, 0>(prm, stream);
+    case 1: return launch_shape<P, 1>(prm, stream);
+    case 2: return launch_shape<P, 2>(prm, stream);
+    case 3: return launch_shape<P, 3>(prm, stream);
   }
   return hipErrorInvalidValue;
 }
 
-// Launch for weight bits P and any activation bits; one explicit
-// instantiation per P lives in gemm_int8_inst.hip (built once per P).
+// Launches for weight bits P (main kernel) and activation bits Q (expansion);
+// the explicit instantiations live in gemm_int8_inst.hip, built once per width.
 template <int P>
-hipError_t launch_for_p(int q, int shape, const Int8Params& prm, hipStream_t stream);
+hipError_t launch_for_p(int shape, const Int8Params& prm, hipStream_t stream);
+template <int Q>
+hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
+                               int mblocks, v4i* out, hipStream_t stream);
 
 }  // namespace int8
 }  // namespace apt

@@ -1,11 +1,12 @@
-// gemm_int8.hip - config checks and dispatch of the reassembled-int8 MFMA
-// route; the kernel is in gemm_int8.h.
+// gemm_int8.hip - config checks, workspace size and dispatch of the
+// reassembled-int8 MFMA route; the kernels are in gemm_int8.h.
 #include "gemm_int8.h"
 
 namespace apt {
 namespace int8 {
 namespace {
 
+// A config names a shape by its tile and wave grid.
 int shape_index(const apt_config_t& cfg) {
   for (int s = 0; s < kNumShapes; ++s)
     if (kShapes[s].bm == cfg.bm && kShapes[s].bn == cfg.bn && kShapes[s].wm == cfg.waves_m &&
@@ -17,30 +18,47 @@ int shape_index(const apt_config_t& cfg) {
 }  // namespace
 }  // namespace int8
 
-using int8::shape_index;
-using int8::Int8Params;
-
 bool int8_config_ok(const apt_config_t& cfg) {
-  return shape_index(cfg) >= 0 && (cfg.bk == 0 || cfg.bk == kChunk) &&
+  return int8::shape_index(cfg) >= 0 && (cfg.bk == 0 || cfg.bk == kChunk) &&
          (cfg.lds_stages == 0 || cfg.lds_stages == 2) && cfg.k_split <= 1;
 }
 
-hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream) {
+size_t int8_workspace_bytes(int M, int K) { return int8::a_frag_bytes(M, K); }
+
+hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
+                            hipStream_t stream) {
+  using namespace int8;
   const int shape = shape_index(cfg);
   if (shape < 0) return hipErrorInvalidValue;
   Int8Params prm;
   prm.g = g;
   prm.nchunks = num_chunks(g.K);
+  prm.nsteps = ((prm.nchunks + 1) & ~1) * kSteps;
   prm.tiles_n = 0;
+  prm.mblocks = (g.M + 31) / 32;
+  prm.a_frag = static_cast<const v4i*>(workspace);
+  v4i* frag = static_cast<v4i*>(workspace);
+  hipError_t e = hipErrorInvalidValue;
+  switch (g.q) {
+    case 1: e = launch_expand_for_q<1>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 2: e = launch_expand_for_q<2>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 3: e = launch_expand_for_q<3>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 4: e = launch_expand_for_q<4>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 5: e = launch_expand_for_q<5>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 6: e = launch_expand_for_q<6>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 7: e = launch_expand_for_q<7>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+    case 8: e = launch_expand_for_q<8>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
+  }
+  if (e != hipSuccess) return e;
   switch (g.p) {
-    case 1: return int8::launch_for_p<1>(g.q, shape, prm, stream);
-    case 2: return int8::launch_for_p<2>(g.q, shape, prm, stream);
-    case 3: return int8::launch_for_p<3>(g.q, shape, prm, stream);
-    case 4: return int8::launch_for_p<4>(g.q, shape, prm, stream);
-    case 5: return int8::launch_for_p<5>(g.q, shape, prm, stream);
-    case 6: return int8::launch_for_p<6>(g.q, shape, prm, stream);
-    case 7: return int8::launch_for_p<7>(g.q, shape, prm, stream);
-    case 8: return int8::launch_for_p<8>(g.q, shape, prm, stream);
+    case 1: return launch_for_p<1>(shape, prm, stream);
+    case 2: return launch_for_p<2>(shape, prm, stream);
+    case 3: return launch_for_p<3>(shape, prm, stream);
+    case 4: return launch_for_p<4>(shape, prm, stream);
+    case 5: return launch_for_p<5>(shape, prm, stream);
+    case 6: return launch_for_p<6>(shape, prm, stream);
+    case 7: return launch_for_p<7>(shape, prm, stream);
+    case 8: return launch_for_p<8>(shape, prm, stream);
   }
   return hipErrorInvalidValue;
 }

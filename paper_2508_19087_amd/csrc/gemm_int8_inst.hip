@@ -1,26 +1,30 @@
 // gemm_int8_inst.hip - instantiates the reassembled-int8 MFMA kernels for one
-// weight bit width, APT_INST_P (the build compiles this file once per width).
+// bit width, APT_INST_P: the main kernel for weight width APT_INST_P and the
+// activation expansion for activation width APT_INST_P (the build compiles
+// this file once per width).
 #include "gemm_int8.h"
 
 namespace apt {
 namespace int8 {
 
 template <int P>
-hipError_t launch_for_p(int q, int shape, const Int8Params& prm, hipStream_t stream) {
-  switch (q) {
-    case 1: return launch_pq<P, 1>(shape, prm, stream);
-    case 2: return launch_pq<P, 2>(shape, prm, stream);
-    case 3: return launch_pq<P, 3>(shape, prm, stream);
-    case 4: return launch_pq<P, 4>(shape, prm, stream);
-    case 5: return launch_pq<P, 5>(shape, prm, stream);
-    case 6: return launch_pq<P, 6>(shape, prm, stream);
-    case 7: return launch_pq<P, 7>(shape, prm, stream);
-    case 8: return launch_pq<P, 8>(shape, prm, stream);
-  }
-  return hipErrorInvalidValue;
+hipError_t launch_for_p(int shape, const Int8Params& prm, hipStream_t stream) {
+  return launch_p_shape<P>(shape, prm, stream);
 }
 
-template hipError_t launch_for_p<APT_INST_P>(int, int, const Int8Params&, hipStream_t);
+template <int Q>
+hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
+                               int mblocks, v4i* out, hipStream_t stream) {
+  const int64_t threads = (int64_t)mblocks * 32 * (nsteps / kSteps);
+  const int blocks = (int)((threads + 255) / 256);
+  hipLaunchKernelGGL(expand_a_kernel<Q>, dim3(blocks), dim3(256), 0, stream, a_packed, M, nchunks,
+                     nsteps, mblocks, out);
+  return hipGetLastError();
+}
+
+template hipError_t launch_for_p<APT_INST_P>(int, const Int8Params&, hipStream_t);
+template hipError_t launch_expand_for_q<APT_INST_P>(const uint32_t*, int, int, int, int, v4i*,
+                                                     hipStream_t);
 
 }  // namespace int8
 }  // namespace apt

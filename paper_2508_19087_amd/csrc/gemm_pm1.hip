@@ -63,9 +63,9 @@ struct PlaneStage {
       const int r = row0 + item / kWordsPerPlane;
       const int w = item % kWordsPerPlane;
       if (r < rows) {
-        const uint32_t* src = packed + (((int64_t)r * nchunks + chunk) * B) * kWordsPerPlane + w;
+        const uint32_t* src = packed + plane_words(r, chunk, 0, nchunks, B) + w;
 #pragma unroll
-        for (int i = 0; i < B; ++i) raw[it][i] = src[i * kWordsPerPlane];
+        for (int i = 0; i < B; ++i) raw[it][i] = src[i * kPlaneStride];
       } else {
 #pragma unroll
         for (int i = 0; i < B; ++i) raw[it][i] = 0u;

@@ -8,14 +8,13 @@
 // Padding bits are zero in both operands, so they XOR to zero and the true K
 // enters the constant term.
 //
-// Work split: a workgroup owns up to 8 activation rows (staged in LDS when they
-// fit) and walks weight rows in a grid-stride loop; a group of LPR lanes shares
-// one weight row, each lane taking every LPR-th 128-element chunk, and the
-// per-lane sums meet in a butterfly over the group.  All 1-bit products of one
+// Work split: a workgroup owns one 8-row group of weight rows and up to 8
+// activation rows (staged in LDS when they fit).  Lane l of wave v takes weight
+// row slot l mod 8 and the chunks c = (l / 8) + 8 v + 32 t, so the 8 lanes that
+// share a chunk read one 128-byte line per plane.  All 1-bit products of an
 // output stay in registers (the register analogue of the paper's fragment-level
-// recovery, Sec. IV-B); nothing intermediate goes to global memory.
-#pragma once
-
+// recovery, Sec. IV-B); partial sums meet through lane shuffles and one LDS
+// exchange, and nothing intermediate goes to global memory.
 #include "apt_internal.h"
 
 namespace apt {
@@ -23,94 +22,95 @@ namespace xorpop {
 
 constexpr int kWave = 64;
 constexpr int kWaves = 4;
-constexpr int kMT = 8;  // activation rows per workgroup
+constexpr int kMT = 8;                       // activation rows per workgroup
+constexpr int kSlots = kWaves * kWave / kRowGroup;  // chunk slots per workgroup (32)
 
 struct XorParams {
   GemmArgs g;
   int nchunks;
-  int lpr_log2;
 };
 
 template <int P, int Q, bool kALds>
 __global__ __launch_bounds__(kWave* kWaves) void gemm_xor_kernel(XorParams prm) {
   extern __shared__ uint4 a_lds[];
+  __shared__ uint32_t red[kWaves][kMT][kRowGroup];
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
   const int m0 = blockIdx.y * kMT;
   const int mrows = min(kMT, g.M - m0);
+  const int n0 = blockIdx.x * kRowGroup;
 
-  const uint4* a_src = reinterpret_cast<const uint4*>(g.a_packed) + (int64_t)m0 * NC * Q;
+  // The activation rows m0 .. m0+7 are one row group: NC * Q * 8 uint4,
+  // ordered (chunk, plane, row).
+  const uint4* a_src = reinterpret_cast<const uint4*>(g.a_packed) + (int64_t)(m0 / kRowGroup) * NC * Q * kRowGroup;
   if (kALds) {
-    // The activation rows m0 .. m0+mrows-1 are contiguous in the packed layout.
-    const int n_vec = mrows * NC * Q;
+    const int n_vec = NC * Q * kRowGroup;
     for (int t = threadIdx.x; t < n_vec; t += blockDim.x) a_lds[t] = a_src[t];
     __syncthreads();
   }
   const uint4* a_base = kALds ? a_lds : a_src;
 
   const int lane = threadIdx.x % kWave;
-  const int wave = blockIdx.x * kWaves + threadIdx.x / kWave;
-  const int total_waves = gridDim.x * kWaves;
-  const int lpr = 1 << prm.lpr_log2;
-  const int rpw = kWave / lpr;
-  const int group = lane >> prm.lpr_log2;
-  const int sub = lane & (lpr - 1);
+  const int wave = threadIdx.x / kWave;
+  const int slot = lane % kRowGroup;
+  const int cs = lane / kRowGroup + (kWave / kRowGroup) * wave;
+  const uint4* w_grp = reinterpret_cast<const uint4*>(g.w_packed) + (int64_t)blockIdx.x * NC * P * kRowGroup;
 
-  const uint32_t kabq = (uint32_t)g.K * ((1u << P) - 1u) * ((1u << Q) - 1u);
-  const uint4* w_all = reinterpret_cast<const uint4*>(g.w_packed);
-
-  for (int n_base = wave * rpw; n_base < g.N; n_base += total_waves * rpw) {
-    const int n = n_base + group;
-    uint32_t S[kMT];
+  uint32_t S[kMT];
 #pragma unroll
-    for (int m = 0; m < kMT; ++m) S[m] = 0u;
-    if (n < g.N) {
-      const uint4* w_row = w_all + (int64_t)n * NC * P;
-      for (int c = sub; c < NC; c += lpr) {
-        uint4 wv[P];
+  for (int m = 0; m < kMT; ++m) S[m] = 0u;
+  for (int c = cs; c < NC; c += kSlots) {
+    uint4 wv[P];
 #pragma unroll
-        for (int i = 0; i < P; ++i) wv[i] = w_row[c * P + i];
-#pragma unroll
-        for (int m = 0; m < kMT; ++m) {
-          if (m < mrows) {
-            const uint4* a_chunk = a_base + ((int64_t)m * NC + c) * Q;
-            uint32_t s = 0u;
-#pragma unroll
-            for (int j = 0; j < Q; ++j) {
-              const uint4 av = a_chunk[j];
-#pragma unroll
-              for (int i = 0; i < P; ++i) {
-                uint32_t cnt = __builtin_popcount(wv[i].x ^ av.x);
-                cnt += __builtin_popcount(wv[i].y ^ av.y);
-                cnt += __builtin_popcount(wv[i].z ^ av.z);
-                cnt += __builtin_popcount(wv[i].w ^ av.w);
-                s += cnt << (i + j);
-              }
-            }
-            S[m] += s;
-          }
-        }
-      }
-    }
-    // Sum the group's partial counts (all lanes take part in the shuffles).
+    for (int i = 0; i < P; ++i) wv[i] = w_grp[(c * P + i) * kRowGroup + slot];
 #pragma unroll
     for (int m = 0; m < kMT; ++m) {
-      for (int off = lpr >> 1; off > 0; off >>= 1) S[m] += __shfl_xor(S[m], off);
-    }
-    if (n < g.N) {
+      if (m < mrows) {
+        uint32_t s = 0u;
 #pragma unroll
-      for (int m = 0; m < kMT; ++m) {
-        if (m < mrows && (m % lpr) == sub) {
-          const int mg = m0 + m;
-          const int32_t c = (int32_t)(kabq - 2u * S[m]);
-          const int64_t o = (int64_t)mg * g.N + n;
-          if (g.c_int32) g.c_int32[o] = c;
-          if (g.c_fp16) {
-            float f = (float)c * __half2float(g.a_scale[mg]);
-            f = f * __half2float(g.w_scale[n]);
-            g.c_fp16[o] = __float2half_rn(f);
+        for (int j = 0; j < Q; ++j) {
+          const uint4 av = a_base[(c * Q + j) * kRowGroup + m];
+#pragma unroll
+          for (int i = 0; i < P; ++i) {
+            uint32_t cnt = __builtin_popcount(wv[i].x ^ av.x);
+            cnt += __builtin_popcount(wv[i].y ^ av.y);
+            cnt += __builtin_popcount(wv[i].z ^ av.z);
+            cnt += __builtin_popcount(wv[i].w ^ av.w);
+            s += cnt << (i + j);
           }
         }
+        S[m] += s;
+      }
+    }
+  }
+  // Sum over the 8 chunk slots of the wave (lanes with equal slot), then over
+  // the 4 waves through LDS.
+#pragma unroll
+  for (int m = 0; m < kMT; ++m) {
+    S[m] += __shfl_xor(S[m], 8);
+    S[m] += __shfl_xor(S[m], 16);
+    S[m] += __shfl_xor(S[m], 32);
+  }
+  if (lane < kRowGroup) {
+#pragma unroll
+    for (int m = 0; m < kMT; ++m) red[wave][m][slot] = S[m];
+  }
+  __syncthreads();
+  if (threadIdx.x < kMT * kRowGroup) {
+    const int m = threadIdx.x / kRowGroup, sl = threadIdx.x % kRowGroup;
+    const int mg = m0 + m, n = n0 + sl;
+    if (m < mrows && n < g.N) {
+      uint32_t tot = 0u;
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) tot += red[v][m][sl];
+      const uint32_t kabq = (uint32_t)g.K * ((1u << P) - 1u) * ((1u << Q) - 1u);
+      const int32_t c = (int32_t)(kabq - 2u * tot);
+      const int64_t o = (int64_t)mg * g.N + n;
+      if (g.c_int32) g.c_int32[o] = c;
+      if (g.c_fp16) {
+        float f = (float)c * __half2float(g.a_scale[mg]);
+        f = f * __half2float(g.w_scale[n]);
+        g.c_fp16[o] = __float2half_rn(f);
       }
     }
   }

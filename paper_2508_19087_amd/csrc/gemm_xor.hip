@@ -5,8 +5,6 @@
 namespace apt {
 
 using xorpop::kMT;
-using xorpop::kWave;
-using xorpop::kWaves;
 using xorpop::XorParams;
 
 bool xor_config_ok(const apt_config_t& cfg) { return cfg.mt == 0 || cfg.mt == kMT; }
@@ -15,14 +13,9 @@ hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t&, hipStream_t s
   XorParams prm;
   prm.g = g;
   prm.nchunks = num_chunks(g.K);
-  int lpr_log2 = 0;
-  while ((2 << lpr_log2) <= kWave && (2 << lpr_log2) <= prm.nchunks) ++lpr_log2;
-  prm.lpr_log2 = lpr_log2;
-  const int rows_per_block = kWaves * (kWave >> lpr_log2);
-  int grid_x = (g.N + rows_per_block - 1) / rows_per_block;
-  if (grid_x > 65535) grid_x = 65535;
+  const int grid_x = padded_rows(g.N) / kRowGroup;
   const int grid_y = (g.M + kMT - 1) / kMT;
-  size_t lds = (size_t)kMT * prm.nchunks * g.q * 16;
+  size_t lds = (size_t)prm.nchunks * g.q * kRowGroup * 16;
   if (lds > 64 * 1024) lds = 0;  // read the activation chunks from global memory instead
   switch (g.p) {
     case 1: return xorpop::launch_for_p<1>(g.q, prm, grid_x, grid_y, lds, stream);

@@ -2,18 +2,20 @@
 // gfx950 (APT-LLM, arXiv 2508.19087: Sec. III-A conversion, Sec. IV-A
 // decomposition and reassembly steps 1-3).
 //
-// One wavefront owns one row and walks it in steps of 1024 codes: lane l
-// converts codes [16 l, 16 l + 16) of the step (one 16-byte load), extracts
-// each plane's 16 bits, and pairs with its neighbour lane to form one 32-bit
-// word per plane.  Conversion flips the sign bit of the b-bit field; the row
-// sum of bipolar values 2u - (2^b - 1) is reduced across the wave.
+// A workgroup of 8 wavefronts owns one 8-row group of the packed layout; each
+// wavefront owns one row and walks it in steps of 1024 codes: lane l converts
+// codes [16 l, 16 l + 16) of the step (one 16-byte load), extracts each
+// plane's 16 bits, and pairs with its neighbour lane to form one 32-bit word
+// per plane.  Conversion flips the sign bit of the b-bit field; the row sum of
+// bipolar values 2u - (2^b - 1) is reduced across the wave.  Wavefronts of the
+// padding rows past the last row write zero words.
 #include "apt_internal.h"
 
 namespace apt {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kWavesPerBlock = 4;
+constexpr int kWavesPerBlock = kRowGroup;
 constexpr int kCodesPerLane = 16;
 constexpr int kCodesPerStep = kWave * kCodesPerLane;  // 1024 = 8 chunks
 
@@ -31,14 +33,13 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
     const int8_t* __restrict__ codes, int rows, int K, int bits, int nchunks,
     uint32_t* __restrict__ packed, int32_t* __restrict__ rowsum) {
   const int lane = threadIdx.x % kWave;
-  const int row = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
-  if (row >= rows) return;  // whole wavefront leaves together
+  const int row = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;  // < padded row count
+  const bool real = row < rows;
 
   const uint32_t field_mask = ((1u << bits) - 1u) * 0x01010101u;
   const uint32_t sign_flip = (1u << (bits - 1)) * 0x01010101u;
   const int kpad = nchunks * kChunk;
-  const int8_t* src = codes + (int64_t)row * K;
-  uint32_t* dst_row = packed + (int64_t)row * nchunks * bits * kWordsPerPlane;
+  const int8_t* src = codes + (int64_t)min(row, rows - 1) * K;
   uint32_t usum = 0;
 
   for (int base = 0; base < kpad; base += kCodesPerStep) {
@@ -46,11 +47,11 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
     uint32_t d[4] = {0u, 0u, 0u, 0u};
     if (kVector) {
       // K % 16 == 0: the lane's 16 codes are all valid or all padding.
-      if (k0 < K) {
+      if (real && k0 < K) {
         uint4 v = *reinterpret_cast<const uint4*>(src + k0);
         d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
       }
-    } else {
+    } else if (real) {
 #pragma unroll
       for (int t = 0; t < kCodesPerLane; ++t) {
         int k = k0 + t;
@@ -58,13 +59,15 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
         d[t / 4] |= b << (8 * (t % 4));
       }
     }
-    // Bipolar words, one per byte; padding codes stay all-zero.
+    // Bipolar words, one per byte; padding codes and padding rows stay all-zero.
     uint32_t u[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       uint32_t valid_bytes = 0xFFFFFFFFu;
       int kt = k0 + 4 * t;
-      if (!kVector) {
+      if (!real) {
+        valid_bytes = 0u;
+      } else if (!kVector) {
         int n_valid = K - kt;
         valid_bytes = n_valid >= 4 ? 0xFFFFFFFFu : (n_valid <= 0 ? 0u : ((1u << (8 * n_valid)) - 1u));
       } else if (k0 >= K) {
@@ -82,12 +85,12 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
                       (gather_plane_nibble(u[2], i) << 8) | (gather_plane_nibble(u[3], i) << 12);
       uint32_t other = __shfl_xor(half, 1);
       if (!upper_half && in_range) {
-        dst_row[((int64_t)chunk * bits + i) * kWordsPerPlane + word] = half | (other << 16);
+        packed[plane_words(row, chunk, i, nchunks, bits) + word] = half | (other << 16);
       }
     }
   }
 
-  if (rowsum != nullptr) {
+  if (rowsum != nullptr && real) {
     for (int off = kWave / 2; off > 0; off >>= 1) usum += __shfl_xor(usum, off);
     if (lane == 0) {
       // sum_k (2 u - (2^b - 1)) over the K real codes
@@ -103,7 +106,7 @@ hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t*
                        int32_t* rowsum, hipStream_t stream) {
   const int nchunks = num_chunks(K);
   dim3 block(kWave * kWavesPerBlock);
-  dim3 grid((rows + kWavesPerBlock - 1) / kWavesPerBlock);
+  dim3 grid(padded_rows(rows) / kWavesPerBlock);
   const bool vec = (K % 16 == 0) && ((reinterpret_cast<uintptr_t>(codes) & 15u) == 0);
   if (vec)
     hipLaunchKernelGGL(pack_kernel<true>, grid, block, 0, stream, codes, rows, K, bits, nchunks,

@@ -23,9 +23,9 @@ struct Int8Shape {
 };
 
 constexpr Int8Shape kInt8Shapes[] = {
-    {256, 256, 2, 2, 1, 1.00},
-    {256, 128, 2, 2, 1, 0.80},
-    {128, 128, 2, 2, 2, 0.70},
+    {256, 256, 4, 2, 1, 1.00},
+    {256, 128, 4, 2, 1, 0.80},
+    {128, 128, 2, 2, 2, 0.60},
 };
 
 apt_config_t base_config(int route) {

@@ -7,15 +7,15 @@ import numpy as np
 import paper_2508_19087_amd as apt
 from oracle import oracle as ref
 
-INT8_SHAPES = [(128, 128, 2, 2), (256, 128, 2, 2), (256, 256, 2, 2)]
+INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 128, 4, 2), (128, 128, 2, 2)]
 
 
 def forced_configs(p: int, q: int):
     """(name, config) of every route/shape the library can be forced to."""
     out = [("xor", apt.apt_config_t.make(apt.APT_ROUTE_XOR))]
     for bm, bn, wm, wn in INT8_SHAPES:
-        out.append(("int8_%dx%d" % (bm, bn),
-                    apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 2)))
+        c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 2)
+        out.append(("int8_%dx%d_w%dx%d" % (bm, bn, wm, wn), c))
     if p <= 7 and q <= 7:
         out.append(("pm1", apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)))
     return out

@@ -20,8 +20,9 @@ def test_exports_every_declared_symbol():
 
 
 @pytest.mark.parametrize("rows,K,bits,want", [
-    (1, 1, 1, 16), (1, 128, 1, 16), (1, 129, 1, 32), (3, 4096, 2, 3 * 32 * 2 * 16),
-    (11008, 4096, 4, 11008 * 32 * 4 * 16), (2, 11008, 8, 2 * 86 * 8 * 16),
+    (1, 1, 1, 8 * 16), (1, 128, 1, 8 * 16), (1, 129, 1, 8 * 32), (3, 4096, 2, 8 * 32 * 2 * 16),
+    (8, 1, 3, 8 * 3 * 16), (9, 1, 3, 16 * 3 * 16),
+    (11008, 4096, 4, 11008 * 32 * 4 * 16), (2, 11008, 8, 8 * 86 * 8 * 16),
     (0, 5, 1, 0), (5, 0, 1, 0), (5, 5, 0, 0), (5, 5, 9, 0)])
 def test_packed_bytes(rows, K, bits, want):
     assert apt.apt_packed_bytes(rows, K, bits) == want
@@ -52,7 +53,13 @@ def test_select_config_valid(shape):
     assert c.route in (apt.APT_ROUTE_XOR, apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_PM1_MFMA)
     if shape[0] <= 8:
         assert c.route == apt.APT_ROUTE_XOR
-    assert apt.apt_gemm_workspace_bytes(*shape, c) == 0
+    M, N, K = shape[:3]
+    ws = apt.apt_gemm_workspace_bytes(*shape, c)
+    if c.route == apt.APT_ROUTE_INT8_MFMA:
+        nce = ((K + 127) // 128 + 1) // 2 * 2
+        assert ws == (M + 31) // 32 * 32 * nce * 128
+    else:
+        assert ws == 0
 
 
 def test_select_config_rejects():
@@ -68,9 +75,12 @@ A, W, C = 0x7F0000000000, 0x7F0000100000, 0x7F0000200000
 RA, RW, S = 0x7F0000300000, 0x7F0000400000, 0x7F0000500000
 
 
+WS = 0x7F0000600000
+
+
 def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=None, c16=None,
-         cfg=None):
-    return apt.apt_gemm(M, N, K, p, q, a, w, ra, rw, c32, sa, sw, c16, cfg, None, 0, None)
+         cfg=None, ws=None, ws_bytes=0):
+    return apt.apt_gemm(M, N, K, p, q, a, w, ra, rw, c32, sa, sw, c16, cfg, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -90,6 +100,12 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
     (dict(p=8, cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)), apt.APT_ERR_UNSUPPORTED),
     (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, k_split=2)), apt.APT_ERR_UNSUPPORTED),
     (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=3)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_WORKSPACE),
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ws=WS,
+          ws_bytes=64 * 256 - 1), apt.APT_ERR_WORKSPACE),
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ws=WS + 8,
+          ws_bytes=1 << 20), apt.APT_ERR_INVALID_ARG),
 ])
 def test_gemm_validation(kw, want):
     assert gemm(**kw) == want

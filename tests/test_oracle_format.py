@@ -65,7 +65,10 @@ def test_golden_packed_layout():
              if l.strip() and not l.startswith("#")}
     R, K, bits = int(lines["R"][0]), int(lines["K"][0]), int(lines["bits"][0])
     u = (np.arange(K) % 4).astype(np.uint8).reshape(R, K)
-    want = np.array([int(w, 16) for w in lines["words"]], dtype=np.uint32)
+    want = np.zeros(int(lines["total"][0]), dtype=np.uint32)
+    for item in lines["nonzero"]:
+        idx, val = item.split(":")
+        want[int(idx)] = int(val, 16)
     got = ref.pack(u, bits)
     assert np.array_equal(got, want)
     back, stray = ref.unpack(got, R, K, bits)
@@ -82,16 +85,16 @@ def _pack_by_dict(u, bits):
         for k in range(K):
             for i in range(bits):
                 if (int(u[r, k]) >> i) & 1:
-                    idx = ((r * nc + k // 128) * bits + i) * 4 + (k % 128) // 32
+                    idx = (((r // 8) * nc + k // 128) * bits + i) * 32 + (r % 8) * 4 + (k % 128) // 32
                     words[idx] = words.get(idx, 0) | (1 << (k % 32))
-    out = np.zeros(R * nc * bits * 4, dtype=np.uint32)
+    out = np.zeros((R + 7) // 8 * 8 * nc * bits * 4, dtype=np.uint32)
     for idx, val in words.items():
         out[idx] = val
     return out
 
 
 @pytest.mark.parametrize("R,K,bits", [(1, 1, 1), (3, 31, 2), (2, 33, 3), (2, 129, 4), (1, 300, 8),
-                                      (4, 128, 5), (2, 257, 7)])
+                                      (4, 128, 5), (2, 257, 7), (9, 200, 3), (16, 130, 2)])
 def test_pack_unpack(R, K, bits):
     g = np.random.default_rng(R * 1000 + K * 10 + bits)
     u = g.integers(0, 1 << bits, size=(R, K)).astype(np.uint8)
@@ -100,9 +103,14 @@ def test_pack_unpack(R, K, bits):
     assert np.array_equal(packed, _pack_by_dict(u, bits))
     back, stray = ref.unpack(packed, R, K, bits)
     assert stray == 0 and np.array_equal(back, u)
+    nc = (K + 127) // 128
     if K % 128:
         bad = packed.copy()
-        nc = (K + 127) // 128
-        last = ((0 * nc + nc - 1) * bits + 0) * 4 + 3
+        last = ((0 * nc + nc - 1) * bits + 0) * 32 + 0 * 4 + 3  # row 0, last chunk, word 3, bit 31
         bad[last] |= np.uint32(1 << 31)
+        assert ref.unpack(bad, R, K, bits)[1] == 1
+    if R % 8:
+        bad = packed.copy()
+        row = R  # first padding row
+        bad[(((row // 8) * nc + 0) * bits + 0) * 32 + (row % 8) * 4] |= np.uint32(1)
         assert ref.unpack(bad, R, K, bits)[1] == 1
