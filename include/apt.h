@@ -77,12 +77,17 @@ enum {
 /* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950
  * terms).  Fields a route does not use are ignored.
  *   route      APT_ROUTE_*
- *   bm, bn     output tile per workgroup (MFMA routes: bm in {64,128,256}, bn in {64,128,256})
- *   bk         K elements staged per pipeline step (MFMA routes: 128)
- *   waves_m, waves_n   wave grid inside a workgroup (MFMA routes)
+ *   bm, bn     output tile per workgroup (int8 MFMA route: 256x256, 256x128 or 128x128)
+ *   bk         K elements staged per pipeline step (MFMA routes: 0 or 128)
+ *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route)
  *   k_split    reserved, must be 0 or 1
- *   lds_stages LDS buffers (MFMA routes: 2)
- *   mt         XOR route: activation rows per workgroup (1, 2, 4 or 8)
+ *   lds_stages LDS buffers (MFMA routes: 0 or 2)
+ *   mt         XOR route: activation rows per workgroup (0 or 8)
+ *   split_n    int8 MFMA route: output columns [split_n, N) use the tail tile
+ *              tail_bm x tail_bn in a second launch, so the main tiles fill
+ *              whole rounds of the 256 compute units; 0 = no tail.  A multiple
+ *              of bn with 0 < split_n < N.
+ *   tail_bm, tail_bn   tail tile (a configured int8 tile shape)
  */
 typedef struct {
   int32_t route;
@@ -91,7 +96,8 @@ typedef struct {
   int32_t k_split;
   int32_t lds_stages;
   int32_t mt;
-  int32_t reserved[3];
+  int32_t split_n;
+  int32_t tail_bm, tail_bn;
 } apt_config_t;
 
 /* Bytes of a packed buffer for `rows` rows of K codes at `bits` bits

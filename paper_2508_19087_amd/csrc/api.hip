@@ -29,7 +29,7 @@ apt_status_t pack_common(const int8_t* codes, int rows, int K, int bits, void* p
 }
 
 // Checks a config against the problem; returns APT_OK or the status to report.
-apt_status_t check_config(const apt_config_t& c, int M, int p, int q, bool have_rowsums) {
+apt_status_t check_config(const apt_config_t& c, int M, int N, int p, int q, bool have_rowsums) {
   if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
   switch (c.route) {
     case APT_ROUTE_XOR:
@@ -37,7 +37,7 @@ apt_status_t check_config(const apt_config_t& c, int M, int p, int q, bool have_
       if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_INT8_MFMA:
-      if (!apt::int8_config_ok(c)) return APT_ERR_INVALID_ARG;
+      if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
       return APT_OK;
     case APT_ROUTE_PM1_MFMA:
@@ -102,7 +102,7 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, c
   else
     c = *cfg;
   const bool have_rowsums = a_rowsum != nullptr && w_rowsum != nullptr;
-  apt_status_t st = check_config(c, M, p, q, have_rowsums);
+  apt_status_t st = check_config(c, M, N, p, q, have_rowsums);
   if (st != APT_OK) return st;
   if (c.route == APT_ROUTE_INT8_MFMA) {
     if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, K))

@@ -52,7 +52,7 @@ bool xor_config_ok(const apt_config_t& cfg);
 // activations expanded into MFMA fragments (int8_workspace_bytes).
 hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
                             hipStream_t stream);
-bool int8_config_ok(const apt_config_t& cfg);
+bool int8_config_ok(const apt_config_t& cfg, int N);
 size_t int8_workspace_bytes(int M, int K);
 
 // Plane-pair +-1 MFMA route (gemm_pm1.hip).

@@ -56,6 +56,7 @@ struct Int8Params {
   GemmArgs g;
   int nchunks;        // NC, chunks of K
   int nsteps;         // k-steps in the activation fragment buffer (even chunk count x 4)
+  int n_begin;        // first output column of this launch
   int tiles_n;
   int mblocks;        // 32-row blocks of the activation fragment buffer
   const v4i* a_frag;  // activation fragments (workspace)
@@ -109,7 +110,9 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
 
 // ---- weight staging -----------------------------------------------------------
 // ROWS weight rows of a tile, each split into SPLIT items of 128/SPLIT elements
-// (4/SPLIT words per plane).  Rows past the matrix edge are clamped to its last
+// (4/SPLIT words per plane).  Consecutive threads take consecutive rows of the
+// same part, so a wave's LDS writes hit distinct banks.  Rows past the matrix
+// edge are clamped to its last
 // row: their products only reach outputs that are never stored, and the code
 // stays branch-free so the scheduler can interleave it with the MFMAs.
 template <int B, int ROWS, int SPLIT, int T>
@@ -127,8 +130,8 @@ struct Stage {
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
       const int item = tid + T * it;
-      const int r = min(row0 + item / SPLIT, rows - 1);
-      const int sub = item % SPLIT;
+      const int r = min(row0 + item % ROWS, rows - 1);
+      const int sub = item / ROWS;
       const uint32_t* src = real ? packed + plane_words(r, chunk, 0, nchunks, B) + sub * kWpi
                                  : kZeroPlanes + (r % kRowGroup) * kWordsPerPlane + sub * kWpi;
 #pragma unroll
@@ -151,8 +154,8 @@ struct Stage {
   __device__ __forceinline__ void store_word(uint8_t* lds_tile, int tid, int u) const {
     const int it = u / kWpi, w = u % kWpi;
     const int item = tid + T * it;
-    const int r = item / SPLIT;
-    const int sub = item % SPLIT;
+    const int r = item % ROWS;
+    const int sub = item / ROWS;
     uint32_t pw[B];
 #pragma unroll
     for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
@@ -172,11 +175,33 @@ struct Stage {
 __host__ __device__ constexpr int offset_of(int b) { return b == 8 ? 1 : 1 - (1 << b); }
 __host__ __device__ constexpr int pad_of(int b) { return b == 8 ? -128 : 0; }
 
+// Scheduling hint for one k-step with N MFMAs: DS reads of the next k-step
+// first, then each MFMA followed by VALU_PER vector instructions of the weight
+// reassembly, with the LDS writes and the activation-fragment loads spread
+// between the MFMAs.  Masks: 0x008 MFMA, 0x002 VALU, 0x100 DS read,
+// 0x200 DS write, 0x020 VMEM read.
+template <int I, int N, int READS, int WRITES, int VMEM, int VALU_PER>
+struct Interleave {
+  static __device__ __forceinline__ void run() {
+    if constexpr (I < READS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (VALU_PER > 0) __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER, 0);
+    if constexpr (WRITES > 0 && I >= N - 2 * WRITES && (I - (N - 2 * WRITES)) % 2 == 1)
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    if constexpr (I < VMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    Interleave<I + 1, N, READS, WRITES, VMEM, VALU_PER>::run();
+  }
+};
+template <int N, int READS, int WRITES, int VMEM, int VALU_PER>
+struct Interleave<N, N, READS, WRITES, VMEM, VALU_PER> {
+  static __device__ __forceinline__ void run() {}
+};
+
 // ---- main kernel --------------------------------------------------------------
 // The MFMA takes the weight fragment as its first operand, so the accumulator
 // of lane l holds D[n][m] for m = l mod 32 and four consecutive n: each lane
 // stores 16 contiguous output bytes.
-template <int P, int BM, int BN, int WM, int WN, int SPLIT>
+template <int P, int BM, int BN, int WM, int WN, int SPLIT, bool HINTS>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm) {
   constexpr int T = WM * WN * kWave;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
@@ -200,7 +225,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
   int tile = blockIdx.x;
   if (ntiles % 8 == 0) tile = (blockIdx.x % 8) * (ntiles / 8) + blockIdx.x / 8;
   const int tm = tile / prm.tiles_n, tn = tile % prm.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * BM, n0 = prm.n_begin + tn * BN;
 
   using SW = Stage<P, BN, SPLIT, T>;
   SW rw0, rw1;
@@ -256,6 +281,11 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
           acc[b][a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[cur][b], afr[ks][a], acc[b][a], 0, 0, 0);
 #pragma unroll
       for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)(next_step + ks) * kFragVecs];
+      if constexpr (HINTS) {
+        constexpr int words = (SW::kWords + kSteps - 1) / kSteps;  // at most, per k-step
+        constexpr int valu = words * 40;
+        Interleave<0, FN * FM, FN, 2 * words, FM, (valu + FN * FM - 1) / (FN * FM)>::run();
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -283,77 +313,108 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
     __syncthreads();
   }
 
-  // Epilogue: affine correction, optional fp16 scaling, 16-byte stores.
+  // Epilogue.  Each 32x32 accumulator block goes through a private LDS slot
+  // of the wave and comes back row by row, so that every store instruction
+  // writes 8 whole 128-byte output rows; the affine correction and the
+  // optional fp16 scaling are applied on the way out.
   const int q = g.q;
   const uint32_t ca = (uint32_t)(q == 8 ? 1 : 1 - (1 << q)), cw = (uint32_t)offset_of(P);
   const uint32_t pad_term =
       4u * (uint32_t)(NCE * kChunk - g.K) * (uint32_t)((q == 8 ? -128 : 0) * pad_of(P));
   const uint32_t const_term = ca * cw * (uint32_t)g.K + pad_term;
+  constexpr int kEpiStride = 32 * 4 + 16;  // bytes per row of a 32x32 int32 block in LDS
+  uint8_t* slot = lds + wave * 32 * kEpiStride;
+  const int er = lane / 8, ec = (lane % 8) * 4;  // read-back row (+8 i) and first column
   const bool vec_ok = (g.N % 4) == 0;
+  uint32_t wterm[FN][4];
+#pragma unroll
+  for (int b = 0; b < FN; ++b)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = min(n0 + wn * WTN + b * 32 + ec + j, g.N - 1);
+      wterm[b][j] = ca * (uint32_t)g.w_rowsum[n];
+    }
 #pragma unroll
   for (int a = 0; a < FM; ++a) {
-    const int m = m0 + wm * WTM + a * 32 + lrow;
-    if (m >= g.M) continue;
-    const uint32_t aterm = cw * (uint32_t)g.a_rowsum[m] - const_term;
-    const float sa = g.c_fp16 ? __half2float(g.a_scale[m]) : 0.f;
+    const int mrow0 = m0 + wm * WTM + a * 32;
+    uint32_t aterm[4];
+    float sa[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = min(mrow0 + er + 8 * i, g.M - 1);
+      aterm[i] = cw * (uint32_t)g.a_rowsum[m] - const_term;
+      sa[i] = g.c_fp16 ? __half2float(g.a_scale[m]) : 0.f;
+    }
 #pragma unroll
     for (int b = 0; b < FN; ++b) {
+      // acc[b][a][4 gi + j] = D[n = 8 gi + 4 (lane / 32) + j][m = lane mod 32]
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
-        const int n4 = n0 + wn * WTN + b * 32 + gi * 8 + (lane / 32) * 4;
-        if (n4 >= g.N) continue;
+        v4i v = {acc[b][a][gi * 4 + 0], acc[b][a][gi * 4 + 1], acc[b][a][gi * 4 + 2],
+                 acc[b][a][gi * 4 + 3]};
+        *reinterpret_cast<v4i*>(slot + lrow * kEpiStride + (gi * 8 + (lane / 32) * 4) * 4) = v;
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // LDS writes of this wave done (lgkmcnt 0)
+      __builtin_amdgcn_wave_barrier();
+      const int ncol = n0 + wn * WTN + b * 32 + ec;
+      const bool full = vec_ok && ncol + 3 < g.N;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = mrow0 + er + 8 * i;
+        const v4i d = *reinterpret_cast<const v4i*>(slot + (er + 8 * i) * kEpiStride + ec * 4);
         int32_t cv[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = min(n4 + j, g.N - 1);
-          cv[j] = (int32_t)(4u * (uint32_t)acc[b][a][gi * 4 + j] + aterm + ca * (uint32_t)g.w_rowsum[n]);
-        }
-        const int64_t o = (int64_t)m * g.N + n4;
-        const bool full = vec_ok && n4 + 3 < g.N;
-        if (g.c_int32) {
-          if (full) {
-            *reinterpret_cast<int4*>(g.c_int32 + o) = make_int4(cv[0], cv[1], cv[2], cv[3]);
-          } else {
-            for (int j = 0; j < 4 && n4 + j < g.N; ++j) g.c_int32[o + j] = cv[j];
+        for (int j = 0; j < 4; ++j) cv[j] = (int32_t)(4u * (uint32_t)d[j] + aterm[i] + wterm[b][j]);
+        if (m < g.M && ncol < g.N) {
+          const int64_t o = (int64_t)m * g.N + ncol;
+          if (g.c_int32) {
+            if (full)
+              *reinterpret_cast<int4*>(g.c_int32 + o) = make_int4(cv[0], cv[1], cv[2], cv[3]);
+            else
+              for (int j = 0; j < 4 && ncol + j < g.N; ++j) g.c_int32[o + j] = cv[j];
           }
-        }
-        if (g.c_fp16) {
-          __half h[4];
+          if (g.c_fp16) {
+            __half h[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int n = min(n4 + j, g.N - 1);
-            h[j] = __float2half_rn((float)cv[j] * sa * __half2float(g.w_scale[n]));
-          }
-          if (full) {
-            *reinterpret_cast<uint2*>(g.c_fp16 + o) = *reinterpret_cast<const uint2*>(h);
-          } else {
-            for (int j = 0; j < 4 && n4 + j < g.N; ++j) g.c_fp16[o + j] = h[j];
+            for (int j = 0; j < 4; ++j) {
+              const int n = min(ncol + j, g.N - 1);
+              h[j] = __float2half_rn((float)cv[j] * sa[i] * __half2float(g.w_scale[n]));
+            }
+            if (full)
+              *reinterpret_cast<uint2*>(g.c_fp16 + o) = *reinterpret_cast<const uint2*>(h);
+            else
+              for (int j = 0; j < 4 && ncol + j < g.N; ++j) g.c_fp16[o + j] = h[j];
           }
         }
       }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the slot is rewritten
+      __builtin_amdgcn_wave_barrier();
     }
   }
 }
 
 struct TileShape {
   int bm, bn, wm, wn, split;
+  bool hints;
 };
 constexpr TileShape kShapes[] = {
-    {256, 256, 4, 2, 2},
-    {256, 256, 2, 4, 2},
-    {256, 128, 4, 2, 4},
-    {128, 128, 2, 2, 2},
+    {256, 256, 4, 2, 2, false},
+    {256, 256, 2, 4, 2, false},
+    {256, 128, 4, 2, 4, false},
+    {128, 128, 2, 2, 2, false},
+    {256, 256, 4, 2, 2, true},
 };
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
+// Launches shape S over output columns [prm.n_begin, prm.n_begin + n_count).
 template <int P, int S>
-hipError_t launch_shape(const Int8Params& prm0, hipStream_t stream) {
+hipError_t launch_shape(const Int8Params& prm0, int n_count, hipStream_t stream) {
   constexpr TileShape sh = kShapes[S];
   Int8Params prm = prm0;
-  prm.tiles_n = (prm.g.N + sh.bn - 1) / sh.bn;
+  prm.tiles_n = (n_count + sh.bn - 1) / sh.bn;
   const int tiles_m = (prm.g.M + sh.bm - 1) / sh.bm;
   const size_t lds = 2 * (size_t)sh.bn * kRowBytes;
-  auto kern = gemm_int8_kernel<P, sh.bm, sh.bn, sh.wm, sh.wn, sh.split>;
+  auto kern = gemm_int8_kernel<P, sh.bm, sh.bn, sh.wm, sh.wn, sh.split, sh.hints>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -362,12 +423,13 @@ hipError_t launch_shape(const Int8Params& prm0, hipStream_t stream) {
 }
 
 template <int P>
-inline hipError_t launch_p_shape(int shape, const Int8Params& prm, hipStream_t stream) {
+inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int n_count, hipStream_t stream) {
   switch (shape) {
-    case 0: return launch_shape<P, 0>(prm, stream);
-    case 1: return launch_shape<P, 1>(prm, stream);
-    case 2: return launch_shape<P, 2>(prm, stream);
-    case 3: return launch_shape<P, 3>(prm, stream);
+    case 0: return launch_shape<P, 0>(prm, n_count, stream);
+    case 1: return launch_shape<P, 1>(prm, n_count, stream);
+    case 2: return launch_shape<P, 2>(prm, n_count, stream);
+    case 3: return launch_shape<P, 3>(prm, n_count, stream);
+    case 4: return launch_shape<P, 4>(prm, n_count, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -375,7 +437,7 @@ inline hipError_t launch_p_shape(int shape, const Int8Params& prm, hipStream_t s
 // Launches for weight bits P (main kernel) and activation bits Q (expansion);
 // the explicit instantiations live in gemm_int8_inst.hip, built once per width.
 template <int P>
-hipError_t launch_for_p(int shape, const Int8Params& prm, hipStream_t stream);
+hipError_t launch_for_p(int shape, const Int8Params& prm, int n_count, hipStream_t stream);
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
                                int mblocks, v4i* out, hipStream_t stream);

@@ -6,21 +6,46 @@ namespace apt {
 namespace int8 {
 namespace {
 
-// A config names a shape by its tile and wave grid.
+// A config names a shape by its tile and wave grid; lds_stages == 3 asks for
+// the variant with explicit instruction-interleaving hints (experimental).
 int shape_index(const apt_config_t& cfg) {
   for (int s = 0; s < kNumShapes; ++s)
     if (kShapes[s].bm == cfg.bm && kShapes[s].bn == cfg.bn && kShapes[s].wm == cfg.waves_m &&
-        kShapes[s].wn == cfg.waves_n)
+        kShapes[s].wn == cfg.waves_n && kShapes[s].hints == (cfg.lds_stages == 3))
       return s;
   return -1;
+}
+
+// The tail tile is named by its size; the first shape of that size is used.
+int tail_index(const apt_config_t& cfg) {
+  for (int s = 0; s < kNumShapes; ++s)
+    if (kShapes[s].bm == cfg.tail_bm && kShapes[s].bn == cfg.tail_bn && !kShapes[s].hints) return s;
+  return -1;
+}
+
+hipError_t launch_p(int p, int shape, const Int8Params& prm, int n_count, hipStream_t stream) {
+  switch (p) {
+    case 1: return launch_for_p<1>(shape, prm, n_count, stream);
+    case 2: return launch_for_p<2>(shape, prm, n_count, stream);
+    case 3: return launch_for_p<3>(shape, prm, n_count, stream);
+    case 4: return launch_for_p<4>(shape, prm, n_count, stream);
+    case 5: return launch_for_p<5>(shape, prm, n_count, stream);
+    case 6: return launch_for_p<6>(shape, prm, n_count, stream);
+    case 7: return launch_for_p<7>(shape, prm, n_count, stream);
+    case 8: return launch_for_p<8>(shape, prm, n_count, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 }  // namespace int8
 
-bool int8_config_ok(const apt_config_t& cfg) {
-  return int8::shape_index(cfg) >= 0 && (cfg.bk == 0 || cfg.bk == kChunk) &&
-         (cfg.lds_stages == 0 || cfg.lds_stages == 2) && cfg.k_split <= 1;
+bool int8_config_ok(const apt_config_t& cfg, int N) {
+  if (int8::shape_index(cfg) < 0 || !(cfg.bk == 0 || cfg.bk == kChunk) || cfg.k_split > 1)
+    return false;
+  if (cfg.split_n == 0) return true;
+  return cfg.split_n > 0 && cfg.split_n < N && cfg.split_n % cfg.bn == 0 &&
+         cfg.split_n % kRowGroup == 0 && int8::tail_index(cfg) >= 0;
 }
 
 size_t int8_workspace_bytes(int M, int K) { return int8::a_frag_bytes(M, K); }
@@ -35,6 +60,7 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
   prm.nchunks = num_chunks(g.K);
   prm.nsteps = ((prm.nchunks + 1) & ~1) * kSteps;
   prm.tiles_n = 0;
+  prm.n_begin = 0;
   prm.mblocks = (g.M + 31) / 32;
   prm.a_frag = static_cast<const v4i*>(workspace);
   v4i* frag = static_cast<v4i*>(workspace);
@@ -50,17 +76,12 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
     case 8: e = launch_expand_for_q<8>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, stream); break;
   }
   if (e != hipSuccess) return e;
-  switch (g.p) {
-    case 1: return launch_for_p<1>(shape, prm, stream);
-    case 2: return launch_for_p<2>(shape, prm, stream);
-    case 3: return launch_for_p<3>(shape, prm, stream);
-    case 4: return launch_for_p<4>(shape, prm, stream);
-    case 5: return launch_for_p<5>(shape, prm, stream);
-    case 6: return launch_for_p<6>(shape, prm, stream);
-    case 7: return launch_for_p<7>(shape, prm, stream);
-    case 8: return launch_for_p<8>(shape, prm, stream);
-  }
-  return hipErrorInvalidValue;
+  prm.n_begin = 0;
+  if (cfg.split_n == 0) return launch_p(g.p, shape, prm, g.N, stream);
+  e = launch_p(g.p, shape, prm, cfg.split_n, stream);
+  if (e != hipSuccess) return e;
+  prm.n_begin = cfg.split_n;
+  return launch_p(g.p, tail_index(cfg), prm, g.N - cfg.split_n, stream);
 }
 
 }  // namespace apt

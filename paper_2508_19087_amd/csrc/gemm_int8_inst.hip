@@ -8,8 +8,8 @@ namespace apt {
 namespace int8 {
 
 template <int P>
-hipError_t launch_for_p(int shape, const Int8Params& prm, hipStream_t stream) {
-  return launch_p_shape<P>(shape, prm, stream);
+hipError_t launch_for_p(int shape, const Int8Params& prm, int n_count, hipStream_t stream) {
+  return launch_p_shape<P>(shape, prm, n_count, stream);
 }
 
 template <int Q>
@@ -22,7 +22,7 @@ hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int
   return hipGetLastError();
 }
 
-template hipError_t launch_for_p<APT_INST_P>(int, const Int8Params&, hipStream_t);
+template hipError_t launch_for_p<APT_INST_P>(int, const Int8Params&, int, hipStream_t);
 template hipError_t launch_expand_for_q<APT_INST_P>(const uint32_t*, int, int, int, int, v4i*,
                                                      hipStream_t);
 

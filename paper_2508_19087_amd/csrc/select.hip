@@ -25,7 +25,7 @@ struct Int8Shape {
 constexpr Int8Shape kInt8Shapes[] = {
     {256, 256, 4, 2, 1, 1.00},
     {256, 128, 4, 2, 1, 0.80},
-    {128, 128, 2, 2, 2, 0.60},
+    {128, 128, 2, 2, 3, 0.40},
 };
 
 apt_config_t base_config(int route) {
@@ -36,9 +36,22 @@ apt_config_t base_config(int route) {
   c.k_split = 0;
   c.lds_stages = 0;
   c.mt = 0;
-  c.reserved[0] = c.reserved[1] = c.reserved[2] = 0;
+  c.split_n = c.tail_bm = c.tail_bn = 0;
   return c;
 }
+
+// Model time of covering n_cols output columns with shape s: rounds of
+// resident tiles x work per tile / tile speed (arbitrary units).
+double model_time(const Int8Shape& s, int M, int n_cols) {
+  const long tiles = (long)((M + s.bm - 1) / s.bm) * ((n_cols + s.bn - 1) / s.bn);
+  const long slots = (long)kComputeUnits * s.per_cu;
+  const long rounds = (tiles + slots - 1) / slots;
+  return (double)rounds * s.bm * s.bn * s.per_cu / s.rel_speed;
+}
+
+constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
+constexpr int kTailShape = kNumInt8Shapes - 1;  // the smallest tile
+constexpr double kLaunchCost = 2.0e4;           // a second launch, in model units
 
 }  // namespace
 
@@ -51,27 +64,46 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
     c.mt = 8;
     return c;
   }
-  // Time model: rounds of resident tiles x work per tile / tile speed.
+  // Candidates: every shape alone, and every shape on the columns that fill
+  // whole rounds with the smallest shape on the rest.
   double best = 0.0;
-  int best_i = 0;
-  for (int i = 0; i < (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0])); ++i) {
+  int best_i = -1, best_split = 0;
+  for (int i = 0; i < kNumInt8Shapes; ++i) {
     const Int8Shape& s = kInt8Shapes[i];
-    const long tiles = (long)((M + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
-    const long slots = (long)kComputeUnits * s.per_cu;
-    const long rounds = (tiles + slots - 1) / slots;
-    const double t = (double)rounds * s.bm * s.bn * s.per_cu / s.rel_speed;
-    if (i == 0 || t < best) {
+    const double t = model_time(s, M, N);
+    if (best_i < 0 || t < best) {
       best = t;
       best_i = i;
+      best_split = 0;
+    }
+    const int tiles_m = (M + s.bm - 1) / s.bm;
+    const int cols_per_round = kComputeUnits * s.per_cu / tiles_m;
+    const int tiles_n = (N + s.bn - 1) / s.bn;
+    if (i == kTailShape || cols_per_round < 1) continue;
+    const int full = tiles_n / cols_per_round * cols_per_round;
+    if (full < 1 || full * s.bn >= N) continue;
+    const int split = full * s.bn;
+    const double ts = model_time(s, M, split) + model_time(kInt8Shapes[kTailShape], M, N - split) +
+                      kLaunchCost;
+    if (ts < best) {
+      best = ts;
+      best_i = i;
+      best_split = split;
     }
   }
+  const Int8Shape& s = kInt8Shapes[best_i];
   apt_config_t c = base_config(APT_ROUTE_INT8_MFMA);
-  c.bm = kInt8Shapes[best_i].bm;
-  c.bn = kInt8Shapes[best_i].bn;
+  c.bm = s.bm;
+  c.bn = s.bn;
   c.bk = kChunk;
-  c.waves_m = kInt8Shapes[best_i].wm;
-  c.waves_n = kInt8Shapes[best_i].wn;
+  c.waves_m = s.wm;
+  c.waves_n = s.wn;
   c.lds_stages = 2;
+  if (best_split > 0) {
+    c.split_n = best_split;
+    c.tail_bm = kInt8Shapes[kTailShape].bm;
+    c.tail_bn = kInt8Shapes[kTailShape].bn;
+  }
   return c;
 }
 

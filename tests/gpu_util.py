@@ -10,12 +10,18 @@ from oracle import oracle as ref
 INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 128, 4, 2), (128, 128, 2, 2)]
 
 
-def forced_configs(p: int, q: int):
-    """(name, config) of every route/shape the library can be forced to."""
+def forced_configs(p: int, q: int, N: int = 0):
+    """(name, config) of every route/shape the library can be forced to; with N,
+    also the split launches (main tiles, then 128x128 tail tiles)."""
     out = [("xor", apt.apt_config_t.make(apt.APT_ROUTE_XOR))]
     for bm, bn, wm, wn in INT8_SHAPES:
         c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 2)
         out.append(("int8_%dx%d_w%dx%d" % (bm, bn, wm, wn), c))
+        split = (N - 1) // bn * bn
+        if N and split >= bn:
+            c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 2, 0, split,
+                                      128, 128)
+            out.append(("int8_%dx%d_w%dx%d_tail@%d" % (bm, bn, wm, wn, split), c))
     if p <= 7 and q <= 7:
         out.append(("pm1", apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)))
     return out

@@ -106,6 +106,12 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
           ws_bytes=64 * 256 - 1), apt.APT_ERR_WORKSPACE),
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ws=WS + 8,
           ws_bytes=1 << 20), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
+                                                 100, 128, 128)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
+                                                 256, 96, 128)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=256, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
+                                                 256, 128, 128)), apt.APT_ERR_INVALID_ARG),
 ])
 def test_gemm_validation(kw, want):
     assert gemm(**kw) == want

@@ -22,7 +22,7 @@ def test_all_bit_widths_every_route(p, q):
         prob = synth.random_problem(g, M, N, K, p, q)
         want = oracle_full(prob)
         packed = pack_problem(prob)
-        for name, cfg in forced_configs(p, q):
+        for name, cfg in forced_configs(p, q, N):
             got, _ = run(prob, cfg=cfg, packed=packed)
             assert_int32_equal(got, want, "%s p=%d q=%d %dx%dx%d" % (name, p, q, M, N, K))
 
@@ -40,7 +40,7 @@ def test_ragged_shapes(M, N, K, p, q):
     packed = pack_problem(prob)
     got, _ = run(prob, packed=packed)  # selected config
     assert_int32_equal(got, want, "auto")
-    for name, cfg in forced_configs(p, q):
+    for name, cfg in forced_configs(p, q, N):
         got, _ = run(prob, cfg=cfg, packed=packed)
         assert_int32_equal(got, want, name)
 
@@ -92,7 +92,7 @@ def test_fp16_epilogue(M, N, K, p, q):
     prob = synth.random_problem(synth.rng(4000, M, N, K), M, N, K, p, q, with_scales=True)
     want = oracle_full(prob)
     packed = pack_problem(prob)
-    for name, cfg in [("auto", None)] + forced_configs(p, q):
+    for name, cfg in [("auto", None)] + forced_configs(p, q, N):
         c32, c16 = run(prob, cfg=cfg, fp16=True, packed=packed)
         assert_int32_equal(c32, want, name)
         assert_fp16_ok(c16, want, prob, name)
