@@ -266,7 +266,7 @@ def main():
     traffic = stored_traffic()
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": traffic,
-                "kernel": "gemm_int8_kernel W4A4 M=2048 N=11008 K=4096",
+                "kernel": "apt_gemm W4A4 M=2048 N=11008 K=4096 (expand_a_kernel + gemm_int8_kernel)",
                 "avg_launch_us": round(gemm_s * 1e6, 2)}
     cfg = wl.apt.select_config(pre.M, pre.N, pre.K, pre.p, pre.q).as_dict()
     result = {
