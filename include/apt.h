@@ -80,7 +80,9 @@ enum {
  *   bm, bn     output tile per workgroup (int8 MFMA route: 256x256, 256x128 or 128x128)
  *   bk         K elements staged per pipeline step (MFMA routes: 0 or 128)
  *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route)
- *   k_split    reserved, must be 0 or 1
+ *   k_split    0 or 1; 2 (int8 MFMA route with a tail) splits each tail tile's K
+ *              range between two workgroups that combine their int32 partial
+ *              sums through the workspace (needs K > 256)
  *   lds_stages LDS buffers (MFMA routes: 0 or 2)
  *   mt         XOR route: activation rows per workgroup (0 or 8)
  *   split_n    int8 MFMA route: output columns [split_n, N) use the tail tile
@@ -129,10 +131,11 @@ apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, 
 apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out);
 
 /* Device workspace bytes apt_gemm needs for this problem and config (cfg
- * NULL or route AUTO = the selected one): the reassembled int8 MFMA route
- * expands the activations once per call into int8 MFMA fragments,
- * ceil(M/32)*32 * K_pad' bytes with K_pad' = K_pad rounded up to a multiple of
- * 256; the other routes need 0.  Returns 0 for invalid sizes. */
+ * NULL or route AUTO = the selected one).  The reassembled int8 MFMA route
+ * expands the activations once per call into int8 MFMA fragments
+ * (ceil(M/32)*32 * K_pad' bytes, K_pad' = K_pad rounded up to a multiple of
+ * 256) and, with k_split 2, keeps one int32 partial tile and one flag per
+ * tail tile; the other routes need 0.  Returns 0 for invalid sizes. */
 size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_config_t* cfg);
 
 /* C = A * W^T on packed operands, with the fused recombination of Sec. III-B

@@ -29,18 +29,20 @@ apt_status_t pack_common(const int8_t* codes, int rows, int K, int bits, void* p
 }
 
 // Checks a config against the problem; returns APT_OK or the status to report.
-apt_status_t check_config(const apt_config_t& c, int M, int N, int p, int q, bool have_rowsums) {
-  if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
+apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int q,
+                          bool have_rowsums) {
   switch (c.route) {
     case APT_ROUTE_XOR:
+      if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
       if (!apt::xor_config_ok(c)) return APT_ERR_INVALID_ARG;
       if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_INT8_MFMA:
-      if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
+      if (!apt::int8_config_ok(c, N, K)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
       return APT_OK;
     case APT_ROUTE_PM1_MFMA:
+      if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
       if (p > 7 || q > 7) return APT_ERR_UNSUPPORTED;
       if (!apt::pm1_config_ok(c, p, q)) return APT_ERR_INVALID_ARG;
       return APT_OK;
@@ -81,7 +83,7 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
   const apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
                              ? apt::select_config(M, N, K, p, q)
                              : *cfg;
-  return c.route == APT_ROUTE_INT8_MFMA ? apt::int8_workspace_bytes(M, K) : 0;
+  return c.route == APT_ROUTE_INT8_MFMA ? apt::int8_workspace_bytes(M, N, K, c) : 0;
 }
 
 apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, const void* w_packed,
@@ -102,10 +104,10 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, c
   else
     c = *cfg;
   const bool have_rowsums = a_rowsum != nullptr && w_rowsum != nullptr;
-  apt_status_t st = check_config(c, M, N, p, q, have_rowsums);
+  apt_status_t st = check_config(c, M, N, K, p, q, have_rowsums);
   if (st != APT_OK) return st;
   if (c.route == APT_ROUTE_INT8_MFMA) {
-    if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, K))
+    if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, N, K, c))
       return APT_ERR_WORKSPACE;
     if (!aligned16(workspace)) return APT_ERR_INVALID_ARG;
   }

@@ -52,8 +52,8 @@ bool xor_config_ok(const apt_config_t& cfg);
 // activations expanded into MFMA fragments (int8_workspace_bytes).
 hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
                             hipStream_t stream);
-bool int8_config_ok(const apt_config_t& cfg, int N);
-size_t int8_workspace_bytes(int M, int K);
+bool int8_config_ok(const apt_config_t& cfg, int N, int K);
+size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg);
 
 // Plane-pair +-1 MFMA route (gemm_pm1.hip).
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);

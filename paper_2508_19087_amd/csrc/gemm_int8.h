@@ -60,6 +60,9 @@ struct Int8Params {
   int tiles_n;
   int mblocks;        // 32-row blocks of the activation fragment buffer
   const v4i* a_frag;  // activation fragments (workspace)
+  int ksplit;         // 1, or 2: each tile's K range is split between two workgroups
+  v4i* partial;       // ksplit 2: one int32 partial tile per tile (workspace)
+  int* flags;         // ksplit 2: partial-ready flag per tile (workspace, zeroed per call)
 };
 
 // Bytes of the activation fragment buffer for M rows and K.
@@ -77,9 +80,13 @@ inline size_t a_frag_bytes(int M, int K) {
 template <int Q>
 __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restrict__ a_packed, int M,
                                                        int nchunks, int nsteps, int mblocks,
-                                                       v4i* __restrict__ out) {
+                                                       v4i* __restrict__ out, int* __restrict__ flags,
+                                                       int nflags) {
   const int rows = mblocks * 32;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  // The split-K flags of this call start cleared (the GEMM launches follow in
+  // stream order).
+  if (t < nflags) flags[t] = 0;
   if (t >= (int64_t)rows * (nsteps / kSteps)) return;
   const int row = (int)(t % rows);
   const int chunk = (int)(t / rows);
@@ -213,18 +220,45 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
   const int NCE = (NC + 1) & ~1;  // even chunk count; a last odd chunk is all padding
+  const int c_mid = ((NCE / 2) + 1) & ~1;  // split point of the two K halves (even)
   const int tid = threadIdx.x;
   const int lane = tid % kWave;
   const int wave = tid / kWave;
   const int wm = wave / WN, wn = wave % WN;
 
-  // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
-  // run of tiles (consecutive tiles share their activation rows) so that its
-  // L2 keeps the shared operand.
-  const int ntiles = gridDim.x;
-  int tile = blockIdx.x;
-  if (ntiles % 8 == 0) tile = (blockIdx.x % 8) * (ntiles / 8) + blockIdx.x / 8;
-  const int tm = tile / prm.tiles_n, tn = tile % prm.tiles_n;
+  // Workgroups are dealt round-robin to the 8 XCDs, each with its own L2.
+  // When the tile grid splits into 4 x 8 blocks of tiles, block k of XCD x
+  // takes tile k of the x-th such block (one block fills the XCD's 32 CUs),
+  // so concurrently running tiles share 4 activation bands and 8 weight
+  // column blocks in that L2.  Otherwise each XCD takes a contiguous run of
+  // row-major tiles.
+  // With ksplit 2, workgroups 2t and 2t+1 share tile t: the even one takes
+  // the first half of K and publishes its partial sums, the odd one takes the
+  // second half, adds the partial and stores the tile.  Workgroups are
+  // dispatched in index order, so a waiting odd workgroup's partner is
+  // always already resident or done.
+  const bool split = prm.ksplit == 2;
+  const int half = split ? (int)(blockIdx.x & 1) : 0;
+  const int bid = split ? (int)(blockIdx.x >> 1) : (int)blockIdx.x;
+  const int ntiles = split ? (int)gridDim.x / 2 : (int)gridDim.x;
+  const int tiles_m = ntiles / prm.tiles_n;
+  int tm, tn;
+  constexpr int kXcds = 8, kSM = 4, kSN = 8;
+  if (split) {
+    tm = bid / prm.tiles_n;
+    tn = bid % prm.tiles_n;
+  } else if (tiles_m % kSM == 0 && prm.tiles_n % kSN == 0 && ntiles % (kXcds * kSM * kSN) == 0) {
+    const int xcd = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
+    const int super = (k / (kSM * kSN)) * kXcds + xcd, in = k % (kSM * kSN);
+    const int supers_n = prm.tiles_n / kSN;
+    tm = (super / supers_n) * kSM + in % kSM;
+    tn = (super % supers_n) * kSN + in / kSM;
+  } else {
+    int tile = bid;
+    if (ntiles % kXcds == 0) tile = (bid % kXcds) * (ntiles / kXcds) + bid / kXcds;
+    tm = tile / prm.tiles_n;
+    tn = tile % prm.tiles_n;
+  }
   const int m0 = tm * BM, n0 = prm.n_begin + tn * BN;
 
   using SW = Stage<P, BN, SPLIT, T>;
@@ -290,27 +324,70 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
     }
   };
 
-  // Prologue: weight chunk 0 into LDS buffer 0, chunk 1 in registers,
-  // activation fragments of chunk 0 in registers.
-  rw0.load(g.w_packed, n0, g.N, NC, 0, tid);
-  rw1.load(g.w_packed, n0, g.N, NC, 1, tid);
+  const int c_begin = (split && half == 1) ? c_mid : 0;
+  const int c_end = (split && half == 0) ? c_mid : NCE;
+
+  // Prologue: weight chunk c_begin into LDS buffer 0, the next one in
+  // registers, activation fragments of chunk c_begin in registers.
+  rw0.load(g.w_packed, n0, g.N, NC, c_begin, tid);
+  rw1.load(g.w_packed, n0, g.N, NC, c_begin + 1, tid);
 #pragma unroll
   for (int ks = 0; ks < kSteps; ++ks)
 #pragma unroll
-    for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)ks * kFragVecs];
+    for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)(c_begin * kSteps + ks) * kFragVecs];
   rw0.store(buf0, tid);
   __syncthreads();
 
   // Two chunks per trip.  While the MFMAs of chunk c run, weight chunk c+1
   // (already in registers) is reassembled into the other LDS buffer and
   // weight chunk c+2 is fetched into the register set just consumed.
-  for (int c = 0; c < NCE; c += 2) {
+  for (int c = c_begin; c < c_end; c += 2) {
     rw0.load(g.w_packed, n0, g.N, NC, c + 2, tid);
     phase(buf0, buf1, rw1, c);
     __syncthreads();
     rw1.load(g.w_packed, n0, g.N, NC, c + 3, tid);
     phase(buf1, buf0, rw0, c + 1);
     __syncthreads();
+  }
+
+  if (split) {
+    // Partial tile in accumulator order: vector ((wave * FN * FM * 4 + f) * 64 + lane).
+    v4i* part = prm.partial + (int64_t)bid * (BM * BN / 4) + wave * (FN * FM * 4) * kWave + lane;
+    if (half == 0) {
+#pragma unroll
+      for (int b = 0; b < FN; ++b)
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            part[((b * FM + a) * 4 + j) * kWave] =
+                v4i{acc[b][a][4 * j], acc[b][a][4 * j + 1], acc[b][a][4 * j + 2], acc[b][a][4 * j + 3]};
+      // Every wave's stores reach device scope (the partner runs on another
+      // XCD, behind another L2) before one thread raises the flag.
+      __threadfence();
+      __syncthreads();
+      if (tid == 0) __hip_atomic_store(prm.flags + bid, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    if (tid == 0) {
+      // Bounded wait: the partner is resident or done, so the flag arrives.
+      for (long spin = 0; spin < (1L << 28); ++spin) {
+        if (__hip_atomic_load(prm.flags + bid, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == 1) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+#pragma unroll
+      for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const v4i pv = __builtin_nontemporal_load(part + ((b * FM + a) * 4 + j) * kWave);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[b][a][4 * j + i] += pv[i];
+        }
   }
 
   // Epilogue.  Each 32x32 accumulator block goes through a private LDS slot
@@ -403,6 +480,7 @@ constexpr TileShape kShapes[] = {
     {256, 128, 4, 2, 4, false},
     {128, 128, 2, 2, 2, false},
     {256, 256, 4, 2, 2, true},
+    {256, 256, 2, 2, 1, false},
 };
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
@@ -418,7 +496,8 @@ hipError_t launch_shape(const Int8Params& prm0, int n_count, hipStream_t stream)
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(tiles_m * prm.tiles_n), dim3(sh.wm * sh.wn * kWave), lds, stream, prm);
+  const int blocks = tiles_m * prm.tiles_n * (prm.ksplit == 2 ? 2 : 1);
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(sh.wm * sh.wn * kWave), lds, stream, prm);
   return hipGetLastError();
 }
 
@@ -430,6 +509,7 @@ inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int n_count, 
     case 2: return launch_shape<P, 2>(prm, n_count, stream);
     case 3: return launch_shape<P, 3>(prm, n_count, stream);
     case 4: return launch_shape<P, 4>(prm, n_count, stream);
+    case 5: return launch_shape<P, 5>(prm, n_count, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -440,7 +520,7 @@ template <int P>
 hipError_t launch_for_p(int shape, const Int8Params& prm, int n_count, hipStream_t stream);
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
-                               int mblocks, v4i* out, hipStream_t stream);
+                               int mblocks, v4i* out, int* flags, int nflags, hipStream_t stream);
 
 }  // namespace int8
 }  // namespace apt

@@ -14,17 +14,18 @@ hipError_t launch_for_p(int shape, const Int8Params& prm, int n_count, hipStream
 
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
-                               int mblocks, v4i* out, hipStream_t stream) {
-  const int64_t threads = (int64_t)mblocks * 32 * (nsteps / kSteps);
+                               int mblocks, v4i* out, int* flags, int nflags, hipStream_t stream) {
+  int64_t threads = (int64_t)mblocks * 32 * (nsteps / kSteps);
+  if (threads < nflags) threads = nflags;
   const int blocks = (int)((threads + 255) / 256);
   hipLaunchKernelGGL(expand_a_kernel<Q>, dim3(blocks), dim3(256), 0, stream, a_packed, M, nchunks,
-                     nsteps, mblocks, out);
+                     nsteps, mblocks, out, flags, nflags);
   return hipGetLastError();
 }
 
 template hipError_t launch_for_p<APT_INST_P>(int, const Int8Params&, int, hipStream_t);
 template hipError_t launch_expand_for_q<APT_INST_P>(const uint32_t*, int, int, int, int, v4i*,
-                                                     hipStream_t);
+                                                     int*, int, hipStream_t);
 
 }  // namespace int8
 }  // namespace apt

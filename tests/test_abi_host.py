@@ -46,6 +46,25 @@ def _shapes():
     return out
 
 
+def _int8_workspace(M, N, K, c):
+    """Activation fragments, then (K-split tail) int32 partial tiles and flags,
+    each region rounded up to 256 bytes."""
+    up = lambda x: (x + 255) // 256 * 256
+    nce = ((K + 127) // 128 + 1) // 2 * 2
+    ws = up((M + 31) // 32 * 32 * nce * 128)
+    if c.k_split == 2:
+        tiles = -(-M // c.tail_bm) * -(-(N - c.split_n) // c.tail_bn)
+        ws += up(tiles * c.tail_bm * c.tail_bn * 4) + up(tiles * 4)
+    return ws
+
+
+def test_workspace_k_split_tail():
+    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 2, 2, 0, 8192, 256, 256)
+    ws = apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c)
+    assert ws == 2048 * 4096 + 88 * 256 * 256 * 4 + 512
+    assert ws == _int8_workspace(2048, 11008, 4096, c)
+
+
 @pytest.mark.parametrize("shape", _shapes())
 def test_select_config_valid(shape):
     st, c = apt.apt_select_config(*shape)
@@ -56,8 +75,7 @@ def test_select_config_valid(shape):
     M, N, K = shape[:3]
     ws = apt.apt_gemm_workspace_bytes(*shape, c)
     if c.route == apt.APT_ROUTE_INT8_MFMA:
-        nce = ((K + 127) // 128 + 1) // 2 * 2
-        assert ws == (M + 31) // 32 * 32 * nce * 128
+        assert ws == _int8_workspace(M, N, K, c)
     else:
         assert ws == 0
 
@@ -112,6 +130,17 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
                                                  256, 96, 128)), apt.APT_ERR_INVALID_ARG),
     (dict(M=64, N=256, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
                                                  256, 128, 128)), apt.APT_ERR_INVALID_ARG),
+    # K split: only with a tail, only for K > 256, only 2, only on the int8 route
+    (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
+                                                         2, 2)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=512, K=256, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
+                                                        2, 2, 0, 256, 256, 256)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
+                                                         3, 2, 0, 256, 256, 256)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
+                                                         2, 2, 0, 256, 256, 256), ws=WS,
+          ws_bytes=64 * 1024), apt.APT_ERR_WORKSPACE),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA, k_split=2)), apt.APT_ERR_UNSUPPORTED),
 ])
 def test_gemm_validation(kw, want):
     assert gemm(**kw) == want

@@ -22,7 +22,7 @@ def test_all_bit_widths_every_route(p, q):
         prob = synth.random_problem(g, M, N, K, p, q)
         want = oracle_full(prob)
         packed = pack_problem(prob)
-        for name, cfg in forced_configs(p, q, N):
+        for name, cfg in forced_configs(p, q, N, K):
             got, _ = run(prob, cfg=cfg, packed=packed)
             assert_int32_equal(got, want, "%s p=%d q=%d %dx%dx%d" % (name, p, q, M, N, K))
 
@@ -40,7 +40,7 @@ def test_ragged_shapes(M, N, K, p, q):
     packed = pack_problem(prob)
     got, _ = run(prob, packed=packed)  # selected config
     assert_int32_equal(got, want, "auto")
-    for name, cfg in forced_configs(p, q, N):
+    for name, cfg in forced_configs(p, q, N, K):
         got, _ = run(prob, cfg=cfg, packed=packed)
         assert_int32_equal(got, want, name)
 
@@ -55,7 +55,7 @@ def test_extreme_values_all_ones_and_zeros():
         want = oracle_full(prob)
         assert want[0, 0] == K * 255 * 255 and want[0, 1] == -K * 255 * 255
         packed = pack_problem(prob)
-        for name, cfg in [("auto", None)] + forced_configs(8, 8):
+        for name, cfg in [("auto", None)] + forced_configs(8, 8, N, K):
             got, _ = run(prob, cfg=cfg, packed=packed)
             assert_int32_equal(got, want, name)
 
@@ -80,7 +80,7 @@ def test_deterministic_repeats():
     prob = synth.random_problem(synth.rng(3000), 300, 700, 1500, 4, 4)
     want = oracle_full(prob)
     packed = pack_problem(prob)
-    for name, cfg in forced_configs(4, 4):
+    for name, cfg in forced_configs(4, 4, 700, 1500):
         for _ in range(20):
             got, _ = run(prob, cfg=cfg, packed=packed)
             assert_int32_equal(got, want, name)
@@ -92,7 +92,7 @@ def test_fp16_epilogue(M, N, K, p, q):
     prob = synth.random_problem(synth.rng(4000, M, N, K), M, N, K, p, q, with_scales=True)
     want = oracle_full(prob)
     packed = pack_problem(prob)
-    for name, cfg in [("auto", None)] + forced_configs(p, q, N):
+    for name, cfg in [("auto", None)] + forced_configs(p, q, N, K):
         c32, c16 = run(prob, cfg=cfg, fp16=True, packed=packed)
         assert_int32_equal(c32, want, name)
         assert_fp16_ok(c16, want, prob, name)
