@@ -77,29 +77,37 @@ enum {
 /* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950
  * terms).  Fields a route does not use are ignored.
  *   route      APT_ROUTE_*
- *   bm, bn     output tile per workgroup (int8 MFMA route: 256x256, 256x128 or 128x128)
+ *   bm, bn     output tile per workgroup (int8 MFMA route: 256x256 with 4x2 or
+ *              2x4 waves, 256x128 with 4x2, 128x128 with 2x2)
  *   bk         K elements staged per pipeline step (MFMA routes: 0 or 128)
  *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route)
- *   k_split    0 or 1; 2 (int8 MFMA route with a tail) splits each tail tile's K
- *              range between two workgroups that combine their int32 partial
- *              sums through the workspace (needs K > 256)
- *   lds_stages LDS buffers (MFMA routes: 0 or 2)
+ *   grid       int8 MFMA route: persistent workgroups, 0..4096.  0 = one
+ *              workgroup per tile.  Otherwise each workgroup takes
+ *              floor(T / grid) whole tiles (T tiles in all) and the K chunks of
+ *              the remaining tiles are divided evenly among all workgroups
+ *              (stream-K); workgroups sharing a tile combine int32 partial
+ *              sums through the workspace.  The result does not depend on it.
+ *   lds_stages depth of the weight LDS ring (int8 MFMA route: 0 or 3; the
+ *              +-1 plane route ignores it)
  *   mt         XOR route: activation rows per workgroup (0 or 8)
- *   split_n    int8 MFMA route: output columns [split_n, N) use the tail tile
- *              tail_bm x tail_bn in a second launch, so the main tiles fill
- *              whole rounds of the 256 compute units; 0 = no tail.  A multiple
- *              of bn with 0 < split_n < N.
- *   tail_bm, tail_bn   tail tile (a configured int8 tile shape)
+ *   split_n    int8 MFMA route: 0, or a multiple of bn with 0 < split_n < N
+ *              and of 8: columns [0, split_n) use the tile above and columns
+ *              [split_n, N) a second launch with tile tail_bm x tail_bn (the
+ *              first configured shape of that size) and tail_grid persistent
+ *              workgroups (same meaning as grid)
+ *   reserved   ignored
  */
 typedef struct {
   int32_t route;
   int32_t bm, bn, bk;
   int32_t waves_m, waves_n;
-  int32_t k_split;
+  int32_t grid;
   int32_t lds_stages;
   int32_t mt;
   int32_t split_n;
   int32_t tail_bm, tail_bn;
+  int32_t tail_grid;
+  int32_t reserved[3];
 } apt_config_t;
 
 /* Bytes of a packed buffer for `rows` rows of K codes at `bits` bits
@@ -134,8 +142,10 @@ apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* 
  * NULL or route AUTO = the selected one).  The reassembled int8 MFMA route
  * expands the activations once per call into int8 MFMA fragments
  * (ceil(M/32)*32 * K_pad' bytes, K_pad' = K_pad rounded up to a multiple of
- * 256) and, with k_split 2, keeps one int32 partial tile and one flag per
- * tail tile; the other routes need 0.  Returns 0 for invalid sizes. */
+ * 256) and, for each launch with a stream-K decomposition (grid > 0 and T
+ * not a multiple of grid), two int32 BM x BN partial tiles per workgroup and
+ * one counter per shared tile, each region rounded up to 256 bytes; the
+ * other routes need 0.  Returns 0 for invalid sizes or configs. */
 size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_config_t* cfg);
 
 /* C = A * W^T on packed operands, with the fused recombination of Sec. III-B

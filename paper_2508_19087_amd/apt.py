@@ -34,19 +34,20 @@ ROUTE_NAMES = {APT_ROUTE_XOR: "xor_popcount", APT_ROUTE_PM1_MFMA: "pm1_planes_mf
 class apt_config_t(ctypes.Structure):
     _fields_ = [("route", ctypes.c_int32), ("bm", ctypes.c_int32), ("bn", ctypes.c_int32),
                 ("bk", ctypes.c_int32), ("waves_m", ctypes.c_int32), ("waves_n", ctypes.c_int32),
-                ("k_split", ctypes.c_int32), ("lds_stages", ctypes.c_int32), ("mt", ctypes.c_int32),
-                ("split_n", ctypes.c_int32), ("tail_bm", ctypes.c_int32), ("tail_bn", ctypes.c_int32)]
+                ("grid", ctypes.c_int32), ("lds_stages", ctypes.c_int32), ("mt", ctypes.c_int32),
+                ("split_n", ctypes.c_int32), ("tail_bm", ctypes.c_int32), ("tail_bn", ctypes.c_int32),
+                ("tail_grid", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_}
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
 
     @classmethod
-    def make(cls, route, bm=0, bn=0, bk=0, waves_m=0, waves_n=0, k_split=0, lds_stages=0, mt=0,
-             split_n=0, tail_bm=0, tail_bn=0):
+    def make(cls, route, bm=0, bn=0, bk=0, waves_m=0, waves_n=0, grid=0, lds_stages=0, mt=0,
+             split_n=0, tail_bm=0, tail_bn=0, tail_grid=0):
         c = cls()
         c.route, c.bm, c.bn, c.bk = route, bm, bn, bk
-        c.waves_m, c.waves_n, c.k_split, c.lds_stages, c.mt = waves_m, waves_n, k_split, lds_stages, mt
-        c.split_n, c.tail_bm, c.tail_bn = split_n, tail_bm, tail_bn
+        c.waves_m, c.waves_n, c.grid, c.lds_stages, c.mt = waves_m, waves_n, grid, lds_stages, mt
+        c.split_n, c.tail_bm, c.tail_bn, c.tail_grid = split_n, tail_bm, tail_bn, tail_grid
         return c
 
 

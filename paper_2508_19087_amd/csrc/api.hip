@@ -31,18 +31,18 @@ apt_status_t pack_common(const int8_t* codes, int rows, int K, int bits, void* p
 // Checks a config against the problem; returns APT_OK or the status to report.
 apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int q,
                           bool have_rowsums) {
+  (void)q;
   switch (c.route) {
     case APT_ROUTE_XOR:
-      if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
       if (!apt::xor_config_ok(c)) return APT_ERR_INVALID_ARG;
       if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_INT8_MFMA:
-      if (!apt::int8_config_ok(c, N, K)) return APT_ERR_INVALID_ARG;
+      if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
+      if (!apt::int8_sizes_ok(M, N, K, p, c)) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_PM1_MFMA:
-      if (c.k_split > 1) return APT_ERR_UNSUPPORTED;
       if (p > 7 || q > 7) return APT_ERR_UNSUPPORTED;
       if (!apt::pm1_config_ok(c, p, q)) return APT_ERR_INVALID_ARG;
       return APT_OK;
@@ -83,7 +83,8 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
   const apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
                              ? apt::select_config(M, N, K, p, q)
                              : *cfg;
-  return c.route == APT_ROUTE_INT8_MFMA ? apt::int8_workspace_bytes(M, N, K, c) : 0;
+  if (c.route != APT_ROUTE_INT8_MFMA || !apt::int8_config_ok(c, N)) return 0;
+  return apt::int8_workspace_bytes(M, N, K, c);
 }
 
 apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, const void* w_packed,

@@ -52,7 +52,9 @@ bool xor_config_ok(const apt_config_t& cfg);
 // activations expanded into MFMA fragments (int8_workspace_bytes).
 hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
                             hipStream_t stream);
-bool int8_config_ok(const apt_config_t& cfg, int N, int K);
+constexpr int kMaxGrid = 4096;  // persistent workgroups of the int8 route, at most
+bool int8_config_ok(const apt_config_t& cfg, int N);
+bool int8_sizes_ok(int M, int N, int K, int p, const apt_config_t& cfg);
 size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg);
 
 // Plane-pair +-1 MFMA route (gemm_pm1.hip).

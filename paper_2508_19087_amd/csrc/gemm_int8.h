@@ -14,11 +14,13 @@
 //   gemm_int8_kernel each workgroup owns one BM x BN output tile and every
 //                    plane pair of it, as the paper's recovery-oriented
 //                    scheduling does (Sec. IV-B).  K advances one 128-element
-//                    chunk per pipeline step: the weight planes of the tile
-//                    are fetched two chunks ahead, reassembled into a
-//                    double-buffered LDS tile while the matrix cores work on
-//                    the previous chunk, and the activation fragments of the
-//                    next chunk are fetched k-step by k-step behind the MFMAs.
+//                    chunk per pipeline step over a 3-stage LDS ring: while
+//                    the matrix cores work on chunk c, the weight planes of
+//                    chunk c+2 (fetched one step earlier) are reassembled into
+//                    the free stage, those of chunk c+3 are fetched, the
+//                    activation fragments of chunk c+1 are fetched k-step by
+//                    k-step behind the MFMAs, and the first weight fragments
+//                    of chunk c+1 are read from LDS before the step's barrier.
 // Only the weights pass through LDS: staging both operands there would need
 // as many LDS bytes per chunk as the MFMAs take cycles, and LDS would bound
 // the kernel.
@@ -26,8 +28,10 @@
 // Operand bytes are y = u (b <= 7) or u - 128 (b == 8) with bipolar value
 // v = 2y + c.  Expanding sum_k v_a v_w over the real K gives the epilogue
 //   C = 4 D - 4 (K_pad - K) y_pad,a y_pad,w + c_w R_a[m] + c_a R_w[n] - c_a c_w K,
-// where D is the MFMA sum over K_pad, y_pad the operand byte of a padding
-// element, and R the row sums of bipolar values from the packers.  The
+// where D is the MFMA sum over K_pad = 128 NC, y_pad the operand byte of a
+// padding element, and R the row sums of bipolar values from the packers.
+// The main loop runs an even number of chunks; a last odd chunk has all-zero
+// activation bytes, so whatever weight bytes meet it add nothing to D.  The
 // arithmetic is done modulo 2^32; the true C fits in int32 (checked by the
 // host), so the wrapped result is exact.
 #pragma once
@@ -43,26 +47,46 @@ constexpr int kRowBytes = kChunk + 16;          // padded LDS row: 128 operand b
 constexpr int kStepBytes = 32;                  // K bytes per MFMA k-step
 constexpr int kSteps = kChunk / kStepBytes;     // k-steps per chunk
 constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes x 16 bytes
+constexpr int kStages = 3;                      // weight LDS ring depth
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-// All-zero plane words: the weight planes of a chunk past the end (the main
-// loop always runs an even number of chunks) are read from here, which makes
-// them padding elements.  Large enough for any in-group offset of 8 planes.
-static __device__ __attribute__((aligned(16))) uint32_t kZeroPlanes[512] = {};
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// One 16-byte streaming global store of output bytes (written once, not
+// re-read).  As a plain store the compiler shares the first element's store
+// with the element-wise edge path and splits the vector into 12 + 4 bytes.
+__device__ __forceinline__ void store16(int32_t* p, v4i v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<v4i*>(p));
+}
+
+// Buffer resource over [base, base + bytes) for raw buffer loads: a
+// wave-uniform base in SGPRs plus a per-lane 32-bit offset and a uniform
+// offset, so the loop's address arithmetic is a scalar add per chunk.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
 
 struct Int8Params {
   GemmArgs g;
   int nchunks;        // NC, chunks of K
   int nsteps;         // k-steps in the activation fragment buffer (even chunk count x 4)
-  int n_begin;        // first output column of this launch
-  int tiles_n;
   int mblocks;        // 32-row blocks of the activation fragment buffer
   const v4i* a_frag;  // activation fragments (workspace)
-  int ksplit;         // 1, or 2: each tile's K range is split between two workgroups
-  v4i* partial;       // ksplit 2: one int32 partial tile per tile (workspace)
-  int* flags;         // ksplit 2: partial-ready flag per tile (workspace, zeroed per call)
+  uint32_t a_bytes;   // bytes of the activation fragment buffer
+  uint32_t w_bytes;   // bytes of the packed weights
+  int n_begin;        // first output column of this launch's tile grid
+  int tiles_n;        // tiles per row of the tile grid
+  int tiles;          // BM x BN tiles
+  int dp_tiles;       // whole tiles per workgroup (the first dp_tiles * G tiles)
+  int sk_pairs;       // chunk pairs of the stream-K tiles (the last ones), shared evenly
+  v4i* partial;       // stream-K: two partial tiles per workgroup (workspace)
+  uint32_t partial_bytes;
+  int* counters;      // stream-K: arrivals per stream-K tile (workspace, zeroed per call)
+  int vec_out;        // outputs take 16-byte (int32) / 8-byte (fp16) row stores
 };
 
 // Bytes of the activation fragment buffer for M rows and K.
@@ -75,18 +99,19 @@ inline size_t a_frag_bytes(int M, int K) {
 // Fragment (mb, ks) holds k-step ks of rows 32 mb .. 32 mb + 31 in MFMA operand
 // order: lane l (vector index ((mb * nsteps + ks) * 64 + l)) carries 16 bytes of
 // row 32 mb + l mod 32, namely bytes 16 (l / 32) .. 16 (l / 32) + 15 of the
-// k-step's 32 reassembled bytes.  Rows past M and chunks past the last one are
-// expanded from all-zero planes (padding elements).
+// k-step's 32 reassembled bytes.  Rows past M are expanded from all-zero
+// planes (padding elements); a chunk past the last one (the odd chunk that
+// makes the count even) is all-zero bytes.
 template <int Q>
 __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restrict__ a_packed, int M,
                                                        int nchunks, int nsteps, int mblocks,
-                                                       v4i* __restrict__ out, int* __restrict__ flags,
-                                                       int nflags) {
+                                                       v4i* __restrict__ out, int* __restrict__ counters,
+                                                       int ncounters) {
   const int rows = mblocks * 32;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  // The split-K flags of this call start cleared (the GEMM launches follow in
-  // stream order).
-  if (t < nflags) flags[t] = 0;
+  // The stream-K arrival counters of this call start cleared (the GEMM
+  // launch follows in stream order).
+  if (t < ncounters) counters[t] = 0;
   if (t >= (int64_t)rows * (nsteps / kSteps)) return;
   const int row = (int)(t % rows);
   const int chunk = (int)(t / rows);
@@ -105,10 +130,14 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
       for (int j = 0; j < Q; ++j) pw[w][j] = 0u;
   }
   const int mb = row / 32, l = row % 32;
+  const bool phantom = chunk >= nchunks;
 #pragma unroll
   for (int w = 0; w < kWordsPerPlane; ++w) {
     uint32_t o[8];
     reassemble_word<Q>(pw[w], o);
+    if (phantom)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) o[t] = 0u;
     v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w) * kFragVecs;
     f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
     f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
@@ -119,96 +148,186 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
 // ROWS weight rows of a tile, each split into SPLIT items of 128/SPLIT elements
 // (4/SPLIT words per plane).  Consecutive threads take consecutive rows of the
 // same part, so a wave's LDS writes hit distinct banks.  Rows past the matrix
-// edge are clamped to its last
-// row: their products only reach outputs that are never stored, and the code
-// stays branch-free so the scheduler can interleave it with the MFMAs.
+// edge are clamped to its last row: their products only reach outputs that are
+// never stored, and the code stays branch-free so the scheduler can interleave
+// it with the MFMAs.  Chunks past the last one are clamped to it; they meet
+// all-zero activation bytes.
 template <int B, int ROWS, int SPLIT, int T>
 struct Stage {
   static constexpr int kWpi = kWordsPerPlane / SPLIT;
   static constexpr int kItems = ROWS * SPLIT / T;
   static_assert(ROWS * SPLIT % T == 0 && kItems >= 1, "items must divide evenly");
+  static constexpr int kWords = kItems * kWpi;  // words reassembled per thread per chunk
   uint32_t raw[kItems][B][kWpi];
 
-  // Loads chunk `chunk` of the item rows; a chunk at or past the end reads the
-  // zero planes, i.e. padding elements.
-  __device__ __forceinline__ void load(const uint32_t* __restrict__ packed, int row0, int rows,
-                                       int nchunks, int chunk, int tid) {
-    const bool real = chunk < nchunks;
+  // Byte offset of item `it`'s plane-0 words of chunk 0 in the packed weights.
+  static __device__ __forceinline__ uint32_t item_offset(int row0, int rows, int nchunks, int tid,
+                                                         int it) {
+    const int item = tid + T * it;
+    const int r = min(row0 + item % ROWS, rows - 1);
+    const int sub = item / ROWS;
+    return (uint32_t)(plane_words(r, 0, 0, nchunks, B) + sub * kWpi) * 4u;
+  }
+
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rsrc, const uint32_t* voff,
+                                       int nchunks, int chunk) {
+    const int soff = min(chunk, nchunks - 1) * B * kPlaneStride * 4;
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
-      const int item = tid + T * it;
-      const int r = min(row0 + item % ROWS, rows - 1);
-      const int sub = item / ROWS;
-      const uint32_t* src = real ? packed + plane_words(r, chunk, 0, nchunks, B) + sub * kWpi
-                                 : kZeroPlanes + (r % kRowGroup) * kWordsPerPlane + sub * kWpi;
 #pragma unroll
       for (int i = 0; i < B; ++i) {
+        const uint32_t vo = voff[it] + i * kPlaneStride * 4;
         if (kWpi == 4) {
-          uint4 v = *reinterpret_cast<const uint4*>(src + i * kPlaneStride);
+          v4u v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, vo, soff, 0);
           raw[it][i][0] = v.x; raw[it][i][1] = v.y; raw[it][i][2] = v.z; raw[it][i][3] = v.w;
         } else if (kWpi == 2) {
-          uint2 v = *reinterpret_cast<const uint2*>(src + i * kPlaneStride);
+          v2u v = __builtin_amdgcn_raw_buffer_load_b64(rsrc, vo, soff, 0);
           raw[it][i][0] = v.x; raw[it][i][1] = v.y;
         } else {
-          raw[it][i][0] = src[i * kPlaneStride];
+          raw[it][i][0] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, vo, soff, 0);
         }
       }
     }
   }
 
-  // Reassembles word u (0 <= u < kWords) of this thread's items into LDS.
-  static constexpr int kWords = kItems * kWpi;
-  __device__ __forceinline__ void store_word(uint8_t* lds_tile, int tid, int u) const {
+  // Half h (0: output dwords 0..3, 1: 4..7) of word u (0 <= u < kWords) of
+  // this thread's items, reassembled and written to LDS.  The low half
+  // leaves the tree's middle level in mid[] for the high half.
+  __device__ __forceinline__ void store_half(uint8_t* lds_tile, int tid, int u, int h,
+                                             uint32_t mid[8]) const {
     const int it = u / kWpi, w = u % kWpi;
     const int item = tid + T * it;
     const int r = item % ROWS;
     const int sub = item / ROWS;
-    uint32_t pw[B];
+    uint32_t o[4];
+    if (h == 0) {
+      uint32_t pw[B];
 #pragma unroll
-    for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
-    uint32_t o[8];
-    reassemble_word<B>(pw, o);
+      for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
+      reassemble_lo<B>(pw, mid, o);
+    } else {
+      reassemble_hi<B>(mid, o);
+    }
     uint4* d4 = reinterpret_cast<uint4*>(lds_tile + r * kRowBytes + (sub * kWpi + w) * kStepBytes);
-    d4[0] = make_uint4(o[0], o[1], o[2], o[3]);
-    d4[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    d4[h] = make_uint4(o[0], o[1], o[2], o[3]);
   }
 
   __device__ __forceinline__ void store(uint8_t* lds_tile, int tid) const {
+    uint32_t mid[8];
 #pragma unroll
-    for (int u = 0; u < kWords; ++u) store_word(lds_tile, tid, u);
+    for (int u = 0; u < kWords; ++u) {
+      store_half(lds_tile, tid, u, 0, mid);
+      store_half(lds_tile, tid, u, 1, mid);
+    }
   }
 };
 
 __host__ __device__ constexpr int offset_of(int b) { return b == 8 ? 1 : 1 - (1 << b); }
 __host__ __device__ constexpr int pad_of(int b) { return b == 8 ? -128 : 0; }
 
-// Scheduling hint for one k-step with N MFMAs: DS reads of the next k-step
-// first, then each MFMA followed by VALU_PER vector instructions of the weight
-// reassembly, with the LDS writes and the activation-fragment loads spread
-// between the MFMAs.  Masks: 0x008 MFMA, 0x002 VALU, 0x100 DS read,
-// 0x200 DS write, 0x020 VMEM read.
-template <int I, int N, int READS, int WRITES, int VMEM, int VALU_PER>
-struct Interleave {
-  static __device__ __forceinline__ void run() {
-    if constexpr (I < READS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    if constexpr (VALU_PER > 0) __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER, 0);
-    if constexpr (WRITES > 0 && I >= N - 2 * WRITES && (I - (N - 2 * WRITES)) % 2 == 1)
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-    if constexpr (I < VMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    Interleave<I + 1, N, READS, WRITES, VMEM, VALU_PER>::run();
-  }
-};
-template <int N, int READS, int WRITES, int VMEM, int VALU_PER>
-struct Interleave<N, N, READS, WRITES, VMEM, VALU_PER> {
-  static __device__ __forceinline__ void run() {}
+// ---- main kernel --------------------------------------------------------------
+// Work decomposition.  The output is cut into T tiles of BM x BN (row-major
+// tile order) and each tile's K into NCE/2 pairs of chunks.  A launch of G
+// persistent workgroups gives workgroup w the whole tiles w, w + G, ...,
+// (dp_tiles - 1) G + w, and splits the chunk pairs of the remaining
+// T - dp_tiles G tiles evenly: workgroup w takes pairs [w S / G, (w+1) S / G)
+// of them (S = sk_pairs), i.e. the end of one tile, possibly whole tiles, and
+// the start of another (stream-K).  A workgroup walks its stream-K pairs
+// first and its whole tiles after, as one continuous chunk stream: the
+// software pipeline runs across tile boundaries, and at the end of each part
+// of a tile the accumulators are flushed:
+//   whole tile        epilogue;
+//   producer part     (starts after the tile's first pair) int32 partial to
+//                     the workspace, then an arrival on the tile's counter;
+//   owner part        (starts at the first pair, ends early) usually finds
+//                     every producer arrived, adds their partials and runs
+//                     the epilogue; otherwise it publishes its own partial
+//                     and arrives as well.
+// Whoever arrives last finishes the tile, so no workgroup ever waits for
+// another.  Partials and counters use device-coherent (sc1) accesses, so the
+// hand-off needs no cache flush: the workgroups of one tile sit on different
+// XCDs, behind different L2s.
+
+// Position in a workgroup's chunk-pair stream.  Every field is uniform.
+struct Cursor {
+  int tile;      // tile index (>= T past the end of the stream)
+  int m0, n0;    // tile origin (a valid tile's past the end)
+  int pair;      // pair within the tile
+  int pend;      // end of this part (exclusive pair)
+  int pbeg;      // first pair of this part
+  int sk_left;   // stream-K pairs after this part
+  int dp_next;   // next whole-tile round
 };
 
-// ---- main kernel --------------------------------------------------------------
+// Walks the stream; tile origins are updated incrementally (no division in
+// the loop): the next stream-K tile is the next tile in row-major order, the
+// next whole tile is G tiles further.
+struct Stream {
+  int G, w, pairs, dp_tiles, sk_base, sk_lo, sk_hi, tiles;
+  int n_begin, n_end;    // output columns of the tile grid: [n_begin, n_begin + tiles_n BN)
+  int bm, bn;
+  int g_m, g_n;           // G tiles as (rows, columns) of the tile grid: G = g_m tiles_n + g_n
+  int dp_m0, dp_n0;       // origin of tile w
+
+  __device__ __forceinline__ void step_origin(Cursor& c, int dm, int dn) const {
+    c.n0 += dn * bn;
+    c.m0 += dm * bm;
+    if (c.n0 >= n_end) {
+      c.n0 -= n_end - n_begin;
+      c.m0 += bm;
+    }
+  }
+  __device__ __forceinline__ void begin_dp(Cursor& c, int round) const {
+    if (round == 0) {
+      c.m0 = dp_m0;
+      c.n0 = dp_n0;
+    } else if (round < dp_tiles) {
+      step_origin(c, g_m, g_n);
+    }
+    c.tile = round < dp_tiles ? round * G + w : 0x7fffffff;  // past the end
+    c.pair = c.pbeg = 0;
+    c.pend = pairs;
+    c.dp_next = round + 1;
+    c.sk_left = 0;
+  }
+  __device__ __forceinline__ Cursor first(int tiles_n) const {
+    // (tile origins are absolute output coordinates)
+    Cursor c;
+    if (sk_hi > sk_lo) {
+      c.tile = sk_base + sk_lo / pairs;
+      c.m0 = c.tile / tiles_n * bm;
+      c.n0 = n_begin + c.tile % tiles_n * bn;
+      c.pair = c.pbeg = sk_lo % pairs;
+      c.pend = min(pairs, c.pair + (sk_hi - sk_lo));
+      c.sk_left = (sk_hi - sk_lo) - (c.pend - c.pair);
+      c.dp_next = 0;
+    } else {
+      begin_dp(c, 0);
+    }
+    return c;
+  }
+  __device__ __forceinline__ void advance(Cursor& c) const {
+    if (++c.pair < c.pend) return;
+    if (c.sk_left > 0) {
+      ++c.tile;
+      step_origin(c, 0, 1);
+      c.pair = c.pbeg = 0;
+      c.pend = min(pairs, c.sk_left);
+      c.sk_left -= c.pend;
+    } else {
+      begin_dp(c, c.dp_next);
+    }
+  }
+  // Workgroup whose stream-K range holds stream-K pair u of S.
+  __device__ __forceinline__ int range_of(int u, int S) const {
+    return (int)((((int64_t)u + 1) * G - 1) / S);
+  }
+};
+
 // The MFMA takes the weight fragment as its first operand, so the accumulator
 // of lane l holds D[n][m] for m = l mod 32 and four consecutive n: each lane
 // stores 16 contiguous output bytes.
-template <int P, int BM, int BN, int WM, int WN, int SPLIT, bool HINTS>
+template <int P, int BM, int BN, int WM, int WN, int SPLIT>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm) {
   constexpr int T = WM * WN * kWave;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
@@ -216,300 +335,393 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
   constexpr int kStageBytes = BN * kRowBytes;
   static_assert(FM >= 1 && FN >= 1, "wave tile too small");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  __shared__ int s_bcast;
 
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
   const int NCE = (NC + 1) & ~1;  // even chunk count; a last odd chunk is all padding
-  const int c_mid = ((NCE / 2) + 1) & ~1;  // split point of the two K halves (even)
   const int tid = threadIdx.x;
   const int lane = tid % kWave;
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform in the wave
   const int wm = wave / WN, wn = wave % WN;
+  // Epilogue terms of the tile being finished, staged in LDS after the ring:
+  // c_a R_w[n] and the scale s_w[n] per column, c_w R_a[m] - const and s_a[m]
+  // per row.
+  uint32_t* const lds_wt = reinterpret_cast<uint32_t*>(lds + kStages * kStageBytes);
+  uint32_t* const lds_at = lds_wt + BN;
+  float* const lds_ws = reinterpret_cast<float*>(lds_at + BM);
+  float* const lds_as = lds_ws + BN;
+  constexpr int kEpiStride = 32 * 4 + 16;  // bytes per row of a 32x32 int32 block in LDS
+  uint8_t* const epi_slot = lds + kStages * kStageBytes + (BN + BM) * 8 + wave * 32 * kEpiStride;
 
-  // Workgroups are dealt round-robin to the 8 XCDs, each with its own L2.
-  // When the tile grid splits into 4 x 8 blocks of tiles, block k of XCD x
-  // takes tile k of the x-th such block (one block fills the XCD's 32 CUs),
-  // so concurrently running tiles share 4 activation bands and 8 weight
-  // column blocks in that L2.  Otherwise each XCD takes a contiguous run of
-  // row-major tiles.
-  // With ksplit 2, workgroups 2t and 2t+1 share tile t: the even one takes
-  // the first half of K and publishes its partial sums, the odd one takes the
-  // second half, adds the partial and stores the tile.  Workgroups are
-  // dispatched in index order, so a waiting odd workgroup's partner is
-  // always already resident or done.
-  const bool split = prm.ksplit == 2;
-  const int half = split ? (int)(blockIdx.x & 1) : 0;
-  const int bid = split ? (int)(blockIdx.x >> 1) : (int)blockIdx.x;
-  const int ntiles = split ? (int)gridDim.x / 2 : (int)gridDim.x;
-  const int tiles_m = ntiles / prm.tiles_n;
-  int tm, tn;
-  constexpr int kXcds = 8, kSM = 4, kSN = 8;
-  if (split) {
-    tm = bid / prm.tiles_n;
-    tn = bid % prm.tiles_n;
-  } else if (tiles_m % kSM == 0 && prm.tiles_n % kSN == 0 && ntiles % (kXcds * kSM * kSN) == 0) {
-    const int xcd = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
-    const int super = (k / (kSM * kSN)) * kXcds + xcd, in = k % (kSM * kSN);
-    const int supers_n = prm.tiles_n / kSN;
-    tm = (super / supers_n) * kSM + in % kSM;
-    tn = (super % supers_n) * kSN + in / kSM;
-  } else {
-    int tile = bid;
-    if (ntiles % kXcds == 0) tile = (bid % kXcds) * (ntiles / kXcds) + bid / kXcds;
-    tm = tile / prm.tiles_n;
-    tn = tile % prm.tiles_n;
-  }
-  const int m0 = tm * BM, n0 = prm.n_begin + tn * BN;
+  Stream st;
+  st.G = gridDim.x;
+  st.w = blockIdx.x;
+  st.pairs = NCE / 2;
+  st.dp_tiles = prm.dp_tiles;
+  st.sk_base = prm.dp_tiles * st.G;
+  st.sk_lo = (int)((int64_t)st.w * prm.sk_pairs / st.G);
+  st.sk_hi = (int)((int64_t)(st.w + 1) * prm.sk_pairs / st.G);
+  st.tiles = prm.tiles;
+  st.n_begin = prm.n_begin;
+  st.n_end = prm.n_begin + prm.tiles_n * BN;
+  st.bm = BM;
+  st.bn = BN;
+  st.g_m = st.G / prm.tiles_n;
+  st.g_n = st.G % prm.tiles_n;
+  st.dp_m0 = st.w / prm.tiles_n * BM;
+  st.dp_n0 = prm.n_begin + st.w % prm.tiles_n * BN;
 
+  // ---- operand sources
   using SW = Stage<P, BN, SPLIT, T>;
   SW rw0, rw1;
-  uint8_t* buf0 = lds;
-  uint8_t* buf1 = lds + kStageBytes;
+  const __amdgpu_buffer_rsrc_t w_rsrc = make_rsrc(g.w_packed, prm.w_bytes);
+  const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(prm.a_frag, prm.a_bytes);
+  // Uniform byte offset of this wave's 32-row fragment block a of a tile.
+  auto a_block = [&](int m0, int a) __attribute__((always_inline)) {
+    const int mb = min((m0 + wm * WTM) / 32 + a, prm.mblocks - 1);
+    return mb * prm.nsteps * kFragVecs * 16;
+  };
+  const uint32_t a_lane = lane * 16;
+  auto load_a = [&](int m0, int chunk, int ks, int a) __attribute__((always_inline)) -> v4i {
+    const int soff = a_block(m0, a) + (min(chunk, NCE - 1) * kSteps + ks) * kFragVecs * 16;
+    return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_lane, soff, 0));
+  };
+  auto w_offsets = [&](int n0, uint32_t* voff) __attribute__((always_inline)) {
+#pragma unroll
+    for (int it = 0; it < SW::kItems; ++it) voff[it] = SW::item_offset(n0, g.N, NC, tid, it);
+  };
 
   v16i acc[FN][FM];
+  auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int b = 0; b < FN; ++b)
+    for (int b = 0; b < FN; ++b)
 #pragma unroll
-    for (int a = 0; a < FM; ++a)
+      for (int a = 0; a < FM; ++a)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[b][a][v] = 0;
-
-  // Activation fragments of this wave: 32-row blocks clamped to the buffer.
-  const v4i* a_ptr[FM];
-#pragma unroll
-  for (int a = 0; a < FM; ++a) {
-    const int mb = min((m0 + wm * WTM) / 32 + a, prm.mblocks - 1);
-    a_ptr[a] = prm.a_frag + (int64_t)mb * prm.nsteps * kFragVecs + lane;
-  }
+        for (int v = 0; v < 16; ++v) acc[b][a][v] = 0;
+  };
+  zero_acc();
   v4i afr[kSteps][FM];
 
   const int lrow = lane % 32;
   const int lk = (lane / 32) * 16;
-
-  // One pipeline phase: the MFMAs of chunk c from LDS buffer `cst`, k-step by
-  // k-step.  During k-step ks the weight fragments of ks+1 are read, one slice
-  // of the next chunk's weight reassembly goes to LDS buffer `sst`, and the
-  // activation fragment registers of ks are refilled with chunk c+1.  A
-  // scheduling fence closes every k-step.
-  auto phase = [&](const uint8_t* cst, uint8_t* sst, const SW& rw, int c) {
-    const uint8_t* w_t = cst + (wn * WTN + lrow) * kRowBytes + lk;
-    const int next_step = min(c + 1, NCE - 1) * kSteps;
-    v4i wf[2][FN];
+  const int w_lane = (wn * WTN + lrow) * kRowBytes + lk;
+  v4i wf[2][FN];
+  auto read_wf = [&](const uint8_t* stage, int ks, v4i* dst) __attribute__((always_inline)) {
 #pragma unroll
-    for (int b = 0; b < FN; ++b) wf[0][b] = *reinterpret_cast<const v4i*>(w_t + b * 32 * kRowBytes);
+    for (int b = 0; b < FN; ++b)
+      dst[b] = *reinterpret_cast<const v4i*>(stage + w_lane + b * 32 * kRowBytes + ks * kStepBytes);
+  };
+
+  // One pipeline step: the MFMAs of one chunk from stage `cst`.  During
+  // k-step ks the weight fragments of ks+1 are read (for the last k-step:
+  // those of the next chunk's first k-step from `nst`, complete since the
+  // previous barrier), a slice of the reassembly of the chunk after next
+  // from `rw` goes to stage `sst`, and the activation registers of ks are
+  // refilled with the next chunk (tile origin a_m0, chunk a_chunk).  A
+  // scheduling fence closes every k-step.
+  constexpr int kHalves = 2 * SW::kWords;
+  auto step = [&](const uint8_t* cst, uint8_t* sst, const uint8_t* nst, const SW& rw, int a_m0,
+                  int a_chunk) __attribute__((always_inline)) {
+    uint32_t mid[8];
 #pragma unroll
     for (int ks = 0; ks < kSteps; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
-      if (ks + 1 < kSteps) {
+      if (ks + 1 < kSteps)
+        read_wf(cst, ks + 1, wf[nxt]);
+      else
+        read_wf(nst, 0, wf[nxt]);
 #pragma unroll
-        for (int b = 0; b < FN; ++b)
-          wf[nxt][b] = *reinterpret_cast<const v4i*>(w_t + b * 32 * kRowBytes + (ks + 1) * kStepBytes);
-      }
-#pragma unroll
-      for (int u = ks * SW::kWords / kSteps; u < (ks + 1) * SW::kWords / kSteps; ++u)
-        rw.store_word(sst, tid, u);
+      for (int hu = 0; hu < kHalves; ++hu)
+        if (hu * kSteps / kHalves == ks) rw.store_half(sst, tid, hu / 2, hu % 2, mid);
 #pragma unroll
       for (int b = 0; b < FN; ++b)
 #pragma unroll
         for (int a = 0; a < FM; ++a)
           acc[b][a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[cur][b], afr[ks][a], acc[b][a], 0, 0, 0);
 #pragma unroll
-      for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)(next_step + ks) * kFragVecs];
-      if constexpr (HINTS) {
-        constexpr int words = (SW::kWords + kSteps - 1) / kSteps;  // at most, per k-step
-        constexpr int valu = words * 40;
-        Interleave<0, FN * FM, FN, 2 * words, FM, (valu + FN * FM - 1) / (FN * FM)>::run();
-      }
+      for (int a = 0; a < FM; ++a) afr[ks][a] = load_a(a_m0, a_chunk, ks, a);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  const int c_begin = (split && half == 1) ? c_mid : 0;
-  const int c_end = (split && half == 0) ? c_mid : NCE;
+  // ---- epilogue constants
+  const int q = g.q;
+  const uint32_t ca = (uint32_t)(q == 8 ? 1 : 1 - (1 << q)), cw = (uint32_t)offset_of(P);
+  const uint32_t pad_term =
+      4u * (uint32_t)(NC * kChunk - g.K) * (uint32_t)((q == 8 ? -128 : 0) * pad_of(P));
+  const uint32_t const_term = ca * cw * (uint32_t)g.K + pad_term;
+  const bool fp16 = g.c_fp16 != nullptr;
+  const bool vec_ok = prm.vec_out != 0;
 
-  // Prologue: weight chunk c_begin into LDS buffer 0, the next one in
-  // registers, activation fragments of chunk c_begin in registers.
-  rw0.load(g.w_packed, n0, g.N, NC, c_begin, tid);
-  rw1.load(g.w_packed, n0, g.N, NC, c_begin + 1, tid);
-#pragma unroll
-  for (int ks = 0; ks < kSteps; ++ks)
-#pragma unroll
-    for (int a = 0; a < FM; ++a) afr[ks][a] = a_ptr[a][(int64_t)(c_begin * kSteps + ks) * kFragVecs];
-  rw0.store(buf0, tid);
-  __syncthreads();
-
-  // Two chunks per trip.  While the MFMAs of chunk c run, weight chunk c+1
-  // (already in registers) is reassembled into the other LDS buffer and
-  // weight chunk c+2 is fetched into the register set just consumed.
-  for (int c = c_begin; c < c_end; c += 2) {
-    rw0.load(g.w_packed, n0, g.N, NC, c + 2, tid);
-    phase(buf0, buf1, rw1, c);
-    __syncthreads();
-    rw1.load(g.w_packed, n0, g.N, NC, c + 3, tid);
-    phase(buf1, buf0, rw0, c + 1);
-    __syncthreads();
-  }
-
-  if (split) {
-    // Partial tile in accumulator order: vector ((wave * FN * FM * 4 + f) * 64 + lane).
-    v4i* part = prm.partial + (int64_t)bid * (BM * BN / 4) + wave * (FN * FM * 4) * kWave + lane;
-    if (half == 0) {
-#pragma unroll
-      for (int b = 0; b < FN; ++b)
-#pragma unroll
-        for (int a = 0; a < FM; ++a)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            part[((b * FM + a) * 4 + j) * kWave] =
-                v4i{acc[b][a][4 * j], acc[b][a][4 * j + 1], acc[b][a][4 * j + 2], acc[b][a][4 * j + 3]};
-      // Every wave's stores reach device scope (the partner runs on another
-      // XCD, behind another L2) before one thread raises the flag.
-      __threadfence();
-      __syncthreads();
-      if (tid == 0) __hip_atomic_store(prm.flags + bid, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-      return;
+  // Epilogue terms of tile (m0, n0): one value per thread, fetched a pair of
+  // chunks before the tile's flush and written to LDS before that pair's
+  // last barrier (the loads are issued before any output store, so waiting
+  // for them never waits for stores).
+  uint32_t term = 0;
+  float scale = 0.f;
+  auto fetch_terms = [&](int m0, int n0) __attribute__((always_inline)) {
+    if (tid < BN) {
+      const int n = min(n0 + tid, g.N - 1);
+      term = ca * (uint32_t)g.w_rowsum[n];
+      if (fp16) scale = __half2float(g.w_scale[n]);
+    } else if (tid < BN + BM) {
+      const int m = min(m0 + tid - BN, g.M - 1);
+      term = cw * (uint32_t)g.a_rowsum[m] - const_term;
+      if (fp16) scale = __half2float(g.a_scale[m]);
     }
-    if (tid == 0) {
-      // Bounded wait: the partner is resident or done, so the flag arrives.
-      for (long spin = 0; spin < (1L << 28); ++spin) {
-        if (__hip_atomic_load(prm.flags + bid, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == 1) break;
-        __builtin_amdgcn_s_sleep(2);
+  };
+  auto stage_terms = [&]() __attribute__((always_inline)) {
+    if (tid < BN + BM) {
+      lds_wt[tid] = term;  // lds_at follows lds_wt
+      lds_ws[tid] = scale;
+    }
+  };
+
+  // Final values of tile (m0, n0): each 32x32 accumulator block goes through
+  // the wave's LDS slot and comes back row by row, so that every store
+  // instruction writes 8 whole 128-byte output rows; the affine correction
+  // and the optional fp16 scaling are applied on the way out.
+  auto epilogue = [&](int m0, int n0) __attribute__((always_inline)) {
+    const int er = lane / 8, ec = (lane % 8) * 4;  // read-back row (+8 i) and first column
+#pragma unroll
+    for (int a = 0; a < FM; ++a) {
+      const int mrow0 = m0 + wm * WTM + a * 32;
+#pragma unroll
+      for (int b = 0; b < FN; ++b) {
+        // acc[b][a][4 gi + j] = D[n = 8 gi + 4 (lane / 32) + j][m = lane mod 32]
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) {
+          v4i v = {acc[b][a][gi * 4 + 0], acc[b][a][gi * 4 + 1], acc[b][a][gi * 4 + 2],
+                   acc[b][a][gi * 4 + 3]};
+          *reinterpret_cast<v4i*>(epi_slot + lrow * kEpiStride + (gi * 8 + (lane / 32) * 4) * 4) = v;
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // LDS writes of this wave done (lgkmcnt 0)
+        __builtin_amdgcn_wave_barrier();
+        const int nl = wn * WTN + b * 32 + ec;  // column in the tile
+        const int ncol = n0 + nl;
+        const bool full = vec_ok && ncol + 3 < g.N;
+        const v4u wt = *reinterpret_cast<const v4u*>(lds_wt + nl);
+        const v4f ws = *reinterpret_cast<const v4f*>(lds_ws + nl);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ml = wm * WTM + a * 32 + er + 8 * i;  // row in the tile
+          const int m = m0 + ml;
+          const v4i d = *reinterpret_cast<const v4i*>(epi_slot + (er + 8 * i) * kEpiStride + ec * 4);
+          const uint32_t at = lds_at[ml];
+          int32_t cv[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) cv[j] = (int32_t)(4u * (uint32_t)d[j] + at + wt[j]);
+          if (m < g.M && ncol < g.N) {
+            const int64_t o = (int64_t)m * g.N + ncol;
+            if (g.c_int32) {
+              if (full)
+                store16(g.c_int32 + o, v4i{cv[0], cv[1], cv[2], cv[3]});
+              else
+                for (int j = 0; j < 4 && ncol + j < g.N; ++j) g.c_int32[o + j] = cv[j];
+            }
+            if (fp16) {
+              const float sa = lds_as[ml];
+              uint32_t hb[2];
+#pragma unroll
+              for (int j = 0; j < 4; j += 2) {
+                const uint32_t h0 = __half_as_ushort(__float2half_rn((float)cv[j] * sa * ws[j]));
+                const uint32_t h1 = __half_as_ushort(__float2half_rn((float)cv[j + 1] * sa * ws[j + 1]));
+                hb[j / 2] = h0 | (h1 << 16);
+              }
+              if (full)
+                *reinterpret_cast<uint2*>(g.c_fp16 + o) = make_uint2(hb[0], hb[1]);
+              else
+                for (int j = 0; j < 4 && ncol + j < g.N; ++j)
+                  g.c_fp16[o + j] = __ushort_as_half((unsigned short)(hb[j / 2] >> (16 * (j % 2))));
+            }
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the slot is rewritten
+        __builtin_amdgcn_wave_barrier();
       }
     }
-    __syncthreads();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  };
+
+  // ---- stream-K partial tiles: accumulator order, device-coherent accesses
+  constexpr int kAccVecs = FN * FM * 4;  // v4i per lane
+  constexpr uint32_t kSlotBytes = (uint32_t)BM * BN * 4;
+  const __amdgpu_buffer_rsrc_t p_rsrc = make_rsrc(prm.partial, prm.partial_bytes);
+  const uint32_t p_lane = (uint32_t)((wave * kAccVecs * kWave + lane) * 16);
+  auto store_partial = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < FN; ++b)
 #pragma unroll
       for (int a = 0; a < FM; ++a)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const v4i pv = __builtin_nontemporal_load(part + ((b * FM + a) * 4 + j) * kWave);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc[b][a][4 * j + i] += pv[i];
+          const v4i v = {acc[b][a][4 * j], acc[b][a][4 * j + 1], acc[b][a][4 * j + 2],
+                         acc[b][a][4 * j + 3]};
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), p_rsrc,
+                                                 p_lane + ((b * FM + a) * 4 + j) * kWave * 16,
+                                                 slot * kSlotBytes, 16 /* sc1 */);
         }
+  };
+  auto add_partial = [&](int slot) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+#pragma unroll
+      for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const v4i v = __builtin_bit_cast(
+              v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                       p_rsrc, p_lane + ((b * FM + a) * 4 + j) * kWave * 16, slot * kSlotBytes, 16));
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[b][a][4 * j + i] += v[i];
+        }
+  };
+  // Publishes this workgroup's partial of stream-K tile u in `slot` and
+  // counts its arrival; true when it is the last of the tile's parts.
+  auto arrive = [&](int slot, int* counter, int parts) __attribute__((always_inline)) {
+    store_partial(slot);
+    __builtin_amdgcn_s_waitcnt(0);  // the partial is at device scope before the arrival
+    __syncthreads();
+    if (tid == 0)
+      s_bcast = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+    __syncthreads();
+    return s_bcast == parts;
+  };
+
+  // End of a part of tile c.tile: epilogue, or the stream-K hand-off.
+  // The workgroups sharing this workgroup's first and last stream-K tiles
+  // (the only ones it can share): [first, last] workgroup of each.
+  int sh_tile[2] = {-1, -1}, sh_first[2] = {0, 0}, sh_last[2] = {0, 0};
+  if (st.sk_hi > st.sk_lo) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int u = (e == 0 ? st.sk_lo : st.sk_hi - 1) / st.pairs;
+      sh_tile[e] = st.sk_base + u;
+      sh_first[e] = st.range_of(u * st.pairs, prm.sk_pairs);
+      sh_last[e] = st.range_of(u * st.pairs + st.pairs - 1, prm.sk_pairs);
+    }
   }
 
-  // Epilogue.  Each 32x32 accumulator block goes through a private LDS slot
-  // of the wave and comes back row by row, so that every store instruction
-  // writes 8 whole 128-byte output rows; the affine correction and the
-  // optional fp16 scaling are applied on the way out.
-  const int q = g.q;
-  const uint32_t ca = (uint32_t)(q == 8 ? 1 : 1 - (1 << q)), cw = (uint32_t)offset_of(P);
-  const uint32_t pad_term =
-      4u * (uint32_t)(NCE * kChunk - g.K) * (uint32_t)((q == 8 ? -128 : 0) * pad_of(P));
-  const uint32_t const_term = ca * cw * (uint32_t)g.K + pad_term;
-  constexpr int kEpiStride = 32 * 4 + 16;  // bytes per row of a 32x32 int32 block in LDS
-  uint8_t* slot = lds + wave * 32 * kEpiStride;
-  const int er = lane / 8, ec = (lane % 8) * 4;  // read-back row (+8 i) and first column
-  const bool vec_ok = (g.N % 4) == 0;
-  uint32_t wterm[FN][4];
-#pragma unroll
-  for (int b = 0; b < FN; ++b)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = min(n0 + wn * WTN + b * 32 + ec + j, g.N - 1);
-      wterm[b][j] = ca * (uint32_t)g.w_rowsum[n];
-    }
-#pragma unroll
-  for (int a = 0; a < FM; ++a) {
-    const int mrow0 = m0 + wm * WTM + a * 32;
-    uint32_t aterm[4];
-    float sa[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = min(mrow0 + er + 8 * i, g.M - 1);
-      aterm[i] = cw * (uint32_t)g.a_rowsum[m] - const_term;
-      sa[i] = g.c_fp16 ? __half2float(g.a_scale[m]) : 0.f;
-    }
-#pragma unroll
-    for (int b = 0; b < FN; ++b) {
-      // acc[b][a][4 gi + j] = D[n = 8 gi + 4 (lane / 32) + j][m = lane mod 32]
-#pragma unroll
-      for (int gi = 0; gi < 4; ++gi) {
-        v4i v = {acc[b][a][gi * 4 + 0], acc[b][a][gi * 4 + 1], acc[b][a][gi * 4 + 2],
-                 acc[b][a][gi * 4 + 3]};
-        *reinterpret_cast<v4i*>(slot + lrow * kEpiStride + (gi * 8 + (lane / 32) * 4) * 4) = v;
+  auto flush = [&](const Cursor& c) __attribute__((always_inline)) {
+    bool finish = true;
+    if (__builtin_expect(c.pbeg != 0 || c.pend != st.pairs, 0)) {
+      const int e = c.tile == sh_tile[0] ? 0 : 1;
+      const int w_first = sh_first[e], w_last = sh_last[e];
+      const int parts = w_last - w_first + 1;
+      int* counter = prm.counters + (c.tile - st.sk_base);
+      if (c.pbeg == 0) {  // owner: the first pairs of the tile, at the end of its range
+        if (tid == 0)
+          s_bcast = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        finish = s_bcast == parts - 1;
+        __syncthreads();
+        if (!finish) finish = arrive(2 * st.w + 1, counter, parts);
+      } else {            // producer: later pairs, at the start of its range
+        finish = arrive(2 * st.w, counter, parts);
       }
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // LDS writes of this wave done (lgkmcnt 0)
-      __builtin_amdgcn_wave_barrier();
-      const int ncol = n0 + wn * WTN + b * 32 + ec;
-      const bool full = vec_ok && ncol + 3 < g.N;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = mrow0 + er + 8 * i;
-        const v4i d = *reinterpret_cast<const v4i*>(slot + (er + 8 * i) * kEpiStride + ec * 4);
-        int32_t cv[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) cv[j] = (int32_t)(4u * (uint32_t)d[j] + aterm[i] + wterm[b][j]);
-        if (m < g.M && ncol < g.N) {
-          const int64_t o = (int64_t)m * g.N + ncol;
-          if (g.c_int32) {
-            if (full)
-              *reinterpret_cast<int4*>(g.c_int32 + o) = make_int4(cv[0], cv[1], cv[2], cv[3]);
-            else
-              for (int j = 0; j < 4 && ncol + j < g.N; ++j) g.c_int32[o + j] = cv[j];
-          }
-          if (g.c_fp16) {
-            __half h[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int n = min(ncol + j, g.N - 1);
-              h[j] = __float2half_rn((float)cv[j] * sa[i] * __half2float(g.w_scale[n]));
-            }
-            if (full)
-              *reinterpret_cast<uint2*>(g.c_fp16 + o) = *reinterpret_cast<const uint2*>(h);
-            else
-              for (int j = 0; j < 4 && ncol + j < g.N; ++j) g.c_fp16[o + j] = h[j];
-          }
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the slot is rewritten
-      __builtin_amdgcn_wave_barrier();
+      if (finish)
+        for (int v = w_first; v <= w_last; ++v)
+          if (v != st.w) add_partial(v == w_first ? 2 * v + 1 : 2 * v);
     }
+    if (finish) epilogue(c.m0, c.n0);
+  };
+
+  // ---- pipeline over the chunk stream.  Chunk 2p+e of the stream is chunk
+  // 2 cur.pair + e of tile cur.tile, for the cursor of pair p.
+  Cursor cp = st.first(prm.tiles_n);
+  Cursor c1 = cp;
+  st.advance(c1);
+  Cursor c2 = c1;
+  st.advance(c2);
+  uint32_t wv0[SW::kItems], wv1[SW::kItems], wv2[SW::kItems];  // weight offsets of cp, c1, c2
+  w_offsets(cp.n0, wv0);
+  w_offsets(c1.n0, wv1);
+  w_offsets(c2.n0, wv2);
+
+  // Prologue: pair cp into stages 0 and 1, the first chunk of c1 in
+  // registers, activation fragments and the first weight fragments of the
+  // first chunk.
+  rw0.load(w_rsrc, wv0, NC, 2 * cp.pair);
+  rw1.load(w_rsrc, wv0, NC, 2 * cp.pair + 1);
+#pragma unroll
+  for (int ks = 0; ks < kSteps; ++ks)
+#pragma unroll
+    for (int a = 0; a < FM; ++a) afr[ks][a] = load_a(cp.m0, 2 * cp.pair, ks, a);
+  rw0.store(lds, tid);
+  rw1.store(lds + kStageBytes, tid);
+  rw0.load(w_rsrc, wv1, NC, 2 * c1.pair);
+  __syncthreads();
+  read_wf(lds, 0, wf[0]);
+
+  int s0 = 0;  // stage of the current pair's first chunk
+  while (cp.tile < prm.tiles) {
+    const int s1 = s0 == 2 ? 0 : s0 + 1, s2 = s1 == 2 ? 0 : s1 + 1;
+    const bool part_end = cp.pair + 1 == cp.pend;
+    if (part_end) fetch_terms(cp.m0, cp.n0);
+    rw1.load(w_rsrc, wv1, NC, 2 * c1.pair + 1);
+    step(lds + s0 * kStageBytes, lds + s2 * kStageBytes, lds + s1 * kStageBytes, rw0,
+         cp.m0, 2 * cp.pair + 1);
+    __syncthreads();
+    rw0.load(w_rsrc, wv2, NC, 2 * c2.pair);
+    step(lds + s1 * kStageBytes, lds + s0 * kStageBytes, lds + s2 * kStageBytes, rw1,
+         c1.m0, 2 * c1.pair);
+    if (part_end) stage_terms();
+    __syncthreads();
+    if (__builtin_expect(part_end, 0)) {
+      flush(cp);
+      zero_acc();
+    }
+    s0 = s2;
+    cp = c1;
+    c1 = c2;
+#pragma unroll
+    for (int it = 0; it < SW::kItems; ++it) { wv0[it] = wv1[it]; wv1[it] = wv2[it]; }
+    const int old_tile = c2.tile;
+    st.advance(c2);
+    if (c2.tile != old_tile) w_offsets(c2.n0, wv2);
   }
 }
 
 struct TileShape {
   int bm, bn, wm, wn, split;
-  bool hints;
 };
 constexpr TileShape kShapes[] = {
-    {256, 256, 4, 2, 2, false},
-    {256, 256, 2, 4, 2, false},
-    {256, 128, 4, 2, 4, false},
-    {128, 128, 2, 2, 2, false},
-    {256, 256, 4, 2, 2, true},
-    {256, 256, 2, 2, 1, false},
+    {256, 256, 4, 2, 2},
+    {256, 256, 2, 4, 2},
+    {256, 128, 4, 2, 4},
+    {128, 128, 2, 2, 2},
 };
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
-// Launches shape S over output columns [prm.n_begin, prm.n_begin + n_count).
+// LDS of shape S: the weight ring, the epilogue terms and one 32x32 int32
+// epilogue slot per wave.
+constexpr size_t lds_bytes(const TileShape& sh) {
+  return kStages * (size_t)sh.bn * kRowBytes + (size_t)(sh.bn + sh.bm) * 8 +
+         (size_t)sh.wm * sh.wn * 32 * (32 * 4 + 16);
+}
+
+// Launches shape S with `grid` persistent workgroups (prm holds the
+// decomposition).
 template <int P, int S>
-hipError_t launch_shape(const Int8Params& prm0, int n_count, hipStream_t stream) {
+hipError_t launch_shape(const Int8Params& prm, int grid, hipStream_t stream) {
   constexpr TileShape sh = kShapes[S];
-  Int8Params prm = prm0;
-  prm.tiles_n = (n_count + sh.bn - 1) / sh.bn;
-  const int tiles_m = (prm.g.M + sh.bm - 1) / sh.bm;
-  const size_t lds = 2 * (size_t)sh.bn * kRowBytes;
-  auto kern = gemm_int8_kernel<P, sh.bm, sh.bn, sh.wm, sh.wn, sh.split, sh.hints>;
+  const size_t lds = lds_bytes(sh);
+  auto kern = gemm_int8_kernel<P, sh.bm, sh.bn, sh.wm, sh.wn, sh.split>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  const int blocks = tiles_m * prm.tiles_n * (prm.ksplit == 2 ? 2 : 1);
-  hipLaunchKernelGGL(kern, dim3(blocks), dim3(sh.wm * sh.wn * kWave), lds, stream, prm);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(sh.wm * sh.wn * kWave), lds, stream, prm);
   return hipGetLastError();
 }
 
 template <int P>
-inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int n_count, hipStream_t stream) {
+inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int grid, hipStream_t stream) {
   switch (shape) {
-    case 0: return launch_shape<P, 0>(prm, n_count, stream);
-    case 1: return launch_shape<P, 1>(prm, n_count, stream);
-    case 2: return launch_shape<P, 2>(prm, n_count, stream);
-    case 3: return launch_shape<P, 3>(prm, n_count, stream);
-    case 4: return launch_shape<P, 4>(prm, n_count, stream);
-    case 5: return launch_shape<P, 5>(prm, n_count, stream);
+    case 0: return launch_shape<P, 0>(prm, grid, stream);
+    case 1: return launch_shape<P, 1>(prm, grid, stream);
+    case 2: return launch_shape<P, 2>(prm, grid, stream);
+    case 3: return launch_shape<P, 3>(prm, grid, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -517,10 +729,11 @@ inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int n_count, 
 // Launches for weight bits P (main kernel) and activation bits Q (expansion);
 // the explicit instantiations live in gemm_int8_inst.hip, built once per width.
 template <int P>
-hipError_t launch_for_p(int shape, const Int8Params& prm, int n_count, hipStream_t stream);
+hipError_t launch_for_p(int shape, const Int8Params& prm, int grid, hipStream_t stream);
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
-                               int mblocks, v4i* out, int* flags, int nflags, hipStream_t stream);
+                               int mblocks, v4i* out, int* counters, int ncounters,
+                               hipStream_t stream);
 
 }  // namespace int8
 }  // namespace apt

@@ -1,123 +1,173 @@
 // gemm_int8.hip - config checks, workspace size and dispatch of the
 // reassembled-int8 MFMA route; the kernels are in gemm_int8.h.
+#include <algorithm>
+
 #include "gemm_int8.h"
 
 namespace apt {
 namespace int8 {
 namespace {
 
-// A config names a shape by its tile and wave grid; lds_stages == 3 asks for
-// the variant with explicit instruction-interleaving hints (experimental).
+// A config names a shape by its tile and wave grid; the weight ring is always
+// kStages deep (lds_stages 0 or kStages).
 int shape_index(const apt_config_t& cfg) {
+  if (cfg.lds_stages != 0 && cfg.lds_stages != kStages) return -1;
   for (int s = 0; s < kNumShapes; ++s)
     if (kShapes[s].bm == cfg.bm && kShapes[s].bn == cfg.bn && kShapes[s].wm == cfg.waves_m &&
-        kShapes[s].wn == cfg.waves_n && kShapes[s].hints == (cfg.lds_stages == 3))
+        kShapes[s].wn == cfg.waves_n)
       return s;
   return -1;
+}
+
+hipError_t launch_p(int p, int shape, const Int8Params& prm, int grid, hipStream_t stream) {
+  switch (p) {
+    case 1: return launch_for_p<1>(shape, prm, grid, stream);
+    case 2: return launch_for_p<2>(shape, prm, grid, stream);
+    case 3: return launch_for_p<3>(shape, prm, grid, stream);
+    case 4: return launch_for_p<4>(shape, prm, grid, stream);
+    case 5: return launch_for_p<5>(shape, prm, grid, stream);
+    case 6: return launch_for_p<6>(shape, prm, grid, stream);
+    case 7: return launch_for_p<7>(shape, prm, grid, stream);
+    case 8: return launch_for_p<8>(shape, prm, grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// The work decomposition of one launch: shape `shape` over output columns
+// [n_begin, n_begin + n_cols) with `grid` persistent workgroups (see
+// gemm_int8_kernel).
+struct Plan {
+  int shape, n_begin, tiles_n, tiles, grid, dp_tiles, sk_tiles, sk_pairs;
+  size_t partial_bytes, counter_bytes;
+};
+
+Plan make_plan(int M, int K, int shape, int n_begin, int n_cols, int grid) {
+  Plan pl;
+  pl.shape = shape;
+  const TileShape& sh = kShapes[shape];
+  pl.n_begin = n_begin;
+  pl.tiles_n = (n_cols + sh.bn - 1) / sh.bn;
+  pl.tiles = ((M + sh.bm - 1) / sh.bm) * pl.tiles_n;
+  const int pairs = ((num_chunks(K) + 1) & ~1) / 2;
+  const int64_t units = (int64_t)pl.tiles * pairs;
+  pl.grid = grid == 0 ? pl.tiles : (int)std::min<int64_t>(grid, units);
+  pl.dp_tiles = pl.tiles / pl.grid;
+  pl.sk_tiles = pl.tiles - pl.dp_tiles * pl.grid;
+  pl.sk_pairs = pl.sk_tiles * pairs;
+  pl.partial_bytes = pl.sk_tiles ? 2 * (size_t)pl.grid * sh.bm * sh.bn * 4 : 0;
+  pl.counter_bytes = (size_t)pl.sk_tiles * 4;
+  return pl;
 }
 
 // The tail tile is named by its size; the first shape of that size is used.
 int tail_index(const apt_config_t& cfg) {
   for (int s = 0; s < kNumShapes; ++s)
-    if (kShapes[s].bm == cfg.tail_bm && kShapes[s].bn == cfg.tail_bn && !kShapes[s].hints) return s;
+    if (kShapes[s].bm == cfg.tail_bm && kShapes[s].bn == cfg.tail_bn) return s;
   return -1;
 }
 
-hipError_t launch_p(int p, int shape, const Int8Params& prm, int n_count, hipStream_t stream) {
-  switch (p) {
-    case 1: return launch_for_p<1>(shape, prm, n_count, stream);
-    case 2: return launch_for_p<2>(shape, prm, n_count, stream);
-    case 3: return launch_for_p<3>(shape, prm, n_count, stream);
-    case 4: return launch_for_p<4>(shape, prm, n_count, stream);
-    case 5: return launch_for_p<5>(shape, prm, n_count, stream);
-    case 6: return launch_for_p<6>(shape, prm, n_count, stream);
-    case 7: return launch_for_p<7>(shape, prm, n_count, stream);
-    case 8: return launch_for_p<8>(shape, prm, n_count, stream);
+// One or two launches: (main over [0, split_n), tail over [split_n, N)).
+int make_plans(int M, int N, int K, const apt_config_t& cfg, Plan* pl) {
+  if (cfg.split_n == 0) {
+    pl[0] = make_plan(M, K, shape_index(cfg), 0, N, cfg.grid);
+    return 1;
   }
-  return hipErrorInvalidValue;
+  pl[0] = make_plan(M, K, shape_index(cfg), 0, cfg.split_n, cfg.grid);
+  pl[1] = make_plan(M, K, tail_index(cfg), cfg.split_n, N - cfg.split_n, cfg.tail_grid);
+  return 2;
 }
 
 }  // namespace
 }  // namespace int8
 
-bool int8_config_ok(const apt_config_t& cfg, int N, int K) {
-  if (int8::shape_index(cfg) < 0 || !(cfg.bk == 0 || cfg.bk == kChunk) || cfg.k_split < 0 ||
-      cfg.k_split > 2)
+bool int8_config_ok(const apt_config_t& cfg, int N) {
+  if (int8::shape_index(cfg) < 0 || !(cfg.bk == 0 || cfg.bk == kChunk) || cfg.grid < 0 ||
+      cfg.grid > kMaxGrid)
     return false;
-  if (cfg.split_n == 0) return cfg.k_split <= 1;
-  if (cfg.k_split == 2 && num_chunks(K) < 3) return false;  // each K half needs a chunk pair
+  if (cfg.split_n == 0) return true;
   return cfg.split_n > 0 && cfg.split_n < N && cfg.split_n % cfg.bn == 0 &&
-         cfg.split_n % kRowGroup == 0 && int8::tail_index(cfg) >= 0;
+         cfg.split_n % kRowGroup == 0 && int8::tail_index(cfg) >= 0 && cfg.tail_grid >= 0 &&
+         cfg.tail_grid <= kMaxGrid;
 }
 
-namespace {
-
-size_t align256(size_t x) { return (x + 255) / 256 * 256; }
-
-// Tiles of the tail launch (0 when the config has none).
-size_t tail_tiles(int M, int N, const apt_config_t& cfg) {
-  if (cfg.split_n == 0) return 0;
-  return (size_t)((M + cfg.tail_bm - 1) / cfg.tail_bm) *
-         ((N - cfg.split_n + cfg.tail_bn - 1) / cfg.tail_bn);
+// The kernels address the packed weights, the activation fragments and the
+// stream-K partial tiles with 32-bit buffer offsets.
+bool int8_sizes_ok(int M, int N, int K, int p, const apt_config_t& cfg) {
+  const uint64_t limit = (uint64_t)1 << 32;
+  int8::Plan pl[2];
+  const int n = int8::make_plans(M, N, K, cfg, pl);
+  for (int i = 0; i < n; ++i)
+    if (pl[i].partial_bytes >= limit) return false;
+  return apt_packed_bytes(N, K, p) < limit && int8::a_frag_bytes(M, K) < limit;
 }
 
-}  // namespace
-
-// Workspace: activation fragments, then (K-split tail) one int32 partial tile
-// and one flag per tail tile.
+// Workspace: activation fragments, then per launch (stream-K) one arrival
+// counter per stream-K tile, then per launch two int32 partial tiles per
+// workgroup.
 size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg) {
-  size_t bytes = align256(int8::a_frag_bytes(M, K));
-  if (cfg.k_split == 2) {
-    const size_t tt = tail_tiles(M, N, cfg);
-    bytes += align256(tt * (size_t)cfg.tail_bm * cfg.tail_bn * 4) + align256(tt * 4);
-  }
+  int8::Plan pl[2];
+  const int n = int8::make_plans(M, N, K, cfg, pl);
+  size_t bytes = int8::align256(int8::a_frag_bytes(M, K));
+  for (int i = 0; i < n; ++i)
+    bytes += int8::align256(pl[i].partial_bytes) + int8::align256(pl[i].counter_bytes);
   return bytes;
 }
 
 hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
                             hipStream_t stream) {
   using namespace int8;
-  const int shape = shape_index(cfg);
-  if (shape < 0) return hipErrorInvalidValue;
-  Int8Params prm;
-  prm.g = g;
-  prm.nchunks = num_chunks(g.K);
-  prm.nsteps = ((prm.nchunks + 1) & ~1) * kSteps;
-  prm.tiles_n = 0;
-  prm.n_begin = 0;
-  prm.mblocks = (g.M + 31) / 32;
-  prm.a_frag = static_cast<const v4i*>(workspace);
-  prm.ksplit = 1;
-  prm.partial = nullptr;
-  prm.flags = nullptr;
-  v4i* frag = static_cast<v4i*>(workspace);
-  int nflags = 0;
-  if (cfg.k_split == 2) {
-    uint8_t* base = static_cast<uint8_t*>(workspace) + align256(a_frag_bytes(g.M, g.K));
-    const size_t tt = tail_tiles(g.M, g.N, cfg);
-    prm.partial = reinterpret_cast<v4i*>(base);
-    prm.flags = reinterpret_cast<int*>(base + align256(tt * (size_t)cfg.tail_bm * cfg.tail_bn * 4));
-    nflags = (int)tt;
+  Plan pl[2];
+  const int nl = make_plans(g.M, g.N, g.K, cfg, pl);
+  Int8Params prm[2];
+  uint8_t* base = static_cast<uint8_t*>(workspace) + align256(a_frag_bytes(g.M, g.K));
+  int* counters = nullptr;
+  int ncounters = 0;
+  for (int i = 0; i < nl; ++i) {
+    Int8Params& p = prm[i];
+    p.g = g;
+    p.nchunks = num_chunks(g.K);
+    p.nsteps = ((p.nchunks + 1) & ~1) * kSteps;
+    p.mblocks = (g.M + 31) / 32;
+    p.a_frag = static_cast<const v4i*>(workspace);
+    p.a_bytes = (uint32_t)a_frag_bytes(g.M, g.K);
+    p.w_bytes = (uint32_t)apt_packed_bytes(g.N, g.K, g.p);
+    p.n_begin = pl[i].n_begin;
+    p.tiles_n = pl[i].tiles_n;
+    p.tiles = pl[i].tiles;
+    p.dp_tiles = pl[i].dp_tiles;
+    p.sk_pairs = pl[i].sk_pairs;
+    p.vec_out = g.N % 4 == 0 && (reinterpret_cast<uintptr_t>(g.c_int32) & 15) == 0 &&
+                (reinterpret_cast<uintptr_t>(g.c_fp16) & 7) == 0;
+    p.partial_bytes = (uint32_t)pl[i].partial_bytes;
   }
+  // Counters of all launches first (one clearing pass), then partial tiles.
+  counters = reinterpret_cast<int*>(base);
+  for (int i = 0; i < nl; ++i) {
+    prm[i].counters = reinterpret_cast<int*>(base);
+    base += align256(pl[i].counter_bytes);
+  }
+  ncounters = (int)(reinterpret_cast<int*>(base) - counters);
+  for (int i = 0; i < nl; ++i) {
+    prm[i].partial = reinterpret_cast<v4i*>(base);
+    base += align256(pl[i].partial_bytes);
+  }
+  v4i* frag = static_cast<v4i*>(workspace);
+  const Int8Params& p0 = prm[0];
   hipError_t e = hipErrorInvalidValue;
   switch (g.q) {
-    case 1: e = launch_expand_for_q<1>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 2: e = launch_expand_for_q<2>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 3: e = launch_expand_for_q<3>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 4: e = launch_expand_for_q<4>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 5: e = launch_expand_for_q<5>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 6: e = launch_expand_for_q<6>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 7: e = launch_expand_for_q<7>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
-    case 8: e = launch_expand_for_q<8>(g.a_packed, g.M, prm.nchunks, prm.nsteps, prm.mblocks, frag, prm.flags, nflags, stream); break;
+    case 1: e = launch_expand_for_q<1>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 2: e = launch_expand_for_q<2>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 3: e = launch_expand_for_q<3>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 4: e = launch_expand_for_q<4>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 5: e = launch_expand_for_q<5>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 6: e = launch_expand_for_q<6>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 7: e = launch_expand_for_q<7>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 8: e = launch_expand_for_q<8>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
   }
-  if (e != hipSuccess) return e;
-  prm.n_begin = 0;
-  if (cfg.split_n == 0) return launch_p(g.p, shape, prm, g.N, stream);
-  e = launch_p(g.p, shape, prm, cfg.split_n, stream);
-  if (e != hipSuccess) return e;
-  prm.n_begin = cfg.split_n;
-  prm.ksplit = cfg.k_split == 2 ? 2 : 1;
-  return launch_p(g.p, tail_index(cfg), prm, g.N - cfg.split_n, stream);
+  for (int i = 0; i < nl && e == hipSuccess; ++i) e = launch_p(g.p, pl[i].shape, prm[i], pl[i].grid, stream);
+  return e;
 }
 
 }  // namespace apt

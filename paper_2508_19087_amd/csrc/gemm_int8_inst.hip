@@ -8,18 +8,19 @@ namespace apt {
 namespace int8 {
 
 template <int P>
-hipError_t launch_for_p(int shape, const Int8Params& prm, int n_count, hipStream_t stream) {
-  return launch_p_shape<P>(shape, prm, n_count, stream);
+hipError_t launch_for_p(int shape, const Int8Params& prm, int grid, hipStream_t stream) {
+  return launch_p_shape<P>(shape, prm, grid, stream);
 }
 
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
-                               int mblocks, v4i* out, int* flags, int nflags, hipStream_t stream) {
+                               int mblocks, v4i* out, int* counters, int ncounters,
+                               hipStream_t stream) {
   int64_t threads = (int64_t)mblocks * 32 * (nsteps / kSteps);
-  if (threads < nflags) threads = nflags;
+  if (threads < ncounters) threads = ncounters;
   const int blocks = (int)((threads + 255) / 256);
   hipLaunchKernelGGL(expand_a_kernel<Q>, dim3(blocks), dim3(256), 0, stream, a_packed, M, nchunks,
-                     nsteps, mblocks, out, flags, nflags);
+                     nsteps, mblocks, out, counters, ncounters);
   return hipGetLastError();
 }
 

@@ -25,17 +25,24 @@
 
 namespace apt {
 
+// (a & mask) | (b & ~mask) as one v_bfi_b32.  Written as an instruction so
+// that the compiler keeps one select per merge instead of distributing the
+// masks over the tree, which costs about twice the instructions.
 __device__ __forceinline__ uint32_t bsel(uint32_t mask, uint32_t a, uint32_t b) {
-  return (a & mask) | (b & ~mask);
+  uint32_t r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "s"(mask), "v"(a), "v"(b));
+  return r;
 }
 
-// Bytes of the unsigned b-bit words u (B <= 7), or of u XOR 0x80 = the signed
-// code (B == 8), for the 32 elements of plane words pw[0..B-1].
+// The tree in two halves, so that a caller can spread one word's work over
+// two scheduling slots: reassemble_lo builds the level-1/2 merges (kept in
+// mid[]) and output dwords 0..3, reassemble_hi output dwords 4..7 from mid[].
 template <int B>
-__device__ __forceinline__ void reassemble_word(const uint32_t* pw, uint32_t out[8]) {
+__device__ __forceinline__ void reassemble_lo(const uint32_t* pw, uint32_t mid[8], uint32_t out[4]) {
   if (B == 1) {
+    mid[0] = pw[0];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) out[t] = (pw[0] >> t) & 0x01010101u;
+    for (int t = 0; t < 4; ++t) out[t] = (pw[0] >> t) & 0x01010101u;
     return;
   }
   auto PL = [&](int i) -> uint32_t { return i < B ? pw[i] : 0u; };
@@ -45,29 +52,56 @@ __device__ __forceinline__ void reassemble_word(const uint32_t* pw, uint32_t out
   uint32_t e23 = bsel(m1, PL(2), PL(3) << 1), o23 = bsel(m1, PL(2) >> 1, PL(3));
   // level 2: nibbles; ee: elements 4f, eo: 4f+2, oe: 4f+1, oo: 4f+3
   const uint32_t m2 = 0x33333333u;
-  uint32_t ee = bsel(m2, e01, e23 << 2), eo = bsel(m2, e01 >> 2, e23);
-  uint32_t oe = bsel(m2, o01, o23 << 2), oo = bsel(m2, o01 >> 2, o23);
+  mid[0] = bsel(m2, e01, e23 << 2);  // ee
+  mid[1] = bsel(m2, o01, o23 << 2);  // oe
+  mid[2] = bsel(m2, e01 >> 2, e23);  // eo
+  mid[3] = bsel(m2, o01 >> 2, o23);  // oo
   const uint32_t m3 = 0x0F0F0F0Fu;
   if (B <= 4) {
     // level 3: nibble 2j -> byte j (element 8j + s), nibble 2j+1 -> element 8j + 4 + s
-    out[0] = ee & m3;         out[4] = (ee >> 4) & m3;
-    out[1] = oe & m3;         out[5] = (oe >> 4) & m3;
-    out[2] = eo & m3;         out[6] = (eo >> 4) & m3;
-    out[3] = oo & m3;         out[7] = (oo >> 4) & m3;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) out[t] = mid[t] & m3;
   } else {
     uint32_t e45 = bsel(m1, PL(4), PL(5) << 1), o45 = bsel(m1, PL(4) >> 1, PL(5));
     uint32_t e67 = bsel(m1, PL(6), PL(7) << 1), o67 = bsel(m1, PL(6) >> 1, PL(7));
-    uint32_t ee2 = bsel(m2, e45, e67 << 2), eo2 = bsel(m2, e45 >> 2, e67);
-    uint32_t oe2 = bsel(m2, o45, o67 << 2), oo2 = bsel(m2, o45 >> 2, o67);
-    out[0] = bsel(m3, ee, ee2 << 4);  out[4] = bsel(m3, ee >> 4, ee2);
-    out[1] = bsel(m3, oe, oe2 << 4);  out[5] = bsel(m3, oe >> 4, oe2);
-    out[2] = bsel(m3, eo, eo2 << 4);  out[6] = bsel(m3, eo >> 4, eo2);
-    out[3] = bsel(m3, oo, oo2 << 4);  out[7] = bsel(m3, oo >> 4, oo2);
-    if (B == 8) {
+    mid[4] = bsel(m2, e45, e67 << 2);
+    mid[5] = bsel(m2, o45, o67 << 2);
+    mid[6] = bsel(m2, e45 >> 2, e67);
+    mid[7] = bsel(m2, o45 >> 2, o67);
 #pragma unroll
-      for (int t = 0; t < 8; ++t) out[t] ^= 0x80808080u;
+    for (int t = 0; t < 4; ++t) {
+      out[t] = bsel(m3, mid[t], mid[4 + t] << 4);
+      if (B == 8) out[t] ^= 0x80808080u;
     }
   }
+}
+
+template <int B>
+__device__ __forceinline__ void reassemble_hi(const uint32_t mid[8], uint32_t out[4]) {
+  if (B == 1) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) out[t] = (mid[0] >> (4 + t)) & 0x01010101u;
+    return;
+  }
+  const uint32_t m3 = 0x0F0F0F0Fu;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    if (B <= 4) {
+      out[t] = (mid[t] >> 4) & m3;
+    } else {
+      out[t] = bsel(m3, mid[t] >> 4, mid[4 + t]);
+      if (B == 8) out[t] ^= 0x80808080u;
+    }
+  }
+}
+
+// Bytes of the unsigned b-bit words u (B <= 7), or of u XOR 0x80 = the signed
+// code (B == 8), for the 32 elements of plane words pw[0..B-1].
+template <int B>
+__device__ __forceinline__ void reassemble_word(const uint32_t* pw, uint32_t out[8]) {
+  uint32_t mid[8];
+  reassemble_lo<B>(pw, mid, out);
+  reassemble_hi<B>(mid, out + 4);
 }
 
 // Operand offset of the reassembled byte y: bipolar value v = 2 y + c.

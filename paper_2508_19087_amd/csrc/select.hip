@@ -7,56 +7,84 @@
 // library is built with.  Decode-sized M takes the XOR + popcount route, which
 // streams the weight planes once; larger M takes the reassembled int8 MFMA
 // route, with the tile shape chosen by a model of how many rounds of tiles the
-// 256 compute units run and how fast each tile shape runs.  A choice never
-// changes results.
+// compute units run, how fast each tile shape runs and what the stream-K
+// partial tiles cost.  A choice never changes results.
+#include <algorithm>
+
 #include "apt_internal.h"
 
 namespace apt {
 namespace {
 
-constexpr int kComputeUnits = 256;
-
 struct Int8Shape {
   int bm, bn, wm, wn;
-  int per_cu;        // workgroups resident per compute unit (LDS-limited)
-  double rel_speed;  // throughput of one resident tile set relative to 256x256
+  int per_cu;           // workgroups resident per compute unit (LDS-limited)
+  double pair_cycles;   // cycles per chunk pair of one workgroup, compute unit full
 };
 
+// Measured on MI355X for K = 4096 tiles (kernel clock about 1.9 GHz).
 constexpr Int8Shape kInt8Shapes[] = {
-    {256, 256, 4, 2, 1, 1.00},
-    {256, 128, 4, 2, 1, 0.80},
-    {128, 128, 2, 2, 3, 0.40},
+    {256, 256, 4, 2, 1, 5200.0},
+    {256, 128, 4, 2, 1, 3000.0},
+    {128, 128, 2, 2, 2, 3000.0},
 };
+constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
+constexpr double kPartialBytesPerCycle = 2500.0;  // device-wide partial-tile traffic rate
+constexpr double kTileFixedCycles = 4000.0;      // start-up and final epilogue of a workgroup
+
+int compute_units() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
+}
 
 apt_config_t base_config(int route) {
   apt_config_t c;
   c.route = route;
   c.bm = c.bn = c.bk = 0;
   c.waves_m = c.waves_n = 0;
-  c.k_split = 0;
+  c.grid = 0;
   c.lds_stages = 0;
   c.mt = 0;
-  c.split_n = c.tail_bm = c.tail_bn = 0;
+  c.split_n = c.tail_bm = c.tail_bn = c.tail_grid = 0;
+  c.reserved[0] = c.reserved[1] = c.reserved[2] = 0;
   return c;
 }
 
-// Model time of covering n_cols output columns with shape s: rounds of
-// resident tiles x work per tile / tile speed (arbitrary units).
-double model_time(const Int8Shape& s, int M, int n_cols) {
-  const long tiles = (long)((M + s.bm - 1) / s.bm) * ((n_cols + s.bn - 1) / s.bn);
-  const long slots = (long)kComputeUnits * s.per_cu;
-  const long rounds = (tiles + slots - 1) / slots;
-  return (double)rounds * s.bm * s.bn * s.per_cu / s.rel_speed;
+// Modelled cycles of shape s with `grid` workgroups (0 = one per tile).
+double model_cycles(const Int8Shape& s, int M, int N, int K, int grid, int cus) {
+  const int64_t tiles = (int64_t)((M + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
+  const int64_t pairs = (((K + kChunk - 1) / kChunk) + 1) / 2;
+  const int64_t slots = (int64_t)cus * s.per_cu;
+  if (grid == 0) {  // one workgroup per tile, in rounds of `slots`
+    const int64_t rounds = (tiles + slots - 1) / slots;
+    return (double)rounds * (pairs * s.pair_cycles + kTileFixedCycles);
+  }
+  const int64_t g = std::min<int64_t>(grid, tiles * pairs);
+  const int64_t dp = tiles / g, sk_tiles = tiles - dp * g;
+  const int64_t sk_pairs = sk_tiles * pairs;
+  const int64_t per_wg = dp * pairs + (sk_pairs + g - 1) / g;
+  const int64_t rounds = (g + slots - 1) / slots;
+  double cycles = (double)rounds * (per_wg * s.pair_cycles + kTileFixedCycles);
+  if (sk_tiles > 0) {
+    // every shared tile: about (parts - 1) partials written and read back
+    const double parts = std::min<double>((double)g, (double)pairs * g / (double)sk_pairs + 1.0);
+    const double bytes = 2.0 * sk_tiles * (parts - 1.0) * s.bm * s.bn * 4.0;
+    cycles += bytes / kPartialBytesPerCycle;
+  }
+  return cycles;
 }
-
-constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
-constexpr int kTailShape = kNumInt8Shapes - 1;  // the smallest tile
-constexpr double kLaunchCost = 2.0e4;           // a second launch, in model units
 
 }  // namespace
 
 apt_config_t select_config(int M, int N, int K, int p, int q) {
-  (void)K;
   (void)p;
   (void)q;
   if (M <= 8) {
@@ -64,31 +92,40 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
     c.mt = 8;
     return c;
   }
-  // Candidates: every shape alone, and every shape on the columns that fill
-  // whole rounds with the smallest shape on the rest.
+  const int cus = compute_units();
+  // Candidates: each shape alone, with one workgroup per tile or a full
+  // persistent grid; and the first shape over the columns that fill whole
+  // rounds of its tiles with each smaller shape (one workgroup per tile) on
+  // the remaining columns.
   double best = 0.0;
-  int best_i = -1, best_split = 0;
-  for (int i = 0; i < kNumInt8Shapes; ++i) {
-    const Int8Shape& s = kInt8Shapes[i];
-    const double t = model_time(s, M, N);
+  int best_i = -1, best_grid = 0, best_split = 0, best_tail = -1;
+  auto consider = [&](double t, int i, int grid, int split, int tail) {
     if (best_i < 0 || t < best) {
       best = t;
       best_i = i;
-      best_split = 0;
-    }
-    const int tiles_m = (M + s.bm - 1) / s.bm;
-    const int cols_per_round = kComputeUnits * s.per_cu / tiles_m;
-    const int tiles_n = (N + s.bn - 1) / s.bn;
-    if (i == kTailShape || cols_per_round < 1) continue;
-    const int full = tiles_n / cols_per_round * cols_per_round;
-    if (full < 1 || full * s.bn >= N) continue;
-    const int split = full * s.bn;
-    const double ts = model_time(s, M, split) + model_time(kInt8Shapes[kTailShape], M, N - split) +
-                      kLaunchCost;
-    if (ts < best) {
-      best = ts;
-      best_i = i;
+      best_grid = grid;
       best_split = split;
+      best_tail = tail;
+    }
+  };
+  for (int i = 0; i < kNumInt8Shapes; ++i) {
+    const Int8Shape& s = kInt8Shapes[i];
+    consider(model_cycles(s, M, N, K, 0, cus), i, 0, 0, -1);
+    consider(model_cycles(s, M, N, K, std::min(cus * s.per_cu, kMaxGrid), cus), i,
+             std::min(cus * s.per_cu, kMaxGrid), 0, -1);
+  }
+  {
+    const Int8Shape& s = kInt8Shapes[0];
+    const int tiles_m = (M + s.bm - 1) / s.bm;
+    const int cols_per_round = cus * s.per_cu / tiles_m;
+    const int tiles_n = (N + s.bn - 1) / s.bn;
+    if (cols_per_round >= 1 && tiles_n > cols_per_round) {
+      const int split = tiles_n / cols_per_round * cols_per_round * s.bn;
+      if (split < N)
+        for (int t = 1; t < kNumInt8Shapes; ++t)
+          consider(model_cycles(s, M, split, K, 0, cus) +
+                       model_cycles(kInt8Shapes[t], M, N - split, K, 0, cus),
+                   0, 0, split, t);
     }
   }
   const Int8Shape& s = kInt8Shapes[best_i];
@@ -98,11 +135,13 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
   c.bk = kChunk;
   c.waves_m = s.wm;
   c.waves_n = s.wn;
-  c.lds_stages = 2;
+  c.lds_stages = 3;
+  c.grid = best_grid;
   if (best_split > 0) {
     c.split_n = best_split;
-    c.tail_bm = kInt8Shapes[kTailShape].bm;
-    c.tail_bn = kInt8Shapes[kTailShape].bn;
+    c.tail_bm = kInt8Shapes[best_tail].bm;
+    c.tail_bn = kInt8Shapes[best_tail].bn;
+    c.tail_grid = 0;
   }
   return c;
 }

@@ -7,26 +7,27 @@ import numpy as np
 import paper_2508_19087_amd as apt
 from oracle import oracle as ref
 
-INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 256, 2, 2), (256, 128, 4, 2), (128, 128, 2, 2)]
+INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 128, 4, 2), (128, 128, 2, 2)]
 
 
 def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
-    """(name, config) of every route/shape the library can be forced to; with N,
-    also the split launches (main tiles, then 128x128 tail tiles), and with K
-    above 256 the K-split tail (256x256 tail tiles, two workgroups each)."""
+    """(name, config) of every route and tile shape the library can be forced
+    to; the int8 shapes with one workgroup per tile (grid 0) and with
+    persistent stream-K grids: 256 workgroups, 7 (many workgroups share each
+    tile) and 300; with N, also split launches (main tiles, then 128x128 tail
+    tiles, one per workgroup and stream-K)."""
+    del K
     out = [("xor", apt.apt_config_t.make(apt.APT_ROUTE_XOR))]
     for bm, bn, wm, wn in INT8_SHAPES:
-        c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 2)
-        out.append(("int8_%dx%d_w%dx%d" % (bm, bn, wm, wn), c))
+        for grid in (0, 256, 7, 300):
+            c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, grid, 3)
+            out.append(("int8_%dx%d_w%dx%d_g%d" % (bm, bn, wm, wn, grid), c))
         split = (N - 1) // bn * bn
         if N and split >= bn:
-            c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 2, 0, split,
-                                      128, 128)
-            out.append(("int8_%dx%d_w%dx%d_tail@%d" % (bm, bn, wm, wn, split), c))
-            if K > 256 and (wm, wn) in ((4, 2), (2, 2)):
-                c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 2, 2, 0,
-                                          split, 256, 256)
-                out.append(("int8_%dx%d_w%dx%d_ksplit_tail@%d" % (bm, bn, wm, wn, split), c))
+            for tg in (0, 5):
+                c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 3, 0, split,
+                                          128, 128, tg)
+                out.append(("int8_%dx%d_w%dx%d_tail@%d_g%d" % (bm, bn, wm, wn, split, tg), c))
     if p <= 7 and q <= 7:
         out.append(("pm1", apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)))
     return out

@@ -47,21 +47,37 @@ def _shapes():
 
 
 def _int8_workspace(M, N, K, c):
-    """Activation fragments, then (K-split tail) int32 partial tiles and flags,
-    each region rounded up to 256 bytes."""
+    """Activation fragments, then (stream-K) per launch one counter per shared
+    tile and two int32 partial tiles per workgroup, each region rounded up to
+    256 bytes."""
     up = lambda x: (x + 255) // 256 * 256
     nce = ((K + 127) // 128 + 1) // 2 * 2
     ws = up((M + 31) // 32 * 32 * nce * 128)
-    if c.k_split == 2:
-        tiles = -(-M // c.tail_bm) * -(-(N - c.split_n) // c.tail_bn)
-        ws += up(tiles * c.tail_bm * c.tail_bn * 4) + up(tiles * 4)
+    launches = [(c.bm, c.bn, N, c.grid)]
+    if c.split_n:
+        launches = [(c.bm, c.bn, c.split_n, c.grid), (c.tail_bm, c.tail_bn, N - c.split_n, c.tail_grid)]
+    for bm, bn, cols, g in launches:
+        tiles = -(-M // bm) * -(-cols // bn)
+        grid = tiles if g == 0 else min(g, tiles * nce // 2)
+        sk_tiles = tiles - tiles // grid * grid
+        if sk_tiles:
+            ws += up(2 * grid * bm * bn * 4) + up(sk_tiles * 4)
     return ws
 
 
-def test_workspace_k_split_tail():
-    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 2, 2, 0, 8192, 256, 256)
+def test_workspace_stream_k():
+    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 256, 3)
     ws = apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c)
-    assert ws == 2048 * 4096 + 88 * 256 * 256 * 4 + 512
+    assert ws == 2048 * 4096 + 512 * 256 * 256 * 4 + 512  # 344 tiles: 88 shared
+    assert ws == _int8_workspace(2048, 11008, 4096, c)
+    c.grid = 0  # one workgroup per tile: fragments only
+    assert apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c) == 2048 * 4096
+    c.grid = 344  # divides the tile count: no stream-K part
+    assert apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c) == 2048 * 4096
+    # a tail launch over [8192, 11008) with 128x128 tiles on 256 workgroups
+    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 0, 3, 0, 8192, 128, 128, 256)
+    ws = apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c)
+    assert ws == 2048 * 4096 + 512 * 128 * 128 * 4 + 512  # 352 tail tiles: 96 shared
     assert ws == _int8_workspace(2048, 11008, 4096, c)
 
 
@@ -116,7 +132,6 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ra=None),
      apt.APT_ERR_INVALID_ARG),
     (dict(p=8, cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)), apt.APT_ERR_UNSUPPORTED),
-    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, k_split=2)), apt.APT_ERR_UNSUPPORTED),
     (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=3)), apt.APT_ERR_INVALID_ARG),
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_WORKSPACE),
@@ -124,23 +139,30 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
           ws_bytes=64 * 256 - 1), apt.APT_ERR_WORKSPACE),
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ws=WS + 8,
           ws_bytes=1 << 20), apt.APT_ERR_INVALID_ARG),
-    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
-                                                 100, 128, 128)), apt.APT_ERR_INVALID_ARG),
-    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
-                                                 256, 96, 128)), apt.APT_ERR_INVALID_ARG),
-    (dict(M=64, N=256, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2, 0,
-                                                 256, 128, 128)), apt.APT_ERR_INVALID_ARG),
-    # K split: only with a tail, only for K > 256, only 2, only on the int8 route
+    # persistent grid: 0..4096 workgroups
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, -1, 3)),
+     apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 4097, 3)),
+     apt.APT_ERR_INVALID_ARG),
     (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
-                                                         2, 2)), apt.APT_ERR_INVALID_ARG),
-    (dict(M=64, N=512, K=256, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
-                                                        2, 2, 0, 256, 256, 256)), apt.APT_ERR_INVALID_ARG),
-    (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
-                                                         3, 2, 0, 256, 256, 256)), apt.APT_ERR_INVALID_ARG),
-    (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
-                                                         2, 2, 0, 256, 256, 256), ws=WS,
+                                                         3, 3), ws=WS,
           ws_bytes=64 * 1024), apt.APT_ERR_WORKSPACE),
-    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA, k_split=2)), apt.APT_ERR_UNSUPPORTED),
+    # tail launch: split_n a multiple of bn inside (0, N), a configured tail tile
+    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 3, 0,
+                                                 100, 128, 128)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 3, 0,
+                                                 256, 96, 128)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=256, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 3, 0,
+                                                 256, 128, 128)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 3, 0,
+                                                 256, 128, 128, -2)), apt.APT_ERR_INVALID_ARG),
+    # the int8 weight ring is 3 deep
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2)),
+     apt.APT_ERR_INVALID_ARG),
+    # packed weights past 4 GiB do not fit the int8 kernels' 32-bit offsets
+    (dict(M=64, N=1 << 20, K=1 << 16, p=1, q=1,
+          cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
 ])
 def test_gemm_validation(kw, want):
     assert gemm(**kw) == want
@@ -158,4 +180,4 @@ def test_pack_validation(kw):
 
 
 def test_config_struct_layout():
-    assert ctypes.sizeof(apt.apt_config_t) == 12 * 4
+    assert ctypes.sizeof(apt.apt_config_t) == 16 * 4
