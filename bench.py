@@ -33,8 +33,9 @@ PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, 8 TB/s
 MALL_BYTES = 256 << 20      # Infinity Cache; cold-weight runs rotate through > 2x this
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2508_19087_amd/csrc/gemm_int8.h", "paper_2508_19087_amd/csrc/reassemble.h",
-                  "paper_2508_19087_amd/csrc/gemm_xor.h", "paper_2508_19087_amd/csrc/select.hip"]
+KERNEL_SOURCES = ["paper_2508_19087_amd/csrc/gemm_int8.h", "paper_2508_19087_amd/csrc/gemm_int8.hip",
+                  "paper_2508_19087_amd/csrc/gemm_int8_inst.hip", "paper_2508_19087_amd/csrc/reassemble.h",
+                  "paper_2508_19087_amd/csrc/select.hip"]
 
 
 def kernel_hash() -> str:
@@ -228,6 +229,67 @@ def cpu_baseline(target_s: float = 12.0):
                        "%.3g effective ops" % (rows - 1, ops))}
 
 
+COPY_BYTES = 256 << 20  # calibration copy for the HBM byte counters
+TRAFFIC_JSON = "gemm_int8_w4a4_2048x11008x4096_traffic.json"
+
+
+def counters_run(reps: int = 3):
+    """For rocprofv3 --pmc: the prefill GEMM `reps` times after one warm-up
+    call, then a plain device copy of COPY_BYTES (read and written once),
+    whose counter readings calibrate the byte counters."""
+    import torch
+    wl = Workload()
+    it = wl.items[2]
+    wl.pack_act(it)
+    for _ in range(reps + 1):
+        wl.gemm(it)
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log("bench: counters run done (%d prefill GEMMs, copy of %d bytes)" % (reps + 1, COPY_BYTES))
+
+
+def write_traffic(fetch_dir: str, write_dir: str, commands: str):
+    """HBM bytes per prefill apt_gemm call from two rocprofv3 --pmc runs of
+    counters_run (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch): the GEMM's
+    kernels summed per call, each counter scaled by what it reads for the
+    calibration copy (COPY_BYTES in each direction)."""
+    import csv
+    import glob
+    import statistics
+
+    def per_kernel(d, counter):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        vals = {}
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
+        return vals
+
+    out = {"kernel_hash": kernel_hash(), "commands": commands}
+    for tag, d, counter in [("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")]:
+        vals = per_kernel(d, counter)
+        copy = [v for k, vs in vals.items() if "copyBuffer" in k for v in vs if v > COPY_BYTES / 4]
+        factor = COPY_BYTES / statistics.median(copy)
+        # the GEMM's kernels: every dispatch after the warm-up call
+        gemm = {k: vs for k, vs in vals.items() if "expand_a_kernel" in k or "gemm_int8_kernel" in k}
+        per_call = 0.0
+        kernels = {}
+        for k, vs in gemm.items():
+            med = statistics.median(vs[1:] if len(vs) > 1 else vs)
+            kernels[k] = round(med * factor)
+            per_call += med * factor
+        out[tag] = {"counter": counter, "calibration_factor": round(factor, 4),
+                    "bytes_per_call": round(per_call), "kernels": kernels}
+    out["traffic_bytes_per_launch"] = out["fetch"]["bytes_per_call"] + out["write"]["bytes_per_call"]
+    path = os.path.join(PROFILES, TRAFFIC_JSON)
+    json.dump(out, open(path, "w"), indent=1)
+    print(json.dumps(out, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -236,7 +298,16 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode-cold", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--counters-run", action="store_true",
+                    help="run the prefill GEMM and a calibration copy for rocprofv3 --pmc, then exit")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarize two rocprofv3 --pmc runs of --counters-run into profiles/")
+    ap.add_argument("--traffic-commands", default="",
+                    help="the commands that produced the --write-traffic directories")
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(args.write_traffic[0], args.write_traffic[1], args.traffic_commands)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(no sharding or collectives); use --gpus 1", file=sys.stderr)
@@ -245,6 +316,9 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.counters_run:
+        counters_run()
+        return
     log("bench: building workload")
     wl = Workload()
     for _ in range(args.warmup):

@@ -107,41 +107,36 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
                                                        int nchunks, int nsteps, int mblocks,
                                                        v4i* __restrict__ out, int* __restrict__ counters,
                                                        int ncounters) {
+  // One thread per (word w, row, chunk), w fastest: 4 threads read one row's
+  // 16 contiguous bytes of a plane, so a wave reads whole 128-byte lines.
   const int rows = mblocks * 32;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   // The stream-K arrival counters of this call start cleared (the GEMM
   // launch follows in stream order).
   if (t < ncounters) counters[t] = 0;
-  if (t >= (int64_t)rows * (nsteps / kSteps)) return;
-  const int row = (int)(t % rows);
-  const int chunk = (int)(t / rows);
-  uint32_t pw[kWordsPerPlane][Q];
+  if (t >= (int64_t)rows * (nsteps / kSteps) * kWordsPerPlane) return;
+  const int w = (int)(t % kWordsPerPlane);
+  const int64_t rc = t / kWordsPerPlane;
+  const int row = (int)(rc % rows);
+  const int chunk = (int)(rc / rows);
+  uint32_t pw[Q];
   if (row < M && chunk < nchunks) {
-    const uint32_t* src = a_packed + plane_words(row, chunk, 0, nchunks, Q);
+    const uint32_t* src = a_packed + plane_words(row, chunk, 0, nchunks, Q) + w;
 #pragma unroll
-    for (int j = 0; j < Q; ++j) {
-      uint4 v = *reinterpret_cast<const uint4*>(src + j * kPlaneStride);
-      pw[0][j] = v.x; pw[1][j] = v.y; pw[2][j] = v.z; pw[3][j] = v.w;
-    }
+    for (int j = 0; j < Q; ++j) pw[j] = src[j * kPlaneStride];
   } else {
 #pragma unroll
-    for (int w = 0; w < kWordsPerPlane; ++w)
-#pragma unroll
-      for (int j = 0; j < Q; ++j) pw[w][j] = 0u;
+    for (int j = 0; j < Q; ++j) pw[j] = 0u;
   }
+  uint32_t o[8];
+  reassemble_word<Q>(pw, o);
+  if (chunk >= nchunks)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = 0u;
   const int mb = row / 32, l = row % 32;
-  const bool phantom = chunk >= nchunks;
-#pragma unroll
-  for (int w = 0; w < kWordsPerPlane; ++w) {
-    uint32_t o[8];
-    reassemble_word<Q>(pw[w], o);
-    if (phantom)
-#pragma unroll
-      for (int t = 0; t < 8; ++t) o[t] = 0u;
-    v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w) * kFragVecs;
-    f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
-    f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
-  }
+  v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w) * kFragVecs;
+  f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+  f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
 }
 
 // ---- weight staging -----------------------------------------------------------

@@ -16,7 +16,7 @@ template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
                                int mblocks, v4i* out, int* counters, int ncounters,
                                hipStream_t stream) {
-  int64_t threads = (int64_t)mblocks * 32 * (nsteps / kSteps);
+  int64_t threads = (int64_t)mblocks * 32 * (nsteps / kSteps) * kWordsPerPlane;
   if (threads < ncounters) threads = ncounters;
   const int blocks = (int)((threads + 255) / 256);
   hipLaunchKernelGGL(expand_a_kernel<Q>, dim3(blocks), dim3(256), 0, stream, a_packed, M, nchunks,
