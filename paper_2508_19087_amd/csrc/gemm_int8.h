@@ -454,23 +454,34 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
   // chunks before the tile's flush and written to LDS before that pair's
   // last barrier (the loads are issued before any output store, so waiting
   // for them never waits for stores).
-  uint32_t term = 0;
-  float scale = 0.f;
+  constexpr int kTermsPerThread = (BN + BM + T - 1) / T;
+  uint32_t term[kTermsPerThread];
+  float scale[kTermsPerThread];
   auto fetch_terms = [&](int m0, int n0) __attribute__((always_inline)) {
-    if (tid < BN) {
-      const int n = min(n0 + tid, g.N - 1);
-      term = ca * (uint32_t)g.w_rowsum[n];
-      if (fp16) scale = __half2float(g.w_scale[n]);
-    } else if (tid < BN + BM) {
-      const int m = min(m0 + tid - BN, g.M - 1);
-      term = cw * (uint32_t)g.a_rowsum[m] - const_term;
-      if (fp16) scale = __half2float(g.a_scale[m]);
+#pragma unroll
+    for (int k = 0; k < kTermsPerThread; ++k) {
+      const int i = tid + k * T;
+      term[k] = 0;
+      scale[k] = 0.f;
+      if (i < BN) {
+        const int n = min(n0 + i, g.N - 1);
+        term[k] = ca * (uint32_t)g.w_rowsum[n];
+        if (fp16) scale[k] = __half2float(g.w_scale[n]);
+      } else if (i < BN + BM) {
+        const int m = min(m0 + i - BN, g.M - 1);
+        term[k] = cw * (uint32_t)g.a_rowsum[m] - const_term;
+        if (fp16) scale[k] = __half2float(g.a_scale[m]);
+      }
     }
   };
   auto stage_terms = [&]() __attribute__((always_inline)) {
-    if (tid < BN + BM) {
-      lds_wt[tid] = term;  // lds_at follows lds_wt
-      lds_ws[tid] = scale;
+#pragma unroll
+    for (int k = 0; k < kTermsPerThread; ++k) {
+      const int i = tid + k * T;
+      if (i < BN + BM) {
+        lds_wt[i] = term[k];  // lds_at follows lds_wt
+        lds_ws[i] = scale[k];
+      }
     }
   };
 

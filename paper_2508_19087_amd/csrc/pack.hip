@@ -28,10 +28,11 @@ __device__ __forceinline__ uint32_t gather_plane_nibble(uint32_t x, int i) {
   return (t * 0x01020408u) >> 24;
 }
 
-template <bool kVector>
+template <bool kVector, int B>
 __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
-    const int8_t* __restrict__ codes, int rows, int K, int bits, int nchunks,
+    const int8_t* __restrict__ codes, int rows, int K, int nchunks,
     uint32_t* __restrict__ packed, int32_t* __restrict__ rowsum) {
+  constexpr int bits = B;
   const int lane = threadIdx.x % kWave;
   const int row = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;  // < padded row count
   const bool real = row < rows;
@@ -42,9 +43,9 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
   const int8_t* src = codes + (int64_t)min(row, rows - 1) * K;
   uint32_t usum = 0;
 
-  for (int base = 0; base < kpad; base += kCodesPerStep) {
+  auto load = [&](int base, uint32_t d[4]) {
     const int k0 = base + lane * kCodesPerLane;
-    uint32_t d[4] = {0u, 0u, 0u, 0u};
+    d[0] = d[1] = d[2] = d[3] = 0u;
     if (kVector) {
       // K % 16 == 0: the lane's 16 codes are all valid or all padding.
       if (real && k0 < K) {
@@ -59,6 +60,9 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
         d[t / 4] |= b << (8 * (t % 4));
       }
     }
+  };
+  auto process = [&](int base, const uint32_t d[4]) {
+    const int k0 = base + lane * kCodesPerLane;
     // Bipolar words, one per byte; padding codes and padding rows stay all-zero.
     uint32_t u[4];
 #pragma unroll
@@ -80,6 +84,7 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
     const int word = (k0 % kChunk) / 32;
     const bool upper_half = (lane & 1) != 0;  // codes 16..31 of the word
     const bool in_range = k0 < kpad;
+#pragma unroll
     for (int i = 0; i < bits; ++i) {
       uint32_t half = gather_plane_nibble(u[0], i) | (gather_plane_nibble(u[1], i) << 4) |
                       (gather_plane_nibble(u[2], i) << 8) | (gather_plane_nibble(u[3], i) << 12);
@@ -88,6 +93,23 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
         packed[plane_words(row, chunk, i, nchunks, bits) + word] = half | (other << 16);
       }
     }
+  };
+
+  // Four steps per trip: their loads are all in flight before the first is
+  // used.
+  constexpr int kGroup = 4;
+  int base = 0;
+  for (; base + kGroup * kCodesPerStep <= kpad; base += kGroup * kCodesPerStep) {
+    uint32_t d[kGroup][4];
+#pragma unroll
+    for (int s = 0; s < kGroup; ++s) load(base + s * kCodesPerStep, d[s]);
+#pragma unroll
+    for (int s = 0; s < kGroup; ++s) process(base + s * kCodesPerStep, d[s]);
+  }
+  for (; base < kpad; base += kCodesPerStep) {
+    uint32_t d[4];
+    load(base, d);
+    process(base, d);
   }
 
   if (rowsum != nullptr && real) {
@@ -100,21 +122,37 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
   }
 }
 
-}  // namespace
-
-hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t* packed,
-                       int32_t* rowsum, hipStream_t stream) {
+template <int B>
+hipError_t launch_pack_bits(const int8_t* codes, int rows, int K, uint32_t* packed, int32_t* rowsum,
+                            hipStream_t stream) {
   const int nchunks = num_chunks(K);
   dim3 block(kWave * kWavesPerBlock);
   dim3 grid(padded_rows(rows) / kWavesPerBlock);
   const bool vec = (K % 16 == 0) && ((reinterpret_cast<uintptr_t>(codes) & 15u) == 0);
   if (vec)
-    hipLaunchKernelGGL(pack_kernel<true>, grid, block, 0, stream, codes, rows, K, bits, nchunks,
+    hipLaunchKernelGGL((pack_kernel<true, B>), grid, block, 0, stream, codes, rows, K, nchunks,
                        packed, rowsum);
   else
-    hipLaunchKernelGGL(pack_kernel<false>, grid, block, 0, stream, codes, rows, K, bits, nchunks,
+    hipLaunchKernelGGL((pack_kernel<false, B>), grid, block, 0, stream, codes, rows, K, nchunks,
                        packed, rowsum);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t* packed,
+                       int32_t* rowsum, hipStream_t stream) {
+  switch (bits) {
+    case 1: return launch_pack_bits<1>(codes, rows, K, packed, rowsum, stream);
+    case 2: return launch_pack_bits<2>(codes, rows, K, packed, rowsum, stream);
+    case 3: return launch_pack_bits<3>(codes, rows, K, packed, rowsum, stream);
+    case 4: return launch_pack_bits<4>(codes, rows, K, packed, rowsum, stream);
+    case 5: return launch_pack_bits<5>(codes, rows, K, packed, rowsum, stream);
+    case 6: return launch_pack_bits<6>(codes, rows, K, packed, rowsum, stream);
+    case 7: return launch_pack_bits<7>(codes, rows, K, packed, rowsum, stream);
+    case 8: return launch_pack_bits<8>(codes, rows, K, packed, rowsum, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace apt
