@@ -36,6 +36,8 @@
 // host), so the wrapped result is exact.
 #pragma once
 
+#include <algorithm>
+
 #include "apt_internal.h"
 #include "reassemble.h"
 
@@ -322,14 +324,15 @@ struct Stream {
 // The MFMA takes the weight fragment as its first operand, so the accumulator
 // of lane l holds D[n][m] for m = l mod 32 and four consecutive n: each lane
 // stores 16 contiguous output bytes.
+// The whole work of workgroup w of G for one tile shape (the kernels below
+// call it; `lds` is the dynamic LDS of the launch).
 template <int P, int BM, int BN, int WM, int WN, int SPLIT>
-__global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm) {
+__device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* lds, int w, int G) {
   constexpr int T = WM * WN * kWave;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   constexpr int FM = WTM / 32, FN = WTN / 32;  // 32x32 fragments per wave
   constexpr int kStageBytes = BN * kRowBytes;
   static_assert(FM >= 1 && FN >= 1, "wave tile too small");
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   __shared__ int s_bcast;
 
   const GemmArgs& g = prm.g;
@@ -350,8 +353,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
   uint8_t* const epi_slot = lds + kStages * kStageBytes + (BN + BM) * 8 + wave * 32 * kEpiStride;
 
   Stream st;
-  st.G = gridDim.x;
-  st.w = blockIdx.x;
+  st.G = G;
+  st.w = w;
   st.pairs = NCE / 2;
   st.dp_tiles = prm.dp_tiles;
   st.sk_base = prm.dp_tiles * st.G;
@@ -689,6 +692,28 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
   }
 }
 
+template <int P, int BM, int BN, int WM, int WN, int SPLIT>
+__global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  gemm_int8_body<P, BM, BN, WM, WN, SPLIT>(prm, lds, blockIdx.x, gridDim.x);
+}
+
+// Two launches' work in one grid: workgroups [0, g0) do shape A over prm_a,
+// the rest shape B over prm_b (same wave count).  Workgroups are dispatched
+// in index order, so B's start on the compute units that A's release, while
+// A's last tiles and output stores are still in flight.
+template <int P, int BMA, int BNA, int WMA, int WNA, int SA, int BMB, int BNB, int WMB, int WNB,
+          int SB>
+__global__ __launch_bounds__(WMA* WNA* kWave) void gemm_int8_pair_kernel(Int8Params prm_a,
+                                                                         Int8Params prm_b, int g0) {
+  static_assert(WMA * WNA == WMB * WNB, "both shapes need the same workgroup size");
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  if ((int)blockIdx.x < g0)
+    gemm_int8_body<P, BMA, BNA, WMA, WNA, SA>(prm_a, lds, blockIdx.x, g0);
+  else
+    gemm_int8_body<P, BMB, BNB, WMB, WNB, SB>(prm_b, lds, blockIdx.x - g0, gridDim.x - g0);
+}
+
 struct TileShape {
   int bm, bn, wm, wn, split;
 };
@@ -732,10 +757,38 @@ inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int grid, hip
   return hipErrorInvalidValue;
 }
 
+// One launch of shapes SA (grid ga) then SB (grid gb), when they pair.
+template <int P, int SA, int SB>
+hipError_t launch_pair_shapes(const Int8Params& pa, int ga, const Int8Params& pb, int gb,
+                              hipStream_t stream) {
+  constexpr TileShape a = kShapes[SA], b = kShapes[SB];
+  const size_t lds = std::max(lds_bytes(a), lds_bytes(b));
+  auto kern = gemm_int8_pair_kernel<P, a.bm, a.bn, a.wm, a.wn, a.split, b.bm, b.bn, b.wm, b.wn,
+                                    b.split>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(ga + gb), dim3(a.wm * a.wn * kWave), lds, stream, pa, pb, ga);
+  return hipGetLastError();
+}
+
+// The shape pairs built as one launch: 256x256 then 256x128 (both 4x2 waves).
+inline bool pair_supported(int sa, int sb) { return sa == 0 && sb == 2; }
+
+template <int P>
+inline hipError_t launch_p_pair(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
+                                int gb, hipStream_t stream) {
+  if (sa == 0 && sb == 2) return launch_pair_shapes<P, 0, 2>(pa, ga, pb, gb, stream);
+  return hipErrorInvalidValue;
+}
+
 // Launches for weight bits P (main kernel) and activation bits Q (expansion);
 // the explicit instantiations live in gemm_int8_inst.hip, built once per width.
 template <int P>
 hipError_t launch_for_p(int shape, const Int8Params& prm, int grid, hipStream_t stream);
+template <int P>
+hipError_t launch_pair_for_p(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
+                             int gb, hipStream_t stream);
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
                                int mblocks, v4i* out, int* counters, int ncounters,

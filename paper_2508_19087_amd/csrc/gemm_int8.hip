@@ -33,6 +33,21 @@ hipError_t launch_p(int p, int shape, const Int8Params& prm, int grid, hipStream
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_pair(int p, int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
+                       int gb, hipStream_t stream) {
+  switch (p) {
+    case 1: return launch_pair_for_p<1>(sa, pa, ga, sb, pb, gb, stream);
+    case 2: return launch_pair_for_p<2>(sa, pa, ga, sb, pb, gb, stream);
+    case 3: return launch_pair_for_p<3>(sa, pa, ga, sb, pb, gb, stream);
+    case 4: return launch_pair_for_p<4>(sa, pa, ga, sb, pb, gb, stream);
+    case 5: return launch_pair_for_p<5>(sa, pa, ga, sb, pb, gb, stream);
+    case 6: return launch_pair_for_p<6>(sa, pa, ga, sb, pb, gb, stream);
+    case 7: return launch_pair_for_p<7>(sa, pa, ga, sb, pb, gb, stream);
+    case 8: return launch_pair_for_p<8>(sa, pa, ga, sb, pb, gb, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 // The work decomposition of one launch: shape `shape` over output columns
@@ -166,6 +181,9 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
     case 7: e = launch_expand_for_q<7>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
     case 8: e = launch_expand_for_q<8>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
   }
+  if (e != hipSuccess) return e;
+  if (nl == 2 && pair_supported(pl[0].shape, pl[1].shape))
+    return launch_pair(g.p, pl[0].shape, prm[0], pl[0].grid, pl[1].shape, prm[1], pl[1].grid, stream);
   for (int i = 0; i < nl && e == hipSuccess; ++i) e = launch_p(g.p, pl[i].shape, prm[i], pl[i].grid, stream);
   return e;
 }

@@ -12,6 +12,12 @@ hipError_t launch_for_p(int shape, const Int8Params& prm, int grid, hipStream_t 
   return launch_p_shape<P>(shape, prm, grid, stream);
 }
 
+template <int P>
+hipError_t launch_pair_for_p(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
+                             int gb, hipStream_t stream) {
+  return launch_p_pair<P>(sa, pa, ga, sb, pb, gb, stream);
+}
+
 template <int Q>
 hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
                                int mblocks, v4i* out, int* counters, int ncounters,
@@ -25,6 +31,8 @@ hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int
 }
 
 template hipError_t launch_for_p<APT_INST_P>(int, const Int8Params&, int, hipStream_t);
+template hipError_t launch_pair_for_p<APT_INST_P>(int, const Int8Params&, int, int,
+                                                   const Int8Params&, int, hipStream_t);
 template hipError_t launch_expand_for_q<APT_INST_P>(const uint32_t*, int, int, int, int, v4i*,
                                                      int*, int, hipStream_t);
 

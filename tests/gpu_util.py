@@ -24,10 +24,13 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
             out.append(("int8_%dx%d_w%dx%d_g%d" % (bm, bn, wm, wn, grid), c))
         split = (N - 1) // bn * bn
         if N and split >= bn:
-            for tg in (0, 5):
-                c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 3, 0, split,
-                                          128, 128, tg)
-                out.append(("int8_%dx%d_w%dx%d_tail@%d_g%d" % (bm, bn, wm, wn, split, tg), c))
+            tails = [(128, 128)] + ([(256, 128)] if (bm, bn, wm, wn) == (256, 256, 4, 2) else [])
+            for tbm, tbn in tails:  # 256x256 + 256x128 runs as one paired launch
+                for tg in (0, 5):
+                    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 3, 0,
+                                              split, tbm, tbn, tg)
+                    out.append(("int8_%dx%d_w%dx%d_tail%dx%d@%d_g%d" % (bm, bn, wm, wn, tbm, tbn, split,
+                                                                        tg), c))
     if p <= 7 and q <= 7:
         out.append(("pm1", apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)))
     return out
