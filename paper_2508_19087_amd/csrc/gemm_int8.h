@@ -722,6 +722,7 @@ constexpr TileShape kShapes[] = {
     {256, 256, 2, 4, 2},
     {256, 128, 4, 2, 4},
     {128, 128, 2, 2, 2},
+    {512, 128, 8, 1, 4},
 };
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
@@ -753,6 +754,7 @@ inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int grid, hip
     case 1: return launch_shape<P, 1>(prm, grid, stream);
     case 2: return launch_shape<P, 2>(prm, grid, stream);
     case 3: return launch_shape<P, 3>(prm, grid, stream);
+    case 4: return launch_shape<P, 4>(prm, grid, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -772,13 +774,15 @@ hipError_t launch_pair_shapes(const Int8Params& pa, int ga, const Int8Params& pb
   return hipGetLastError();
 }
 
-// The shape pairs built as one launch: 256x256 then 256x128 (both 4x2 waves).
-inline bool pair_supported(int sa, int sb) { return sa == 0 && sb == 2; }
+// The shape pairs built as one launch (8 waves each): 256x256 or 512x128
+// main tiles, then 256x128 tail tiles.
+inline bool pair_supported(int sa, int sb) { return (sa == 0 || sa == 4) && sb == 2; }
 
 template <int P>
 inline hipError_t launch_p_pair(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
                                 int gb, hipStream_t stream) {
   if (sa == 0 && sb == 2) return launch_pair_shapes<P, 0, 2>(pa, ga, pb, gb, stream);
+  if (sa == 4 && sb == 2) return launch_pair_shapes<P, 4, 2>(pa, ga, pb, gb, stream);
   return hipErrorInvalidValue;
 }
 

@@ -25,9 +25,14 @@ struct Int8Shape {
 // Measured on MI355X for K = 4096 tiles (kernel clock about 1.9 GHz).
 constexpr Int8Shape kInt8Shapes[] = {
     {256, 256, 4, 2, 1, 5200.0},
+    {512, 128, 8, 1, 1, 4800.0},
     {256, 128, 4, 2, 1, 3000.0},
     {128, 128, 2, 2, 2, 3000.0},
 };
+// Main shapes that pair with a tail shape in one launch (same wave count):
+// the first two above with the third.
+constexpr int kNumMainShapes = 2;
+constexpr int kPairTail = 2;
 constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
 constexpr double kPartialBytesPerCycle = 2500.0;  // device-wide partial-tile traffic rate
 constexpr double kTileFixedCycles = 4000.0;      // start-up and final epilogue of a workgroup
@@ -114,18 +119,20 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
     consider(model_cycles(s, M, N, K, std::min(cus * s.per_cu, kMaxGrid), cus), i,
              std::min(cus * s.per_cu, kMaxGrid), 0, -1);
   }
-  {
-    const Int8Shape& s = kInt8Shapes[0];
+  for (int i = 0; i < kNumMainShapes; ++i) {
+    const Int8Shape& s = kInt8Shapes[i];
     const int tiles_m = (M + s.bm - 1) / s.bm;
     const int cols_per_round = cus * s.per_cu / tiles_m;
     const int tiles_n = (N + s.bn - 1) / s.bn;
     if (cols_per_round >= 1 && tiles_n > cols_per_round) {
       const int split = tiles_n / cols_per_round * cols_per_round * s.bn;
       if (split < N)
-        for (int t = 1; t < kNumInt8Shapes; ++t)
+        for (int t = kNumMainShapes; t < kNumInt8Shapes; ++t)
+          // a paired launch saves the second launch's start-up and drain
           consider(model_cycles(s, M, split, K, 0, cus) +
-                       model_cycles(kInt8Shapes[t], M, N - split, K, 0, cus),
-                   0, 0, split, t);
+                       model_cycles(kInt8Shapes[t], M, N - split, K, 0, cus) -
+                       (t == kPairTail ? kTileFixedCycles : 0.0),
+                   i, 0, split, t);
     }
   }
   const Int8Shape& s = kInt8Shapes[best_i];
