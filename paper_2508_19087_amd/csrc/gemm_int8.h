@@ -85,6 +85,7 @@ struct Int8Params {
   int tiles;          // BM x BN tiles
   int dp_tiles;       // whole tiles per workgroup (the first dp_tiles * G tiles)
   int sk_pairs;       // chunk pairs of the stream-K tiles (the last ones), shared evenly
+  int sk_grid;        // workgroups [0, sk_grid) share them
   v4i* partial;       // stream-K: two partial tiles per workgroup (workspace)
   uint32_t partial_bytes;
   int* counters;      // stream-K: arrivals per stream-K tile (workspace, zeroed per call)
@@ -227,9 +228,12 @@ __host__ __device__ constexpr int pad_of(int b) { return b == 8 ? -128 : 0; }
 // tile order) and each tile's K into NCE/2 pairs of chunks.  A launch of G
 // persistent workgroups gives workgroup w the whole tiles w, w + G, ...,
 // (dp_tiles - 1) G + w, and splits the chunk pairs of the remaining
-// T - dp_tiles G tiles evenly: workgroup w takes pairs [w S / G, (w+1) S / G)
-// of them (S = sk_pairs), i.e. the end of one tile, possibly whole tiles, and
-// the start of another (stream-K).  A workgroup walks its stream-K pairs
+// T - dp_tiles G tiles evenly among the first G' <= G workgroups: workgroup
+// w < G' takes pairs [w S / G', (w+1) S / G') of them (S = sk_pairs), i.e. the
+// end of one tile, possibly whole tiles, and the start of another
+// (stream-K).  The host keeps G' at most twice the stream-K tile count, so a
+// tile has about two parts: every further part costs a partial tile written
+// and read back.  A workgroup walks its stream-K pairs
 // first and its whole tiles after, as one continuous chunk stream: the
 // software pipeline runs across tile boundaries, and at the end of each part
 // of a tile the accumulators are flushed:
@@ -260,7 +264,7 @@ struct Cursor {
 // the loop): the next stream-K tile is the next tile in row-major order, the
 // next whole tile is G tiles further.
 struct Stream {
-  int G, w, pairs, dp_tiles, sk_base, sk_lo, sk_hi, tiles;
+  int G, w, pairs, dp_tiles, sk_base, sk_lo, sk_hi, sk_g, tiles;
   int n_begin, n_end;    // output columns of the tile grid: [n_begin, n_begin + tiles_n BN)
   int bm, bn;
   int g_m, g_n;           // G tiles as (rows, columns) of the tile grid: G = g_m tiles_n + g_n
@@ -315,9 +319,9 @@ struct Stream {
       begin_dp(c, c.dp_next);
     }
   }
-  // Workgroup whose stream-K range holds stream-K pair u of S.
+  // Workgroup whose stream-K range holds stream-K pair u of S (G' = sk_g).
   __device__ __forceinline__ int range_of(int u, int S) const {
-    return (int)((((int64_t)u + 1) * G - 1) / S);
+    return (int)((((int64_t)u + 1) * sk_g - 1) / S);
   }
 };
 
@@ -358,8 +362,9 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   st.pairs = NCE / 2;
   st.dp_tiles = prm.dp_tiles;
   st.sk_base = prm.dp_tiles * st.G;
-  st.sk_lo = (int)((int64_t)st.w * prm.sk_pairs / st.G);
-  st.sk_hi = (int)((int64_t)(st.w + 1) * prm.sk_pairs / st.G);
+  st.sk_g = prm.sk_grid;
+  st.sk_lo = st.w < st.sk_g ? (int)((int64_t)st.w * prm.sk_pairs / st.sk_g) : 0;
+  st.sk_hi = st.w < st.sk_g ? (int)((int64_t)(st.w + 1) * prm.sk_pairs / st.sk_g) : 0;
   st.tiles = prm.tiles;
   st.n_begin = prm.n_begin;
   st.n_end = prm.n_begin + prm.tiles_n * BN;

@@ -54,7 +54,7 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // [n_begin, n_begin + n_cols) with `grid` persistent workgroups (see
 // gemm_int8_kernel).
 struct Plan {
-  int shape, n_begin, tiles_n, tiles, grid, dp_tiles, sk_tiles, sk_pairs;
+  int shape, n_begin, tiles_n, tiles, grid, dp_tiles, sk_tiles, sk_pairs, sk_grid;
   size_t partial_bytes, counter_bytes;
 };
 
@@ -71,6 +71,8 @@ Plan make_plan(int M, int K, int shape, int n_begin, int n_cols, int grid) {
   pl.dp_tiles = pl.tiles / pl.grid;
   pl.sk_tiles = pl.tiles - pl.dp_tiles * pl.grid;
   pl.sk_pairs = pl.sk_tiles * pairs;
+  // about two parts per stream-K tile: more parts only add partial traffic
+  pl.sk_grid = (int)std::min<int64_t>(pl.grid, std::max<int64_t>(1, 2 * (int64_t)pl.sk_tiles));
   pl.partial_bytes = pl.sk_tiles ? 2 * (size_t)pl.grid * sh.bm * sh.bn * 4 : 0;
   pl.counter_bytes = (size_t)pl.sk_tiles * 4;
   return pl;
@@ -153,6 +155,7 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
     p.tiles = pl[i].tiles;
     p.dp_tiles = pl[i].dp_tiles;
     p.sk_pairs = pl[i].sk_pairs;
+    p.sk_grid = pl[i].sk_grid;
     p.vec_out = g.N % 4 == 0 && (reinterpret_cast<uintptr_t>(g.c_int32) & 15) == 0 &&
                 (reinterpret_cast<uintptr_t>(g.c_fp16) & 7) == 0;
     p.partial_bytes = (uint32_t)pl[i].partial_bytes;
