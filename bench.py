@@ -128,6 +128,54 @@ def prefill_call_time(wl, calls: int) -> float:
     return e0.elapsed_time(e1) * 1e-3 / calls
 
 
+def route_table(calls: int = 20):
+    """Route choice evidence (Sec. V): every route the library has, forced on
+    the prefill GEMM and on the two M=1 decode GEMMs of the step, warm
+    weights, events around `calls` back-to-back apt_gemm calls."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    import synth
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+    C = apt.apt_config_t.make
+    routes = [("selected", None),
+              ("xor+popcount", C(apt.APT_ROUTE_XOR)),
+              ("+-1 planes int8 MFMA", C(apt.APT_ROUTE_PM1_MFMA)),
+              ("reassembled int8 MFMA 256x128 g256", C(apt.APT_ROUTE_INT8_MFMA, 256, 128, 128, 4, 2, 256, 3)),
+              ("reassembled int8 MFMA 128x128 g512", C(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 512, 3))]
+    out = {}
+    for prob in [synth.w4a4_prefill(), synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]:
+        a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
+        w = apt.pack(dev(prob.w_codes), prob.p)
+        row = {}
+        for name, cfg in routes:
+            if cfg is not None and cfg.route == apt.APT_ROUTE_PM1_MFMA and max(prob.p, prob.q) > 7:
+                continue
+            c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+            wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            sp = torch.cuda.current_stream().cuda_stream
+
+            def call():
+                apt.check(apt.apt_gemm(prob.M, prob.N, prob.K, prob.p, prob.q, a.data.data_ptr(),
+                                       w.data.data_ptr(), a.rowsum.data_ptr(), w.rowsum.data_ptr(),
+                                       c32.data_ptr(), None, None, None, cfg, ws.data_ptr(), wsb, sp),
+                          "apt_gemm")
+            for _ in range(3):
+                call()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(calls):
+                call()
+            e1.record()
+            torch.cuda.synchronize()
+            row[name] = round(e0.elapsed_time(e1) * 1e3 / calls, 2)
+        out[prob.name] = row
+    return out
+
+
 def decode_cold(wl, reps: int = 3):
     """The M=1 decode GEMMs with cold weights: rotate through enough packed
     weight copies (> 2x the Infinity Cache) that every launch reads HBM."""
@@ -319,6 +367,8 @@ def main():
                     help="run the prefill GEMM and a calibration copy for rocprofv3 --pmc, then exit")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs of --counters-run into profiles/")
+    ap.add_argument("--routes", action="store_true",
+                    help="print the route-choice table (us per call of every route) and exit")
     ap.add_argument("--traffic-commands", default="",
                     help="the commands that produced the --write-traffic directories")
     args = ap.parse_args()
@@ -335,6 +385,9 @@ def main():
     torch.cuda.set_device(0)
     if args.counters_run:
         counters_run()
+        return
+    if args.routes:
+        print(json.dumps(route_table(), indent=1), flush=True)
         return
     log("bench: building workload")
     wl = Workload()
