@@ -374,6 +374,14 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   st.g_n = st.G % prm.tiles_n;
   st.dp_m0 = st.w / prm.tiles_n * BM;
   st.dp_n0 = prm.n_begin + st.w % prm.tiles_n * BN;
+  if (prm.dp_tiles == 1 && prm.sk_pairs == 0 && prm.tiles % 8 == 0 && G == prm.tiles) {
+    // One round of whole tiles: workgroups are dealt round-robin to the 8
+    // XCDs (w mod 8), so give each XCD a contiguous run of row-major tiles;
+    // its L2 then holds fewer activation bands.
+    const int t = (w % 8) * (prm.tiles / 8) + w / 8;
+    st.dp_m0 = t / prm.tiles_n * BM;
+    st.dp_n0 = prm.n_begin + t % prm.tiles_n * BN;
+  }
 
   // ---- operand sources
   using SW = Stage<P, BN, SPLIT, T>;
