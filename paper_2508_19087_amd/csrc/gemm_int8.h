@@ -6,21 +6,23 @@
 // every plane pair of an element pair; the paper's Sec. III-B sum over plane
 // products is the same number by distributivity.
 //
-// Two kernels:
+// Kernels:
 //   expand_a_kernel  once per call, the activations' planes are reassembled
 //                    into operand bytes laid out as ready-made MFMA fragments
 //                    (a workspace buffer), so the main kernel loads them with
 //                    whole-line 1 KB reads straight into registers;
-//   gemm_int8_kernel each workgroup owns one BM x BN output tile and every
-//                    plane pair of it, as the paper's recovery-oriented
-//                    scheduling does (Sec. IV-B).  K advances one 128-element
-//                    chunk per pipeline step over a 3-stage LDS ring: while
-//                    the matrix cores work on chunk c, the weight planes of
-//                    chunk c+2 (fetched one step earlier) are reassembled into
-//                    the free stage, those of chunk c+3 are fetched, the
-//                    activation fragments of chunk c+1 are fetched k-step by
-//                    k-step behind the MFMAs, and the first weight fragments
-//                    of chunk c+1 are read from LDS before the step's barrier.
+//   gemm_int8_kernel persistent workgroups walking whole tiles and stream-K
+//                    shares of tiles (gemm_int8_body); a tile part covers
+//                    every plane pair of its outputs, as the paper's
+//                    recovery-oriented scheduling does (Sec. IV-B);
+//   gemm_int8_pair_kernel two such launches (main and tail tile shapes) in
+//                    one grid.
+// In the body, K advances one 128-element chunk per pipeline step over a
+// 3-stage LDS ring: while the matrix cores work on chunk c, the weight planes
+// of chunk c+2 (fetched one step earlier) are reassembled into the free
+// stage, those of chunk c+3 are fetched, the activation fragments of chunk
+// c+1 are fetched k-step by k-step behind the MFMAs, and the first weight
+// fragments of chunk c+1 are read from LDS before the step's barrier.
 // Only the weights pass through LDS: staging both operands there would need
 // as many LDS bytes per chunk as the MFMAs take cycles, and LDS would bound
 // the kernel.
