@@ -184,3 +184,31 @@ def fp16_close(g: np.ndarray, E: np.ndarray) -> np.ndarray:
     g = np.asarray(g, dtype=np.float16).astype(np.float64)
     d = np.abs(g - E)
     return (d <= FP16_REL_TOL * np.abs(E)) | (d <= FP16_ABS_TOL)
+
+
+def quantize_fp16(x: np.ndarray, q: int):
+    """Per-token quantization of fp16 activations to q-bit bipolar-INT codes.
+
+    The paper quantizes activations linearly and rewrites the signed-INT
+    quantizer in bipolar form (Sec. III-A: value 2x + 1, scale s/2); it does
+    not fix the rounding.  This follows the reading used throughout this
+    repository: the bipolar scale of row m is
+        s_m = fp16(absmax_k |x[m,k]| / (2^q - 1))      (fp32 divide, RNE)
+    so the largest magnitude lands on the outermost odd level, and each
+    element goes to the odd level 2 floor(t / 2) + 1 of t = x / s_m (fp32
+    divide), clamped to +-(2^q - 1): the nearest odd integer, ties upward.
+    A row whose scale is 0 gets t = 0 (level +1; its values dequantize to 0).
+    Returns (signed codes int8 [M][K] with value 2 code + 1, scales fp16 [M]).
+    Inputs must be finite.
+    """
+    x32 = np.asarray(x, dtype=np.float16).astype(np.float32)
+    levels = np.float32((1 << q) - 1)
+    absmax = np.max(np.abs(x32), axis=1) if x32.shape[1] else np.zeros(x32.shape[0], np.float32)
+    s16 = (absmax / levels).astype(np.float16)
+    s = s16.astype(np.float32)[:, None]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        t = np.where(s > 0, x32 / np.where(s > 0, s, np.float32(1)), np.float32(0)).astype(np.float32)
+    v = np.float32(2) * np.floor(t / np.float32(2)) + np.float32(1)
+    v = np.clip(v, -levels, levels)
+    codes = ((v - 1) / 2).astype(np.int64).astype(np.int8)
+    return codes, s16
