@@ -128,6 +128,47 @@ def prefill_call_time(wl, calls: int) -> float:
     return e0.elapsed_time(e1) * 1e-3 / calls
 
 
+def quantize_fp16_rates(calls: int = 50):
+    """The fused fp16 activation quantizer + packer on the activation shapes
+    of the step (prefill 2048x4096 at 4 bits, decode 1x4096 at 2 bits):
+    average microseconds per call over `calls` back-to-back calls between two
+    events on the stream they run on, and the rate of its algorithmic bytes
+    (fp16 input read once, packed planes, row sums and scales written once)
+    against the HBM peak."""
+    import torch
+
+    import paper_2508_19087_amd as apt
+    import synth
+    out = []
+    stream = torch.cuda.current_stream()
+    for M, K, q in [(2048, synth.HIDDEN, 4), (1, synth.HIDDEN, 2)]:
+        x = torch.from_numpy(synth.fp16_activations(synth.rng(80, M, K), M, K)).cuda()
+        nb = apt.apt_packed_bytes(M, K, q)
+        buf = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        rs = torch.empty(M, dtype=torch.int32, device="cuda")
+        sc = torch.empty(M, dtype=torch.float16, device="cuda")
+
+        def call():
+            apt.check(apt.apt_quantize_pack_activations_fp16(
+                x.data_ptr(), M, K, q, buf.data_ptr(), rs.data_ptr(), sc.data_ptr(),
+                stream.cuda_stream), "apt_quantize_pack_activations_fp16")
+        for _ in range(3):
+            call()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(calls):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / calls
+        nbytes = 2 * M * K + nb + 4 * M + 2 * M
+        gbs = nbytes / us / 1e3
+        out.append({"M": M, "K": K, "q": q, "us": round(us, 2), "bytes": nbytes,
+                    "GB/s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
+    return out
+
+
 def route_table(calls: int = 20):
     """Route choice evidence (Sec. V): every route the library has, forced on
     the prefill GEMM and on the two M=1 decode GEMMs of the step, warm
@@ -427,6 +468,8 @@ def main():
                    "prefill_config": cfg},
         "roofline": roofline,
     }
+    log("bench: fp16 activation quantizer")
+    result["quantize_fp16"] = quantize_fp16_rates()
     if not args.no_decode_cold:
         log("bench: decode GEMMs with cold weights")
         result["decode_cold"] = decode_cold(wl)

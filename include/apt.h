@@ -132,6 +132,28 @@ apt_status_t apt_pack_weights(const int8_t* w_codes, int N, int K, int p,
 apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, int q,
                                            void* a_packed, int32_t* a_rowsum, void* stream);
 
+/* Quantizes fp16 activations per row (token) to q-bit bipolar-INT codes and
+ * packs them as apt_quantize_pack_activations does, in one kernel.  The paper
+ * quantizes activations linearly and rewrites the quantizer in bipolar form,
+ * value 2x + 1 with half the signed scale (Sec. III-A); it fixes neither the
+ * scale rule nor the rounding, so this library uses, per row m:
+ *   s_m = fp16(absmax_k |a[m][k]| / (2^q - 1))   (IEEE fp32 divide, then RNE)
+ *   level(a) = 2 floor(t / 2) + 1 of t = a / s_m (IEEE fp32 divide), clamped
+ *              to +-(2^q - 1): the nearest odd integer to t, ties upward;
+ *   t = 0 (level +1, dequantizing to 0) when s_m = 0.
+ * s_m is the bipolar scale the GEMM's fp16 epilogue takes as a_scale.
+ *   a_fp16    device, fp16 bits [M][K] row-major; values must be finite (a NaN
+ *             or infinity yields unspecified codes and scale for its row)
+ *   a_packed  device, apt_packed_bytes(M, K, q) bytes, 16-byte aligned, fully written
+ *   a_rowsum  device, int32 [M] or NULL; receives the row sums defined above
+ *   a_scale   device, fp16 bits [M]; receives s_m
+ * Errors: APT_ERR_INVALID_ARG for M < 1, K < 1, q outside [1, 8], a NULL
+ * input, packed or scale pointer, or a misaligned packed pointer; APT_ERR_HIP
+ * on launch failure. */
+apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, int K, int q,
+                                                void* a_packed, int32_t* a_rowsum,
+                                                uint16_t* a_scale, void* stream);
+
 /* Host-only.  Chooses the route and tile shape for (M, N, K, p, q) from the
  * table measured on MI355X, falling back to the nearest entry (Sec. V-B,
  * lookup table and approximate matching).  The choice never changes results.

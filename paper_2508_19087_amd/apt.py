@@ -74,6 +74,9 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.argtypes = [_vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp, _vp, _vp]
             f.restype = ctypes.c_int
+        L.apt_quantize_pack_activations_fp16.argtypes = [_vp, ctypes.c_int, ctypes.c_int,
+                                                         ctypes.c_int, _vp, _vp, _vp, _vp]
+        L.apt_quantize_pack_activations_fp16.restype = ctypes.c_int
         L.apt_select_config.argtypes = [ctypes.c_int] * 5 + [ctypes.POINTER(apt_config_t)]
         L.apt_select_config.restype = ctypes.c_int
         L.apt_gemm_workspace_bytes.argtypes = [ctypes.c_int] * 5 + [ctypes.POINTER(apt_config_t)]
@@ -106,6 +109,12 @@ def apt_pack_weights(w_codes, N, K, p, w_packed, w_rowsum, stream) -> int:
 
 def apt_quantize_pack_activations(a_codes, M, K, q, a_packed, a_rowsum, stream) -> int:
     return lib().apt_quantize_pack_activations(a_codes, M, K, q, a_packed, a_rowsum, stream)
+
+
+def apt_quantize_pack_activations_fp16(a_fp16, M, K, q, a_packed, a_rowsum, a_scale,
+                                       stream) -> int:
+    return lib().apt_quantize_pack_activations_fp16(a_fp16, M, K, q, a_packed, a_rowsum, a_scale,
+                                                    stream)
 
 
 def apt_select_config(M, N, K, p, q):
@@ -177,6 +186,25 @@ def pack(codes, bits: int, activations: bool = False, stream=None) -> Packed:
     check(fn(codes.data_ptr(), rows, K, bits, buf.data_ptr(), rs.data_ptr(), _stream_ptr(stream)),
           fn.__name__)
     return Packed(buf, rs, rows, K, bits)
+
+
+def quantize_pack(x, bits: int, stream=None):
+    """Quantizes fp16 activations x [M][K] (a CUDA tensor) per row to bipolar
+    codes and packs them on the device.  Returns (Packed, fp16 scales [M])."""
+    torch = _torch()
+    assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2
+    x = x.contiguous()
+    rows, K = x.shape
+    nbytes = apt_packed_bytes(rows, K, bits)
+    if nbytes == 0:
+        raise AptError(APT_ERR_INVALID_ARG, "apt_packed_bytes")
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+    rs = torch.empty(rows, dtype=torch.int32, device=x.device)
+    scale = torch.empty(rows, dtype=torch.float16, device=x.device)
+    check(apt_quantize_pack_activations_fp16(x.data_ptr(), rows, K, bits, buf.data_ptr(),
+                                             rs.data_ptr(), scale.data_ptr(), _stream_ptr(stream)),
+          "apt_quantize_pack_activations_fp16")
+    return Packed(buf, rs, rows, K, bits), scale
 
 
 def gemm(a: Packed, w: Packed, out_int32: bool = True, a_scale=None, w_scale=None,

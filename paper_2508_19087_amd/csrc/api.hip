@@ -71,6 +71,16 @@ apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, 
   return pack_common(a_codes, M, K, q, a_packed, a_rowsum, stream);
 }
 
+apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, int K, int q,
+                                                void* a_packed, int32_t* a_rowsum,
+                                                uint16_t* a_scale, void* stream) {
+  if (M < 1 || K < 1 || !bits_ok(q) || a_fp16 == nullptr || a_packed == nullptr ||
+      a_scale == nullptr || !aligned16(a_packed))
+    return APT_ERR_INVALID_ARG;
+  return hip_status(apt::launch_quantize_pack(a_fp16, M, K, q, static_cast<uint32_t*>(a_packed),
+                                              a_rowsum, a_scale, static_cast<hipStream_t>(stream)));
+}
+
 apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out) {
   if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q) || out == nullptr)
     return APT_ERR_INVALID_ARG;

@@ -19,15 +19,6 @@ constexpr int kWavesPerBlock = kRowGroup;
 constexpr int kCodesPerLane = 16;
 constexpr int kCodesPerStep = kWave * kCodesPerLane;  // 1024 = 8 chunks
 
-// Bits i of the four bytes of x, gathered into bits 0..3 (byte j -> bit j).
-// (x >> i) & 0x01010101 has the bits at 0, 8, 16, 24; the multiply by
-// 2^24 + 2^17 + 2^10 + 2^3 moves byte j's bit to position 24 + j with no
-// carries into bits 24..27, so the top byte holds the nibble.
-__device__ __forceinline__ uint32_t gather_plane_nibble(uint32_t x, int i) {
-  uint32_t t = (x >> i) & 0x01010101u;
-  return (t * 0x01020408u) >> 24;
-}
-
 template <bool kVector, int B>
 __global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
     const int8_t* __restrict__ codes, int rows, int K, int nchunks,

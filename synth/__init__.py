@@ -61,6 +61,21 @@ def scales(g: np.random.Generator, n: int, lo: float, hi: float) -> np.ndarray:
     return g.uniform(lo, hi, size=n).astype(np.float16)
 
 
+def fp16_activations(g: np.random.Generator, rows: int, K: int,
+                     outlier_frac: float = 0.01) -> np.ndarray:
+    """fp16 activations [rows][K] shaped like a decoder layer's linear inputs:
+    a Gaussian body whose per-token spread is log-normal (median 1), and a few
+    outlier channels (``outlier_frac`` of K, the same channels in every row)
+    whose magnitude is 10-50x larger."""
+    tok = np.exp(g.normal(0.0, 0.75, size=(rows, 1)))
+    x = g.normal(0.0, 1.0, size=(rows, K)) * tok
+    n_out = int(round(outlier_frac * K))
+    if n_out:
+        ch = g.choice(K, size=n_out, replace=False)
+        x[:, ch] *= g.uniform(10.0, 50.0, size=n_out)
+    return x.astype(np.float16)
+
+
 W_SCALE_RANGE = (0.005, 0.05)  # per output channel
 A_SCALE_RANGE = (0.01, 0.1)    # per token
 

@@ -12,7 +12,7 @@ import synth
 def test_exports_every_declared_symbol():
     names = apt.header_functions()
     assert set(names) == {"apt_packed_bytes", "apt_pack_weights", "apt_quantize_pack_activations",
-                          "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
+                          "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
                           "apt_status_string"}
     L = apt.lib()
     for n in names:
@@ -177,6 +177,18 @@ def test_pack_validation(kw):
         st = fn(args["codes"], args["rows"], args["K"], args["bits"], args["packed"],
                 args["rowsum"], None)
         assert st == apt.APT_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(rows=0), dict(K=0), dict(bits=0), dict(bits=9),
+                                dict(x=None), dict(packed=None), dict(packed=A + 4),
+                                dict(scale=None)])
+def test_quantize_fp16_validation(kw):
+    """Rejected before any HIP call (the pointers are never dereferenced)."""
+    args = dict(x=A, rows=4, K=64, bits=3, packed=W, rowsum=None, scale=A + 2)
+    args.update(kw)
+    st = apt.apt_quantize_pack_activations_fp16(args["x"], args["rows"], args["K"], args["bits"],
+                                                args["packed"], args["rowsum"], args["scale"], None)
+    assert st == apt.APT_ERR_INVALID_ARG
 
 
 def test_config_struct_layout():
