@@ -121,7 +121,8 @@ size_t apt_packed_bytes(int rows, int K, int bits);
  *   w_packed  device, apt_packed_bytes(N, K, p) bytes, 16-byte aligned, fully written
  *   w_rowsum  device, int32 [N] or NULL; receives the row sums defined above
  * Errors: APT_ERR_INVALID_ARG for N < 1, K < 1, p outside [1, 8], NULL codes or
- * packed pointer, or a misaligned packed pointer; APT_ERR_HIP on launch failure. */
+ * packed pointer, or a misaligned packed pointer; APT_ERR_UNSUPPORTED for
+ * K > 2^30; APT_ERR_HIP on launch failure. */
 apt_status_t apt_pack_weights(const int8_t* w_codes, int N, int K, int p,
                               void* w_packed, int32_t* w_rowsum, void* stream);
 
@@ -148,8 +149,8 @@ apt_status_t apt_quantize_pack_activations(const int8_t* a_codes, int M, int K, 
  *   a_rowsum  device, int32 [M] or NULL; receives the row sums defined above
  *   a_scale   device, fp16 bits [M]; receives s_m
  * Errors: APT_ERR_INVALID_ARG for M < 1, K < 1, q outside [1, 8], a NULL
- * input, packed or scale pointer, or a misaligned packed pointer; APT_ERR_HIP
- * on launch failure. */
+ * input, packed or scale pointer, or a misaligned packed pointer;
+ * APT_ERR_UNSUPPORTED for K > 2^30; APT_ERR_HIP on launch failure. */
 apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, int K, int q,
                                                 void* a_packed, int32_t* a_rowsum,
                                                 uint16_t* a_scale, void* stream);

@@ -19,11 +19,15 @@ bool fits_int32(int K, int p, int q) {
 
 apt_status_t hip_status(hipError_t e) { return e == hipSuccess ? APT_OK : APT_ERR_HIP; }
 
+// The packers index a row's elements with 32-bit ints.
+constexpr int kMaxPackK = 1 << 30;
+
 apt_status_t pack_common(const int8_t* codes, int rows, int K, int bits, void* packed,
                          int32_t* rowsum, void* stream) {
   if (rows < 1 || K < 1 || !bits_ok(bits) || codes == nullptr || packed == nullptr ||
       !aligned16(packed))
     return APT_ERR_INVALID_ARG;
+  if (K > kMaxPackK) return APT_ERR_UNSUPPORTED;
   return hip_status(apt::launch_pack(codes, rows, K, bits, static_cast<uint32_t*>(packed), rowsum,
                                      static_cast<hipStream_t>(stream)));
 }
@@ -77,6 +81,7 @@ apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, i
   if (M < 1 || K < 1 || !bits_ok(q) || a_fp16 == nullptr || a_packed == nullptr ||
       a_scale == nullptr || !aligned16(a_packed))
     return APT_ERR_INVALID_ARG;
+  if (K > kMaxPackK) return APT_ERR_UNSUPPORTED;
   return hip_status(apt::launch_quantize_pack(a_fp16, M, K, q, static_cast<uint32_t*>(a_packed),
                                               a_rowsum, a_scale, static_cast<hipStream_t>(stream)));
 }

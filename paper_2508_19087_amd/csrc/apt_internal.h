@@ -27,21 +27,12 @@ __host__ __device__ __forceinline__ int64_t plane_words(int r, int c, int i, int
          (r % kRowGroup) * kWordsPerPlane;
 }
 
-// Bits i of the four bytes of x, gathered into bits 0..3 (byte j -> bit j).
-// (x >> i) & 0x01010101 has the bits at 0, 8, 16, 24; the multiply by
-// 2^24 + 2^17 + 2^10 + 2^3 moves byte j's bit to position 24 + j with no
-// carries into bits 24..27, so the top byte holds the nibble.
-__device__ __forceinline__ uint32_t gather_plane_nibble(uint32_t x, int i) {
-  uint32_t t = (x >> i) & 0x01010101u;
-  return (t * 0x01020408u) >> 24;
-}
-
 // Launch of the converter + bit-plane packer (pack.hip).
 hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t* packed,
                        int32_t* rowsum, hipStream_t stream);
 // Per-row quantization of fp16 rows to b-bit bipolar codes, then the same
 // packing; writes the fp16 bits of each row's bipolar scale to scale[row]
-// (quantize.hip).
+// (pack.hip).
 hipError_t launch_quantize_pack(const uint16_t* x, int rows, int K, int bits, uint32_t* packed,
                                 int32_t* rowsum, uint16_t* scale, hipStream_t stream);
 

@@ -1,132 +1,377 @@
 // pack.hip - signed-INT -> bipolar-INT conversion and bit-plane packing for
 // gfx950 (APT-LLM, arXiv 2508.19087: Sec. III-A conversion, Sec. IV-A
-// decomposition and reassembly steps 1-3).
+// decomposition and reassembly steps 1-3), from int8 codes or, quantizing
+// per row (token) on the way, from fp16 activations.
 //
-// A workgroup of 8 wavefronts owns one 8-row group of the packed layout; each
-// wavefront owns one row and walks it in steps of 1024 codes: lane l converts
-// codes [16 l, 16 l + 16) of the step (one 16-byte load), extracts each
-// plane's 16 bits, and pairs with its neighbour lane to form one 32-bit word
-// per plane.  Conversion flips the sign bit of the b-bit field; the row sum of
-// bipolar values 2u - (2^b - 1) is reduced across the wave.  Wavefronts of the
-// padding rows past the last row write zero words.
+// Quantizer of an fp16 row (the bipolar form of a linear quantizer, Sec.
+// III-A; the scale rule and the rounding are this library's choice, the paper
+// fixes neither): s = fp16(absmax_k |x[k]| / (2^b - 1)) with an IEEE fp32
+// divide, so the largest magnitude lands on the outermost odd level; element
+// x goes to the odd level 2 floor(t / 2) + 1 of t = x / s clamped to
+// +-(2^b - 1), i.e. to the signed code floor(t / 2) clamped to
+// [-2^(b-1), 2^(b-1) - 1].  A row with s = 0 gets t = 0.
+//
+// One workgroup per row; the last row's workgroup also writes the zero words
+// of the padding rows of its 8-row group.  The row is split over the
+// workgroup's nw waves in steps of 1024 elements: wave w takes steps w, w + nw,
+// ...; lane l of a step takes elements [16 l, 16 l + 16) (buffer loads whose
+// range is the row, so reads past K return 0).  When every wave
+// has at most 4 steps (K <= 32768) the loaded values stay in registers: the
+// fp16 source folds the row's largest magnitude first (pass 1, reduced over
+// the workgroup through LDS) and quantizes from registers, so HBM sees every
+// input byte once.  Longer rows are walked in rounds of 4 steps per wave (and
+// loaded twice by the fp16 source).
+//
+// Conversion: u = (x mod 2^b) XOR 2^(b-1), four codes per dword.  Packing: the
+// 16 bipolar words of a lane (one byte each) go through an 8x8 bit-matrix
+// transpose per 8 elements, which leaves plane i of those elements in byte i;
+// for b <= 4 the high nibbles are zero and the transpose reduces to two delta
+// swaps on one dword.  Lanes 2m and 2m+1 hold the two 16-bit halves of one
+// plane word; per pair of planes they swap halves with one DPP move, and the
+// even lane stores plane i, the odd lane plane i+1.  The row sum of bipolar
+// values 2u - (2^b - 1) is reduced over the workgroup.
+//
+// Workgroups are dispatched to the 8 XCDs round robin; when the row count is a
+// multiple of 8, rows are assigned so that consecutive workgroups on one XCD
+// take consecutive rows, and the 8 rows of a packed row group, which share
+// every 128-byte plane segment (16 bytes each), meet in that XCD's L2.
+//
+// Division in the quantizer: instead of a correctly rounded fp32 divide per
+// element, each row computes r = RN(1 / s) once and each element
+//     h0 = fma(x, r / 2, +0),  e = fma(-h0, 2 s, x),  h = fma(e, r / 2, h0),
+// the quotient correction of Markstein's division with a correctly rounded
+// reciprocal, applied to the half quotient.  h equals RN(x / s) / 2 (up to the
+// sign of a zero) for every finite fp16 x and positive finite fp16 s; the test
+// suite checks all of those pairs on the CPU.
+#include <algorithm>
+
 #include "apt_internal.h"
 
 namespace apt {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kWavesPerBlock = kRowGroup;
-constexpr int kCodesPerLane = 16;
-constexpr int kCodesPerStep = kWave * kCodesPerLane;  // 1024 = 8 chunks
+constexpr int kMaxWaves = 8;
+constexpr int kLaneElems = 16;
+constexpr int kStep = kWave * kLaneElems;  // 1024 elements = 8 chunks
+constexpr int kMaxCachedSteps = 4;
+constexpr int kTargetWaves = 4096;  // 16 per CU
+constexpr int kXcds = 8;
+constexpr uint32_t kRawBufferFlags = 0x00020000u;
 
-template <bool kVector, int B>
-__global__ __launch_bounds__(kWave* kWavesPerBlock) void pack_kernel(
-    const int8_t* __restrict__ codes, int rows, int K, int nchunks,
-    uint32_t* __restrict__ packed, int32_t* __restrict__ rowsum) {
-  constexpr int bits = B;
-  const int lane = threadIdx.x % kWave;
-  const int row = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;  // < padded row count
-  const bool real = row < rows;
+typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-  const uint32_t field_mask = ((1u << bits) - 1u) * 0x01010101u;
-  const uint32_t sign_flip = (1u << (bits - 1)) * 0x01010101u;
-  const int kpad = nchunks * kChunk;
-  const int8_t* src = codes + (int64_t)min(row, rows - 1) * K;
-  uint32_t usum = 0;
+// Signed b-bit codes, one byte each.
+template <bool kVec, int B>
+struct CodeRow {
+  static constexpr int kDwords = kLaneElems / 4;
+  static constexpr int kElemBytes = 1;
+  static constexpr bool kVector = kVec;
+  static constexpr bool kScaled = false;
 
-  auto load = [&](int base, uint32_t d[4]) {
-    const int k0 = base + lane * kCodesPerLane;
-    d[0] = d[1] = d[2] = d[3] = 0u;
+  // The lane's 16 codes from element k0 on.
+  __device__ static void load(__amdgpu_buffer_rsrc_t rsrc, int k0, uint32_t d[kDwords]) {
     if (kVector) {
-      // K % 16 == 0: the lane's 16 codes are all valid or all padding.
-      if (real && k0 < K) {
-        uint4 v = *reinterpret_cast<const uint4*>(src + k0);
-        d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-      }
-    } else if (real) {
+      // K % 16 == 0: the lane's 16 codes are all in the row or all past it.
+      const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (uint32_t)k0, 0, 0);
 #pragma unroll
-      for (int t = 0; t < kCodesPerLane; ++t) {
-        int k = k0 + t;
-        uint32_t b = (k < K) ? (uint32_t)(uint8_t)src[k] : 0u;
-        d[t / 4] |= b << (8 * (t % 4));
+      for (int t = 0; t < 4; ++t) d[t] = v[t];
+    } else {
+#pragma unroll
+      for (int t = 0; t < kDwords; ++t) {
+        uint32_t w = 0u;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          w |= (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(rsrc, (uint32_t)(k0 + 4 * t + q), 0, 0)
+               << (8 * q);
+        d[t] = w;
       }
     }
-  };
-  auto process = [&](int base, const uint32_t d[4]) {
-    const int k0 = base + lane * kCodesPerLane;
-    // Bipolar words, one per byte; padding codes and padding rows stay all-zero.
-    uint32_t u[4];
+  }
+  // Bipolar words u = (x mod 2^b) XOR 2^(b-1), one per byte (Sec. III-A).
+  __device__ static void words(const uint32_t d[kDwords], float, float, uint32_t u[4]) {
+    constexpr uint32_t field = ((1u << B) - 1u) * 0x01010101u;
+    constexpr uint32_t flip = (1u << (B - 1)) * 0x01010101u;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) u[t] = (d[t] & field) ^ flip;
+  }
+};
+
+// fp16 activations, quantized with the row's scale.
+template <bool kVec, int B>
+struct HalfRow {
+  static constexpr int kDwords = kLaneElems / 2;
+  static constexpr int kElemBytes = 2;
+  static constexpr bool kVector = kVec;
+  static constexpr bool kScaled = true;
+
+  // The lane's 16 values from element k0 on (fp16 bits, two per dword).
+  __device__ static void load(__amdgpu_buffer_rsrc_t rsrc, int k0, uint32_t d[kDwords]) {
+    const uint32_t off = (uint32_t)k0 * 2u;
+    if (kVector) {
+      const u32x4_t v0 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
+      const u32x4_t v1 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off + 16u, 0, 0);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        d[t] = v0[t];
+        d[4 + t] = v1[t];
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < kDwords; ++t) {
+        const uint32_t h0 = __builtin_amdgcn_raw_buffer_load_b16(rsrc, off + 4u * t, 0, 0);
+        const uint32_t h1 = __builtin_amdgcn_raw_buffer_load_b16(rsrc, off + 4u * t + 2u, 0, 0);
+        d[t] = (h0 & 0xFFFFu) | (h1 << 16);
+      }
+    }
+  }
+  // Largest |x| of the lane's values as fp16 bits, one maximum per 16-bit
+  // half: for finite values the order of |x| is the integer order of the bits
+  // without the sign.
+  __device__ static ushort2_t fold_max(ushort2_t m, const uint32_t d[kDwords]) {
+#pragma unroll
+    for (int t = 0; t < kDwords; ++t)
+      m = __builtin_elementwise_max(m, __builtin_bit_cast(ushort2_t, d[t] & 0x7FFF7FFFu));
+    return m;
+  }
+  // Bipolar words of the lane's 16 values, one per byte (element 4t + q in
+  // byte q of u[t]).  The signed code c = floor(h) clamped to the b-bit range
+  // goes into a byte as two's complement; the word is then
+  // (c mod 2^b) XOR 2^(b-1) = c + 2^(b-1), four bytes at once.  A zero's sign
+  // in h0 does not change floor(h).
+  __device__ static void words(const uint32_t d[kDwords], float rh, float s2, uint32_t u[4]) {
+#pragma clang fp contract(off)
+    constexpr int clo = -(1 << (B - 1)), chi = (1 << (B - 1)) - 1;
+    constexpr uint32_t field = ((1u << B) - 1u) * 0x01010101u;
+    constexpr uint32_t flip = (1u << (B - 1)) * 0x01010101u;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      uint32_t valid_bytes = 0xFFFFFFFFu;
-      int kt = k0 + 4 * t;
-      if (!real) {
-        valid_bytes = 0u;
-      } else if (!kVector) {
-        int n_valid = K - kt;
-        valid_bytes = n_valid >= 4 ? 0xFFFFFFFFu : (n_valid <= 0 ? 0u : ((1u << (8 * n_valid)) - 1u));
-      } else if (k0 >= K) {
-        valid_bytes = 0u;
+      uint32_t acc = 0u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = 4 * t + q;
+        const uint32_t bits = (d[j / 2] >> (16 * (j % 2))) & 0xFFFFu;
+        const float x = __half2float(__ushort_as_half((unsigned short)bits));
+        const float h0 = __builtin_fmaf(x, rh, 0.0f);
+        const float e = __builtin_fmaf(-h0, s2, x);
+        const float h = __builtin_fmaf(e, rh, h0);  // RN(x / s) / 2
+        int c;  // floor(h) as int32 in one instruction (saturating)
+        asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(c) : "v"(h));
+        c = min(max(c, clo), chi);
+        // byte q of acc <- low byte of c; the other bytes stay
+        const uint32_t sel = q == 1 ? 0x03020400u : q == 2 ? 0x03040100u : 0x04020100u;
+        acc = q == 0 ? (uint32_t)c : __builtin_amdgcn_perm((uint32_t)c, acc, sel);
       }
-      u[t] = ((d[t] & field_mask) ^ sign_flip) & valid_bytes;
-      usum = __builtin_amdgcn_sad_u8(u[t], 0u, usum);
+      u[t] = (acc & field) ^ flip;
     }
-    const int chunk = k0 / kChunk;
-    const int word = (k0 % kChunk) / 32;
-    const bool upper_half = (lane & 1) != 0;  // codes 16..31 of the word
-    const bool in_range = k0 < kpad;
-#pragma unroll
-    for (int i = 0; i < bits; ++i) {
-      uint32_t half = gather_plane_nibble(u[0], i) | (gather_plane_nibble(u[1], i) << 4) |
-                      (gather_plane_nibble(u[2], i) << 8) | (gather_plane_nibble(u[3], i) << 12);
-      uint32_t other = __shfl_xor(half, 1);
-      if (!upper_half && in_range) {
-        packed[plane_words(row, chunk, i, nchunks, bits) + word] = half | (other << 16);
-      }
-    }
-  };
-
-  // Four steps per trip: their loads are all in flight before the first is
-  // used.
-  constexpr int kGroup = 4;
-  int base = 0;
-  for (; base + kGroup * kCodesPerStep <= kpad; base += kGroup * kCodesPerStep) {
-    uint32_t d[kGroup][4];
-#pragma unroll
-    for (int s = 0; s < kGroup; ++s) load(base + s * kCodesPerStep, d[s]);
-#pragma unroll
-    for (int s = 0; s < kGroup; ++s) process(base + s * kCodesPerStep, d[s]);
   }
-  for (; base < kpad; base += kCodesPerStep) {
-    uint32_t d[4];
-    load(base, d);
-    process(base, d);
-  }
+};
 
-  if (rowsum != nullptr && real) {
-    for (int off = kWave / 2; off > 0; off >>= 1) usum += __shfl_xor(usum, off);
-    if (lane == 0) {
-      // sum_k (2 u - (2^b - 1)) over the K real codes
-      uint32_t top = (1u << bits) - 1u;
-      rowsum[row] = (int32_t)(2u * usum - top * (uint32_t)K);
-    }
+// Delta swaps of an 8x8 bit-matrix transpose (bit 8r + c <-> bit 8c + r of a
+// 64-bit value, rows r = bytes): distance 7 and 14 stay inside each dword,
+// distance 28 moves nibbles between the dwords.  The three commute.
+__device__ __forceinline__ uint32_t swap7(uint32_t x) {
+  const uint32_t t = (x ^ (x >> 7)) & 0x00AA00AAu;
+  return x ^ t ^ (t << 7);
+}
+__device__ __forceinline__ uint32_t swap14(uint32_t x) {
+  const uint32_t t = (x ^ (x >> 14)) & 0x0000CCCCu;
+  return x ^ t ^ (t << 14);
+}
+
+// Transposes the bytes lo (rows 0..3) and hi (rows 4..7): afterwards bit j of
+// byte i is bit i of the former byte j.  With b <= 4 every byte is below 16:
+// the distance-28 swap just moves hi's low nibbles up into lo (hi becomes 0).
+template <int B>
+__device__ __forceinline__ void transpose8x8(uint32_t& lo, uint32_t& hi) {
+  if (B <= 4) {
+    lo = swap14(swap7(lo | (hi << 4)));
+    hi = 0u;
+  } else {
+    lo = swap14(swap7(lo));
+    hi = swap14(swap7(hi));
+    const uint32_t t = (lo ^ (hi << 4)) & 0xF0F0F0F0u;
+    lo ^= t;
+    hi ^= t >> 4;
   }
 }
 
-template <int B>
-hipError_t launch_pack_bits(const int8_t* codes, int rows, int K, uint32_t* packed, int32_t* rowsum,
-                            hipStream_t stream) {
+// kSteps: steps each wave keeps in registers (1, 2 or 4), or 0 for rows too
+// long for that.  groups = rows / 8 selects the XCD-aware row order (rows a
+// multiple of 8), 0 the plain one.  scale is written by the fp16 source only.
+template <class Src, int B, int kSteps>
+__global__ __launch_bounds__(kWave* kMaxWaves) void pack_rows_kernel(
+    const uint8_t* __restrict__ src, int rows, int K, int nchunks, int groups,
+    uint32_t* __restrict__ packed, int32_t* __restrict__ rowsum, uint16_t* __restrict__ scale) {
+  constexpr int kHeld = kSteps > 0 ? kSteps : kMaxCachedSteps;
+  __shared__ uint32_t lds_red[kMaxWaves];
+  const int nw = blockDim.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const int row = groups > 0 ? (blockIdx.x % kXcds) * groups + blockIdx.x / kXcds : blockIdx.x;
+  // the last row also writes the padding rows of its row group (uniform)
+  const int pad_rows = row == rows - 1 ? (rows + kRowGroup - 1) / kRowGroup * kRowGroup - rows : 0;
+  const int kpad = nchunks * kChunk;
+  const int nsteps = (kpad + kStep - 1) / kStep;
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(src + (int64_t)row * K * Src::kElemBytes), 0,
+      (uint32_t)K * Src::kElemBytes, kRawBufferFlags);
+  auto k_of = [&](int j) { return j * kStep + lane * kLaneElems; };
+
+  uint32_t d[kHeld][Src::kDwords];
+  float rh = 0.0f, s2 = 0.0f;
+  if constexpr (Src::kScaled) {
+    // Pass 1: the row's largest magnitude, then its scale.
+    ushort2_t mm = {0, 0};
+    for (int j0 = wave; j0 < nsteps; j0 += kHeld * nw) {
+#pragma unroll
+      for (int t = 0; t < kHeld; ++t) Src::load(rsrc, k_of(j0 + t * nw), d[t]);
+#pragma unroll
+      for (int t = 0; t < kHeld; ++t) mm = Src::fold_max(mm, d[t]);
+      if (kSteps > 0) break;  // one round covers all steps; d stays for pass 2
+    }
+    uint32_t m = max((uint32_t)mm.x, (uint32_t)mm.y);
+    for (int off = kWave / 2; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+    if (lane == 0) lds_red[wave] = m;
+    __syncthreads();
+    m = 0u;
+    for (int w = 0; w < nw; ++w) m = max(m, lds_red[w]);
+    __syncthreads();  // lds_red is reused for the row sum
+    const float absmax = __half2float(__ushort_as_half((unsigned short)m));
+    const __half s16 = __float2half_rn(__fdiv_rn(absmax, (float)((1 << B) - 1)));
+    const float s = __half2float(s16);
+    rh = s > 0.0f ? __fdiv_rn(1.0f, s) * 0.5f : 0.0f;  // s = 0: every h is 0
+    s2 = s * 2.0f;
+    if (threadIdx.x == 0) scale[row] = __half_as_ushort(s16);
+  } else if (kSteps > 0) {
+#pragma unroll
+    for (int t = 0; t < kHeld; ++t) Src::load(rsrc, k_of(wave + t * nw), d[t]);
+  }
+
+  // Pass 2: convert (or quantize) and pack.
+  uint32_t usum = 0u;
+  const bool odd = (lane & 1) != 0;
+  const uint32_t join = odd ? 0x03020706u : 0x05040100u;
+  auto process = [&](int j, const uint32_t* dd) __attribute__((always_inline)) {
+    const int k0 = k_of(j);
+    uint32_t u[4];
+    Src::words(dd, rh, s2, u);
+    // padding elements: all-zero words
+    if (Src::kVector) {
+      const uint32_t valid = k0 < K ? 0xFFFFFFFFu : 0u;  // K % 16 == 0
+#pragma unroll
+      for (int t = 0; t < 4; ++t) u[t] &= valid;
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int n_valid = K - (k0 + 4 * t);
+        u[t] &= n_valid >= 4 ? 0xFFFFFFFFu : (n_valid <= 0 ? 0u : ((1u << (8 * n_valid)) - 1u));
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) usum = __builtin_amdgcn_sad_u8(u[t], 0u, usum);
+    // Planes of elements 0..7 (a) and 8..15 (b): byte i = plane i (i < 4 in lo).
+    uint32_t alo = u[0], ahi = u[1], blo = u[2], bhi = u[3];
+    transpose8x8<B>(alo, ahi);
+    transpose8x8<B>(blo, bhi);
+    if (k0 >= kpad) return;
+    uint32_t* dst = packed + plane_words(row, k0 / kChunk, 0, nchunks, B) + (k0 % kChunk) / 32;
+#pragma unroll
+    for (int i = 0; i < B; i += 2) {
+      const uint32_t sa = i < 4 ? alo : ahi, sb = i < 4 ? blo : bhi;
+      const int bi = i % 4;
+      // y = [a_i, b_i, a_i+1, b_i+1]: this lane's 16 bits of plane i, then of plane i+1
+      const uint32_t y = __builtin_amdgcn_perm(
+          sb, sa, (uint32_t)(bi | (4 + bi) << 8 | (bi + 1) << 16 | (5 + bi) << 24));
+      const uint32_t z = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)y, 0xB1, 0xF, 0xF, false);  // lane ^ 1
+      const uint32_t wv = __builtin_amdgcn_perm(z, y, join);  // even: plane i, odd: plane i+1
+      if (!odd || i + 1 < B) {
+        uint32_t* w = dst + (i + (odd ? 1 : 0)) * kPlaneStride;
+        *w = wv;
+        for (int r = 1; r <= pad_rows; ++r) w[r * kWordsPerPlane] = 0u;
+      }
+    }
+  };
+  if (kSteps > 0) {
+#pragma unroll
+    for (int t = 0; t < kHeld; ++t) {
+      const int j = wave + t * nw;
+      if (j < nsteps) process(j, d[t]);
+    }
+  } else {
+    for (int j0 = wave; j0 < nsteps; j0 += kHeld * nw) {
+#pragma unroll
+      for (int t = 0; t < kHeld; ++t) Src::load(rsrc, k_of(j0 + t * nw), d[t]);
+#pragma unroll
+      for (int t = 0; t < kHeld; ++t)
+        if (j0 + t * nw < nsteps) process(j0 + t * nw, d[t]);
+    }
+  }
+
+  if (rowsum != nullptr) {
+    for (int off = kWave / 2; off > 0; off >>= 1) usum += __shfl_xor(usum, off);
+    if (nw > 1) {
+      if (lane == 0) lds_red[wave] = usum;
+      __syncthreads();
+      usum = 0u;
+      for (int w = 0; w < nw; ++w) usum += lds_red[w];
+    }
+    if (threadIdx.x == 0)
+      // sum_k (2 u - (2^b - 1)) over the K real elements
+      rowsum[row] = (int32_t)(2u * usum - ((1u << B) - 1u) * (uint32_t)K);
+  }
+}
+
+template <class Src, int B>
+hipError_t launch_rows(const void* src, int rows, int K, uint32_t* packed, int32_t* rowsum,
+                       uint16_t* scale, hipStream_t stream) {
   const int nchunks = num_chunks(K);
-  dim3 block(kWave * kWavesPerBlock);
-  dim3 grid(padded_rows(rows) / kWavesPerBlock);
-  const bool vec = (K % 16 == 0) && ((reinterpret_cast<uintptr_t>(codes) & 15u) == 0);
-  if (vec)
-    hipLaunchKernelGGL((pack_kernel<true, B>), grid, block, 0, stream, codes, rows, K, nchunks,
-                       packed, rowsum);
+  const int nsteps = (nchunks * kChunk + kStep - 1) / kStep;
+  // Fewest waves per row that hold the row in registers (the per-row
+  // reductions and the scale cost the same in every wave), but more while the
+  // whole grid has fewer than kTargetWaves waves.
+  const int max_nw = std::min(nsteps, kMaxWaves);
+  int nw = std::min((nsteps + kMaxCachedSteps - 1) / kMaxCachedSteps, max_nw);
+  while (nw < max_nw && (int64_t)rows * nw < kTargetWaves) nw = std::min(2 * nw, max_nw);
+  const int per_wave = (nsteps + nw - 1) / nw;
+  const int groups = rows % kRowGroup == 0 ? rows / kRowGroup : 0;
+  const dim3 block(kWave * nw), grid(rows);
+  const uint8_t* s = static_cast<const uint8_t*>(src);
+  if (per_wave == 1)
+    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 1>), grid, block, 0, stream, s, rows, K, nchunks,
+                       groups, packed, rowsum, scale);
+  else if (per_wave == 2)
+    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 2>), grid, block, 0, stream, s, rows, K, nchunks,
+                       groups, packed, rowsum, scale);
+  else if (per_wave <= kMaxCachedSteps)
+    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 4>), grid, block, 0, stream, s, rows, K, nchunks,
+                       groups, packed, rowsum, scale);
   else
-    hipLaunchKernelGGL((pack_kernel<false, B>), grid, block, 0, stream, codes, rows, K, nchunks,
-                       packed, rowsum);
+    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 0>), grid, block, 0, stream, s, rows, K, nchunks,
+                       groups, packed, rowsum, scale);
   return hipGetLastError();
+}
+
+// The 16-byte load path needs whole 16-element groups and a 16-byte aligned base.
+bool vector_ok(const void* p, int K) {
+  return K % 16 == 0 && (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+template <int B>
+hipError_t launch_pack_bits(const int8_t* codes, int rows, int K, uint32_t* packed,
+                            int32_t* rowsum, hipStream_t stream) {
+  if (vector_ok(codes, K))
+    return launch_rows<CodeRow<true, B>, B>(codes, rows, K, packed, rowsum, nullptr, stream);
+  return launch_rows<CodeRow<false, B>, B>(codes, rows, K, packed, rowsum, nullptr, stream);
+}
+
+template <int B>
+hipError_t launch_quantize_bits(const uint16_t* x, int rows, int K, uint32_t* packed,
+                                int32_t* rowsum, uint16_t* scale, hipStream_t stream) {
+  if (vector_ok(x, K))
+    return launch_rows<HalfRow<true, B>, B>(x, rows, K, packed, rowsum, scale, stream);
+  return launch_rows<HalfRow<false, B>, B>(x, rows, K, packed, rowsum, scale, stream);
 }
 
 }  // namespace
@@ -142,6 +387,21 @@ hipError_t launch_pack(const int8_t* codes, int rows, int K, int bits, uint32_t*
     case 6: return launch_pack_bits<6>(codes, rows, K, packed, rowsum, stream);
     case 7: return launch_pack_bits<7>(codes, rows, K, packed, rowsum, stream);
     case 8: return launch_pack_bits<8>(codes, rows, K, packed, rowsum, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_quantize_pack(const uint16_t* x, int rows, int K, int bits, uint32_t* packed,
+                                int32_t* rowsum, uint16_t* scale, hipStream_t stream) {
+  switch (bits) {
+    case 1: return launch_quantize_bits<1>(x, rows, K, packed, rowsum, scale, stream);
+    case 2: return launch_quantize_bits<2>(x, rows, K, packed, rowsum, scale, stream);
+    case 3: return launch_quantize_bits<3>(x, rows, K, packed, rowsum, scale, stream);
+    case 4: return launch_quantize_bits<4>(x, rows, K, packed, rowsum, scale, stream);
+    case 5: return launch_quantize_bits<5>(x, rows, K, packed, rowsum, scale, stream);
+    case 6: return launch_quantize_bits<6>(x, rows, K, packed, rowsum, scale, stream);
+    case 7: return launch_quantize_bits<7>(x, rows, K, packed, rowsum, scale, stream);
+    case 8: return launch_quantize_bits<8>(x, rows, K, packed, rowsum, scale, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -191,5 +191,14 @@ def test_quantize_fp16_validation(kw):
     assert st == apt.APT_ERR_INVALID_ARG
 
 
+def test_pack_rejects_huge_rows():
+    """K > 2^30 is refused before any HIP call (32-bit element indexing)."""
+    K = (1 << 30) + 1
+    for fn in (apt.apt_pack_weights, apt.apt_quantize_pack_activations):
+        assert fn(A, 1, K, 2, W, None, None) == apt.APT_ERR_UNSUPPORTED
+    assert apt.apt_quantize_pack_activations_fp16(A, 1, K, 2, W, None, A + 2, None) == \
+        apt.APT_ERR_UNSUPPORTED
+
+
 def test_config_struct_layout():
     assert ctypes.sizeof(apt.apt_config_t) == 16 * 4
