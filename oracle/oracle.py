@@ -9,6 +9,10 @@ this module wraps them with ctypes and adds the fp16 scale epilogue, which is
 evaluated exactly in float64 and rounded to fp16 by numpy (round to nearest
 even).  Exactness: |C| < 2^31 and each fp16 scale carries 11 significant bits,
 so C * s_a * s_w needs at most 31 + 11 + 11 = 53 bits and is exact in float64.
+It also holds the zero-point epilogue of two linear quantizers in bipolar form
+(``dequant_matmul``, the definition; ``affine_epilogue``, the expanded form
+from the integer GEMM and the row sums) and the per-token fp16 activation
+quantizer (``quantize_fp16``).
 """
 from __future__ import annotations
 
@@ -212,3 +216,62 @@ def quantize_fp16(x: np.ndarray, q: int):
     v = np.clip(v, -levels, levels)
     codes = ((v - 1) / 2).astype(np.int64).astype(np.int8)
     return codes, s16
+
+
+# ---- linear quantizers with a zero-point (Sec. III-A) ---------------------------
+#
+# A linear quantizer stores X = s * x + z for a signed code x.  Sec. III-A
+# rewrites it in bipolar form: with the bipolar value x' = 2x + 1,
+#     X = (s / 2) * x' + (z - s / 2),
+# i.e. bipolar scale s' = s / 2 and bipolar zero z' = z - s / 2.  With a
+# per-token (s'_a, z'_a) for the activations and a per-channel (s'_w, z'_w)
+# for the weights, the product of the dequantized operands is
+#     Y[m,n] = sum_k (s'_a[m] a'[m,k] + z'_a[m]) (s'_w[n] w'[n,k] + z'_w[n]).
+
+def dequant_matmul(a_codes: np.ndarray, w_codes: np.ndarray, p: int, q: int, a_scale, a_zero,
+                   w_scale, w_zero) -> np.ndarray:
+    """The definition: dequantize both operands from their bipolar values and
+    bipolar (scale, zero) and multiply them in float64."""
+    sa = np.asarray(a_scale, dtype=np.float16).astype(np.float64)[:, None]
+    za = np.asarray(a_zero, dtype=np.float16).astype(np.float64)[:, None]
+    sw = np.asarray(w_scale, dtype=np.float16).astype(np.float64)[:, None]
+    zw = np.asarray(w_zero, dtype=np.float16).astype(np.float64)[:, None]
+    A = sa * values(a_codes, q).astype(np.float64) + za
+    W = sw * values(w_codes, p).astype(np.float64) + zw
+    return A @ W.T
+
+
+def affine_epilogue(C: np.ndarray, a_rowsum: np.ndarray, w_rowsum: np.ndarray, K: int, a_scale,
+                    a_zero, w_scale, w_zero):
+    """(E, T): the expanded form of the same product from the integer GEMM and
+    the bipolar row sums R_a[m] = sum_k a'[m,k], R_w[n] = sum_k w'[n,k]:
+        E = s'_a s'_w C + s'_a z'_w R_a + z'_a s'_w R_w + K z'_a z'_w,
+    each term exact in float64 (at most 31 + 11 + 11 significant bits), and
+    T = the sum of the terms' magnitudes, which bounds the rounding error of a
+    float32 evaluation."""
+    sa = np.asarray(a_scale, dtype=np.float16).astype(np.float64)[:, None]
+    za = np.asarray(a_zero, dtype=np.float16).astype(np.float64)[:, None]
+    sw = np.asarray(w_scale, dtype=np.float16).astype(np.float64)[None, :]
+    zw = np.asarray(w_zero, dtype=np.float16).astype(np.float64)[None, :]
+    Cd = np.asarray(C, dtype=np.int64).astype(np.float64)
+    Ra = np.asarray(a_rowsum, dtype=np.int64).astype(np.float64)[:, None]
+    Rw = np.asarray(w_rowsum, dtype=np.int64).astype(np.float64)[None, :]
+    terms = (sa * sw * Cd, sa * zw * Ra, za * sw * Rw, float(K) * za * zw)
+    E = terms[0] + terms[1] + terms[2] + terms[3]
+    T = np.abs(terms[0]) + np.abs(terms[1]) + np.abs(terms[2]) + np.abs(terms[3])
+    return E, T
+
+
+# A float32 evaluation of the four terms (two roundings per product, three
+# per sum, one per int32 -> float32 conversion) is off by at most about
+# 6 * 2^-24 * T; the fp16 result adds half an ulp (2^-11 relative, 2^-25 in
+# the subnormal range).  The tolerance leaves a margin over both.
+AFFINE_T_TOL = 2.0 ** -20
+
+
+def fp16_affine_close(g: np.ndarray, E: np.ndarray, T: np.ndarray) -> np.ndarray:
+    """Element-wise acceptance of a GPU fp16 result g of the affine epilogue:
+    |g - E| <= 1e-3 |E| + 2^-20 T + 2^-25."""
+    g = np.asarray(g, dtype=np.float16).astype(np.float64)
+    d = np.abs(g - E)
+    return d <= FP16_REL_TOL * np.abs(E) + AFFINE_T_TOL * T + FP16_ABS_TOL

@@ -94,6 +94,8 @@ class Problem:
     w_scale: Optional[np.ndarray] = None
     a_scale: Optional[np.ndarray] = None
     meta: dict = field(default_factory=dict)
+    w_zero: Optional[np.ndarray] = None
+    a_zero: Optional[np.ndarray] = None
 
     @property
     def ops(self) -> int:
@@ -146,3 +148,30 @@ def random_problem(g: np.random.Generator, M: int, N: int, K: int, p: int, q: in
                    with_scales: bool = False) -> Problem:
     return make("rand_%dx%dx%d_w%da%d" % (M, N, K, p, q), M, N, K, p, q, g,
                 with_scales=with_scales)
+
+
+def zero_points(g: np.random.Generator, scale: np.ndarray, bits: int) -> np.ndarray:
+    """Bipolar zero-points z' for bipolar scales s' (fp16): an asymmetric
+    quantizer whose grid centre is shifted by up to a quarter of its half
+    range s' (2^b - 1), i.e. z' ~ U(-1/4, 1/4) s' (2^b - 1), cast to fp16."""
+    half = np.asarray(scale, dtype=np.float64) * ((1 << bits) - 1)
+    return (g.uniform(-0.25, 0.25, size=half.shape) * half).astype(np.float16)
+
+
+def affine_problem(name: str, M: int, N: int, K: int, p: int, q: int,
+                   g: np.random.Generator) -> Problem:
+    """Codes, fp16 scales and fp16 zero-points of two linear quantizers in
+    bipolar form.  Draw order: weight codes, activation codes, weight scales,
+    activation scales, weight zeros, activation zeros."""
+    prob = make(name, M, N, K, p, q, g, with_scales=True)
+    prob.w_zero = zero_points(g, prob.w_scale, p)
+    prob.a_zero = zero_points(g, prob.a_scale, q)
+    return prob
+
+
+def layer_w2a4_affine(layer: str, M: int) -> Problem:
+    """One linear of the W2A4 7B-class decoder layer with per-channel and
+    per-token scales and zero-points, seed 6."""
+    N, K = LAYER_SHAPES[layer]
+    idx = list(LAYER_SHAPES).index(layer)
+    return affine_problem("w2a4_affine_%s_m%d" % (layer, M), M, N, K, 2, 4, rng(6, idx, M))
