@@ -200,6 +200,32 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q,
                       const apt_config_t* cfg,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* C = A * W^T as apt_gemm, with an fp16 epilogue for linear quantizers that
+ * have a zero-point.  Sec. III-A writes a linear quantizer as X = s * x + z
+ * and rewrites it for bipolar values x' = 2x + 1 as X = (s/2) x' + (z - s/2):
+ * bipolar scale s' = s/2, bipolar zero z' = z - s/2.  With per-token (s'_a,
+ * z'_a) and per-channel (s'_w, z'_w) bipolar parameters, the product of the
+ * dequantized operands sum_k (s'_a a'[m][k] + z'_a)(s'_w w'[n][k] + z'_w) is
+ *   Y[m][n] = s'_a s'_w C + s'_a z'_w R_a[m] + z'_a (s'_w R_w[n] + K z'_w),
+ * with C the int32 product and R the bipolar row sums from the packers.
+ *   a_packed, w_packed, cfg, workspace, workspace_bytes, stream  as apt_gemm
+ *   a_rowsum, w_rowsum  device int32 [M] / [N] from the packers (required)
+ *   a_scale, a_zero     device fp16 bits [M], per-token s'_a and z'_a
+ *   w_scale, w_zero     device fp16 bits [N], per-channel s'_w and z'_w
+ *   c_fp16    device fp16 bits [M][N] row-major: fp16_rne of Y evaluated in
+ *             fp32 as s'_a (s'_w C + z'_w R_a) + z'_a (s'_w R_w + K z'_w)
+ *   c_int32   device int32 [M][N] row-major (the integer product C), or NULL
+ * Errors: as apt_gemm, and APT_ERR_INVALID_ARG when a row-sum, scale,
+ * zero-point or the c_fp16 pointer is NULL. */
+apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q,
+                             const void* a_packed, const void* w_packed,
+                             const int32_t* a_rowsum, const int32_t* w_rowsum,
+                             const uint16_t* a_scale, const uint16_t* a_zero,
+                             const uint16_t* w_scale, const uint16_t* w_zero,
+                             uint16_t* c_fp16, int32_t* c_int32,
+                             const apt_config_t* cfg,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* apt_status_string(apt_status_t status);
 

@@ -84,6 +84,9 @@ def lib() -> ctypes.CDLL:
         L.apt_gemm.argtypes = ([ctypes.c_int] * 5 + [_vp] * 8 + [ctypes.POINTER(apt_config_t)] +
                                [_vp, ctypes.c_size_t, _vp])
         L.apt_gemm.restype = ctypes.c_int
+        L.apt_gemm_affine.argtypes = ([ctypes.c_int] * 5 + [_vp] * 10 +
+                                      [ctypes.POINTER(apt_config_t)] + [_vp, ctypes.c_size_t, _vp])
+        L.apt_gemm_affine.restype = ctypes.c_int
         L.apt_status_string.argtypes = [ctypes.c_int]
         L.apt_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -133,6 +136,15 @@ def apt_gemm(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_s
     return lib().apt_gemm(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32,
                           a_scale, w_scale, c_fp16, ctypes.byref(cfg) if cfg is not None else None,
                           workspace, workspace_bytes, stream)
+
+
+def apt_gemm_affine(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, a_scale, a_zero,
+                    w_scale, w_zero, c_fp16, c_int32, cfg, workspace, workspace_bytes,
+                    stream) -> int:
+    return lib().apt_gemm_affine(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, a_scale,
+                                 a_zero, w_scale, w_zero, c_fp16, c_int32,
+                                 ctypes.byref(cfg) if cfg is not None else None, workspace,
+                                 workspace_bytes, stream)
 
 
 def status_string(status: int) -> str:
@@ -227,6 +239,28 @@ def gemm(a: Packed, w: Packed, out_int32: bool = True, a_scale=None, w_scale=Non
                    _ptr(a.rowsum), _ptr(w.rowsum), _ptr(c32), _ptr(a_scale), _ptr(w_scale),
                    _ptr(c16), cfg, ws_ptr, ws_len, _stream_ptr(stream)), "apt_gemm")
     return c32, c16
+
+
+def gemm_affine(a: Packed, w: Packed, a_scale, a_zero, w_scale, w_zero, out_int32: bool = False,
+                cfg: apt_config_t | None = None, stream=None, workspace=None):
+    """fp16 product of two zero-point quantizers in bipolar form (scales and
+    zeros are fp16 CUDA tensors [M] / [N]).  Returns (c_fp16, c_int32 or None)."""
+    torch = _torch()
+    assert a.K == w.K
+    M, N, K = a.rows, w.rows, a.K
+    dev = a.data.device
+    c16 = torch.empty((M, N), dtype=torch.float16, device=dev)
+    c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
+    ws_bytes = apt_gemm_workspace_bytes(M, N, K, w.bits, a.bits, cfg)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    check(apt_gemm_affine(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
+                          _ptr(a.rowsum), _ptr(w.rowsum), _ptr(a_scale), _ptr(a_zero),
+                          _ptr(w_scale), _ptr(w_zero), _ptr(c16), _ptr(c32), cfg, ws_ptr, ws_len,
+                          _stream_ptr(stream)), "apt_gemm_affine")
+    return c16, c32
 
 
 def select_config(M, N, K, p, q) -> apt_config_t:

@@ -102,11 +102,18 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
   return apt::int8_workspace_bytes(M, N, K, c);
 }
 
-apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, const void* w_packed,
-                      const int32_t* a_rowsum, const int32_t* w_rowsum, int32_t* c_int32,
-                      const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
-                      const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
-                      void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by apt_gemm and apt_gemm_affine once their own arguments are
+// checked: the common validation, config resolution and launch.
+apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed,
+                         const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                         int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                         uint16_t* c_fp16, const uint16_t* a_zero, const uint16_t* w_zero,
+                         const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
+                         void* stream) {
   if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return APT_ERR_INVALID_ARG;
   if (a_packed == nullptr || w_packed == nullptr || !aligned16(a_packed) || !aligned16(w_packed))
     return APT_ERR_INVALID_ARG;
@@ -138,6 +145,8 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, c
   g.a_scale = reinterpret_cast<const __half*>(a_scale);
   g.w_scale = reinterpret_cast<const __half*>(w_scale);
   g.c_fp16 = reinterpret_cast<__half*>(c_fp16);
+  g.a_zero = reinterpret_cast<const __half*>(a_zero);
+  g.w_zero = reinterpret_cast<const __half*>(w_zero);
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (c.route) {
     case APT_ROUTE_XOR: return hip_status(apt::launch_gemm_xor(g, c, s));
@@ -145,6 +154,33 @@ apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, c
     case APT_ROUTE_PM1_MFMA: return hip_status(apt::launch_gemm_pm1(g, c, s));
   }
   return APT_ERR_INVALID_ARG;
+}
+
+}  // namespace
+
+extern "C" {
+
+apt_status_t apt_gemm(int M, int N, int K, int p, int q, const void* a_packed, const void* w_packed,
+                      const int32_t* a_rowsum, const int32_t* w_rowsum, int32_t* c_int32,
+                      const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
+                      const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  return gemm_common(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale,
+                     w_scale, c_fp16, nullptr, nullptr, cfg, workspace, workspace_bytes, stream);
+}
+
+apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q, const void* a_packed,
+                             const void* w_packed, const int32_t* a_rowsum,
+                             const int32_t* w_rowsum, const uint16_t* a_scale,
+                             const uint16_t* a_zero, const uint16_t* w_scale,
+                             const uint16_t* w_zero, uint16_t* c_fp16, int32_t* c_int32,
+                             const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  if (a_rowsum == nullptr || w_rowsum == nullptr || a_scale == nullptr || a_zero == nullptr ||
+      w_scale == nullptr || w_zero == nullptr || c_fp16 == nullptr)
+    return APT_ERR_INVALID_ARG;
+  return gemm_common(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale,
+                     w_scale, c_fp16, a_zero, w_zero, cfg, workspace, workspace_bytes, stream);
 }
 
 const char* apt_status_string(apt_status_t status) {

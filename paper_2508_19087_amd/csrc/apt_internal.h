@@ -47,7 +47,20 @@ struct GemmArgs {
   const __half* a_scale;
   const __half* w_scale;
   __half* c_fp16;
+  // Zero-points of the fp16 epilogue (both set or both NULL); with them the
+  // row sums are required.
+  const __half* a_zero;
+  const __half* w_zero;
 };
+
+// fp16 epilogue value (float32 arithmetic; the caller rounds to fp16) of an
+// output C of two linear quantizers in bipolar form (Sec. III-A: scale s/2,
+// zero z - s/2): s_a s_w C + s_a z_w R_a + z_a (s_w R_w + K z_w), with
+// `colterm` = s_w R_w + K z_w precomputed per output column.
+__device__ __forceinline__ float affine_value(int32_t c, float sa, float sw, float zw, float ra,
+                                              float za, float colterm) {
+  return sa * (sw * (float)c + zw * ra) + za * colterm;
+}
 
 // XOR + popcount route (gemm_xor.hip).  Any shape.
 hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);

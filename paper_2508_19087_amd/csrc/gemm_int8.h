@@ -350,13 +350,16 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   const int wm = wave / WN, wn = wave % WN;
   // Epilogue terms of the tile being finished, staged in LDS after the ring:
   // c_a R_w[n] and the scale s_w[n] per column, c_w R_a[m] - const and s_a[m]
-  // per row.
+  // per row; with zero-points also z_w[n] and s_w R_w[n] + K z_w[n] per
+  // column, float(R_a[m]) and z_a[m] per row.
   uint32_t* const lds_wt = reinterpret_cast<uint32_t*>(lds + kStages * kStageBytes);
   uint32_t* const lds_at = lds_wt + BN;
   float* const lds_ws = reinterpret_cast<float*>(lds_at + BM);
   float* const lds_as = lds_ws + BN;
+  float* const lds_zt = lds_as + BM;   // z_w[n] | float(R_a[m])
+  float* const lds_zc = lds_zt + BN + BM;  // s_w R_w[n] + K z_w[n] | z_a[m]
   constexpr int kEpiStride = 32 * 4 + 16;  // bytes per row of a 32x32 int32 block in LDS
-  uint8_t* const epi_slot = lds + kStages * kStageBytes + (BN + BM) * 8 + wave * 32 * kEpiStride;
+  uint8_t* const epi_slot = lds + kStages * kStageBytes + (BN + BM) * 16 + wave * 32 * kEpiStride;
 
   Stream st;
   st.G = G;
@@ -492,13 +495,32 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
       }
     }
   };
-  auto stage_terms = [&]() __attribute__((always_inline)) {
+  // With zero-points the extra terms are read here, just before they are
+  // staged: once per tile, off the main loop's register budget.
+  const bool affine = g.a_zero != nullptr;
+  auto stage_terms = [&](int m0, int n0) __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < kTermsPerThread; ++k) {
       const int i = tid + k * T;
       if (i < BN + BM) {
         lds_wt[i] = term[k];  // lds_at follows lds_wt
         lds_ws[i] = scale[k];
+      }
+    }
+    if (affine) {
+#pragma unroll
+      for (int k = 0; k < kTermsPerThread; ++k) {
+        const int i = tid + k * T;
+        if (i < BN) {
+          const int n = min(n0 + i, g.N - 1);
+          const float zw = __half2float(g.w_zero[n]);
+          lds_zt[i] = zw;
+          lds_zc[i] = __half2float(g.w_scale[n]) * (float)g.w_rowsum[n] + (float)g.K * zw;
+        } else if (i < BN + BM) {
+          const int m = min(m0 + i - BN, g.M - 1);
+          lds_zt[i] = (float)g.a_rowsum[m];
+          lds_zc[i] = __half2float(g.a_zero[m]);
+        }
       }
     }
   };
@@ -547,11 +569,22 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
             }
             if (fp16) {
               const float sa = lds_as[ml];
+              float f[4];
+              if (affine) {
+                const v4f zw = *reinterpret_cast<const v4f*>(lds_zt + nl);
+                const v4f col = *reinterpret_cast<const v4f*>(lds_zc + nl);
+                const float ra = lds_zt[BN + ml], za = lds_zc[BN + ml];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) f[j] = affine_value(cv[j], sa, ws[j], zw[j], ra, za, col[j]);
+              } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) f[j] = (float)cv[j] * sa * ws[j];
+              }
               uint32_t hb[2];
 #pragma unroll
               for (int j = 0; j < 4; j += 2) {
-                const uint32_t h0 = __half_as_ushort(__float2half_rn((float)cv[j] * sa * ws[j]));
-                const uint32_t h1 = __half_as_ushort(__float2half_rn((float)cv[j + 1] * sa * ws[j + 1]));
+                const uint32_t h0 = __half_as_ushort(__float2half_rn(f[j]));
+                const uint32_t h1 = __half_as_ushort(__float2half_rn(f[j + 1]));
                 hb[j / 2] = h0 | (h1 << 16);
               }
               if (full)
@@ -690,7 +723,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     rw0.load(w_rsrc, wv2, NC, 2 * c2.pair);
     step(lds + s1 * kStageBytes, lds + s0 * kStageBytes, lds + s2 * kStageBytes, rw1,
          c1.m0, 2 * c1.pair);
-    if (part_end) stage_terms();
+    if (part_end) stage_terms(cp.m0, cp.n0);
     __syncthreads();
     if (__builtin_expect(part_end, 0)) {
       flush(cp);
@@ -744,7 +777,7 @@ constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 // LDS of shape S: the weight ring, the epilogue terms and one 32x32 int32
 // epilogue slot per wave.
 constexpr size_t lds_bytes(const TileShape& sh) {
-  return kStages * (size_t)sh.bn * kRowBytes + (size_t)(sh.bn + sh.bm) * 8 +
+  return kStages * (size_t)sh.bn * kRowBytes + (size_t)(sh.bn + sh.bm) * 16 +
          (size_t)sh.wm * sh.wn * 32 * (32 * 4 + 16);
 }
 

@@ -146,6 +146,10 @@ __global__ __launch_bounds__(kThreads) void gemm_pm1_kernel(Pm1Params prm) {
   const int n = n0 + wn * WTN + lrow;
   if (n >= g.N) return;
   const float sw_f = g.c_fp16 ? __half2float(g.w_scale[n]) : 0.f;
+  // zero-point terms of column n (the zeros need the row sums)
+  const bool affine = g.a_zero != nullptr;
+  const float zw_f = affine ? __half2float(g.w_zero[n]) : 0.f;
+  const float col_f = affine ? sw_f * (float)g.w_rowsum[n] + (float)g.K * zw_f : 0.f;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int m = m0 + wm * WTM + (v / 4) * 8 + (lane / 32) * 4 + (v % 4);
@@ -154,8 +158,15 @@ __global__ __launch_bounds__(kThreads) void gemm_pm1_kernel(Pm1Params prm) {
       const int64_t o = (int64_t)m * g.N + n;
       if (g.c_int32) g.c_int32[o] = cval;
       if (g.c_fp16) {
-        float f = (float)cval * __half2float(g.a_scale[m]);
-        g.c_fp16[o] = __float2half_rn(f * sw_f);
+        float f;
+        if (affine) {
+          f = affine_value(cval, __half2float(g.a_scale[m]), sw_f, zw_f, (float)g.a_rowsum[m],
+                           __half2float(g.a_zero[m]), col_f);
+        } else {
+          f = (float)cval * __half2float(g.a_scale[m]);
+          f = f * sw_f;
+        }
+        g.c_fp16[o] = __float2half_rn(f);
       }
     }
   }

@@ -108,8 +108,16 @@ __global__ __launch_bounds__(kWave* kWaves) void gemm_xor_kernel(XorParams prm) 
       const int64_t o = (int64_t)mg * g.N + n;
       if (g.c_int32) g.c_int32[o] = c;
       if (g.c_fp16) {
-        float f = (float)c * __half2float(g.a_scale[mg]);
-        f = f * __half2float(g.w_scale[n]);
+        float f;
+        if (g.a_zero) {
+          const float sw = __half2float(g.w_scale[n]), zw = __half2float(g.w_zero[n]);
+          f = affine_value(c, __half2float(g.a_scale[mg]), sw, zw, (float)g.a_rowsum[mg],
+                           __half2float(g.a_zero[mg]),
+                           sw * (float)g.w_rowsum[n] + (float)g.K * zw);
+        } else {
+          f = (float)c * __half2float(g.a_scale[mg]);
+          f = f * __half2float(g.w_scale[n]);
+        }
         g.c_fp16[o] = __float2half_rn(f);
       }
     }

@@ -13,7 +13,7 @@ def test_exports_every_declared_symbol():
     names = apt.header_functions()
     assert set(names) == {"apt_packed_bytes", "apt_pack_weights", "apt_quantize_pack_activations",
                           "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
-                          "apt_status_string"}
+                          "apt_gemm_affine", "apt_status_string"}
     L = apt.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -166,6 +166,27 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
 ])
 def test_gemm_validation(kw, want):
     assert gemm(**kw) == want
+
+
+def gemm_affine(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, sa=S, za=S + 64, sw=S + 128,
+                zw=S + 192, c16=C, c32=None, cfg=None, ws=None, ws_bytes=0):
+    return apt.apt_gemm_affine(M, N, K, p, q, a, w, ra, rw, sa, za, sw, zw, c16, c32, cfg, ws,
+                               ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(ra=None), apt.APT_ERR_INVALID_ARG), (dict(rw=None), apt.APT_ERR_INVALID_ARG),
+    (dict(sa=None), apt.APT_ERR_INVALID_ARG), (dict(za=None), apt.APT_ERR_INVALID_ARG),
+    (dict(sw=None), apt.APT_ERR_INVALID_ARG), (dict(zw=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c16=None, c32=C), apt.APT_ERR_INVALID_ARG), (dict(M=0), apt.APT_ERR_INVALID_ARG),
+    (dict(q=0), apt.APT_ERR_INVALID_ARG), (dict(a=A + 4), apt.APT_ERR_INVALID_ARG),
+    (dict(K=33026, p=8, q=8), apt.APT_ERR_UNSUPPORTED),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=5)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_WORKSPACE),
+])
+def test_gemm_affine_validation(kw, want):
+    assert gemm_affine(**kw) == want
 
 
 @pytest.mark.parametrize("kw", [dict(rows=0), dict(K=0), dict(bits=0), dict(bits=9),
