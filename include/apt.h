@@ -26,7 +26,8 @@
  *     Calls that take a stream validate their arguments on the host, enqueue
  *     their kernels on that stream and return without synchronising.
  *   - No call launches anything when validation fails.
- *   - The library holds no mutable global state; calls are thread-safe.
+ *   - The only mutable state the library holds is the configuration table that
+ *     apt_search_config fills; a lock guards it, and calls are thread-safe.
  *   - Codes outside the signed b-bit range are reduced modulo 2^b (only the low
  *     b bits of each int8 code are used).
  *
@@ -155,9 +156,12 @@ apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, i
                                                 void* a_packed, int32_t* a_rowsum,
                                                 uint16_t* a_scale, void* stream);
 
-/* Host-only.  Chooses the route and tile shape for (M, N, K, p, q) from the
- * table measured on MI355X, falling back to the nearest entry (Sec. V-B,
- * lookup table and approximate matching).  The choice never changes results.
+/* Host-only.  Chooses the route and tile shape for (M, N, K, p, q) (Sec. V-B:
+ * lookup table, approximate matching): the config apt_search_config recorded
+ * for exactly this problem, if any; otherwise a model of the MI355X kernels
+ * (rounds of resident tiles per compute unit, measured cycles per chunk pair
+ * of each tile shape, stream-K partial traffic), which stands in for the
+ * approximate match.  The choice never changes results.
  * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8] or out == NULL. */
 apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out);
 
@@ -225,6 +229,44 @@ apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q,
                              uint16_t* c_fp16, int32_t* c_int32,
                              const apt_config_t* cfg,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Device workspace bytes apt_search_config needs for this problem: the most
+ * that any config it times needs (apt_gemm_workspace_bytes).  Returns 0 for
+ * invalid sizes or bit widths. */
+size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q);
+
+/* The best-kernel search module (Sec. V-B): times every configuration the
+ * library can run for (M, N, K, p, q) on the caller's operands, records the
+ * fastest in the configuration table, so that apt_select_config and apt_gemm
+ * with cfg NULL use it for this problem from then on, and returns it.  The
+ * candidates are the XOR route, the +-1 plane route (p, q <= 7), every int8
+ * tile shape with one workgroup per tile and with one persistent round of
+ * workgroups, and the split launches of a main and a tail shape.  Each is
+ * run twice to warm up, then timed over 5 back-to-back calls between two HIP
+ * events on `stream`.  The call blocks until the timing has finished.  All
+ * candidates compute the same result, so it never changes results.
+ *   a_packed, w_packed, a_rowsum, w_rowsum  device, as apt_gemm (required)
+ *   c_int32   device int32 [M][N]; overwritten by the timed calls
+ *   workspace, workspace_bytes  device scratch of at least
+ *             apt_search_workspace_bytes(...) bytes, 16-byte aligned (NULL when 0)
+ *   best      host; receives the chosen config
+ *   best_us   host or NULL; receives its mean time per call in microseconds
+ * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8], a NULL or
+ * misaligned operand, row-sum, output or best pointer, or a misaligned
+ * workspace; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31 or no
+ * candidate can run; APT_ERR_WORKSPACE when the workspace is missing or too
+ * small; APT_ERR_HIP when a launch or an event call fails. */
+apt_status_t apt_search_config(int M, int N, int K, int p, int q,
+                               const void* a_packed, const void* w_packed,
+                               const int32_t* a_rowsum, const int32_t* w_rowsum,
+                               int32_t* c_int32, void* workspace, size_t workspace_bytes,
+                               void* stream, apt_config_t* best, float* best_us);
+
+/* Empties the configuration table that apt_search_config fills. */
+void apt_config_table_clear(void);
+
+/* Number of problems in the configuration table. */
+int apt_config_table_size(void);
 
 /* Static, NUL-terminated description of a status code. */
 const char* apt_status_string(apt_status_t status);

@@ -67,6 +67,10 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise ImportError("libapt.so is not built (run __graft_entry__.build() or "
                               "python paper_2508_19087_amd/build.py): %s" % LIB_PATH)
+        # torch's HIP runtime must be loaded first: the library's libamdhip64
+        # dependency then binds to the runtime that owns torch's device memory
+        # and streams, not to a second copy of it.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         L.apt_packed_bytes.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.apt_packed_bytes.restype = ctypes.c_size_t
@@ -87,6 +91,15 @@ def lib() -> ctypes.CDLL:
         L.apt_gemm_affine.argtypes = ([ctypes.c_int] * 5 + [_vp] * 10 +
                                       [ctypes.POINTER(apt_config_t)] + [_vp, ctypes.c_size_t, _vp])
         L.apt_gemm_affine.restype = ctypes.c_int
+        L.apt_search_workspace_bytes.argtypes = [ctypes.c_int] * 5
+        L.apt_search_workspace_bytes.restype = ctypes.c_size_t
+        L.apt_search_config.argtypes = ([ctypes.c_int] * 5 + [_vp] * 6 + [ctypes.c_size_t, _vp,
+                                        ctypes.POINTER(apt_config_t), ctypes.POINTER(ctypes.c_float)])
+        L.apt_search_config.restype = ctypes.c_int
+        L.apt_config_table_clear.argtypes = []
+        L.apt_config_table_clear.restype = None
+        L.apt_config_table_size.argtypes = []
+        L.apt_config_table_size.restype = ctypes.c_int
         L.apt_status_string.argtypes = [ctypes.c_int]
         L.apt_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -145,6 +158,29 @@ def apt_gemm_affine(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, a_sca
                                  a_zero, w_scale, w_zero, c_fp16, c_int32,
                                  ctypes.byref(cfg) if cfg is not None else None, workspace,
                                  workspace_bytes, stream)
+
+
+def apt_search_workspace_bytes(M, N, K, p, q) -> int:
+    return int(lib().apt_search_workspace_bytes(M, N, K, p, q))
+
+
+def apt_search_config(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, workspace,
+                      workspace_bytes, stream):
+    """(status, apt_config_t, microseconds per call)."""
+    c = apt_config_t()
+    us = ctypes.c_float(0.0)
+    st = lib().apt_search_config(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32,
+                                 workspace, workspace_bytes, stream, ctypes.byref(c),
+                                 ctypes.byref(us))
+    return st, c, float(us.value)
+
+
+def apt_config_table_clear() -> None:
+    lib().apt_config_table_clear()
+
+
+def apt_config_table_size() -> int:
+    return int(lib().apt_config_table_size())
 
 
 def status_string(status: int) -> str:
@@ -261,6 +297,25 @@ def gemm_affine(a: Packed, w: Packed, a_scale, a_zero, w_scale, w_zero, out_int3
                           _ptr(w_scale), _ptr(w_zero), _ptr(c16), _ptr(c32), cfg, ws_ptr, ws_len,
                           _stream_ptr(stream)), "apt_gemm_affine")
     return c16, c32
+
+
+def search_config(a: Packed, w: Packed, stream=None):
+    """Runs the search module on packed operands (device tensors); returns
+    (best apt_config_t, microseconds per call).  The result is recorded in the
+    library's table for this (M, N, K, p, q)."""
+    torch = _torch()
+    assert a.K == w.K
+    M, N, K = a.rows, w.rows, a.K
+    dev = a.data.device
+    c32 = torch.empty((M, N), dtype=torch.int32, device=dev)
+    ws_bytes = apt_search_workspace_bytes(M, N, K, w.bits, a.bits)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes > 0 else None
+    st, c, us = apt_search_config(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
+                                  a.rowsum.data_ptr(), w.rowsum.data_ptr(), c32.data_ptr(),
+                                  ws.data_ptr() if ws is not None else None, ws_bytes,
+                                  _stream_ptr(stream))
+    check(st, "apt_search_config")
+    return c, us
 
 
 def select_config(M, N, K, p, q) -> apt_config_t:

@@ -4,6 +4,8 @@
 // neither the device nor the runtime.
 #include <string.h>
 
+#include <algorithm>
+
 #include "apt_internal.h"
 
 namespace {
@@ -182,6 +184,87 @@ apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q, const void* a_pa
   return gemm_common(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale,
                      w_scale, c_fp16, a_zero, w_zero, cfg, workspace, workspace_bytes, stream);
 }
+
+size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q) {
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return 0;
+  apt_config_t cand[apt::kMaxCandidates];
+  const int n = apt::candidate_configs(M, N, K, p, q, cand, apt::kMaxCandidates);
+  size_t most = 0;
+  for (int i = 0; i < n; ++i)
+    if (cand[i].route == APT_ROUTE_INT8_MFMA && apt::int8_config_ok(cand[i], N))
+      most = std::max(most, apt::int8_workspace_bytes(M, N, K, cand[i]));
+  return most;
+}
+
+apt_status_t apt_search_config(int M, int N, int K, int p, int q, const void* a_packed,
+                               const void* w_packed, const int32_t* a_rowsum,
+                               const int32_t* w_rowsum, int32_t* c_int32, void* workspace,
+                               size_t workspace_bytes, void* stream, apt_config_t* best,
+                               float* best_us) {
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return APT_ERR_INVALID_ARG;
+  if (a_packed == nullptr || w_packed == nullptr || !aligned16(a_packed) || !aligned16(w_packed) ||
+      a_rowsum == nullptr || w_rowsum == nullptr || c_int32 == nullptr || best == nullptr)
+    return APT_ERR_INVALID_ARG;
+  if (!fits_int32(K, p, q)) return APT_ERR_UNSUPPORTED;
+  const size_t need = apt_search_workspace_bytes(M, N, K, p, q);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return APT_ERR_WORKSPACE;
+  if (workspace != nullptr && !aligned16(workspace)) return APT_ERR_INVALID_ARG;
+
+  apt_config_t cand[apt::kMaxCandidates];
+  const int n = apt::candidate_configs(M, N, K, p, q, cand, apt::kMaxCandidates);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess) return APT_ERR_HIP;
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return APT_ERR_HIP;
+  }
+  constexpr int kWarm = 2, kTimed = 5;
+  apt_status_t st = APT_OK;
+  int best_i = -1;
+  float best_t = 0.f;
+  auto call = [&](const apt_config_t& c) {
+    return gemm_common(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, nullptr,
+                       nullptr, nullptr, nullptr, nullptr, &c, workspace, workspace_bytes, stream);
+  };
+  for (int i = 0; i < n && st == APT_OK; ++i) {
+    apt_status_t r = call(cand[i]);
+    if (r == APT_ERR_HIP) {
+      st = r;
+      break;
+    }
+    if (r != APT_OK) continue;  // a candidate this problem cannot take
+    for (int w = 1; w < kWarm && st == APT_OK; ++w) st = call(cand[i]);
+    if (st != APT_OK || hipEventRecord(e0, s) != hipSuccess) {
+      st = APT_ERR_HIP;
+      break;
+    }
+    for (int t = 0; t < kTimed && st == APT_OK; ++t) st = call(cand[i]);
+    float ms = 0.f;
+    if (st != APT_OK || hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+        hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+      st = APT_ERR_HIP;
+      break;
+    }
+    const float us = ms * 1000.f / kTimed;
+    if (best_i < 0 || us < best_t) {
+      best_i = i;
+      best_t = us;
+    }
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (st != APT_OK) return st;
+  if (best_i < 0) return APT_ERR_UNSUPPORTED;
+  apt::table_store(M, N, K, p, q, cand[best_i]);
+  *best = cand[best_i];
+  if (best_us != nullptr) *best_us = best_t;
+  return APT_OK;
+}
+
+void apt_config_table_clear(void) { apt::table_clear(); }
+
+int apt_config_table_size(void) { return apt::table_size(); }
 
 const char* apt_status_string(apt_status_t status) {
   switch (status) {

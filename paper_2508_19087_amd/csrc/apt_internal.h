@@ -79,7 +79,15 @@ size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg);
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
 bool pm1_config_ok(const apt_config_t& cfg, int p, int q);
 
-// Host-side selector (select.cpp).
+// Host-side selector (select.hip): the search module's table first, then the
+// model.
 apt_config_t select_config(int M, int N, int K, int p, int q);
+bool table_lookup(int M, int N, int K, int p, int q, apt_config_t* out);
+void table_store(int M, int N, int K, int p, int q, const apt_config_t& c);
+void table_clear();
+int table_size();
+// Configs the search module times for a problem (at most max_out of them).
+constexpr int kMaxCandidates = 32;
+int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int max_out);
 
 }  // namespace apt

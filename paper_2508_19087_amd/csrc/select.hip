@@ -1,6 +1,11 @@
 // select.hip - host-side kernel-config selector (APT-LLM, arXiv 2508.19087,
 // Sec. V: tunable hyperparameters, lookup table, approximate matching).
 //
+// Lookup table: configs found by the search module (apt_search_config, Sec.
+// V-B "best kernel search") are kept per (M, N, K, p, q) and win over the
+// model below for exactly that problem; every other problem takes the model,
+// which plays the part of the paper's approximate matching.
+//
 // The paper searches, per (M, N, K, bits), the block/warp shapes that satisfy
 // its tile constraint and stores the fastest in a table.  Here the
 // configuration space is the route plus the workgroup tile and wave grid the
@@ -10,6 +15,9 @@
 // compute units run, how fast each tile shape runs and what the stream-K
 // partial tiles cost.  A choice never changes results.
 #include <algorithm>
+#include <array>
+#include <map>
+#include <mutex>
 
 #include "apt_internal.h"
 
@@ -89,9 +97,92 @@ double model_cycles(const Int8Shape& s, int M, int N, int K, int grid, int cus) 
 
 }  // namespace
 
+namespace {
+
+// The table; its lock makes the library's only mutable state safe to share
+// between threads.
+std::mutex g_table_mu;
+std::map<std::array<int, 5>, apt_config_t> g_table;
+
+}  // namespace
+
+bool table_lookup(int M, int N, int K, int p, int q, apt_config_t* out) {
+  std::lock_guard<std::mutex> lock(g_table_mu);
+  auto it = g_table.find({M, N, K, p, q});
+  if (it == g_table.end()) return false;
+  *out = it->second;
+  return true;
+}
+
+void table_store(int M, int N, int K, int p, int q, const apt_config_t& c) {
+  std::lock_guard<std::mutex> lock(g_table_mu);
+  g_table[{M, N, K, p, q}] = c;
+}
+
+void table_clear() {
+  std::lock_guard<std::mutex> lock(g_table_mu);
+  g_table.clear();
+}
+
+int table_size() {
+  std::lock_guard<std::mutex> lock(g_table_mu);
+  return (int)g_table.size();
+}
+
+// Every config the search module times for (M, N, K, p, q): the XOR route,
+// the +-1 plane route where its operands fit (p, q <= 7), each int8 tile shape
+// with one workgroup per tile and with a persistent grid of one round of
+// workgroups, and the split launches the model considers (a main shape over
+// whole rounds of columns, a smaller shape on the rest).
+int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int max_out) {
+  (void)K;
+  int n = 0;
+  auto add = [&](const apt_config_t& c) {
+    if (n < max_out) out[n++] = c;
+  };
+  apt_config_t x = base_config(APT_ROUTE_XOR);
+  x.mt = 8;
+  add(x);
+  if (p <= 7 && q <= 7) add(base_config(APT_ROUTE_PM1_MFMA));
+  const int cus = compute_units();
+  auto int8_cfg = [&](const Int8Shape& s, int grid) {
+    apt_config_t c = base_config(APT_ROUTE_INT8_MFMA);
+    c.bm = s.bm;
+    c.bn = s.bn;
+    c.bk = kChunk;
+    c.waves_m = s.wm;
+    c.waves_n = s.wn;
+    c.lds_stages = 3;
+    c.grid = grid;
+    return c;
+  };
+  for (int i = 0; i < kNumInt8Shapes; ++i) {
+    const Int8Shape& s = kInt8Shapes[i];
+    add(int8_cfg(s, 0));
+    add(int8_cfg(s, std::min(cus * s.per_cu, kMaxGrid)));
+  }
+  for (int i = 0; i < kNumMainShapes; ++i) {
+    const Int8Shape& s = kInt8Shapes[i];
+    const int tiles_m = (M + s.bm - 1) / s.bm;
+    const int cols_per_round = cus * s.per_cu / tiles_m;
+    const int tiles_n = (N + s.bn - 1) / s.bn;
+    if (cols_per_round < 1 || tiles_n <= cols_per_round) continue;
+    const int split = tiles_n / cols_per_round * cols_per_round * s.bn;
+    if (split >= N) continue;
+    for (int t = kNumMainShapes; t < kNumInt8Shapes; ++t) {
+      apt_config_t c = int8_cfg(s, 0);
+      c.split_n = split;
+      c.tail_bm = kInt8Shapes[t].bm;
+      c.tail_bn = kInt8Shapes[t].bn;
+      add(c);
+    }
+  }
+  return n;
+}
+
 apt_config_t select_config(int M, int N, int K, int p, int q) {
-  (void)p;
-  (void)q;
+  apt_config_t hit;
+  if (table_lookup(M, N, K, p, q, &hit)) return hit;
   if (M <= 8) {
     apt_config_t c = base_config(APT_ROUTE_XOR);
     c.mt = 8;

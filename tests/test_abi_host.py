@@ -13,7 +13,8 @@ def test_exports_every_declared_symbol():
     names = apt.header_functions()
     assert set(names) == {"apt_packed_bytes", "apt_pack_weights", "apt_quantize_pack_activations",
                           "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
-                          "apt_gemm_affine", "apt_status_string"}
+                          "apt_gemm_affine", "apt_search_workspace_bytes", "apt_search_config",
+                          "apt_config_table_clear", "apt_config_table_size", "apt_status_string"}
     L = apt.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -223,3 +224,45 @@ def test_pack_rejects_huge_rows():
 
 def test_config_struct_layout():
     assert ctypes.sizeof(apt.apt_config_t) == 16 * 4
+
+
+def search(M=64, N=300, K=1000, p=2, q=4, a=A, w=W, ra=RA, rw=RW, c32=C, ws=None, ws_bytes=0):
+    return apt.apt_search_config(M, N, K, p, q, a, w, ra, rw, c32, ws, ws_bytes, None)[0]
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(M=0), apt.APT_ERR_INVALID_ARG), (dict(p=9), apt.APT_ERR_INVALID_ARG),
+    (dict(a=None), apt.APT_ERR_INVALID_ARG), (dict(w=W + 4), apt.APT_ERR_INVALID_ARG),
+    (dict(ra=None), apt.APT_ERR_INVALID_ARG), (dict(rw=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c32=None), apt.APT_ERR_INVALID_ARG),
+    (dict(K=33026, p=8, q=8), apt.APT_ERR_UNSUPPORTED),
+    (dict(), apt.APT_ERR_WORKSPACE),                      # q = 4: stream-K candidates need room
+    (dict(ws=WS, ws_bytes=1024), apt.APT_ERR_WORKSPACE),
+    (dict(ws=WS + 8, ws_bytes=1 << 40), apt.APT_ERR_INVALID_ARG),
+])
+def test_search_validation(kw, want):
+    """Every case is rejected on the host before any HIP call."""
+    assert search(**kw) == want
+
+
+def test_search_best_pointer_required():
+    L = apt.lib()
+    st = L.apt_search_config(64, 300, 1000, 2, 4, A, W, RA, RW, C, WS, 1 << 40, None, None, None)
+    assert st == apt.APT_ERR_INVALID_ARG
+
+
+def test_search_workspace_covers_every_selectable_config():
+    for shape in _shapes():
+        need = apt.apt_search_workspace_bytes(*shape)
+        assert need >= apt.apt_gemm_workspace_bytes(*shape, None)
+        # each int8 tile shape with a persistent round of workgroups is a candidate
+        M, N, K, p, q = shape
+        for bm, bn, wm, wn in [(256, 256, 4, 2), (256, 128, 4, 2), (512, 128, 8, 1)]:
+            c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 256, 3)
+            assert need >= apt.apt_gemm_workspace_bytes(M, N, K, p, q, c)
+    assert apt.apt_search_workspace_bytes(0, 1, 1, 1, 1) == 0
+
+
+def test_config_table_starts_empty_and_clears():
+    apt.apt_config_table_clear()
+    assert apt.apt_config_table_size() == 0
