@@ -217,6 +217,73 @@ def route_table(calls: int = 20):
     return out
 
 
+def search_table(calls: int = 20):
+    """Config selection evidence (Sec. V-B): for every workload shape, the
+    model's config and the best-kernel search module's pick (apt_search_config
+    over every runnable config), each timed with events around `calls`
+    back-to-back apt_gemm calls (warm weights, int32 output)."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    import synth
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+    probs = [synth.w2a2_decode(M, N) for M in (1, 4, 8) for N in (4096, synth.MLP)]
+    probs += [synth.w4a4_prefill()] + [synth.sweep_down(i) for i in range(len(synth.SWEEP_BITS))]
+    probs += [synth.layer_w2a4(name, M) for M in (1, 1024) for name in ("q", "gate", "down")]
+
+    def short(c):
+        if c.route == apt.APT_ROUTE_XOR:
+            return "xor"
+        if c.route == apt.APT_ROUTE_PM1_MFMA:
+            return "pm1"
+        t = "int8 %dx%d/%dx%d g%d" % (c.bm, c.bn, c.waves_m, c.waves_n, c.grid)
+        if c.split_n:
+            t += " +%dx%d@%d g%d" % (c.tail_bm, c.tail_bn, c.split_n, c.tail_grid)
+        return t
+
+    rows = []
+    apt.apt_config_table_clear()
+    for prob in probs:
+        a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
+        w = apt.pack(dev(prob.w_codes), prob.p)
+        c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+        sp = torch.cuda.current_stream().cuda_stream
+
+        def timed(cfg):
+            wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+
+            def call():
+                apt.check(apt.apt_gemm(prob.M, prob.N, prob.K, prob.p, prob.q, a.data.data_ptr(),
+                                       w.data.data_ptr(), a.rowsum.data_ptr(), w.rowsum.data_ptr(),
+                                       c32.data_ptr(), None, None, None, cfg, ws.data_ptr(), wsb, sp),
+                          "apt_gemm")
+            for _ in range(3):
+                call()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(calls):
+                call()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3 / calls
+
+        model = apt.select_config(prob.M, prob.N, prob.K, prob.p, prob.q)
+        t_model = timed(model)
+        best, t_search = apt.search_config(a, w)
+        t_best = timed(best)
+        rows.append({"problem": prob.name, "model": short(model), "model_us": round(t_model, 2),
+                     "searched": short(best), "searched_us": round(t_best, 2),
+                     "search_timing_us": round(t_search, 2)})
+        log("bench: search %s: model %s %.2f us, searched %s %.2f us"
+            % (prob.name, short(model), t_model, short(best), t_best))
+        del a, w, c32
+    apt.apt_config_table_clear()
+    return rows
+
+
 def decode_cold(wl, reps: int = 3):
     """The M=1 decode GEMMs with cold weights: rotate through enough packed
     weight copies (> 2x the Infinity Cache) that every launch reads HBM."""
@@ -410,6 +477,9 @@ def main():
                     help="summarize two rocprofv3 --pmc runs of --counters-run into profiles/")
     ap.add_argument("--routes", action="store_true",
                     help="print the route-choice table (us per call of every route) and exit")
+    ap.add_argument("--search", action="store_true",
+                    help="print the model's and the search module's config for every workload "
+                         "shape, with their times, and exit")
     ap.add_argument("--traffic-commands", default="",
                     help="the commands that produced the --write-traffic directories")
     args = ap.parse_args()
@@ -429,6 +499,9 @@ def main():
         return
     if args.routes:
         print(json.dumps(route_table(), indent=1), flush=True)
+        return
+    if args.search:
+        print(json.dumps(search_table(), indent=1), flush=True)
         return
     log("bench: building workload")
     wl = Workload()
