@@ -523,13 +523,18 @@ def main():
     pre = wl.pre
     achieved = pre.ops / gemm_s / 1e12
     traffic = stored_traffic()
+    sel = wl.apt.select_config(pre.M, pre.N, pre.K, pre.p, pre.q)
+    cfg = sel.as_dict()
+    tiles = "%dx%d tiles (%dx%d waves)" % (sel.bm, sel.bn, sel.waves_m, sel.waves_n)
+    if sel.split_n:
+        tiles += " over columns [0, %d) and %dx%d tiles over the rest" % (sel.split_n, sel.tail_bm,
+                                                                          sel.tail_bn)
+    tiles += ", one workgroup per tile" if sel.grid == 0 else ", %d persistent workgroups" % sel.grid
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": traffic,
                 "kernel": "apt_gemm W4A4 M=2048 N=11008 K=4096: expand_a_kernel + gemm_int8 kernel "
-                          "(one paired launch of the main and tail tiles), %d back-to-back calls"
-                          % args.roofline_calls,
+                          "(%s), %d back-to-back calls" % (tiles, args.roofline_calls),
                 "avg_launch_us": round(gemm_s * 1e6, 2)}
-    cfg = wl.apt.select_config(pre.M, pre.N, pre.K, pre.p, pre.q).as_dict()
     result = {
         "metric": METRIC, "value": round(wl.ops / step_s / 1e12, 3), "unit": "TOPS",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,

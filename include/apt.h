@@ -79,7 +79,8 @@ enum {
  * terms).  Fields a route does not use are ignored.
  *   route      APT_ROUTE_*
  *   bm, bn     output tile per workgroup (int8 MFMA route: 256x256 with 4x2 or
- *              2x4 waves, 256x128 with 4x2, 128x128 with 2x2)
+ *              2x4 waves, 512x128 with 8x1, 256x128 with 4x2 or 4x1, 128x128
+ *              with 2x2; the 4-wave shapes run two workgroups per compute unit)
  *   bk         K elements staged per pipeline step (MFMA routes: 0 or 128)
  *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route)
  *   grid       int8 MFMA route: persistent workgroups, 0..4096.  0 = one
@@ -93,9 +94,11 @@ enum {
  *   mt         XOR route: activation rows per workgroup (0 or 8)
  *   split_n    int8 MFMA route: 0, or a multiple of bn with 0 < split_n < N
  *              and of 8: columns [0, split_n) use the tile above and columns
- *              [split_n, N) a second launch with tile tail_bm x tail_bn (the
- *              first configured shape of that size) and tail_grid persistent
- *              workgroups (same meaning as grid)
+ *              [split_n, N) a second launch with tile tail_bm x tail_bn (of
+ *              the shapes of that size, the one with the main tile's wave
+ *              count, else the first) and tail_grid persistent workgroups
+ *              (same meaning as grid); main and tail share one launch when
+ *              their wave counts match and the pair is built
  *   reserved   ignored
  */
 typedef struct {

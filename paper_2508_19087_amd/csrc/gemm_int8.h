@@ -741,7 +741,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
 }
 
 template <int P, int BM, int BN, int WM, int WN, int SPLIT>
-__global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm) {
+__global__ __launch_bounds__(WM* WN* kWave, (WM * WN == 4) ? 2 : 1) void gemm_int8_kernel(Int8Params prm) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   gemm_int8_body<P, BM, BN, WM, WN, SPLIT>(prm, lds, blockIdx.x, gridDim.x);
 }
@@ -752,7 +752,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_int8_kernel(Int8Params prm
 // A's last tiles and output stores are still in flight.
 template <int P, int BMA, int BNA, int WMA, int WNA, int SA, int BMB, int BNB, int WMB, int WNB,
           int SB>
-__global__ __launch_bounds__(WMA* WNA* kWave) void gemm_int8_pair_kernel(Int8Params prm_a,
+__global__ __launch_bounds__(WMA* WNA* kWave, (WMA * WNA == 4) ? 2 : 1) void gemm_int8_pair_kernel(Int8Params prm_a,
                                                                          Int8Params prm_b, int g0) {
   static_assert(WMA * WNA == WMB * WNB, "both shapes need the same workgroup size");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -771,6 +771,7 @@ constexpr TileShape kShapes[] = {
     {256, 128, 4, 2, 4},
     {128, 128, 2, 2, 2},
     {512, 128, 8, 1, 4},
+    {256, 128, 4, 1, 2},
 };
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
@@ -803,6 +804,7 @@ inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int grid, hip
     case 2: return launch_shape<P, 2>(prm, grid, stream);
     case 3: return launch_shape<P, 3>(prm, grid, stream);
     case 4: return launch_shape<P, 4>(prm, grid, stream);
+    case 5: return launch_shape<P, 5>(prm, grid, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -822,15 +824,20 @@ hipError_t launch_pair_shapes(const Int8Params& pa, int ga, const Int8Params& pb
   return hipGetLastError();
 }
 
-// The shape pairs built as one launch (8 waves each): 256x256 or 512x128
-// main tiles, then 256x128 tail tiles.
-inline bool pair_supported(int sa, int sb) { return (sa == 0 || sa == 4) && sb == 2; }
+// The shape pairs built as one launch (same wave count): 256x256 or 512x128
+// main tiles with 256x128 (4x2) tail tiles (8 waves); 256x128 (4x1) main
+// tiles with 128x128 or 256x128 (4x1) tail tiles (4 waves).
+inline bool pair_supported(int sa, int sb) {
+  return ((sa == 0 || sa == 4) && sb == 2) || (sa == 5 && (sb == 3 || sb == 5));
+}
 
 template <int P>
 inline hipError_t launch_p_pair(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
                                 int gb, hipStream_t stream) {
   if (sa == 0 && sb == 2) return launch_pair_shapes<P, 0, 2>(pa, ga, pb, gb, stream);
   if (sa == 4 && sb == 2) return launch_pair_shapes<P, 4, 2>(pa, ga, pb, gb, stream);
+  if (sa == 5 && sb == 3) return launch_pair_shapes<P, 5, 3>(pa, ga, pb, gb, stream);
+  if (sa == 5 && sb == 5) return launch_pair_shapes<P, 5, 5>(pa, ga, pb, gb, stream);
   return hipErrorInvalidValue;
 }
 

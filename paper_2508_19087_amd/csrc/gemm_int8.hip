@@ -78,11 +78,18 @@ Plan make_plan(int M, int K, int shape, int n_begin, int n_cols, int grid) {
   return pl;
 }
 
-// The tail tile is named by its size; the first shape of that size is used.
+// The tail tile is named by its size: of the shapes of that size, the one
+// with the main shape's wave count (so that the two can share a launch), else
+// the first.
 int tail_index(const apt_config_t& cfg) {
+  int first = -1;
+  const int waves = cfg.waves_m * cfg.waves_n;
   for (int s = 0; s < kNumShapes; ++s)
-    if (kShapes[s].bm == cfg.tail_bm && kShapes[s].bn == cfg.tail_bn) return s;
-  return -1;
+    if (kShapes[s].bm == cfg.tail_bm && kShapes[s].bn == cfg.tail_bn) {
+      if (kShapes[s].wm * kShapes[s].wn == waves) return s;
+      if (first < 0) first = s;
+    }
+  return first;
 }
 
 // One or two launches: (main over [0, split_n), tail over [split_n, N)).

@@ -26,24 +26,30 @@ namespace {
 
 struct Int8Shape {
   int bm, bn, wm, wn;
-  int per_cu;           // workgroups resident per compute unit (LDS-limited)
-  double pair_cycles;   // cycles per chunk pair of one workgroup, compute unit full
+  int per_cu;            // workgroups resident per compute unit (registers and LDS)
+  double pair_us;        // microseconds per chunk pair of one workgroup, per_cu of them on its CU
+  double pair_alone_us;  // the same with the workgroup alone on its compute unit
+  double fixed_us;       // launch, first loads and the last epilogue of one full round
 };
 
-// Measured on MI355X for K = 4096 tiles (kernel clock about 1.9 GHz).
+// Measured on MI355X at W4A4, M = 2048, K = 2048 and 6144 (the K slope gives
+// the pair time, its intercept the fixed time), with one full round of tiles
+// and, for the 4-wave shapes, half a round (one workgroup per compute unit).
 constexpr Int8Shape kInt8Shapes[] = {
-    {256, 256, 4, 2, 1, 5200.0},
-    {512, 128, 8, 1, 1, 4800.0},
-    {256, 128, 4, 2, 1, 3000.0},
-    {128, 128, 2, 2, 2, 3000.0},
+    {256, 256, 4, 2, 1, 3.74, 3.74, 19.6},
+    {512, 128, 8, 1, 1, 2.81, 2.81, 21.4},
+    {256, 128, 4, 1, 2, 3.39, 1.81, 12.9},
+    {256, 128, 4, 2, 1, 2.04, 2.04, 12.3},
+    {128, 128, 2, 2, 2, 1.88, 1.17, 12.2},
 };
-// Main shapes that pair with a tail shape in one launch (same wave count):
-// the first two above with the third.
-constexpr int kNumMainShapes = 2;
-constexpr int kPairTail = 2;
 constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
-constexpr double kPartialBytesPerCycle = 2500.0;  // device-wide partial-tile traffic rate
-constexpr double kTileFixedCycles = 4000.0;      // start-up and final epilogue of a workgroup
+// Main shapes of a split launch (the first three above) and their tails (the
+// last three); a main and a tail with the same wave count share one launch.
+constexpr int kNumMainShapes = 3;
+constexpr int kFirstTail = 2;
+// Device-wide rate at which stream-K partial tiles are written and read back
+// (bytes per microsecond), as the stream-K launches measured on MI355X show.
+constexpr double kPartialBytesPerUs = 2.5e6;
 
 int compute_units() {
   static int cus = 0;
@@ -71,28 +77,65 @@ apt_config_t base_config(int route) {
   return c;
 }
 
-// Modelled cycles of shape s with `grid` workgroups (0 = one per tile).
-double model_cycles(const Int8Shape& s, int M, int N, int K, int grid, int cus) {
+// Modelled microseconds of shape s with `grid` workgroups (0 = one per
+// tile), without the fixed time.  Workgroups run in rounds of cus * per_cu;
+// a last partial round of at most one workgroup per compute unit runs at the
+// alone rate.
+double model_loop_us(const Int8Shape& s, int M, int N, int K, int grid, int cus) {
   const int64_t tiles = (int64_t)((M + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
   const int64_t pairs = (((K + kChunk - 1) / kChunk) + 1) / 2;
   const int64_t slots = (int64_t)cus * s.per_cu;
-  if (grid == 0) {  // one workgroup per tile, in rounds of `slots`
-    const int64_t rounds = (tiles + slots - 1) / slots;
-    return (double)rounds * (pairs * s.pair_cycles + kTileFixedCycles);
+  auto round_us = [&](int64_t wgs, int64_t wg_pairs) {
+    return (double)wg_pairs * (wgs <= cus ? s.pair_alone_us : s.pair_us);
+  };
+  if (grid == 0) {
+    const int64_t full = tiles / slots, rem = tiles % slots;
+    return (double)full * round_us(slots, pairs) + (rem ? round_us(rem, pairs) : 0.0);
   }
   const int64_t g = std::min<int64_t>(grid, tiles * pairs);
   const int64_t dp = tiles / g, sk_tiles = tiles - dp * g;
   const int64_t sk_pairs = sk_tiles * pairs;
-  const int64_t per_wg = dp * pairs + (sk_pairs + g - 1) / g;
-  const int64_t rounds = (g + slots - 1) / slots;
-  double cycles = (double)rounds * (per_wg * s.pair_cycles + kTileFixedCycles);
+  // stream-K pairs go to min(g, 2 * sk_tiles) workgroups (the launch's rule)
+  const int64_t sk_g = sk_tiles ? std::min<int64_t>(g, 2 * sk_tiles) : 0;
+  const int64_t per_wg = dp * pairs + (sk_g ? (sk_pairs + sk_g - 1) / sk_g : 0);
+  const int64_t active = dp ? g : sk_g;
+  const int64_t rounds = (active + slots - 1) / slots;
+  double us = (double)rounds * round_us(std::min(active, slots), per_wg);
   if (sk_tiles > 0) {
-    // every shared tile: about (parts - 1) partials written and read back
-    const double parts = std::min<double>((double)g, (double)pairs * g / (double)sk_pairs + 1.0);
-    const double bytes = 2.0 * sk_tiles * (parts - 1.0) * s.bm * s.bn * 4.0;
-    cycles += bytes / kPartialBytesPerCycle;
+    // every shared tile: (parts - 1) partials written and read back; a tile
+    // has sk_g / sk_tiles parts, one more where part bounds fall inside it
+    const double parts = (double)sk_g / (double)sk_tiles + 0.5;
+    const double bytes = 2.0 * sk_tiles * std::max(0.0, parts - 1.0) * s.bm * s.bn * 4.0;
+    us += bytes / kPartialBytesPerUs;
   }
-  return cycles;
+  return us;
+}
+
+double model_us(const Int8Shape& s, int M, int N, int K, int grid, int cus) {
+  return model_loop_us(s, M, N, K, grid, cus) + s.fixed_us;
+}
+
+// The tail shape a split config with main shape i and tail size of shape t
+// runs: of the shapes of that size, the one with the main shape's wave count
+// (the library's rule), else t itself.
+bool tail_runs_as(int i, int t) {
+  const Int8Shape &m = kInt8Shapes[i], &ts = kInt8Shapes[t];
+  for (int u = 0; u < kNumInt8Shapes; ++u) {
+    const Int8Shape& o = kInt8Shapes[u];
+    if (u != t && o.bm == ts.bm && o.bn == ts.bn && o.wm * o.wn == m.wm * m.wn) return false;
+  }
+  return true;
+}
+
+// Columns [0, split) that fill whole rounds of shape s's tiles, or 0 when
+// there is no such split short of N.
+int split_columns(const Int8Shape& s, int M, int N, int cus) {
+  const int tiles_m = (M + s.bm - 1) / s.bm;
+  const int cols_per_round = cus * s.per_cu / tiles_m;
+  const int tiles_n = (N + s.bn - 1) / s.bn;
+  if (cols_per_round < 1 || tiles_n <= cols_per_round) return 0;
+  const int split = tiles_n / cols_per_round * cols_per_round * s.bn;
+  return split < N ? split : 0;
 }
 
 }  // namespace
@@ -163,13 +206,10 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
   }
   for (int i = 0; i < kNumMainShapes; ++i) {
     const Int8Shape& s = kInt8Shapes[i];
-    const int tiles_m = (M + s.bm - 1) / s.bm;
-    const int cols_per_round = cus * s.per_cu / tiles_m;
-    const int tiles_n = (N + s.bn - 1) / s.bn;
-    if (cols_per_round < 1 || tiles_n <= cols_per_round) continue;
-    const int split = tiles_n / cols_per_round * cols_per_round * s.bn;
-    if (split >= N) continue;
-    for (int t = kNumMainShapes; t < kNumInt8Shapes; ++t) {
+    const int split = split_columns(s, M, N, cus);
+    if (split == 0) continue;
+    for (int t = kFirstTail; t < kNumInt8Shapes; ++t) {
+      if (!tail_runs_as(i, t)) continue;
       apt_config_t c = int8_cfg(s, 0);
       c.split_n = split;
       c.tail_bm = kInt8Shapes[t].bm;
@@ -189,10 +229,10 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
     return c;
   }
   const int cus = compute_units();
-  // Candidates: each shape alone, with one workgroup per tile or a full
-  // persistent grid; and the first shape over the columns that fill whole
-  // rounds of its tiles with each smaller shape (one workgroup per tile) on
-  // the remaining columns.
+  // Candidates: each shape alone, with one workgroup per tile or a
+  // persistent grid of one round; and each main shape over the columns that
+  // fill whole rounds of its tiles, with each tail shape (one workgroup per
+  // tile) on the remaining columns.
   double best = 0.0;
   int best_i = -1, best_grid = 0, best_split = 0, best_tail = -1;
   auto consider = [&](double t, int i, int grid, int split, int tail) {
@@ -206,24 +246,22 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
   };
   for (int i = 0; i < kNumInt8Shapes; ++i) {
     const Int8Shape& s = kInt8Shapes[i];
-    consider(model_cycles(s, M, N, K, 0, cus), i, 0, 0, -1);
-    consider(model_cycles(s, M, N, K, std::min(cus * s.per_cu, kMaxGrid), cus), i,
-             std::min(cus * s.per_cu, kMaxGrid), 0, -1);
+    const int round = std::min(cus * s.per_cu, kMaxGrid);
+    consider(model_us(s, M, N, K, 0, cus), i, 0, 0, -1);
+    consider(model_us(s, M, N, K, round, cus), i, round, 0, -1);
   }
   for (int i = 0; i < kNumMainShapes; ++i) {
     const Int8Shape& s = kInt8Shapes[i];
-    const int tiles_m = (M + s.bm - 1) / s.bm;
-    const int cols_per_round = cus * s.per_cu / tiles_m;
-    const int tiles_n = (N + s.bn - 1) / s.bn;
-    if (cols_per_round >= 1 && tiles_n > cols_per_round) {
-      const int split = tiles_n / cols_per_round * cols_per_round * s.bn;
-      if (split < N)
-        for (int t = kNumMainShapes; t < kNumInt8Shapes; ++t)
-          // a paired launch saves the second launch's start-up and drain
-          consider(model_cycles(s, M, split, K, 0, cus) +
-                       model_cycles(kInt8Shapes[t], M, N - split, K, 0, cus) -
-                       (t == kPairTail ? kTileFixedCycles : 0.0),
-                   i, 0, split, t);
+    const int split = split_columns(s, M, N, cus);
+    if (split == 0) continue;
+    for (int t = kFirstTail; t < kNumInt8Shapes; ++t) {
+      if (!tail_runs_as(i, t)) continue;
+      const Int8Shape& ts = kInt8Shapes[t];
+      // one launch when the wave counts match: one fixed time, else two
+      const bool paired = ts.wm * ts.wn == s.wm * s.wn;
+      consider(model_loop_us(s, M, split, K, 0, cus) + model_loop_us(ts, M, N - split, K, 0, cus) +
+                   (paired ? std::max(s.fixed_us, ts.fixed_us) : s.fixed_us + ts.fixed_us),
+               i, 0, split, t);
     }
   }
   const Int8Shape& s = kInt8Shapes[best_i];

@@ -7,7 +7,8 @@ import numpy as np
 import paper_2508_19087_amd as apt
 from oracle import oracle as ref
 
-INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 128, 4, 2), (128, 128, 2, 2), (512, 128, 8, 1)]
+INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 128, 4, 2), (128, 128, 2, 2), (512, 128, 8, 1),
+               (256, 128, 4, 1)]
 
 
 def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
@@ -24,8 +25,10 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
             out.append(("int8_%dx%d_w%dx%d_g%d" % (bm, bn, wm, wn, grid), c))
         split = (N - 1) // bn * bn
         if N and split >= bn:
-            tails = [(128, 128)] + ([(256, 128)] if (wm, wn) in ((4, 2), (8, 1)) else [])
-            for tbm, tbn in tails:  # 256x256 + 256x128 runs as one paired launch
+            tails = [(128, 128)] + ([(256, 128)] if (wm, wn) in ((4, 2), (8, 1), (4, 1)) else [])
+            # paired launches: 256x256 or 512x128 + 256x128 (8 waves); 256x128 (4x1) + 128x128
+            # or 256x128 (4 waves)
+            for tbm, tbn in tails:
                 for tg in (0, 5):
                     c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, 0, 3, 0,
                                               split, tbm, tbn, tg)
