@@ -16,7 +16,10 @@ hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t&, hipStream_t s
   const int grid_x = padded_rows(g.N) / kRowGroup;
   const int grid_y = (g.M + kMT - 1) / kMT;
   size_t lds = (size_t)prm.nchunks * g.q * kRowGroup * 16;
-  if (lds > 64 * 1024) lds = 0;  // read the activation chunks from global memory instead
+  // Read the activation chunks from global memory instead of staging them
+  // when they do not fit, or when only one activation row is real: staging
+  // would copy 8 rows and put a barrier between the two memory latencies.
+  if (lds > 64 * 1024 || g.M == 1) lds = 0;
   switch (g.p) {
     case 1: return xorpop::launch_for_p<1>(g.q, prm, grid_x, grid_y, lds, stream);
     case 2: return xorpop::launch_for_p<2>(g.q, prm, grid_x, grid_y, lds, stream);
