@@ -72,11 +72,15 @@ enum {
   APT_ROUTE_AUTO = 0,       /* let apt_select_config decide */
   APT_ROUTE_XOR = 1,        /* XOR + popcount on packed words, cross-lane reduction (Sec. III-B, 1-bit XOR form) */
   APT_ROUTE_PM1_MFMA = 2,   /* every (i, j) plane pair as +-1 int8 operands on the int8 matrix cores */
-  APT_ROUTE_INT8_MFMA = 3   /* planes reassembled in LDS into one int8 operand, one int8 MFMA per element pair */
+  APT_ROUTE_INT8_MFMA = 3,  /* planes reassembled in LDS into one int8 operand, one int8 MFMA per element pair */
+  APT_ROUTE_FP4_MFMA = 4    /* as APT_ROUTE_INT8_MFMA with the bipolar values as FP4 (E2M1) operands of the
+                               block-scaled MFMA: p, q <= 2 and K (2^p-1)(2^q-1) < 2^24 */
 };
 
 /* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950
- * terms).  Fields a route does not use are ignored.
+ * terms).  Fields a route does not use are ignored.  Everything said of the
+ * int8 MFMA route below holds for the FP4 MFMA route too (same tile shapes,
+ * grids and split launches).
  *   route      APT_ROUTE_*
  *   bm, bn     output tile per workgroup (int8 MFMA route: 256x256 with 4x2 or
  *              2x4 waves, 512x128 with 8x1, 256x128 with 4x2 or 4x1, 128x128
@@ -172,10 +176,11 @@ apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* 
  * NULL or route AUTO = the selected one).  The reassembled int8 MFMA route
  * expands the activations once per call into int8 MFMA fragments
  * (ceil(M/32)*32 * K_pad' bytes, K_pad' = K_pad rounded up to a multiple of
- * 256) and, for each launch with a stream-K decomposition (grid > 0 and T
- * not a multiple of grid), two int32 BM x BN partial tiles per workgroup and
- * one counter per shared tile, each region rounded up to 256 bytes; the
- * other routes need 0.  Returns 0 for invalid sizes or configs. */
+ * 256; the FP4 MFMA route stores half of that: two values per byte) and,
+ * for each launch with a stream-K decomposition (grid > 0 and T not a
+ * multiple of grid), two int32 BM x BN partial tiles per workgroup and one
+ * counter per shared tile, each region rounded up to 256 bytes; the other
+ * routes need 0.  Returns 0 for invalid sizes or configs. */
 size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_config_t* cfg);
 
 /* C = A * W^T on packed operands, with the fused recombination of Sec. III-B
@@ -197,7 +202,8 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
  * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8], NULL or
  * misaligned packed pointers, both outputs NULL, c_fp16 without both scales, a
  * route needing row sums without them, a misaligned workspace, or an invalid
- * cfg; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31; APT_ERR_WORKSPACE
+ * cfg; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31, or when an FP4
+ * route is forced with p or q > 2 or K (2^p-1)(2^q-1) >= 2^24; APT_ERR_WORKSPACE
  * when the workspace is missing or too small; APT_ERR_HIP on launch failure. */
 apt_status_t apt_gemm(int M, int N, int K, int p, int q,
                       const void* a_packed, const void* w_packed,
@@ -244,7 +250,8 @@ size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q);
  * with cfg NULL use it for this problem from then on, and returns it.  The
  * candidates are the XOR route, the +-1 plane route (p, q <= 7), every int8
  * tile shape with one workgroup per tile and with one persistent round of
- * workgroups, and the split launches of a main and a tail shape.  Each is
+ * workgroups, and the split launches of a main and a tail shape, each of
+ * these also with FP4 operands where the FP4 route applies.  Each is
  * run twice to warm up, then timed over 5 back-to-back calls between two HIP
  * events on `stream`.  The call blocks until the timing has finished.  All
  * candidates compute the same result, so it never changes results.

@@ -43,6 +43,13 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
       if (!apt::xor_config_ok(c)) return APT_ERR_INVALID_ARG;
       if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
       return APT_OK;
+    case APT_ROUTE_FP4_MFMA:
+      // E2M1 holds bipolar values of at most 2 bits; fp32 sums stay exact
+      // integers below 2^24
+      if (p > 2 || q > 2) return APT_ERR_UNSUPPORTED;
+      if ((int64_t)K * ((1 << p) - 1) * ((1 << q) - 1) >= ((int64_t)1 << 24))
+        return APT_ERR_UNSUPPORTED;
+      [[fallthrough]];
     case APT_ROUTE_INT8_MFMA:
       if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
@@ -100,7 +107,8 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
   const apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
                              ? apt::select_config(M, N, K, p, q)
                              : *cfg;
-  if (c.route != APT_ROUTE_INT8_MFMA || !apt::int8_config_ok(c, N)) return 0;
+  if (c.route != APT_ROUTE_INT8_MFMA && c.route != APT_ROUTE_FP4_MFMA) return 0;
+  if (check_config(c, M, N, K, p, q, true) != APT_OK) return 0;
   return apt::int8_workspace_bytes(M, N, K, c);
 }
 
@@ -131,7 +139,7 @@ apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed
   const bool have_rowsums = a_rowsum != nullptr && w_rowsum != nullptr;
   apt_status_t st = check_config(c, M, N, K, p, q, have_rowsums);
   if (st != APT_OK) return st;
-  if (c.route == APT_ROUTE_INT8_MFMA) {
+  if (c.route == APT_ROUTE_INT8_MFMA || c.route == APT_ROUTE_FP4_MFMA) {
     if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, N, K, c))
       return APT_ERR_WORKSPACE;
     if (!aligned16(workspace)) return APT_ERR_INVALID_ARG;
@@ -152,7 +160,8 @@ apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (c.route) {
     case APT_ROUTE_XOR: return hip_status(apt::launch_gemm_xor(g, c, s));
-    case APT_ROUTE_INT8_MFMA: return hip_status(apt::launch_gemm_int8(g, c, workspace, s));
+    case APT_ROUTE_INT8_MFMA:
+    case APT_ROUTE_FP4_MFMA: return hip_status(apt::launch_gemm_int8(g, c, workspace, s));
     case APT_ROUTE_PM1_MFMA: return hip_status(apt::launch_gemm_pm1(g, c, s));
   }
   return APT_ERR_INVALID_ARG;
@@ -191,7 +200,8 @@ size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q) {
   const int n = apt::candidate_configs(M, N, K, p, q, cand, apt::kMaxCandidates);
   size_t most = 0;
   for (int i = 0; i < n; ++i)
-    if (cand[i].route == APT_ROUTE_INT8_MFMA && apt::int8_config_ok(cand[i], N))
+    if ((cand[i].route == APT_ROUTE_INT8_MFMA || cand[i].route == APT_ROUTE_FP4_MFMA) &&
+        apt::int8_config_ok(cand[i], N))
       most = std::max(most, apt::int8_workspace_bytes(M, N, K, cand[i]));
   return most;
 }

@@ -47,14 +47,30 @@ namespace apt {
 namespace int8 {
 
 constexpr int kWave = 64;
-constexpr int kRowBytes = kChunk + 16;          // padded LDS row: 128 operand bytes + 16
-constexpr int kStepBytes = 32;                  // K bytes per MFMA k-step
-constexpr int kSteps = kChunk / kStepBytes;     // k-steps per chunk
+constexpr int kStepBytes = 32;                  // operand bytes per row and MFMA k-step
 constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes x 16 bytes
+
+// Operand format of the contraction (template parameter F):
+//   F = 0: int8 operand bytes, one v_mfma_i32_32x32x32_i8 per 32 elements of k;
+//   F = 1: FP4 (E2M1) operand nibbles for weights and activations of at most 2
+//          bits, one v_mfma_scale_f32_32x32x64_f8f6f4 (unit scales) per 64
+//          elements of k: the same operand bytes and issue cycles per MFMA as
+//          int8 for twice the multiply-adds.  Its fp32 sums are exact
+//          integers while K (2^p - 1)(2^q - 1) < 2^24 (the host checks).
+// Per chunk, k-step ks of lane half h holds (F = 0) half h of word ks's bytes,
+// or (F = 1) word 2 ks + h's nibbles; both operands use the same order.
+template <int F>
+struct Fmt {
+  static constexpr int kStepK = F ? 64 : 32;                   // k per MFMA
+  static constexpr int kSteps = kChunk / kStepK;               // k-steps per chunk
+  static constexpr int kRowBytes = kSteps * kStepBytes + 16;   // padded LDS row of a chunk
+};
 constexpr int kStages = 3;                      // weight LDS ring depth
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
@@ -66,6 +82,9 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void store16(int32_t* p, v4i v) {
   __builtin_nontemporal_store(v, reinterpret_cast<v4i*>(p));
 }
+
+// An empty instruction that reads x: code computing x cannot be moved past it.
+__device__ __forceinline__ void keep_here(const v16i& x) { asm volatile("" ::"v"(x)); }
 
 // Buffer resource over [base, base + bytes) for raw buffer loads: a
 // wave-uniform base in SGPRs plus a per-lane 32-bit offset and a uniform
@@ -94,20 +113,21 @@ struct Int8Params {
   int vec_out;        // outputs take 16-byte (int32) / 8-byte (fp16) row stores
 };
 
-// Bytes of the activation fragment buffer for M rows and K.
-inline size_t a_frag_bytes(int M, int K) {
+// Bytes of the activation fragment buffer for M rows and K (F = 1: nibbles).
+inline size_t a_frag_bytes(int M, int K, bool fp4 = false) {
   const int nce = (num_chunks(K) + 1) & ~1;
-  return (size_t)((M + 31) / 32) * 32 * nce * kChunk;
+  return (size_t)((M + 31) / 32) * 32 * nce * (fp4 ? kChunk / 2 : kChunk);
 }
 
 // ---- activation expansion ---------------------------------------------------
 // Fragment (mb, ks) holds k-step ks of rows 32 mb .. 32 mb + 31 in MFMA operand
 // order: lane l (vector index ((mb * nsteps + ks) * 64 + l)) carries 16 bytes of
 // row 32 mb + l mod 32, namely bytes 16 (l / 32) .. 16 (l / 32) + 15 of the
-// k-step's 32 reassembled bytes.  Rows past M are expanded from all-zero
-// planes (padding elements); a chunk past the last one (the odd chunk that
-// makes the count even) is all-zero bytes.
-template <int Q>
+// k-step's 32 reassembled bytes (F = 1: the 16 nibble bytes of one plane
+// word).  Rows past M are expanded from all-zero planes (padding elements); a
+// chunk past the last one (the odd chunk that makes the count even) is
+// all-zero bytes, which are 0 in both formats.
+template <int Q, int F>
 __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restrict__ a_packed, int M,
                                                        int nchunks, int nsteps, int mblocks,
                                                        v4i* __restrict__ out, int* __restrict__ counters,
@@ -119,6 +139,7 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
   // The stream-K arrival counters of this call start cleared (the GEMM
   // launch follows in stream order).
   if (t < ncounters) counters[t] = 0;
+  constexpr int kSteps = Fmt<F>::kSteps;
   if (t >= (int64_t)rows * (nsteps / kSteps) * kWordsPerPlane) return;
   const int w = (int)(t % kWordsPerPlane);
   const int64_t rc = t / kWordsPerPlane;
@@ -133,15 +154,23 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
 #pragma unroll
     for (int j = 0; j < Q; ++j) pw[j] = 0u;
   }
-  uint32_t o[8];
-  reassemble_word<Q>(pw, o);
-  if (chunk >= nchunks)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] = 0u;
   const int mb = row / 32, l = row % 32;
-  v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w) * kFragVecs;
-  f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
-  f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+  if (F) {
+    // word w -> k-step w / 2, lane half w mod 2
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+    if (chunk < nchunks) fp4_word<(Q <= 2 ? Q : 2)>(pw, o);
+    v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w / 2) * kFragVecs;
+    f[(w % 2) * 32 + l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+  } else {
+    uint32_t o[8];
+    reassemble_word<Q>(pw, o);
+    if (chunk >= nchunks)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = 0u;
+    v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w) * kFragVecs;
+    f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+  }
 }
 
 // ---- weight staging -----------------------------------------------------------
@@ -152,8 +181,9 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
 // never stored, and the code stays branch-free so the scheduler can interleave
 // it with the MFMAs.  Chunks past the last one are clamped to it; they meet
 // all-zero activation bytes.
-template <int B, int ROWS, int SPLIT, int T>
+template <int B, int ROWS, int SPLIT, int T, int F>
 struct Stage {
+  static constexpr int kRowBytes = Fmt<F>::kRowBytes;
   static constexpr int kWpi = kWordsPerPlane / SPLIT;
   static constexpr int kItems = ROWS * SPLIT / T;
   static_assert(ROWS * SPLIT % T == 0 && kItems >= 1, "items must divide evenly");
@@ -192,7 +222,8 @@ struct Stage {
 
   // Half h (0: output dwords 0..3, 1: 4..7) of word u (0 <= u < kWords) of
   // this thread's items, reassembled and written to LDS.  The low half
-  // leaves the tree's middle level in mid[] for the high half.
+  // leaves the tree's middle level in mid[] for the high half.  FP4: the
+  // whole word's 16 nibble bytes in half 0, nothing in half 1.
   __device__ __forceinline__ void store_half(uint8_t* lds_tile, int tid, int u, int h,
                                              uint32_t mid[8]) const {
     const int it = u / kWpi, w = u % kWpi;
@@ -200,6 +231,17 @@ struct Stage {
     const int r = item % ROWS;
     const int sub = item / ROWS;
     uint32_t o[4];
+    if (F) {
+      if (h != 0) return;
+      uint32_t pw[B];
+#pragma unroll
+      for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
+      fp4_word<(B <= 2 ? B : 2)>(pw, o);
+      const int wc = sub * kWpi + w;  // word of the chunk -> k-step wc / 2, lane half wc mod 2
+      *reinterpret_cast<uint4*>(lds_tile + r * kRowBytes + (wc / 2) * kStepBytes + (wc % 2) * 16) =
+          make_uint4(o[0], o[1], o[2], o[3]);
+      return;
+    }
     if (h == 0) {
       uint32_t pw[B];
 #pragma unroll
@@ -332,8 +374,11 @@ struct Stream {
 // stores 16 contiguous output bytes.
 // The whole work of workgroup w of G for one tile shape (the kernels below
 // call it; `lds` is the dynamic LDS of the launch).
-template <int P, int BM, int BN, int WM, int WN, int SPLIT>
+template <int P, int F, int BM, int BN, int WM, int WN, int SPLIT>
 __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* lds, int w, int G) {
+  static_assert(F == 0 || P <= 2, "FP4 operands hold weights of at most 2 bits");
+  constexpr int kSteps = Fmt<F>::kSteps;
+  constexpr int kRowBytes = Fmt<F>::kRowBytes;
   constexpr int T = WM * WN * kWave;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   constexpr int FM = WTM / 32, FN = WTN / 32;  // 32x32 fragments per wave
@@ -389,7 +434,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   }
 
   // ---- operand sources
-  using SW = Stage<P, BN, SPLIT, T>;
+  using SW = Stage<P, BN, SPLIT, T, F>;
   SW rw0, rw1;
   const __amdgpu_buffer_rsrc_t w_rsrc = make_rsrc(g.w_packed, prm.w_bytes);
   const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(prm.a_frag, prm.a_bytes);
@@ -455,7 +500,16 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
       for (int b = 0; b < FN; ++b)
 #pragma unroll
         for (int a = 0; a < FM; ++a)
-          acc[b][a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[cur][b], afr[ks][a], acc[b][a], 0, 0, 0);
+          if (F) {
+            // E2M1 x E2M1 (format code 4 for both), unit E8M0 scales (127)
+            const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3], 0, 0, 0, 0};
+            const v8i ab = {afr[ks][a][0], afr[ks][a][1], afr[ks][a][2], afr[ks][a][3], 0, 0, 0, 0};
+            acc[b][a] = __builtin_bit_cast(
+                v16i, __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                          wa, ab, __builtin_bit_cast(v16f, acc[b][a]), 4, 4, 0, 127, 0, 127));
+          } else {
+            acc[b][a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[cur][b], afr[ks][a], acc[b][a], 0, 0, 0);
+          }
 #pragma unroll
       for (int a = 0; a < FM; ++a) afr[ks][a] = load_a(a_m0, a_chunk, ks, a);
       __builtin_amdgcn_sched_barrier(0);
@@ -463,10 +517,17 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   };
 
   // ---- epilogue constants
+  // F = 0: C = 4 D + c_w R_a + c_a R_w - c_a c_w K - pad_term (kernel header).
+  // F = 1: the operands are the bipolar values themselves, so C = D less the
+  // padding elements inside the last real chunk: their all-zero planes stand
+  // for -(2^p - 1) and -(2^q - 1), whose products add (K_pad - K)(2^p-1)(2^q-1).
   const int q = g.q;
-  const uint32_t ca = (uint32_t)(q == 8 ? 1 : 1 - (1 << q)), cw = (uint32_t)offset_of(P);
+  constexpr uint32_t kMul = F ? 1u : 4u;
+  const uint32_t ca = F ? 0u : (uint32_t)(q == 8 ? 1 : 1 - (1 << q));
+  const uint32_t cw = F ? 0u : (uint32_t)offset_of(P);
   const uint32_t pad_term =
-      4u * (uint32_t)(NC * kChunk - g.K) * (uint32_t)((q == 8 ? -128 : 0) * pad_of(P));
+      F ? (uint32_t)(NC * kChunk - g.K) * ((1u << P) - 1u) * ((1u << q) - 1u)
+        : 4u * (uint32_t)(NC * kChunk - g.K) * (uint32_t)((q == 8 ? -128 : 0) * pad_of(P));
   const uint32_t const_term = ca * cw * (uint32_t)g.K + pad_term;
   const bool fp16 = g.c_fp16 != nullptr;
   const bool vec_ok = prm.vec_out != 0;
@@ -533,7 +594,6 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     const int er = lane / 8, ec = (lane % 8) * 4;  // read-back row (+8 i) and first column
 #pragma unroll
     for (int a = 0; a < FM; ++a) {
-      const int mrow0 = m0 + wm * WTM + a * 32;
 #pragma unroll
       for (int b = 0; b < FN; ++b) {
         // acc[b][a][4 gi + j] = D[n = 8 gi + 4 (lane / 32) + j][m = lane mod 32]
@@ -558,7 +618,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
           const uint32_t at = lds_at[ml];
           int32_t cv[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) cv[j] = (int32_t)(4u * (uint32_t)d[j] + at + wt[j]);
+          for (int j = 0; j < 4; ++j) cv[j] = (int32_t)(kMul * (uint32_t)d[j] + at + wt[j]);
           if (m < g.M && ncol < g.N) {
             const int64_t o = (int64_t)m * g.N + ncol;
             if (g.c_int32) {
@@ -661,6 +721,16 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   }
 
   auto flush = [&](const Cursor& c) __attribute__((always_inline)) {
+    if (F) {
+      // FP4: the fp32 sums are exact integers; partials and the epilogue
+      // work on their int32 values.  Converted as whole vectors: a bit cast
+      // of one vector element is taken from element 0 by this compiler.
+#pragma unroll
+      for (int b = 0; b < FN; ++b)
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+          acc[b][a] = __builtin_convertvector(__builtin_bit_cast(v16f, acc[b][a]), v16i);
+    }
     bool finish = true;
     if (__builtin_expect(c.pbeg != 0 || c.pend != st.pairs, 0)) {
       const int e = c.tile == sh_tile[0] ? 0 : 1;
@@ -723,6 +793,16 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     rw0.load(w_rsrc, wv2, NC, 2 * c2.pair);
     step(lds + s1 * kStageBytes, lds + s0 * kStageBytes, lds + s2 * kStageBytes, rw1,
          c1.m0, 2 * c1.pair);
+    if (F) {
+      // An empty use of every accumulator here keeps the scaled MFMAs in
+      // their k-steps: without one, the machine code sinker moves all of the
+      // pair's MFMAs past the conditional blocks below, and the next
+      // chunk's activation registers then spill.  (No instruction is emitted.)
+#pragma unroll
+      for (int b = 0; b < FN; ++b)
+#pragma unroll
+        for (int a = 0; a < FM; ++a) keep_here(acc[b][a]);
+    }
     if (part_end) stage_terms(cp.m0, cp.n0);
     __syncthreads();
     if (__builtin_expect(part_end, 0)) {
@@ -740,26 +820,26 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   }
 }
 
-template <int P, int BM, int BN, int WM, int WN, int SPLIT>
+template <int P, int F, int BM, int BN, int WM, int WN, int SPLIT>
 __global__ __launch_bounds__(WM* WN* kWave, (WM * WN == 4) ? 2 : 1) void gemm_int8_kernel(Int8Params prm) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  gemm_int8_body<P, BM, BN, WM, WN, SPLIT>(prm, lds, blockIdx.x, gridDim.x);
+  gemm_int8_body<P, F, BM, BN, WM, WN, SPLIT>(prm, lds, blockIdx.x, gridDim.x);
 }
 
 // Two launches' work in one grid: workgroups [0, g0) do shape A over prm_a,
 // the rest shape B over prm_b (same wave count).  Workgroups are dispatched
 // in index order, so B's start on the compute units that A's release, while
 // A's last tiles and output stores are still in flight.
-template <int P, int BMA, int BNA, int WMA, int WNA, int SA, int BMB, int BNB, int WMB, int WNB,
-          int SB>
+template <int P, int F, int BMA, int BNA, int WMA, int WNA, int SA, int BMB, int BNB, int WMB,
+          int WNB, int SB>
 __global__ __launch_bounds__(WMA* WNA* kWave, (WMA * WNA == 4) ? 2 : 1) void gemm_int8_pair_kernel(Int8Params prm_a,
                                                                          Int8Params prm_b, int g0) {
   static_assert(WMA * WNA == WMB * WNB, "both shapes need the same workgroup size");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   if ((int)blockIdx.x < g0)
-    gemm_int8_body<P, BMA, BNA, WMA, WNA, SA>(prm_a, lds, blockIdx.x, g0);
+    gemm_int8_body<P, F, BMA, BNA, WMA, WNA, SA>(prm_a, lds, blockIdx.x, g0);
   else
-    gemm_int8_body<P, BMB, BNB, WMB, WNB, SB>(prm_b, lds, blockIdx.x - g0, gridDim.x - g0);
+    gemm_int8_body<P, F, BMB, BNB, WMB, WNB, SB>(prm_b, lds, blockIdx.x - g0, gridDim.x - g0);
 }
 
 struct TileShape {
@@ -777,18 +857,19 @@ constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
 // LDS of shape S: the weight ring, the epilogue terms and one 32x32 int32
 // epilogue slot per wave.
+template <int F>
 constexpr size_t lds_bytes(const TileShape& sh) {
-  return kStages * (size_t)sh.bn * kRowBytes + (size_t)(sh.bn + sh.bm) * 16 +
+  return kStages * (size_t)sh.bn * Fmt<F>::kRowBytes + (size_t)(sh.bn + sh.bm) * 16 +
          (size_t)sh.wm * sh.wn * 32 * (32 * 4 + 16);
 }
 
 // Launches shape S with `grid` persistent workgroups (prm holds the
 // decomposition).
-template <int P, int S>
+template <int P, int F, int S>
 hipError_t launch_shape(const Int8Params& prm, int grid, hipStream_t stream) {
   constexpr TileShape sh = kShapes[S];
-  const size_t lds = lds_bytes(sh);
-  auto kern = gemm_int8_kernel<P, sh.bm, sh.bn, sh.wm, sh.wn, sh.split>;
+  const size_t lds = lds_bytes<F>(sh);
+  auto kern = gemm_int8_kernel<P, F, sh.bm, sh.bn, sh.wm, sh.wn, sh.split>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -796,26 +877,26 @@ hipError_t launch_shape(const Int8Params& prm, int grid, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int P>
+template <int P, int F>
 inline hipError_t launch_p_shape(int shape, const Int8Params& prm, int grid, hipStream_t stream) {
   switch (shape) {
-    case 0: return launch_shape<P, 0>(prm, grid, stream);
-    case 1: return launch_shape<P, 1>(prm, grid, stream);
-    case 2: return launch_shape<P, 2>(prm, grid, stream);
-    case 3: return launch_shape<P, 3>(prm, grid, stream);
-    case 4: return launch_shape<P, 4>(prm, grid, stream);
-    case 5: return launch_shape<P, 5>(prm, grid, stream);
+    case 0: return launch_shape<P, F, 0>(prm, grid, stream);
+    case 1: return launch_shape<P, F, 1>(prm, grid, stream);
+    case 2: return launch_shape<P, F, 2>(prm, grid, stream);
+    case 3: return launch_shape<P, F, 3>(prm, grid, stream);
+    case 4: return launch_shape<P, F, 4>(prm, grid, stream);
+    case 5: return launch_shape<P, F, 5>(prm, grid, stream);
   }
   return hipErrorInvalidValue;
 }
 
 // One launch of shapes SA (grid ga) then SB (grid gb), when they pair.
-template <int P, int SA, int SB>
+template <int P, int F, int SA, int SB>
 hipError_t launch_pair_shapes(const Int8Params& pa, int ga, const Int8Params& pb, int gb,
                               hipStream_t stream) {
   constexpr TileShape a = kShapes[SA], b = kShapes[SB];
-  const size_t lds = std::max(lds_bytes(a), lds_bytes(b));
-  auto kern = gemm_int8_pair_kernel<P, a.bm, a.bn, a.wm, a.wn, a.split, b.bm, b.bn, b.wm, b.wn,
+  const size_t lds = std::max(lds_bytes<F>(a), lds_bytes<F>(b));
+  auto kern = gemm_int8_pair_kernel<P, F, a.bm, a.bn, a.wm, a.wn, a.split, b.bm, b.bn, b.wm, b.wn,
                                     b.split>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -831,25 +912,26 @@ inline bool pair_supported(int sa, int sb) {
   return ((sa == 0 || sa == 4) && sb == 2) || (sa == 5 && (sb == 3 || sb == 5));
 }
 
-template <int P>
+template <int P, int F>
 inline hipError_t launch_p_pair(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
                                 int gb, hipStream_t stream) {
-  if (sa == 0 && sb == 2) return launch_pair_shapes<P, 0, 2>(pa, ga, pb, gb, stream);
-  if (sa == 4 && sb == 2) return launch_pair_shapes<P, 4, 2>(pa, ga, pb, gb, stream);
-  if (sa == 5 && sb == 3) return launch_pair_shapes<P, 5, 3>(pa, ga, pb, gb, stream);
-  if (sa == 5 && sb == 5) return launch_pair_shapes<P, 5, 5>(pa, ga, pb, gb, stream);
+  if (sa == 0 && sb == 2) return launch_pair_shapes<P, F, 0, 2>(pa, ga, pb, gb, stream);
+  if (sa == 4 && sb == 2) return launch_pair_shapes<P, F, 4, 2>(pa, ga, pb, gb, stream);
+  if (sa == 5 && sb == 3) return launch_pair_shapes<P, F, 5, 3>(pa, ga, pb, gb, stream);
+  if (sa == 5 && sb == 5) return launch_pair_shapes<P, F, 5, 5>(pa, ga, pb, gb, stream);
   return hipErrorInvalidValue;
 }
 
-// Launches for weight bits P (main kernel) and activation bits Q (expansion);
-// the explicit instantiations live in gemm_int8_inst.hip, built once per width.
+// Launches for weight bits P (main kernel) and activation bits Q (expansion),
+// int8 or (fp4, P or Q <= 2) FP4 operands; the explicit instantiations live
+// in gemm_int8_inst.hip, built once per width.
 template <int P>
-hipError_t launch_for_p(int shape, const Int8Params& prm, int grid, hipStream_t stream);
+hipError_t launch_for_p(bool fp4, int shape, const Int8Params& prm, int grid, hipStream_t stream);
 template <int P>
-hipError_t launch_pair_for_p(int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
-                             int gb, hipStream_t stream);
+hipError_t launch_pair_for_p(bool fp4, int sa, const Int8Params& pa, int ga, int sb,
+                             const Int8Params& pb, int gb, hipStream_t stream);
 template <int Q>
-hipError_t launch_expand_for_q(const uint32_t* a_packed, int M, int nchunks, int nsteps,
+hipError_t launch_expand_for_q(bool fp4, const uint32_t* a_packed, int M, int nchunks, int nsteps,
                                int mblocks, v4i* out, int* counters, int ncounters,
                                hipStream_t stream);
 

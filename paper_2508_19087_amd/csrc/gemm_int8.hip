@@ -19,34 +19,37 @@ int shape_index(const apt_config_t& cfg) {
   return -1;
 }
 
-hipError_t launch_p(int p, int shape, const Int8Params& prm, int grid, hipStream_t stream) {
+hipError_t launch_p(int p, bool fp4, int shape, const Int8Params& prm, int grid,
+                    hipStream_t stream) {
   switch (p) {
-    case 1: return launch_for_p<1>(shape, prm, grid, stream);
-    case 2: return launch_for_p<2>(shape, prm, grid, stream);
-    case 3: return launch_for_p<3>(shape, prm, grid, stream);
-    case 4: return launch_for_p<4>(shape, prm, grid, stream);
-    case 5: return launch_for_p<5>(shape, prm, grid, stream);
-    case 6: return launch_for_p<6>(shape, prm, grid, stream);
-    case 7: return launch_for_p<7>(shape, prm, grid, stream);
-    case 8: return launch_for_p<8>(shape, prm, grid, stream);
+    case 1: return launch_for_p<1>(fp4, shape, prm, grid, stream);
+    case 2: return launch_for_p<2>(fp4, shape, prm, grid, stream);
+    case 3: return launch_for_p<3>(fp4, shape, prm, grid, stream);
+    case 4: return launch_for_p<4>(fp4, shape, prm, grid, stream);
+    case 5: return launch_for_p<5>(fp4, shape, prm, grid, stream);
+    case 6: return launch_for_p<6>(fp4, shape, prm, grid, stream);
+    case 7: return launch_for_p<7>(fp4, shape, prm, grid, stream);
+    case 8: return launch_for_p<8>(fp4, shape, prm, grid, stream);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_pair(int p, int sa, const Int8Params& pa, int ga, int sb, const Int8Params& pb,
-                       int gb, hipStream_t stream) {
+hipError_t launch_pair(int p, bool fp4, int sa, const Int8Params& pa, int ga, int sb,
+                       const Int8Params& pb, int gb, hipStream_t stream) {
   switch (p) {
-    case 1: return launch_pair_for_p<1>(sa, pa, ga, sb, pb, gb, stream);
-    case 2: return launch_pair_for_p<2>(sa, pa, ga, sb, pb, gb, stream);
-    case 3: return launch_pair_for_p<3>(sa, pa, ga, sb, pb, gb, stream);
-    case 4: return launch_pair_for_p<4>(sa, pa, ga, sb, pb, gb, stream);
-    case 5: return launch_pair_for_p<5>(sa, pa, ga, sb, pb, gb, stream);
-    case 6: return launch_pair_for_p<6>(sa, pa, ga, sb, pb, gb, stream);
-    case 7: return launch_pair_for_p<7>(sa, pa, ga, sb, pb, gb, stream);
-    case 8: return launch_pair_for_p<8>(sa, pa, ga, sb, pb, gb, stream);
+    case 1: return launch_pair_for_p<1>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 2: return launch_pair_for_p<2>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 3: return launch_pair_for_p<3>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 4: return launch_pair_for_p<4>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 5: return launch_pair_for_p<5>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 6: return launch_pair_for_p<6>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 7: return launch_pair_for_p<7>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 8: return launch_pair_for_p<8>(fp4, sa, pa, ga, sb, pb, gb, stream);
   }
   return hipErrorInvalidValue;
 }
+
+bool is_fp4(const apt_config_t& cfg) { return cfg.route == APT_ROUTE_FP4_MFMA; }
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -124,7 +127,7 @@ bool int8_sizes_ok(int M, int N, int K, int p, const apt_config_t& cfg) {
   const int n = int8::make_plans(M, N, K, cfg, pl);
   for (int i = 0; i < n; ++i)
     if (pl[i].partial_bytes >= limit) return false;
-  return apt_packed_bytes(N, K, p) < limit && int8::a_frag_bytes(M, K) < limit;
+  return apt_packed_bytes(N, K, p) < limit && int8::a_frag_bytes(M, K, int8::is_fp4(cfg)) < limit;
 }
 
 // Workspace: activation fragments, then per launch (stream-K) one arrival
@@ -133,7 +136,7 @@ bool int8_sizes_ok(int M, int N, int K, int p, const apt_config_t& cfg) {
 size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg) {
   int8::Plan pl[2];
   const int n = int8::make_plans(M, N, K, cfg, pl);
-  size_t bytes = int8::align256(int8::a_frag_bytes(M, K));
+  size_t bytes = int8::align256(int8::a_frag_bytes(M, K, int8::is_fp4(cfg)));
   for (int i = 0; i < n; ++i)
     bytes += int8::align256(pl[i].partial_bytes) + int8::align256(pl[i].counter_bytes);
   return bytes;
@@ -145,17 +148,18 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
   Plan pl[2];
   const int nl = make_plans(g.M, g.N, g.K, cfg, pl);
   Int8Params prm[2];
-  uint8_t* base = static_cast<uint8_t*>(workspace) + align256(a_frag_bytes(g.M, g.K));
+  const bool fp4 = is_fp4(cfg);
+  uint8_t* base = static_cast<uint8_t*>(workspace) + align256(a_frag_bytes(g.M, g.K, fp4));
   int* counters = nullptr;
   int ncounters = 0;
   for (int i = 0; i < nl; ++i) {
     Int8Params& p = prm[i];
     p.g = g;
     p.nchunks = num_chunks(g.K);
-    p.nsteps = ((p.nchunks + 1) & ~1) * kSteps;
+    p.nsteps = ((p.nchunks + 1) & ~1) * (fp4 ? Fmt<1>::kSteps : Fmt<0>::kSteps);
     p.mblocks = (g.M + 31) / 32;
     p.a_frag = static_cast<const v4i*>(workspace);
-    p.a_bytes = (uint32_t)a_frag_bytes(g.M, g.K);
+    p.a_bytes = (uint32_t)a_frag_bytes(g.M, g.K, fp4);
     p.w_bytes = (uint32_t)apt_packed_bytes(g.N, g.K, g.p);
     p.n_begin = pl[i].n_begin;
     p.tiles_n = pl[i].tiles_n;
@@ -182,19 +186,21 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
   const Int8Params& p0 = prm[0];
   hipError_t e = hipErrorInvalidValue;
   switch (g.q) {
-    case 1: e = launch_expand_for_q<1>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 2: e = launch_expand_for_q<2>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 3: e = launch_expand_for_q<3>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 4: e = launch_expand_for_q<4>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 5: e = launch_expand_for_q<5>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 6: e = launch_expand_for_q<6>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 7: e = launch_expand_for_q<7>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 8: e = launch_expand_for_q<8>(g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 1: e = launch_expand_for_q<1>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 2: e = launch_expand_for_q<2>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 3: e = launch_expand_for_q<3>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 4: e = launch_expand_for_q<4>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 5: e = launch_expand_for_q<5>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 6: e = launch_expand_for_q<6>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 7: e = launch_expand_for_q<7>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 8: e = launch_expand_for_q<8>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
   }
   if (e != hipSuccess) return e;
   if (nl == 2 && pair_supported(pl[0].shape, pl[1].shape))
-    return launch_pair(g.p, pl[0].shape, prm[0], pl[0].grid, pl[1].shape, prm[1], pl[1].grid, stream);
-  for (int i = 0; i < nl && e == hipSuccess; ++i) e = launch_p(g.p, pl[i].shape, prm[i], pl[i].grid, stream);
+    return launch_pair(g.p, fp4, pl[0].shape, prm[0], pl[0].grid, pl[1].shape, prm[1], pl[1].grid,
+                       stream);
+  for (int i = 0; i < nl && e == hipSuccess; ++i)
+    e = launch_p(g.p, fp4, pl[i].shape, prm[i], pl[i].grid, stream);
   return e;
 }
 

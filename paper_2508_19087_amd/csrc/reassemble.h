@@ -104,6 +104,40 @@ __device__ __forceinline__ void reassemble_word(const uint32_t* pw, uint32_t out
   reassemble_hi<B>(mid, out + 4);
 }
 
+// FP4 operand nibbles (OCP E2M1: sign bit 3, exponent bits 2..1 with bias
+// 1, mantissa bit 0) of the 32 elements of plane words pw[0..B-1], B <= 2.
+// Every bipolar value of up to 2 bits is exact in E2M1: +-1 = e 01 m 0,
+// +-3 = e 10 m 1.
+//   B = 1: v = 2u - 1,  nibble = (~u) << 3 | 0b0010;
+//   B = 2: v = 2u - 3 with u = 2h + l: negative when h = 0, |v| = 3 when
+//          h == l; nibble = (~h) << 3 | x << 2 | (~x) << 1 | x, x = ~(h ^ l).
+// The four nibble bit-planes are merged as the first two levels of the byte
+// tree: output dword t, nibble f holds element 4f + t (t = 0..3).
+template <int B>
+__device__ __forceinline__ void fp4_word(const uint32_t* pw, uint32_t out[4]) {
+  static_assert(B == 1 || B == 2, "E2M1 holds bipolar values of up to 2 bits");
+  uint32_t n0, n1, n2, n3;  // nibble bit-planes, bit 0 .. bit 3
+  if (B == 1) {
+    n0 = 0u;
+    n1 = ~0u;
+    n2 = 0u;
+    n3 = ~pw[0];
+  } else {
+    const uint32_t x = ~(pw[0] ^ pw[1]);
+    n0 = x;
+    n1 = ~x;
+    n2 = x;
+    n3 = ~pw[1];
+  }
+  const uint32_t m1 = 0x55555555u, m2 = 0x33333333u;
+  const uint32_t e01 = bsel(m1, n0, n1 << 1), o01 = bsel(m1, n0 >> 1, n1);
+  const uint32_t e23 = bsel(m1, n2, n3 << 1), o23 = bsel(m1, n2 >> 1, n3);
+  out[0] = bsel(m2, e01, e23 << 2);  // elements 4f
+  out[1] = bsel(m2, o01, o23 << 2);  // elements 4f + 1
+  out[2] = bsel(m2, e01 >> 2, e23);  // elements 4f + 2
+  out[3] = bsel(m2, o01 >> 2, o23);  // elements 4f + 3
+}
+
 // Operand offset of the reassembled byte y: bipolar value v = 2 y + c.
 //   B <= 7: y = u,        v = 2u - (2^B - 1)  ->  c = 1 - 2^B
 //   B == 8: y = u - 128,  v = 2u - 255        ->  c = 1

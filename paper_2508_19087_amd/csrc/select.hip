@@ -50,6 +50,15 @@ constexpr int kFirstTail = 2;
 // Device-wide rate at which stream-K partial tiles are written and read back
 // (bytes per microsecond), as the stream-K launches measured on MI355X show.
 constexpr double kPartialBytesPerUs = 2.5e6;
+// Pair time of the FP4 route relative to the int8 route with the same tile
+// (half the MFMAs, operand loads and LDS reads per pair; measured on MI355X).
+constexpr double kFp4PairFactor = 0.6;
+
+// The FP4 route can run (p, q) over K: E2M1 operands of at most 2 bits and
+// exact fp32 sums.
+bool fp4_ok(int K, int p, int q) {
+  return p <= 2 && q <= 2 && (int64_t)K * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
+}
 
 int compute_units() {
   static int cus = 0;
@@ -81,12 +90,13 @@ apt_config_t base_config(int route) {
 // tile), without the fixed time.  Workgroups run in rounds of cus * per_cu;
 // a last partial round of at most one workgroup per compute unit runs at the
 // alone rate.
-double model_loop_us(const Int8Shape& s, int M, int N, int K, int grid, int cus) {
+double model_loop_us(const Int8Shape& s, int M, int N, int K, int grid, int cus,
+                     double factor = 1.0) {
   const int64_t tiles = (int64_t)((M + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
   const int64_t pairs = (((K + kChunk - 1) / kChunk) + 1) / 2;
   const int64_t slots = (int64_t)cus * s.per_cu;
   auto round_us = [&](int64_t wgs, int64_t wg_pairs) {
-    return (double)wg_pairs * (wgs <= cus ? s.pair_alone_us : s.pair_us);
+    return (double)wg_pairs * factor * (wgs <= cus ? s.pair_alone_us : s.pair_us);
   };
   if (grid == 0) {
     const int64_t full = tiles / slots, rem = tiles % slots;
@@ -111,8 +121,8 @@ double model_loop_us(const Int8Shape& s, int M, int N, int K, int grid, int cus)
   return us;
 }
 
-double model_us(const Int8Shape& s, int M, int N, int K, int grid, int cus) {
-  return model_loop_us(s, M, N, K, grid, cus) + s.fixed_us;
+double model_us(const Int8Shape& s, int M, int N, int K, int grid, int cus, double factor = 1.0) {
+  return model_loop_us(s, M, N, K, grid, cus, factor) + s.fixed_us;
 }
 
 // The tail shape a split config with main shape i and tail size of shape t
@@ -178,7 +188,6 @@ int table_size() {
 // workgroups, and the split launches the model considers (a main shape over
 // whole rounds of columns, a smaller shape on the rest).
 int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int max_out) {
-  (void)K;
   int n = 0;
   auto add = [&](const apt_config_t& c) {
     if (n < max_out) out[n++] = c;
@@ -204,6 +213,7 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
     add(int8_cfg(s, 0));
     add(int8_cfg(s, std::min(cus * s.per_cu, kMaxGrid)));
   }
+  const int n_int8_single = n;
   for (int i = 0; i < kNumMainShapes; ++i) {
     const Int8Shape& s = kInt8Shapes[i];
     const int split = split_columns(s, M, N, cus);
@@ -214,6 +224,15 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
       c.split_n = split;
       c.tail_bm = kInt8Shapes[t].bm;
       c.tail_bn = kInt8Shapes[t].bn;
+      add(c);
+    }
+  }
+  // the same tile configs with FP4 operands where they apply
+  if (fp4_ok(K, p, q)) {
+    const int end = n;
+    for (int j = n_int8_single - 2 * kNumInt8Shapes; j < end; ++j) {
+      apt_config_t c = out[j];
+      c.route = APT_ROUTE_FP4_MFMA;
       add(c);
     }
   }
@@ -235,6 +254,8 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
   // tile) on the remaining columns.
   double best = 0.0;
   int best_i = -1, best_grid = 0, best_split = 0, best_tail = -1;
+  bool best_fp4 = false;
+  bool fp4 = false;
   auto consider = [&](double t, int i, int grid, int split, int tail) {
     if (best_i < 0 || t < best) {
       best = t;
@@ -242,30 +263,37 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
       best_grid = grid;
       best_split = split;
       best_tail = tail;
+      best_fp4 = fp4;
     }
   };
-  for (int i = 0; i < kNumInt8Shapes; ++i) {
-    const Int8Shape& s = kInt8Shapes[i];
-    const int round = std::min(cus * s.per_cu, kMaxGrid);
-    consider(model_us(s, M, N, K, 0, cus), i, 0, 0, -1);
-    consider(model_us(s, M, N, K, round, cus), i, round, 0, -1);
-  }
-  for (int i = 0; i < kNumMainShapes; ++i) {
-    const Int8Shape& s = kInt8Shapes[i];
-    const int split = split_columns(s, M, N, cus);
-    if (split == 0) continue;
-    for (int t = kFirstTail; t < kNumInt8Shapes; ++t) {
-      if (!tail_runs_as(i, t)) continue;
-      const Int8Shape& ts = kInt8Shapes[t];
-      // one launch when the wave counts match: one fixed time, else two
-      const bool paired = ts.wm * ts.wn == s.wm * s.wn;
-      consider(model_loop_us(s, M, split, K, 0, cus) + model_loop_us(ts, M, N - split, K, 0, cus) +
-                   (paired ? std::max(s.fixed_us, ts.fixed_us) : s.fixed_us + ts.fixed_us),
-               i, 0, split, t);
+  // int8 operands, then (where they apply) FP4 operands
+  for (int f = 0; f < (fp4_ok(K, p, q) ? 2 : 1); ++f) {
+    fp4 = f == 1;
+    const double factor = fp4 ? kFp4PairFactor : 1.0;
+    for (int i = 0; i < kNumInt8Shapes; ++i) {
+      const Int8Shape& s = kInt8Shapes[i];
+      const int round = std::min(cus * s.per_cu, kMaxGrid);
+      consider(model_us(s, M, N, K, 0, cus, factor), i, 0, 0, -1);
+      consider(model_us(s, M, N, K, round, cus, factor), i, round, 0, -1);
+    }
+    for (int i = 0; i < kNumMainShapes; ++i) {
+      const Int8Shape& s = kInt8Shapes[i];
+      const int split = split_columns(s, M, N, cus);
+      if (split == 0) continue;
+      for (int t = kFirstTail; t < kNumInt8Shapes; ++t) {
+        if (!tail_runs_as(i, t)) continue;
+        const Int8Shape& ts = kInt8Shapes[t];
+        // one launch when the wave counts match: one fixed time, else two
+        const bool paired = ts.wm * ts.wn == s.wm * s.wn;
+        consider(model_loop_us(s, M, split, K, 0, cus, factor) +
+                     model_loop_us(ts, M, N - split, K, 0, cus, factor) +
+                     (paired ? std::max(s.fixed_us, ts.fixed_us) : s.fixed_us + ts.fixed_us),
+                 i, 0, split, t);
+      }
     }
   }
   const Int8Shape& s = kInt8Shapes[best_i];
-  apt_config_t c = base_config(APT_ROUTE_INT8_MFMA);
+  apt_config_t c = base_config(best_fp4 ? APT_ROUTE_FP4_MFMA : APT_ROUTE_INT8_MFMA);
   c.bm = s.bm;
   c.bn = s.bn;
   c.bk = kChunk;

@@ -34,6 +34,15 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
                                               split, tbm, tbn, tg)
                     out.append(("int8_%dx%d_w%dx%d_tail%dx%d@%d_g%d" % (bm, bn, wm, wn, tbm, tbn, split,
                                                                         tg), c))
+    if p <= 2 and q <= 2:  # the same tile configs with FP4 (E2M1) operands
+        fp4 = []
+        for name, c in out:
+            if c.route == apt.APT_ROUTE_INT8_MFMA:
+                f = apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, c.bm, c.bn, c.bk, c.waves_m,
+                                          c.waves_n, c.grid, c.lds_stages, c.mt, c.split_n, c.tail_bm,
+                                          c.tail_bn, c.tail_grid)
+                fp4.append(("fp4" + name[4:], f))
+        out += fp4
     if p <= 7 and q <= 7:
         out.append(("pm1", apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)))
     return out

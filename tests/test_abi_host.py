@@ -53,7 +53,8 @@ def _int8_workspace(M, N, K, c):
     256 bytes."""
     up = lambda x: (x + 255) // 256 * 256
     nce = ((K + 127) // 128 + 1) // 2 * 2
-    ws = up((M + 31) // 32 * 32 * nce * 128)
+    # int8 bytes, or FP4 nibbles (half as many bytes)
+    ws = up((M + 31) // 32 * 32 * nce * (64 if c.route == apt.APT_ROUTE_FP4_MFMA else 128))
     launches = [(c.bm, c.bn, N, c.grid)]
     if c.split_n:
         launches = [(c.bm, c.bn, c.split_n, c.grid), (c.tail_bm, c.tail_bn, N - c.split_n, c.tail_grid)]
@@ -86,12 +87,16 @@ def test_workspace_stream_k():
 def test_select_config_valid(shape):
     st, c = apt.apt_select_config(*shape)
     assert st == apt.APT_OK
-    assert c.route in (apt.APT_ROUTE_XOR, apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_PM1_MFMA)
+    assert c.route in (apt.APT_ROUTE_XOR, apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_PM1_MFMA,
+                       apt.APT_ROUTE_FP4_MFMA)
+    if c.route == apt.APT_ROUTE_FP4_MFMA:
+        M, N, K, p, q = shape
+        assert p <= 2 and q <= 2 and K * ((1 << p) - 1) * ((1 << q) - 1) < 1 << 24
     if shape[0] <= 8:
         assert c.route == apt.APT_ROUTE_XOR
     M, N, K = shape[:3]
     ws = apt.apt_gemm_workspace_bytes(*shape, c)
-    if c.route == apt.APT_ROUTE_INT8_MFMA:
+    if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA):
         assert ws == _int8_workspace(M, N, K, c)
     else:
         assert ws == 0
@@ -159,6 +164,18 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
                                                  256, 128, 128, -2)), apt.APT_ERR_INVALID_ARG),
     # the int8 weight ring is 3 deep
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2)),
+     apt.APT_ERR_INVALID_ARG),
+    # FP4 operands: at most 2 bits each, and fp32 sums below 2^24
+    (dict(p=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(q=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(K=(1 << 24) // 9 + 1, p=2, q=2,
+          cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_WORKSPACE),
+    (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 96, 128, 128, 2, 2)),
      apt.APT_ERR_INVALID_ARG),
     # packed weights past 4 GiB do not fit the int8 kernels' 32-bit offsets
     (dict(M=64, N=1 << 20, K=1 << 16, p=1, q=1,
@@ -266,3 +283,15 @@ def test_search_workspace_covers_every_selectable_config():
 def test_config_table_starts_empty_and_clears():
     apt.apt_config_table_clear()
     assert apt.apt_config_table_size() == 0
+
+
+def test_fp4_workspace_is_half_the_int8_fragments():
+    i8 = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)
+    f4 = apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)
+    for M, K in [(64, 1000), (100, 4096), (2048, 4096)]:
+        a = apt.apt_gemm_workspace_bytes(M, 512, K, 2, 2, i8)
+        b = apt.apt_gemm_workspace_bytes(M, 512, K, 2, 2, f4)
+        nce = ((K + 127) // 128 + 1) // 2 * 2
+        assert a == (M + 31) // 32 * 32 * nce * 128
+        assert b == (M + 31) // 32 * 32 * nce * 64
+    assert apt.apt_gemm_workspace_bytes(64, 512, 1000, 3, 2, f4) == 0  # p = 3: not runnable

@@ -114,3 +114,50 @@ def test_pack_unpack(R, K, bits):
         row = R  # first padding row
         bad[(((row // 8) * nc + 0) * bits + 0) * 32 + (row % 8) * 4] |= np.uint32(1)
         assert ref.unpack(bad, R, K, bits)[1] == 1
+
+
+# ---- FP4 (E2M1) operands: what the FP4 route relies on ------------------------
+
+def e2m1_value(nibble: int) -> float:
+    """OCP E2M1 decoding: sign bit 3, exponent bits 2..1 (bias 1), mantissa
+    bit 0; exponent 0 is subnormal (0.5 * mantissa)."""
+    s = -1.0 if nibble & 8 else 1.0
+    e = (nibble >> 1) & 3
+    m = nibble & 1
+    return s * (0.5 * m if e == 0 else 2.0 ** (e - 1) * (1.0 + 0.5 * m))
+
+
+def test_e2m1_codes_of_bipolar_values():
+    """Every bipolar value of 1 or 2 bits is exact in E2M1, with the nibbles the
+    FP4 route builds from the planes: b = 1: (~u) << 3 | 0b0010; b = 2 with
+    u = 2h + l: (~h) << 3 | x << 2 | (~x) << 1 | x, x = ~(h ^ l)."""
+    for u in (0, 1):
+        v = int(ref.decode(np.array([u], np.uint8), 1)[0])
+        nib = ((1 - u) << 3) | 0b0010
+        assert e2m1_value(nib) == v == 2 * u - 1
+    for u in range(4):
+        h, l = u >> 1, u & 1
+        x = 1 - (h ^ l)
+        nib = ((1 - h) << 3) | (x << 2) | ((1 - x) << 1) | x
+        v = int(ref.decode(np.array([u], np.uint8), 2)[0])
+        assert e2m1_value(nib) == v == 2 * u - 3
+    # 3-bit values (+-5, +-7) are not E2M1 values: the route stops at 2 bits
+    values = {e2m1_value(n) for n in range(16)}
+    assert 5.0 not in values and 7.0 not in values
+
+
+def test_fp32_sums_exact_below_2_24():
+    """The FP4 route accumulates in fp32: with K (2^p-1)(2^q-1) < 2^24 every
+    partial sum is an integer below 2^24 in magnitude, so any order of fp32
+    additions is exact; just past the bound an fp32 sum can lose a unit."""
+    g = np.random.default_rng(5)
+    for p, q in [(1, 1), (1, 2), (2, 2)]:
+        K = (1 << 24) // (((1 << p) - 1) * ((1 << q) - 1)) - 1
+        va = np.full(K, (1 << q) - 1, np.int64)
+        vw = np.full(K, (1 << p) - 1, np.int64)
+        prod = (va * vw).astype(np.float32)
+        assert float(np.cumsum(prod, dtype=np.float32)[-1]) == float((va * vw).sum())
+        small = g.choice([-3, -1, 1, 3], size=5000).astype(np.float32)
+        assert float(np.sum(small, dtype=np.float32)) == float(small.astype(np.int64).sum())
+    over = np.full((1 << 24) // 9 + 2, 9.0, np.float32)
+    assert float(np.cumsum(over, dtype=np.float32)[-1]) != 9.0 * over.size
