@@ -74,7 +74,8 @@ enum {
   APT_ROUTE_PM1_MFMA = 2,   /* every (i, j) plane pair as +-1 int8 operands on the int8 matrix cores */
   APT_ROUTE_INT8_MFMA = 3,  /* planes reassembled in LDS into one int8 operand, one int8 MFMA per element pair */
   APT_ROUTE_FP4_MFMA = 4    /* as APT_ROUTE_INT8_MFMA with the bipolar values as FP4 (E2M1) operands of the
-                               block-scaled MFMA: p, q <= 2 and K (2^p-1)(2^q-1) < 2^24 */
+                               block-scaled MFMA: p, q <= 2 and K_pad (2^p-1)(2^q-1) < 2^24,
+                               K_pad = K rounded up to a multiple of 128 */
 };
 
 /* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950
@@ -203,7 +204,7 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
  * misaligned packed pointers, both outputs NULL, c_fp16 without both scales, a
  * route needing row sums without them, a misaligned workspace, or an invalid
  * cfg; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31, or when an FP4
- * route is forced with p or q > 2 or K (2^p-1)(2^q-1) >= 2^24; APT_ERR_WORKSPACE
+ * route is forced with p or q > 2 or K_pad (2^p-1)(2^q-1) >= 2^24; APT_ERR_WORKSPACE
  * when the workspace is missing or too small; APT_ERR_HIP on launch failure. */
 apt_status_t apt_gemm(int M, int N, int K, int p, int q,
                       const void* a_packed, const void* w_packed,

@@ -44,11 +44,7 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
       if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_FP4_MFMA:
-      // E2M1 holds bipolar values of at most 2 bits; fp32 sums stay exact
-      // integers below 2^24
-      if (p > 2 || q > 2) return APT_ERR_UNSUPPORTED;
-      if ((int64_t)K * ((1 << p) - 1) * ((1 << q) - 1) >= ((int64_t)1 << 24))
-        return APT_ERR_UNSUPPORTED;
+      if (!apt::fp4_route_ok(K, p, q)) return APT_ERR_UNSUPPORTED;
       [[fallthrough]];
     case APT_ROUTE_INT8_MFMA:
       if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;

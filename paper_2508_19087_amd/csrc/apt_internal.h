@@ -19,6 +19,15 @@ constexpr int kRowGroup = 8;
 constexpr int kPlaneStride = kRowGroup * kWordsPerPlane;  // words from plane i to plane i+1
 
 inline int num_chunks(int K) { return (K + kChunk - 1) / kChunk; }
+
+// The FP4 MFMA route applies to (p, q) over K: E2M1 holds bipolar values of
+// at most 2 bits, and its fp32 sums stay exact while no partial sum can reach
+// 2^24 in magnitude.  The MFMAs also sum the padding elements of the last
+// chunk (each -(2^p - 1) times -(2^q - 1)), so the bound is on the padded K.
+inline bool fp4_route_ok(int K, int p, int q) {
+  return p <= 2 && q <= 2 &&
+         (int64_t)num_chunks(K) * kChunk * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
+}
 inline int padded_rows(int R) { return (R + kRowGroup - 1) / kRowGroup * kRowGroup; }
 
 // Word offset of the 4 words of plane i, chunk c, row r.

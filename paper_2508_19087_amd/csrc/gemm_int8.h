@@ -56,7 +56,8 @@ constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes
 //          bits, one v_mfma_scale_f32_32x32x64_f8f6f4 (unit scales) per 64
 //          elements of k: the same operand bytes and issue cycles per MFMA as
 //          int8 for twice the multiply-adds.  Its fp32 sums are exact
-//          integers while K (2^p - 1)(2^q - 1) < 2^24 (the host checks).
+//          integers while K_pad (2^p - 1)(2^q - 1) < 2^24, K_pad = K rounded up
+//          to a chunk (the host checks).
 // Per chunk, k-step ks of lane half h holds (F = 0) half h of word ks's bytes,
 // or (F = 1) word 2 ks + h's nibbles; both operands use the same order.
 template <int F>

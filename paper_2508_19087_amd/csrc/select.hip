@@ -24,23 +24,28 @@
 namespace apt {
 namespace {
 
-struct Int8Shape {
-  int bm, bn, wm, wn;
-  int per_cu;            // workgroups resident per compute unit (registers and LDS)
+struct ShapeTimes {
   double pair_us;        // microseconds per chunk pair of one workgroup, per_cu of them on its CU
   double pair_alone_us;  // the same with the workgroup alone on its compute unit
   double fixed_us;       // launch, first loads and the last epilogue of one full round
 };
 
-// Measured on MI355X at W4A4, M = 2048, K = 2048 and 6144 (the K slope gives
-// the pair time, its intercept the fixed time), with one full round of tiles
-// and, for the 4-wave shapes, half a round (one workgroup per compute unit).
+struct Int8Shape {
+  int bm, bn, wm, wn;
+  int per_cu;            // workgroups resident per compute unit (registers and LDS)
+  ShapeTimes t[2];       // int8 operands, FP4 operands
+};
+
+// Measured on MI355X with M = 2048, K = 2048 and 6144 (the K slope gives the
+// pair time, its intercept the fixed time), with one full round of tiles and,
+// for the 4-wave shapes, half a round (one workgroup per compute unit): int8
+// operands at W4A4, FP4 operands at W2A2 (their only use).
 constexpr Int8Shape kInt8Shapes[] = {
-    {256, 256, 4, 2, 1, 3.74, 3.74, 19.6},
-    {512, 128, 8, 1, 1, 2.81, 2.81, 21.4},
-    {256, 128, 4, 1, 2, 3.39, 1.81, 12.9},
-    {256, 128, 4, 2, 1, 2.04, 2.04, 12.3},
-    {128, 128, 2, 2, 2, 1.88, 1.17, 12.2},
+    {256, 256, 4, 2, 1, {{3.74, 3.74, 19.6}, {1.87, 1.87, 19.7}}},
+    {512, 128, 8, 1, 1, {{2.81, 2.81, 21.4}, {1.71, 1.71, 20.1}}},
+    {256, 128, 4, 1, 2, {{3.39, 1.81, 12.9}, {1.70, 1.01, 14.0}}},
+    {256, 128, 4, 2, 1, {{2.04, 2.04, 12.3}, {1.14, 1.14, 11.8}}},
+    {128, 128, 2, 2, 2, {{1.88, 1.17, 12.2}, {1.17, 0.90, 9.0}}},
 };
 constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
 // Main shapes of a split launch (the first three above) and their tails (the
@@ -50,15 +55,6 @@ constexpr int kFirstTail = 2;
 // Device-wide rate at which stream-K partial tiles are written and read back
 // (bytes per microsecond), as the stream-K launches measured on MI355X show.
 constexpr double kPartialBytesPerUs = 2.5e6;
-// Pair time of the FP4 route relative to the int8 route with the same tile
-// (half the MFMAs, operand loads and LDS reads per pair; measured on MI355X).
-constexpr double kFp4PairFactor = 0.6;
-
-// The FP4 route can run (p, q) over K: E2M1 operands of at most 2 bits and
-// exact fp32 sums.
-bool fp4_ok(int K, int p, int q) {
-  return p <= 2 && q <= 2 && (int64_t)K * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
-}
 
 int compute_units() {
   static int cus = 0;
@@ -86,17 +82,16 @@ apt_config_t base_config(int route) {
   return c;
 }
 
-// Modelled microseconds of shape s with `grid` workgroups (0 = one per
-// tile), without the fixed time.  Workgroups run in rounds of cus * per_cu;
-// a last partial round of at most one workgroup per compute unit runs at the
-// alone rate.
-double model_loop_us(const Int8Shape& s, int M, int N, int K, int grid, int cus,
-                     double factor = 1.0) {
+// Modelled microseconds of shape s with operand format f (0 int8, 1 FP4) and
+// `grid` workgroups (0 = one per tile), without the fixed time.  Workgroups
+// run in rounds of cus * per_cu; a last partial round of at most one
+// workgroup per compute unit runs at the alone rate.
+double model_loop_us(const Int8Shape& s, int f, int M, int N, int K, int grid, int cus) {
   const int64_t tiles = (int64_t)((M + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
   const int64_t pairs = (((K + kChunk - 1) / kChunk) + 1) / 2;
   const int64_t slots = (int64_t)cus * s.per_cu;
   auto round_us = [&](int64_t wgs, int64_t wg_pairs) {
-    return (double)wg_pairs * factor * (wgs <= cus ? s.pair_alone_us : s.pair_us);
+    return (double)wg_pairs * (wgs <= cus ? s.t[f].pair_alone_us : s.t[f].pair_us);
   };
   if (grid == 0) {
     const int64_t full = tiles / slots, rem = tiles % slots;
@@ -121,8 +116,8 @@ double model_loop_us(const Int8Shape& s, int M, int N, int K, int grid, int cus,
   return us;
 }
 
-double model_us(const Int8Shape& s, int M, int N, int K, int grid, int cus, double factor = 1.0) {
-  return model_loop_us(s, M, N, K, grid, cus, factor) + s.fixed_us;
+double model_us(const Int8Shape& s, int f, int M, int N, int K, int grid, int cus) {
+  return model_loop_us(s, f, M, N, K, grid, cus) + s.t[f].fixed_us;
 }
 
 // The tail shape a split config with main shape i and tail size of shape t
@@ -228,7 +223,7 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
     }
   }
   // the same tile configs with FP4 operands where they apply
-  if (fp4_ok(K, p, q)) {
+  if (fp4_route_ok(K, p, q)) {
     const int end = n;
     for (int j = n_int8_single - 2 * kNumInt8Shapes; j < end; ++j) {
       apt_config_t c = out[j];
@@ -267,14 +262,13 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
     }
   };
   // int8 operands, then (where they apply) FP4 operands
-  for (int f = 0; f < (fp4_ok(K, p, q) ? 2 : 1); ++f) {
+  for (int f = 0; f < (fp4_route_ok(K, p, q) ? 2 : 1); ++f) {
     fp4 = f == 1;
-    const double factor = fp4 ? kFp4PairFactor : 1.0;
     for (int i = 0; i < kNumInt8Shapes; ++i) {
       const Int8Shape& s = kInt8Shapes[i];
       const int round = std::min(cus * s.per_cu, kMaxGrid);
-      consider(model_us(s, M, N, K, 0, cus, factor), i, 0, 0, -1);
-      consider(model_us(s, M, N, K, round, cus, factor), i, round, 0, -1);
+      consider(model_us(s, f, M, N, K, 0, cus), i, 0, 0, -1);
+      consider(model_us(s, f, M, N, K, round, cus), i, round, 0, -1);
     }
     for (int i = 0; i < kNumMainShapes; ++i) {
       const Int8Shape& s = kInt8Shapes[i];
@@ -285,9 +279,10 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
         const Int8Shape& ts = kInt8Shapes[t];
         // one launch when the wave counts match: one fixed time, else two
         const bool paired = ts.wm * ts.wn == s.wm * s.wn;
-        consider(model_loop_us(s, M, split, K, 0, cus, factor) +
-                     model_loop_us(ts, M, N - split, K, 0, cus, factor) +
-                     (paired ? std::max(s.fixed_us, ts.fixed_us) : s.fixed_us + ts.fixed_us),
+        const double fs = s.t[f].fixed_us, ft = ts.t[f].fixed_us;
+        consider(model_loop_us(s, f, M, split, K, 0, cus) +
+                     model_loop_us(ts, f, M, N - split, K, 0, cus) +
+                     (paired ? std::max(fs, ft) : fs + ft),
                  i, 0, split, t);
       }
     }

@@ -173,6 +173,11 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
     (dict(K=(1 << 24) // 9 + 1, p=2, q=2,
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_UNSUPPORTED),
+    # the bound counts the padding elements of the last chunk: K below 2^24 / 9 whose
+    # padded length is not
+    (dict(K=(1 << 24) // 9 // 128 * 128 + 1, p=2, q=2,
+          cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
     (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_WORKSPACE),
     (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 96, 128, 128, 2, 2)),
