@@ -185,14 +185,19 @@ def route_table(calls: int = 20):
               ("xor+popcount", C(apt.APT_ROUTE_XOR)),
               ("+-1 planes int8 MFMA", C(apt.APT_ROUTE_PM1_MFMA)),
               ("reassembled int8 MFMA 256x128 g256", C(apt.APT_ROUTE_INT8_MFMA, 256, 128, 128, 4, 2, 256, 3)),
-              ("reassembled int8 MFMA 128x128 g512", C(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 512, 3))]
+              ("reassembled int8 MFMA 128x128 g512", C(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 512, 3)),
+              ("reassembled FP4 MFMA 128x128 g512", C(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2, 512, 3))]
     out = {}
-    for prob in [synth.w4a4_prefill(), synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]:
+    # the step's GEMMs, and the W1A1 down projection, where the FP4 form applies
+    for prob in [synth.w4a4_prefill(), synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP),
+                 synth.sweep_down(0)]:
         a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
         w = apt.pack(dev(prob.w_codes), prob.p)
         row = {}
         for name, cfg in routes:
             if cfg is not None and cfg.route == apt.APT_ROUTE_PM1_MFMA and max(prob.p, prob.q) > 7:
+                continue
+            if cfg is not None and cfg.route == apt.APT_ROUTE_FP4_MFMA and max(prob.p, prob.q) > 2:
                 continue
             c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
             wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
@@ -238,7 +243,8 @@ def search_table(calls: int = 20):
             return "xor"
         if c.route == apt.APT_ROUTE_PM1_MFMA:
             return "pm1"
-        t = "int8 %dx%d/%dx%d g%d" % (c.bm, c.bn, c.waves_m, c.waves_n, c.grid)
+        t = "%s %dx%d/%dx%d g%d" % ("fp4" if c.route == apt.APT_ROUTE_FP4_MFMA else "int8",
+                                    c.bm, c.bn, c.waves_m, c.waves_n, c.grid)
         if c.split_n:
             t += " +%dx%d@%d g%d" % (c.tail_bm, c.tail_bn, c.split_n, c.tail_grid)
         return t
