@@ -73,8 +73,9 @@ enum {
   APT_ROUTE_XOR = 1,        /* XOR + popcount on packed words, cross-lane reduction (Sec. III-B, 1-bit XOR form) */
   APT_ROUTE_PM1_MFMA = 2,   /* every (i, j) plane pair as +-1 int8 operands on the int8 matrix cores */
   APT_ROUTE_INT8_MFMA = 3,  /* planes reassembled in LDS into one int8 operand, one int8 MFMA per element pair */
-  APT_ROUTE_FP4_MFMA = 4    /* as APT_ROUTE_INT8_MFMA with the bipolar values as FP4 (E2M1) operands of the
-                               block-scaled MFMA: p, q <= 2 and K_pad (2^p-1)(2^q-1) < 2^24,
+  APT_ROUTE_FP4_MFMA = 4    /* as APT_ROUTE_INT8_MFMA with the bipolar values as operands of the
+                               block-scaled MFMA: FP4 (E2M1) weights, p <= 2, and FP4 (q <= 2) or
+                               FP8 E4M3 (q <= 4) activations; K_pad (2^p-1)(2^q-1) < 2^24,
                                K_pad = K rounded up to a multiple of 128 */
 };
 
@@ -168,8 +169,9 @@ apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, i
  * lookup table, approximate matching): the config apt_search_config recorded
  * for exactly this problem, if any; otherwise a model of the MI355X kernels
  * (rounds of resident tiles per compute unit, measured cycles per chunk pair
- * of each tile shape, stream-K partial traffic), which stands in for the
- * approximate match.  The choice never changes results.
+ * of each tile shape, stream-K partial traffic; the FP4 route only with FP4
+ * activations, q <= 2), which stands in for the approximate match.  The
+ * choice never changes results.
  * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8] or out == NULL. */
 apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out);
 
@@ -177,7 +179,8 @@ apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* 
  * NULL or route AUTO = the selected one).  The reassembled int8 MFMA route
  * expands the activations once per call into int8 MFMA fragments
  * (ceil(M/32)*32 * K_pad' bytes, K_pad' = K_pad rounded up to a multiple of
- * 256; the FP4 MFMA route stores half of that: two values per byte) and,
+ * 256; the FP4 MFMA route with q <= 2 stores half of that: two values per
+ * byte) and,
  * for each launch with a stream-K decomposition (grid > 0 and T not a
  * multiple of grid), two int32 BM x BN partial tiles per workgroup and one
  * counter per shared tile, each region rounded up to 256 bytes; the other
@@ -204,7 +207,7 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
  * misaligned packed pointers, both outputs NULL, c_fp16 without both scales, a
  * route needing row sums without them, a misaligned workspace, or an invalid
  * cfg; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31, or when an FP4
- * route is forced with p or q > 2 or K_pad (2^p-1)(2^q-1) >= 2^24; APT_ERR_WORKSPACE
+ * route is forced with p > 2, q > 4 or K_pad (2^p-1)(2^q-1) >= 2^24; APT_ERR_WORKSPACE
  * when the workspace is missing or too small; APT_ERR_HIP on launch failure. */
 apt_status_t apt_gemm(int M, int N, int K, int p, int q,
                       const void* a_packed, const void* w_packed,

@@ -37,7 +37,6 @@ apt_status_t pack_common(const int8_t* codes, int rows, int K, int bits, void* p
 // Checks a config against the problem; returns APT_OK or the status to report.
 apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int q,
                           bool have_rowsums) {
-  (void)q;
   switch (c.route) {
     case APT_ROUTE_XOR:
       if (!apt::xor_config_ok(c)) return APT_ERR_INVALID_ARG;
@@ -49,7 +48,7 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
     case APT_ROUTE_INT8_MFMA:
       if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
-      if (!apt::int8_sizes_ok(M, N, K, p, c)) return APT_ERR_UNSUPPORTED;
+      if (!apt::int8_sizes_ok(M, N, K, p, q, c)) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_PM1_MFMA:
       if (p > 7 || q > 7) return APT_ERR_UNSUPPORTED;
@@ -105,7 +104,7 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
                              : *cfg;
   if (c.route != APT_ROUTE_INT8_MFMA && c.route != APT_ROUTE_FP4_MFMA) return 0;
   if (check_config(c, M, N, K, p, q, true) != APT_OK) return 0;
-  return apt::int8_workspace_bytes(M, N, K, c);
+  return apt::int8_workspace_bytes(M, N, K, q, c);
 }
 
 }  // extern "C"
@@ -136,7 +135,7 @@ apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed
   apt_status_t st = check_config(c, M, N, K, p, q, have_rowsums);
   if (st != APT_OK) return st;
   if (c.route == APT_ROUTE_INT8_MFMA || c.route == APT_ROUTE_FP4_MFMA) {
-    if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, N, K, c))
+    if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, N, K, q, c))
       return APT_ERR_WORKSPACE;
     if (!aligned16(workspace)) return APT_ERR_INVALID_ARG;
   }
@@ -198,7 +197,7 @@ size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q) {
   for (int i = 0; i < n; ++i)
     if ((cand[i].route == APT_ROUTE_INT8_MFMA || cand[i].route == APT_ROUTE_FP4_MFMA) &&
         apt::int8_config_ok(cand[i], N))
-      most = std::max(most, apt::int8_workspace_bytes(M, N, K, cand[i]));
+      most = std::max(most, apt::int8_workspace_bytes(M, N, K, q, cand[i]));
   return most;
 }
 

@@ -20,12 +20,13 @@ constexpr int kPlaneStride = kRowGroup * kWordsPerPlane;  // words from plane i 
 
 inline int num_chunks(int K) { return (K + kChunk - 1) / kChunk; }
 
-// The FP4 MFMA route applies to (p, q) over K: E2M1 holds bipolar values of
-// at most 2 bits, and its fp32 sums stay exact while no partial sum can reach
-// 2^24 in magnitude.  The MFMAs also sum the padding elements of the last
-// chunk (each -(2^p - 1) times -(2^q - 1)), so the bound is on the padded K.
+// The FP4 MFMA route applies to (p, q) over K: E2M1 holds bipolar weights of
+// at most 2 bits, E2M1 (q <= 2) or E4M3 (q <= 4) the activations, and the
+// fp32 sums stay exact while no partial sum can reach 2^24 in magnitude.  The
+// MFMAs also sum the padding elements of the last chunk (each -(2^p - 1)
+// times -(2^q - 1)), so the bound is on the padded K.
 inline bool fp4_route_ok(int K, int p, int q) {
-  return p <= 2 && q <= 2 &&
+  return p <= 2 && q <= 4 &&
          (int64_t)num_chunks(K) * kChunk * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
 }
 inline int padded_rows(int R) { return (R + kRowGroup - 1) / kRowGroup * kRowGroup; }
@@ -81,8 +82,8 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
                             hipStream_t stream);
 constexpr int kMaxGrid = 4096;  // persistent workgroups of the int8 route, at most
 bool int8_config_ok(const apt_config_t& cfg, int N);
-bool int8_sizes_ok(int M, int N, int K, int p, const apt_config_t& cfg);
-size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg);
+bool int8_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg);
+size_t int8_workspace_bytes(int M, int N, int K, int q, const apt_config_t& cfg);
 
 // Plane-pair +-1 MFMA route (gemm_pm1.hip).
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);

@@ -55,16 +55,25 @@ constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes
 //   F = 1: FP4 (E2M1) operand nibbles for weights and activations of at most 2
 //          bits, one v_mfma_scale_f32_32x32x64_f8f6f4 (unit scales) per 64
 //          elements of k: the same operand bytes and issue cycles per MFMA as
-//          int8 for twice the multiply-adds.  Its fp32 sums are exact
-//          integers while K_pad (2^p - 1)(2^q - 1) < 2^24, K_pad = K rounded up
-//          to a chunk (the host checks).
+//          int8 for twice the multiply-adds;
+//   F = 2: FP4 weights (at most 2 bits) with FP8 (E4M3) activation bytes (at
+//          most 4 bits: every odd value up to 15 is exact in E4M3), the same
+//          MFMA with a mixed operand format, 64 elements of k per MFMA at
+//          about 1.15x the int8 multiply-add rate.
+// With F > 0 the fp32 sums are exact integers while K_pad (2^p - 1)(2^q - 1)
+// < 2^24, K_pad = K rounded up to a chunk (the host checks).
 // Per chunk, k-step ks of lane half h holds (F = 0) half h of word ks's bytes,
-// or (F = 1) word 2 ks + h's nibbles; both operands use the same order.
+// or (F > 0) word 2 ks + h's weight nibbles; nibble 8 t + f is element 4 f + t
+// of the word.  The FP8 operand covers k in 16-element blocks: lane half h
+// holds elements 16 h .. 16 h + 15 of the k-step's first 32 in bytes 0..15
+// and of its second 32 in bytes 16..31, which puts nibble n of word 2 ks + x
+// (n = 16 h + j) against byte 16 x + j of lane half h.
 template <int F>
 struct Fmt {
   static constexpr int kStepK = F ? 64 : 32;                   // k per MFMA
   static constexpr int kSteps = kChunk / kStepK;               // k-steps per chunk
   static constexpr int kRowBytes = kSteps * kStepBytes + 16;   // padded LDS row of a chunk
+  static constexpr int kAVecs = F == 2 ? 2 : 1;                // 16-byte activation vectors per lane and k-step
 };
 constexpr int kStages = 3;                      // weight LDS ring depth
 
@@ -114,10 +123,23 @@ struct Int8Params {
   int vec_out;        // outputs take 16-byte (int32) / 8-byte (fp16) row stores
 };
 
-// Bytes of the activation fragment buffer for M rows and K (F = 1: nibbles).
-inline size_t a_frag_bytes(int M, int K, bool fp4 = false) {
+// Bytes of the activation fragment buffer for M rows and K in operand format
+// fmt (F = 1: nibbles, otherwise bytes).
+inline size_t a_frag_bytes(int M, int K, int fmt = 0) {
   const int nce = (num_chunks(K) + 1) & ~1;
-  return (size_t)((M + 31) / 32) * 32 * nce * (fp4 ? kChunk / 2 : kChunk);
+  return (size_t)((M + 31) / 32) * 32 * nce * (fmt == 1 ? kChunk / 2 : kChunk);
+}
+
+// E4M3 bits of the bipolar value 2u - (2^Q - 1) (Q <= 4: odd, |v| <= 15).
+template <int Q>
+__device__ __forceinline__ uint32_t e4m3_bipolar(uint32_t u) {
+  static_assert(Q <= 4, "E4M3 holds bipolar values of at most 4 bits exactly");
+  const int v = 2 * (int)u - ((1 << Q) - 1);
+  const int a = v < 0 ? -v : v;
+  // |v| = 1, 3, ..., 15: exponent field 7 + floor(log2 |v|), 3 mantissa bits
+  const int e = a >= 8 ? 3 : a >= 4 ? 2 : a >= 2 ? 1 : 0;
+  const uint32_t bits = (uint32_t)(((e + 7) << 3) | (((a << 3) >> e) & 7));
+  return v < 0 ? bits | 0x80u : bits;
 }
 
 // ---- activation expansion ---------------------------------------------------
@@ -125,9 +147,11 @@ inline size_t a_frag_bytes(int M, int K, bool fp4 = false) {
 // order: lane l (vector index ((mb * nsteps + ks) * 64 + l)) carries 16 bytes of
 // row 32 mb + l mod 32, namely bytes 16 (l / 32) .. 16 (l / 32) + 15 of the
 // k-step's 32 reassembled bytes (F = 1: the 16 nibble bytes of one plane
-// word).  Rows past M are expanded from all-zero planes (padding elements); a
+// word).  F = 2: two 16-byte vectors per lane, ((mb * nsteps + ks) * 2 + x) *
+// 64 + l, with the E4M3 bytes of word 2 ks + x that lane half l / 32 meets
+// (Fmt).  Rows past M are expanded from all-zero planes (padding elements); a
 // chunk past the last one (the odd chunk that makes the count even) is
-// all-zero bytes, which are 0 in both formats.
+// all-zero bytes, which are 0 in every format.
 template <int Q, int F>
 __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restrict__ a_packed, int M,
                                                        int nchunks, int nsteps, int mblocks,
@@ -156,7 +180,26 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
     for (int j = 0; j < Q; ++j) pw[j] = 0u;
   }
   const int mb = row / 32, l = row % 32;
-  if (F) {
+  if (F == 2) {
+    // word w -> k-step w / 2, vector w mod 2; byte j of lane half h is element
+    // 4 (j mod 8) + 2 h + j / 8 of the word
+    uint32_t o[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (chunk < nchunks) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int e = 4 * (j % 8) + 2 * h + j / 8;
+          uint32_t u = 0u;
+#pragma unroll
+          for (int i = 0; i < Q; ++i) u |= ((pw[i] >> e) & 1u) << i;
+          o[4 * h + j / 4] |= e4m3_bipolar<(Q <= 4 ? Q : 4)>(u) << (8 * (j % 4));
+        }
+    }
+    v4i* f = out + (((int64_t)mb * nsteps + chunk * kSteps + w / 2) * 2 + w % 2) * kFragVecs;
+    f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+  } else if (F) {
     // word w -> k-step w / 2, lane half w mod 2
     uint32_t o[4] = {0u, 0u, 0u, 0u};
     if (chunk < nchunks) fp4_word<(Q <= 2 ? Q : 2)>(pw, o);
@@ -379,6 +422,7 @@ template <int P, int F, int BM, int BN, int WM, int WN, int SPLIT>
 __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* lds, int w, int G) {
   static_assert(F == 0 || P <= 2, "FP4 operands hold weights of at most 2 bits");
   constexpr int kSteps = Fmt<F>::kSteps;
+  constexpr int kAVecs = Fmt<F>::kAVecs;
   constexpr int kRowBytes = Fmt<F>::kRowBytes;
   constexpr int T = WM * WN * kWave;
   constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
@@ -442,11 +486,12 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   // Uniform byte offset of this wave's 32-row fragment block a of a tile.
   auto a_block = [&](int m0, int a) __attribute__((always_inline)) {
     const int mb = min((m0 + wm * WTM) / 32 + a, prm.mblocks - 1);
-    return mb * prm.nsteps * kFragVecs * 16;
+    return mb * prm.nsteps * kAVecs * kFragVecs * 16;
   };
   const uint32_t a_lane = lane * 16;
-  auto load_a = [&](int m0, int chunk, int ks, int a) __attribute__((always_inline)) -> v4i {
-    const int soff = a_block(m0, a) + (min(chunk, NCE - 1) * kSteps + ks) * kFragVecs * 16;
+  // vector x (F = 2: 0 or 1) of k-step ks of the fragment block
+  auto load_a = [&](int m0, int chunk, int ks, int a, int x = 0) __attribute__((always_inline)) -> v4i {
+    const int soff = a_block(m0, a) + ((min(chunk, NCE - 1) * kSteps + ks) * kAVecs + x) * kFragVecs * 16;
     return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_lane, soff, 0));
   };
   auto w_offsets = [&](int n0, uint32_t* voff) __attribute__((always_inline)) {
@@ -464,7 +509,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
         for (int v = 0; v < 16; ++v) acc[b][a][v] = 0;
   };
   zero_acc();
-  v4i afr[kSteps][FM];
+  v4i afr[kSteps * kAVecs][FM];  // vector x of k-step ks at ks * kAVecs + x
 
   const int lrow = lane % 32;
   const int lk = (lane / 32) * 16;
@@ -501,7 +546,15 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
       for (int b = 0; b < FN; ++b)
 #pragma unroll
         for (int a = 0; a < FM; ++a)
-          if (F) {
+          if (F == 2) {
+            // E2M1 weights (format code 4) x E4M3 activations (code 0), unit E8M0 scales (127)
+            const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3], 0, 0, 0, 0};
+            const v4i a0 = afr[2 * ks][a], a1 = afr[2 * ks + 1][a];
+            const v8i ab = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+            acc[b][a] = __builtin_bit_cast(
+                v16i, __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                          wa, ab, __builtin_bit_cast(v16f, acc[b][a]), 4, 0, 0, 127, 0, 127));
+          } else if (F) {
             // E2M1 x E2M1 (format code 4 for both), unit E8M0 scales (127)
             const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3], 0, 0, 0, 0};
             const v8i ab = {afr[ks][a][0], afr[ks][a][1], afr[ks][a][2], afr[ks][a][3], 0, 0, 0, 0};
@@ -512,7 +565,9 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
             acc[b][a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[cur][b], afr[ks][a], acc[b][a], 0, 0, 0);
           }
 #pragma unroll
-      for (int a = 0; a < FM; ++a) afr[ks][a] = load_a(a_m0, a_chunk, ks, a);
+      for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int x = 0; x < kAVecs; ++x) afr[ks * kAVecs + x][a] = load_a(a_m0, a_chunk, ks, a, x);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -775,7 +830,9 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
 #pragma unroll
   for (int ks = 0; ks < kSteps; ++ks)
 #pragma unroll
-    for (int a = 0; a < FM; ++a) afr[ks][a] = load_a(cp.m0, 2 * cp.pair, ks, a);
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+      for (int x = 0; x < kAVecs; ++x) afr[ks * kAVecs + x][a] = load_a(cp.m0, 2 * cp.pair, ks, a, x);
   rw0.store(lds, tid);
   rw1.store(lds + kStageBytes, tid);
   rw0.load(w_rsrc, wv1, NC, 2 * c1.pair);
@@ -923,16 +980,17 @@ inline hipError_t launch_p_pair(int sa, const Int8Params& pa, int ga, int sb, co
   return hipErrorInvalidValue;
 }
 
-// Launches for weight bits P (main kernel) and activation bits Q (expansion),
-// int8 or (fp4, P or Q <= 2) FP4 operands; the explicit instantiations live
-// in gemm_int8_inst.hip, built once per width.
+// Launches for weight bits P (main kernel) and activation bits Q (expansion)
+// in operand format fmt (0 int8; 1 FP4, P and Q <= 2; 2 FP4 weights with FP8
+// activations, P <= 2, Q <= 4; other combinations return hipErrorInvalidValue);
+// the explicit instantiations live in gemm_int8_inst.hip, built once per width.
 template <int P>
-hipError_t launch_for_p(bool fp4, int shape, const Int8Params& prm, int grid, hipStream_t stream);
+hipError_t launch_for_p(int fmt, int shape, const Int8Params& prm, int grid, hipStream_t stream);
 template <int P>
-hipError_t launch_pair_for_p(bool fp4, int sa, const Int8Params& pa, int ga, int sb,
+hipError_t launch_pair_for_p(int fmt, int sa, const Int8Params& pa, int ga, int sb,
                              const Int8Params& pb, int gb, hipStream_t stream);
 template <int Q>
-hipError_t launch_expand_for_q(bool fp4, const uint32_t* a_packed, int M, int nchunks, int nsteps,
+hipError_t launch_expand_for_q(int fmt, const uint32_t* a_packed, int M, int nchunks, int nsteps,
                                int mblocks, v4i* out, int* counters, int ncounters,
                                hipStream_t stream);
 

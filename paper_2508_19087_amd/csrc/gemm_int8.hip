@@ -19,37 +19,42 @@ int shape_index(const apt_config_t& cfg) {
   return -1;
 }
 
-hipError_t launch_p(int p, bool fp4, int shape, const Int8Params& prm, int grid,
+hipError_t launch_p(int p, int fmt, int shape, const Int8Params& prm, int grid,
                     hipStream_t stream) {
   switch (p) {
-    case 1: return launch_for_p<1>(fp4, shape, prm, grid, stream);
-    case 2: return launch_for_p<2>(fp4, shape, prm, grid, stream);
-    case 3: return launch_for_p<3>(fp4, shape, prm, grid, stream);
-    case 4: return launch_for_p<4>(fp4, shape, prm, grid, stream);
-    case 5: return launch_for_p<5>(fp4, shape, prm, grid, stream);
-    case 6: return launch_for_p<6>(fp4, shape, prm, grid, stream);
-    case 7: return launch_for_p<7>(fp4, shape, prm, grid, stream);
-    case 8: return launch_for_p<8>(fp4, shape, prm, grid, stream);
+    case 1: return launch_for_p<1>(fmt, shape, prm, grid, stream);
+    case 2: return launch_for_p<2>(fmt, shape, prm, grid, stream);
+    case 3: return launch_for_p<3>(fmt, shape, prm, grid, stream);
+    case 4: return launch_for_p<4>(fmt, shape, prm, grid, stream);
+    case 5: return launch_for_p<5>(fmt, shape, prm, grid, stream);
+    case 6: return launch_for_p<6>(fmt, shape, prm, grid, stream);
+    case 7: return launch_for_p<7>(fmt, shape, prm, grid, stream);
+    case 8: return launch_for_p<8>(fmt, shape, prm, grid, stream);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_pair(int p, bool fp4, int sa, const Int8Params& pa, int ga, int sb,
+hipError_t launch_pair(int p, int fmt, int sa, const Int8Params& pa, int ga, int sb,
                        const Int8Params& pb, int gb, hipStream_t stream) {
   switch (p) {
-    case 1: return launch_pair_for_p<1>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 2: return launch_pair_for_p<2>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 3: return launch_pair_for_p<3>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 4: return launch_pair_for_p<4>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 5: return launch_pair_for_p<5>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 6: return launch_pair_for_p<6>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 7: return launch_pair_for_p<7>(fp4, sa, pa, ga, sb, pb, gb, stream);
-    case 8: return launch_pair_for_p<8>(fp4, sa, pa, ga, sb, pb, gb, stream);
+    case 1: return launch_pair_for_p<1>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 2: return launch_pair_for_p<2>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 3: return launch_pair_for_p<3>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 4: return launch_pair_for_p<4>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 5: return launch_pair_for_p<5>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 6: return launch_pair_for_p<6>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 7: return launch_pair_for_p<7>(fmt, sa, pa, ga, sb, pb, gb, stream);
+    case 8: return launch_pair_for_p<8>(fmt, sa, pa, ga, sb, pb, gb, stream);
   }
   return hipErrorInvalidValue;
 }
 
-bool is_fp4(const apt_config_t& cfg) { return cfg.route == APT_ROUTE_FP4_MFMA; }
+// Operand format of a config (the F of the kernels): int8 for the int8 route;
+// for the FP4 route FP4 activations when q <= 2, FP8 activations otherwise.
+int operand_format(const apt_config_t& cfg, int q) {
+  if (cfg.route != APT_ROUTE_FP4_MFMA) return 0;
+  return q <= 2 ? 1 : 2;
+}
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -121,22 +126,23 @@ bool int8_config_ok(const apt_config_t& cfg, int N) {
 
 // The kernels address the packed weights, the activation fragments and the
 // stream-K partial tiles with 32-bit buffer offsets.
-bool int8_sizes_ok(int M, int N, int K, int p, const apt_config_t& cfg) {
+bool int8_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
   const uint64_t limit = (uint64_t)1 << 32;
   int8::Plan pl[2];
   const int n = int8::make_plans(M, N, K, cfg, pl);
   for (int i = 0; i < n; ++i)
     if (pl[i].partial_bytes >= limit) return false;
-  return apt_packed_bytes(N, K, p) < limit && int8::a_frag_bytes(M, K, int8::is_fp4(cfg)) < limit;
+  return apt_packed_bytes(N, K, p) < limit &&
+         int8::a_frag_bytes(M, K, int8::operand_format(cfg, q)) < limit;
 }
 
 // Workspace: activation fragments, then per launch (stream-K) one arrival
 // counter per stream-K tile, then per launch two int32 partial tiles per
 // workgroup.
-size_t int8_workspace_bytes(int M, int N, int K, const apt_config_t& cfg) {
+size_t int8_workspace_bytes(int M, int N, int K, int q, const apt_config_t& cfg) {
   int8::Plan pl[2];
   const int n = int8::make_plans(M, N, K, cfg, pl);
-  size_t bytes = int8::align256(int8::a_frag_bytes(M, K, int8::is_fp4(cfg)));
+  size_t bytes = int8::align256(int8::a_frag_bytes(M, K, int8::operand_format(cfg, q)));
   for (int i = 0; i < n; ++i)
     bytes += int8::align256(pl[i].partial_bytes) + int8::align256(pl[i].counter_bytes);
   return bytes;
@@ -148,18 +154,18 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
   Plan pl[2];
   const int nl = make_plans(g.M, g.N, g.K, cfg, pl);
   Int8Params prm[2];
-  const bool fp4 = is_fp4(cfg);
-  uint8_t* base = static_cast<uint8_t*>(workspace) + align256(a_frag_bytes(g.M, g.K, fp4));
+  const int fmt = operand_format(cfg, g.q);
+  uint8_t* base = static_cast<uint8_t*>(workspace) + align256(a_frag_bytes(g.M, g.K, fmt));
   int* counters = nullptr;
   int ncounters = 0;
   for (int i = 0; i < nl; ++i) {
     Int8Params& p = prm[i];
     p.g = g;
     p.nchunks = num_chunks(g.K);
-    p.nsteps = ((p.nchunks + 1) & ~1) * (fp4 ? Fmt<1>::kSteps : Fmt<0>::kSteps);
+    p.nsteps = ((p.nchunks + 1) & ~1) * (fmt ? Fmt<1>::kSteps : Fmt<0>::kSteps);
     p.mblocks = (g.M + 31) / 32;
     p.a_frag = static_cast<const v4i*>(workspace);
-    p.a_bytes = (uint32_t)a_frag_bytes(g.M, g.K, fp4);
+    p.a_bytes = (uint32_t)a_frag_bytes(g.M, g.K, fmt);
     p.w_bytes = (uint32_t)apt_packed_bytes(g.N, g.K, g.p);
     p.n_begin = pl[i].n_begin;
     p.tiles_n = pl[i].tiles_n;
@@ -186,21 +192,21 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
   const Int8Params& p0 = prm[0];
   hipError_t e = hipErrorInvalidValue;
   switch (g.q) {
-    case 1: e = launch_expand_for_q<1>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 2: e = launch_expand_for_q<2>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 3: e = launch_expand_for_q<3>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 4: e = launch_expand_for_q<4>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 5: e = launch_expand_for_q<5>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 6: e = launch_expand_for_q<6>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 7: e = launch_expand_for_q<7>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
-    case 8: e = launch_expand_for_q<8>(fp4, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 1: e = launch_expand_for_q<1>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 2: e = launch_expand_for_q<2>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 3: e = launch_expand_for_q<3>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 4: e = launch_expand_for_q<4>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 5: e = launch_expand_for_q<5>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 6: e = launch_expand_for_q<6>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 7: e = launch_expand_for_q<7>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
+    case 8: e = launch_expand_for_q<8>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
   }
   if (e != hipSuccess) return e;
   if (nl == 2 && pair_supported(pl[0].shape, pl[1].shape))
-    return launch_pair(g.p, fp4, pl[0].shape, prm[0], pl[0].grid, pl[1].shape, prm[1], pl[1].grid,
+    return launch_pair(g.p, fmt, pl[0].shape, prm[0], pl[0].grid, pl[1].shape, prm[1], pl[1].grid,
                        stream);
   for (int i = 0; i < nl && e == hipSuccess; ++i)
-    e = launch_p(g.p, fp4, pl[i].shape, prm[i], pl[i].grid, stream);
+    e = launch_p(g.p, fmt, pl[i].shape, prm[i], pl[i].grid, stream);
   return e;
 }
 

@@ -39,7 +39,9 @@ struct Int8Shape {
 // Measured on MI355X with M = 2048, K = 2048 and 6144 (the K slope gives the
 // pair time, its intercept the fixed time), with one full round of tiles and,
 // for the 4-wave shapes, half a round (one workgroup per compute unit): int8
-// operands at W4A4, FP4 operands at W2A2 (their only use).
+// operands at W4A4, FP4 operands at W2A2 (their only use in the model: FP4
+// weights with FP8 activations measured no faster than int8 operands, so that
+// form is left to the search module).
 constexpr Int8Shape kInt8Shapes[] = {
     {256, 256, 4, 2, 1, {{3.74, 3.74, 19.6}, {1.87, 1.87, 19.7}}},
     {512, 128, 8, 1, 1, {{2.81, 2.81, 21.4}, {1.71, 1.71, 20.1}}},
@@ -181,7 +183,8 @@ int table_size() {
 // the +-1 plane route where its operands fit (p, q <= 7), each int8 tile shape
 // with one workgroup per tile and with a persistent grid of one round of
 // workgroups, and the split launches the model considers (a main shape over
-// whole rounds of columns, a smaller shape on the rest).
+// whole rounds of columns, a smaller shape on the rest); each of these again
+// on the FP4 route where it applies (FP4 or FP8 activations).
 int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int max_out) {
   int n = 0;
   auto add = [&](const apt_config_t& c) {
@@ -261,8 +264,8 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
       best_fp4 = fp4;
     }
   };
-  // int8 operands, then (where they apply) FP4 operands
-  for (int f = 0; f < (fp4_route_ok(K, p, q) ? 2 : 1); ++f) {
+  // int8 operands, then (where they apply) FP4 operands for both sides
+  for (int f = 0; f < (fp4_route_ok(K, p, q) && q <= 2 ? 2 : 1); ++f) {
     fp4 = f == 1;
     for (int i = 0; i < kNumInt8Shapes; ++i) {
       const Int8Shape& s = kInt8Shapes[i];

@@ -34,7 +34,7 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
                                               split, tbm, tbn, tg)
                     out.append(("int8_%dx%d_w%dx%d_tail%dx%d@%d_g%d" % (bm, bn, wm, wn, tbm, tbn, split,
                                                                         tg), c))
-    if p <= 2 and q <= 2:  # the same tile configs with FP4 (E2M1) operands
+    if p <= 2 and q <= 4:  # the same tile configs with FP4 weights (FP4 or FP8 activations)
         fp4 = []
         for name, c in out:
             if c.route == apt.APT_ROUTE_INT8_MFMA:

@@ -47,14 +47,15 @@ def _shapes():
     return out
 
 
-def _int8_workspace(M, N, K, c):
+def _int8_workspace(M, N, K, c, q=4):
     """Activation fragments, then (stream-K) per launch one counter per shared
     tile and two int32 partial tiles per workgroup, each region rounded up to
     256 bytes."""
     up = lambda x: (x + 255) // 256 * 256
     nce = ((K + 127) // 128 + 1) // 2 * 2
-    # int8 bytes, or FP4 nibbles (half as many bytes)
-    ws = up((M + 31) // 32 * 32 * nce * (64 if c.route == apt.APT_ROUTE_FP4_MFMA else 128))
+    # int8 or FP8 bytes, or FP4 nibbles (half as many bytes: FP4 route with q <= 2)
+    nib = c.route == apt.APT_ROUTE_FP4_MFMA and q <= 2
+    ws = up((M + 31) // 32 * 32 * nce * (64 if nib else 128))
     launches = [(c.bm, c.bn, N, c.grid)]
     if c.split_n:
         launches = [(c.bm, c.bn, c.split_n, c.grid), (c.tail_bm, c.tail_bn, N - c.split_n, c.tail_grid)]
@@ -91,13 +92,14 @@ def test_select_config_valid(shape):
                        apt.APT_ROUTE_FP4_MFMA)
     if c.route == apt.APT_ROUTE_FP4_MFMA:
         M, N, K, p, q = shape
-        assert p <= 2 and q <= 2 and K * ((1 << p) - 1) * ((1 << q) - 1) < 1 << 24
+        k_pad = (K + 127) // 128 * 128
+        assert p <= 2 and q <= 4 and k_pad * ((1 << p) - 1) * ((1 << q) - 1) < 1 << 24
     if shape[0] <= 8:
         assert c.route == apt.APT_ROUTE_XOR
-    M, N, K = shape[:3]
+    M, N, K, p, q = shape
     ws = apt.apt_gemm_workspace_bytes(*shape, c)
     if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA):
-        assert ws == _int8_workspace(M, N, K, c)
+        assert ws == _int8_workspace(M, N, K, c, q)
     else:
         assert ws == 0
 
@@ -165,10 +167,14 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
     # the int8 weight ring is 3 deep
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 2)),
      apt.APT_ERR_INVALID_ARG),
-    # FP4 operands: at most 2 bits each, and fp32 sums below 2^24
+    # FP4 route: weights of at most 2 bits, activations of at most 4 bits (FP4 up to
+    # 2, FP8 up to 4), and fp32 sums below 2^24
     (dict(p=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_UNSUPPORTED),
-    (dict(q=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+    (dict(q=5, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(K=(1 << 24) // 45 + 1, p=2, q=4,
+          cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_UNSUPPORTED),
     (dict(K=(1 << 24) // 9 + 1, p=2, q=2,
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
@@ -179,6 +185,8 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_UNSUPPORTED),
     (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_WORKSPACE),
+    (dict(M=64, p=2, q=4, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_WORKSPACE),
     (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 96, 128, 128, 2, 2)),
      apt.APT_ERR_INVALID_ARG),
@@ -291,6 +299,7 @@ def test_config_table_starts_empty_and_clears():
 
 
 def test_fp4_workspace_is_half_the_int8_fragments():
+    """FP4 activations (q <= 2) take half a byte per element, FP8 ones (q = 3, 4) a byte."""
     i8 = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)
     f4 = apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)
     for M, K in [(64, 1000), (100, 4096), (2048, 4096)]:
@@ -299,4 +308,7 @@ def test_fp4_workspace_is_half_the_int8_fragments():
         nce = ((K + 127) // 128 + 1) // 2 * 2
         assert a == (M + 31) // 32 * 32 * nce * 128
         assert b == (M + 31) // 32 * 32 * nce * 64
+        for q in (3, 4):
+            assert apt.apt_gemm_workspace_bytes(M, 512, K, 2, q, f4) == a
     assert apt.apt_gemm_workspace_bytes(64, 512, 1000, 3, 2, f4) == 0  # p = 3: not runnable
+    assert apt.apt_gemm_workspace_bytes(64, 512, 1000, 2, 5, f4) == 0  # q = 5: not runnable

@@ -45,26 +45,29 @@ def test_ragged_shapes(M, N, K, p, q):
         assert_int32_equal(got, want, name)
 
 
-def test_fp4_exact_at_its_bound():
-    """The FP4 route sums in fp32 and takes W2A2 while K_pad * 9 < 2^24 (K_pad = K rounded up
-    to 128; the padding products are +9 too).  At the largest such K_pad with every product
-    +9, the running sum climbs to one step below 2^24; rows with mixed signs and a K whose
-    last chunk is padded go through the same configs."""
-    p = q = 2
-    k_pad = ((1 << 24) - 1) // 9 // 128 * 128
+@pytest.mark.parametrize("q", [2, 4])
+def test_fp4_exact_at_its_bound(q):
+    """The FP4 route sums in fp32 and takes W2Aq while K_pad (2^2-1)(2^q-1) < 2^24 (K_pad = K
+    rounded up to 128; the padding products count too).  At the largest such K_pad with every
+    product at its maximum (+9 with FP4 activations, +45 with FP8 ones), the running sum climbs
+    to one step below 2^24; rows with mixed signs and a K whose last chunk is padded go
+    through the same configs."""
+    p = 2
+    top = 3 * ((1 << q) - 1)
+    k_pad = ((1 << 24) - 1) // top // 128 * 128
     fp4 = [(n, c) for n, c in forced_configs(p, q, 10, k_pad) if c.route == apt.APT_ROUTE_FP4_MFMA]
     assert fp4
     for K in (k_pad, k_pad - 57):
-        g = synth.rng(2500, K)
+        g = synth.rng(2500, K, q)
         M, N = 3, 10
-        a = np.ones((M, K), np.int8)           # code 1: value +3
-        w = np.ones((N, K), np.int8)
-        w[1::2] = -2                           # code -2: value -3
+        a = np.full((M, K), (1 << (q - 1)) - 1, np.int8)  # largest code: value 2^q - 1
+        w = np.ones((N, K), np.int8)                     # code 1: value +3
+        w[1::2] = -2                                     # code -2: value -3
         a[2] = synth.uniform_codes(g, 1, K, q)[0]
         w[2] = synth.uniform_codes(g, 1, K, p)[0]
         prob = synth.Problem("fp4 bound", M, N, K, p, q, w, a)
         want = oracle_full(prob)
-        assert want[0, 0] == 9 * K and want[0, 1] == -9 * K
+        assert want[0, 0] == top * K and want[0, 1] == -top * K
         packed = pack_problem(prob)
         for name, cfg in fp4:
             got, _ = run(prob, cfg=cfg, packed=packed)

@@ -161,3 +161,45 @@ def test_fp32_sums_exact_below_2_24():
         assert float(np.sum(small, dtype=np.float32)) == float(small.astype(np.int64).sum())
     over = np.full((1 << 24) // 9 + 2, 9.0, np.float32)
     assert float(np.cumsum(over, dtype=np.float32)[-1]) != 9.0 * over.size
+
+
+# ---- FP8 (E4M3) activations of the FP4 route (q = 3, 4) -------------------------
+
+def e4m3_value(byte: int) -> float:
+    """OCP E4M3 decoding: sign bit 7, exponent bits 6..3 (bias 7), mantissa
+    bits 2..0; exponent 0 is subnormal (2^-6 * mantissa / 8); 0x7F and 0xFF
+    are NaN."""
+    if byte & 0x7F == 0x7F:
+        return float("nan")
+    s = -1.0 if byte & 0x80 else 1.0
+    e = (byte >> 3) & 15
+    m = byte & 7
+    return s * (2.0 ** -6 * m / 8 if e == 0 else 2.0 ** (e - 7) * (1.0 + m / 8))
+
+
+def test_e4m3_codes_of_bipolar_values():
+    """Every bipolar value of up to 4 bits (odd, |v| <= 15) is exact in E4M3,
+    with exponent field 7 + floor(log2 |v|) and the next three bits of |v| as
+    mantissa (the bytes the FP4 route's activation expansion writes); 17, the
+    first odd value past 4 bits, is not an E4M3 value."""
+    table = {e4m3_value(b): b for b in range(256) if e4m3_value(b) == e4m3_value(b)}
+    for q in range(1, 5):
+        for u in range(1 << q):
+            v = int(ref.decode(np.array([u], np.uint8), q)[0])
+            assert v == 2 * u - ((1 << q) - 1)
+            a = abs(v)
+            e = a.bit_length() - 1
+            byte = ((e + 7) << 3) | (((a << 3) >> e) & 7) | (0x80 if v < 0 else 0)
+            assert e4m3_value(byte) == v
+            assert table[float(v)] == byte
+    assert 17.0 not in table
+
+
+def test_fp32_sums_exact_with_fp8_activations():
+    """W2A4 through the FP4 route: products up to 3 * 15 = 45; with
+    K_pad * 45 < 2^24 every fp32 partial sum is an exact integer."""
+    k_pad = ((1 << 24) - 1) // 45 // 128 * 128
+    prod = np.full(k_pad, 45.0, np.float32)
+    assert float(np.cumsum(prod, dtype=np.float32)[-1]) == 45.0 * k_pad
+    over = np.full((1 << 24) // 45 + 2, 45.0, np.float32)
+    assert float(np.cumsum(over, dtype=np.float32)[-1]) != 45.0 * over.size
