@@ -188,16 +188,17 @@ def route_table(calls: int = 20):
               ("reassembled int8 MFMA 128x128 g512", C(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 512, 3)),
               ("reassembled FP4 MFMA 128x128 g512", C(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2, 512, 3))]
     out = {}
-    # the step's GEMMs, and the W1A1 down projection, where the FP4 form applies
+    # the step's GEMMs, the W1A1 down projection (FP4 route with FP4 activations) and the
+    # W2A4 down projection at 1024 tokens (FP4 route with FP8 activations)
     for prob in [synth.w4a4_prefill(), synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP),
-                 synth.sweep_down(0)]:
+                 synth.sweep_down(0), synth.layer_w2a4("down", 1024)]:
         a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
         w = apt.pack(dev(prob.w_codes), prob.p)
         row = {}
         for name, cfg in routes:
             if cfg is not None and cfg.route == apt.APT_ROUTE_PM1_MFMA and max(prob.p, prob.q) > 7:
                 continue
-            if cfg is not None and cfg.route == apt.APT_ROUTE_FP4_MFMA and max(prob.p, prob.q) > 2:
+            if cfg is not None and cfg.route == apt.APT_ROUTE_FP4_MFMA and (prob.p > 2 or prob.q > 4):
                 continue
             c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
             wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)

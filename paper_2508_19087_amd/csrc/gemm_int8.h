@@ -592,23 +592,26 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   // chunks before the tile's flush and written to LDS before that pair's
   // last barrier (the loads are issued before any output store, so waiting
   // for them never waits for stores).
+  // The loaded words are kept as they arrive and combined only when they are
+  // staged, a chunk later: arithmetic right after the loads would make the
+  // wave wait for every load in flight (the loads complete in order).
   constexpr int kTermsPerThread = (BN + BM + T - 1) / T;
-  uint32_t term[kTermsPerThread];
-  float scale[kTermsPerThread];
+  uint32_t rowsum[kTermsPerThread];
+  uint16_t scale_bits[kTermsPerThread];
   auto fetch_terms = [&](int m0, int n0) __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < kTermsPerThread; ++k) {
       const int i = tid + k * T;
-      term[k] = 0;
-      scale[k] = 0.f;
+      rowsum[k] = 0;
+      scale_bits[k] = 0;
       if (i < BN) {
         const int n = min(n0 + i, g.N - 1);
-        term[k] = ca * (uint32_t)g.w_rowsum[n];
-        if (fp16) scale[k] = __half2float(g.w_scale[n]);
+        rowsum[k] = (uint32_t)g.w_rowsum[n];
+        if (fp16) scale_bits[k] = __half_as_ushort(g.w_scale[n]);
       } else if (i < BN + BM) {
         const int m = min(m0 + i - BN, g.M - 1);
-        term[k] = cw * (uint32_t)g.a_rowsum[m] - const_term;
-        if (fp16) scale[k] = __half2float(g.a_scale[m]);
+        rowsum[k] = (uint32_t)g.a_rowsum[m];
+        if (fp16) scale_bits[k] = __half_as_ushort(g.a_scale[m]);
       }
     }
   };
@@ -620,8 +623,9 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     for (int k = 0; k < kTermsPerThread; ++k) {
       const int i = tid + k * T;
       if (i < BN + BM) {
-        lds_wt[i] = term[k];  // lds_at follows lds_wt
-        lds_ws[i] = scale[k];
+        // c_a R_w[n] per column, c_w R_a[m] - const per row; lds_at follows lds_wt
+        lds_wt[i] = i < BN ? ca * rowsum[k] : cw * rowsum[k] - const_term;
+        lds_ws[i] = __half2float(__ushort_as_half(scale_bits[k]));
       }
     }
     if (affine) {
@@ -824,18 +828,21 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
 
   // Prologue: pair cp into stages 0 and 1, the first chunk of c1 in
   // registers, activation fragments and the first weight fragments of the
-  // first chunk.
+  // first chunk.  The loads leave in the loop's own order (weight words of
+  // the next chunk, then activation fragments), so that the wait counts the
+  // compiler derives at the loop head, which cover both ways in, only wait
+  // for the loads each k-step needs.
   rw0.load(w_rsrc, wv0, NC, 2 * cp.pair);
   rw1.load(w_rsrc, wv0, NC, 2 * cp.pair + 1);
+  rw0.store(lds, tid);
+  rw1.store(lds + kStageBytes, tid);
+  rw0.load(w_rsrc, wv1, NC, 2 * c1.pair);
 #pragma unroll
   for (int ks = 0; ks < kSteps; ++ks)
 #pragma unroll
     for (int a = 0; a < FM; ++a)
 #pragma unroll
       for (int x = 0; x < kAVecs; ++x) afr[ks * kAVecs + x][a] = load_a(cp.m0, 2 * cp.pair, ks, a, x);
-  rw0.store(lds, tid);
-  rw1.store(lds + kStageBytes, tid);
-  rw0.load(w_rsrc, wv1, NC, 2 * c1.pair);
   __syncthreads();
   read_wf(lds, 0, wf[0]);
 
