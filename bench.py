@@ -528,7 +528,7 @@ def main():
         write_traffic(args.write_traffic[0], args.write_traffic[1], args.traffic_commands)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(no sharding or collectives); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
