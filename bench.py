@@ -381,6 +381,143 @@ def decode_cold(wl, reps: int = 4):
     return out
 
 
+def decode_layer_cold(wl, reps: int = 4):
+    """One token through the linears of the W2A4 7B-class decoder layer with
+    cold weights: q/k/v fused along N (one packed [3*4096][4096] matrix against
+    their shared input), o, gate/up fused (N = 2*11008) and down, four apt_gemm
+    launches with fp16 output per layer.  Enough layer copies (> 2x the
+    Infinity Cache) are rotated in one HIP graph that every launch reads HBM;
+    every replay's outputs are checked against the eager result."""
+    torch, apt, np = wl.torch, wl.apt, wl.np
+    import synth
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+    groups = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+    gemms = []
+    bytes_alg = 0.0
+    ops = 0
+    for parts in groups:
+        probs = [synth.layer_w2a4(name, 1) for name in parts]
+        p0 = probs[0]
+        w_codes = np.concatenate([pr.w_codes for pr in probs], 0)
+        N, K, M = w_codes.shape[0], p0.K, 1
+        g = {"N": N, "K": K, "p": p0.p, "q": p0.q}
+        g["w"] = apt.pack(dev(w_codes), p0.p)
+        g["a"] = apt.pack(dev(p0.a_codes), p0.q, activations=True)
+        g["sa"] = dev(p0.a_scale)
+        g["sw"] = dev(np.concatenate([pr.w_scale for pr in probs]))
+        g["c16"] = torch.empty((M, N), dtype=torch.float16, device="cuda")
+        wsb = apt.apt_gemm_workspace_bytes(M, N, K, p0.p, p0.q, None)
+        g["ws"], g["ws_bytes"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda"), wsb
+        gemms.append(g)
+        bytes_alg += (N * K * p0.p + M * K * p0.q) / 8 + M * N * 2 + 2 * (M + N)
+        ops += 2 * M * N * K
+    layer_bytes = sum(g["w"].data.numel() for g in gemms)
+    copies = max(8, int(2 * MALL_BYTES // layer_bytes) + 1)
+    wcopies = [[apt.Packed(g["w"].data.clone(), g["w"].rowsum.clone(), g["N"], g["K"], g["p"])
+                for g in gemms] for _ in range(copies)]
+
+    def run(ws_list, sp):
+        for g, w in zip(gemms, ws_list):
+            st = apt.apt_gemm(1, g["N"], g["K"], g["p"], g["q"], g["a"].data.data_ptr(),
+                              w.data.data_ptr(), g["a"].rowsum.data_ptr(), w.rowsum.data_ptr(), None,
+                              g["sa"].data_ptr(), g["sw"].data_ptr(), g["c16"].data_ptr(), None,
+                              g["ws"].data_ptr(), g["ws_bytes"], sp)
+            apt.check(st, "apt_gemm")
+    run([g["w"] for g in gemms], wl.sp)
+    torch.cuda.synchronize()
+    refs = [g["c16"].clone() for g in gemms]
+
+    def launch(sp):
+        for ws_list in wcopies:
+            run(ws_list, sp)
+    graph = graph_of(torch, launch)
+    times = []
+    for r in range(reps):
+        for g in gemms:
+            g["c16"].zero_()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        assert all(torch.equal(g["c16"], ref) for g, ref in zip(gemms, refs)), "layer graph replay"
+        if r > 0:
+            times.append(e0.elapsed_time(e1) / copies)
+    t = sorted(times)[len(times) // 2] * 1e-3
+    return {"us_per_layer": round(t * 1e6, 3), "launches_per_layer": len(gemms),
+            "algorithmic_bytes": int(bytes_alg), "achieved_GBs": round(bytes_alg / t / 1e9, 1),
+            "peak_GBs": PEAK_HBM_GBS, "frac": round(bytes_alg / t / 1e9 / PEAK_HBM_GBS, 4),
+            "layer_copies": copies, "effective_TOPS": round(ops / t / 1e12, 4),
+            "method": "HIP graph of %d layers (q/k/v fused, o, gate/up fused, down), one per cold "
+                      "copy of the layer's weights; fp16 output" % copies}
+
+
+def decode_sweep(reps: int = 4):
+    """Cold-weight time of one M=1 W2A4 GEMM (K = 4096, int32 output) against
+    N, each as one HIP graph over enough weight copies (> 2x the Infinity
+    Cache) that every launch reads HBM: the per-launch fixed cost and the
+    streaming rate of the decode route."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    g = np.random.default_rng(1)
+    K, p, q = 4096, 2, 4
+    rows = []
+    for N in (4096, 12288, 22016, 44032, 88064):
+        wc = torch.from_numpy(g.integers(-2, 2, (N, K), dtype=np.int8)).cuda()
+        ac = torch.from_numpy(g.integers(-8, 8, (1, K), dtype=np.int8)).cuda()
+        w = apt.pack(wc, p)
+        a = apt.pack(ac, q, activations=True)
+        nb = w.data.numel()
+        copies = max(8, int(2 * MALL_BYTES // nb) + 1)
+        ws = [apt.Packed(w.data.clone(), w.rowsum.clone(), N, K, p) for _ in range(copies)]
+        c32 = torch.empty((1, N), dtype=torch.int32, device="cuda")
+
+        def launch(sp, ws=ws, a=a, c32=c32, N=N):
+            for wi in ws:
+                apt.check(apt.apt_gemm(1, N, K, p, q, a.data.data_ptr(), wi.data.data_ptr(),
+                                       a.rowsum.data_ptr(), wi.rowsum.data_ptr(), c32.data_ptr(),
+                                       None, None, None, None, None, 0, sp), "apt_gemm")
+        gr = graph_of(torch, launch)
+        ts = []
+        for r in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            gr.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            if r > 0:
+                ts.append(e0.elapsed_time(e1) * 1e3 / copies)
+        t = sorted(ts)[len(ts) // 2]
+        bytes_alg = (N * K * p + K * q) / 8 + 4 * N
+        rows.append({"N": N, "K": K, "weight_bytes": nb, "copies": copies, "us": round(t, 3),
+                     "GB/s": round(bytes_alg / t / 1e3, 1),
+                     "frac_hbm": round(bytes_alg / t / 1e3 / PEAK_HBM_GBS, 4)})
+        log("bench: decode sweep N=%d %.2f us" % (N, t))
+        del ws, gr
+    # the launch floor in the same setting: a graph of one-element kernels
+    one = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def tiny(sp):
+        for _ in range(200):
+            one.add_(1)
+    gt = graph_of(torch, tiny)
+    ts = []
+    for r in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        gt.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if r > 0:
+            ts.append(e0.elapsed_time(e1) * 1e3 / 200)
+    rows.append({"launch_floor_us": round(sorted(ts)[len(ts) // 2], 3),
+                 "method": "HIP graph of 200 one-element kernels (torch add_), us per kernel"})
+    return rows
+
+
 def stored_traffic():
     """HBM traffic of the prefill GEMM from the committed rocprofv3 counter
     summary, if it was taken on the current kernel sources."""
@@ -521,6 +658,8 @@ def main():
     ap.add_argument("--search", action="store_true",
                     help="print the model's and the search module's config for every workload "
                          "shape, with their times, and exit")
+    ap.add_argument("--decode-sweep", action="store_true",
+                    help="print the cold-weight time of one M=1 W2A4 GEMM against N and exit")
     ap.add_argument("--traffic-commands", default="",
                     help="the commands that produced the --write-traffic directories")
     args = ap.parse_args()
@@ -543,6 +682,9 @@ def main():
         return
     if args.search:
         print(json.dumps(search_table(), indent=1), flush=True)
+        return
+    if args.decode_sweep:
+        print(json.dumps(decode_sweep(), indent=1), flush=True)
         return
     log("bench: building workload")
     wl = Workload()
@@ -592,6 +734,8 @@ def main():
     if not args.no_decode_cold:
         log("bench: decode GEMMs with cold weights")
         result["decode_cold"] = decode_cold(wl)
+        log("bench: one-token W2A4 decoder layer with cold weights")
+        result["decode_cold"]["w2a4_layer_m1"] = decode_layer_cold(wl)
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
