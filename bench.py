@@ -21,6 +21,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -575,7 +576,41 @@ def cpu_baseline(target_s: float = 12.0):
             "kind": "oracle", "seconds": round(t, 2),
             "sample": ("both M=1 W2A2 decode GEMMs in full (with fp16 epilogue) + rows 0..%d of the "
                        "2048x11008x4096 W4A4 GEMM, bipolar conversion and decoding included; "
-                       "%.3g effective ops" % (rows - 1, ops))}
+                       "%.3g effective ops" % (rows - 1, ops)),
+            "one_core": oracle_one_core()}
+
+
+ONE_CORE_SCRIPT = """
+import json, sys, time
+sys.path.insert(0, sys.argv[1])
+import synth
+from oracle import oracle as ref
+out = {"threads": ref.num_threads()}
+for name, probs in (("w1a2_16x512x512", [synth.w1a2_small()]),
+                    ("w2a2_decode_m1_both", [synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)])):
+    ts = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        for p in probs:
+            C = ref.gemm(p.a_codes, p.w_codes, p.p, p.q)
+            if p.a_scale is not None:
+                ref.epilogue(C, p.a_scale, p.w_scale)
+        ts.append(time.perf_counter() - t0)
+    out[name] = {"seconds": round(sorted(ts)[1], 4), "ops": sum(p.ops for p in probs)}
+print(json.dumps(out))
+"""
+
+
+def oracle_one_core():
+    """The oracle on one core (OpenMP limited to one thread in a child process)
+    for the small W1A2 GEMM and the two M=1 decode GEMMs: median of 3 runs,
+    conversion and decoding included."""
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", ONE_CORE_SCRIPT, ROOT], capture_output=True,
+                       text=True, env=env, timeout=600)
+    if r.returncode != 0:
+        return {"error": r.stderr[-400:]}
+    return json.loads(r.stdout.strip().splitlines()[-1])
 
 
 COPY_BYTES = 256 << 20  # calibration copy for the HBM byte counters
