@@ -59,7 +59,7 @@ constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes
 //   F = 2: FP4 weights (at most 2 bits) with FP8 (E4M3) activation bytes (at
 //          most 4 bits: every odd value up to 15 is exact in E4M3), the same
 //          MFMA with a mixed operand format, 64 elements of k per MFMA at
-//          about 1.15x the int8 multiply-add rate.
+//          about 1.15x the int8 multiply-add rate (register-only loop).
 // With F > 0 the fp32 sums are exact integers while K_pad (2^p - 1)(2^q - 1)
 // < 2^24, K_pad = K rounded up to a chunk (the host checks).
 // Per chunk, k-step ks of lane half h holds (F = 0) half h of word ks's bytes,
@@ -574,7 +574,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
 
   // ---- epilogue constants
   // F = 0: C = 4 D + c_w R_a + c_a R_w - c_a c_w K - pad_term (kernel header).
-  // F = 1: the operands are the bipolar values themselves, so C = D less the
+  // F > 0: the operands are the bipolar values themselves, so C = D less the
   // padding elements inside the last real chunk: their all-zero planes stand
   // for -(2^p - 1) and -(2^q - 1), whose products add (K_pad - K)(2^p-1)(2^q-1).
   const int q = g.q;
