@@ -519,6 +519,65 @@ def decode_sweep(reps: int = 4):
     return rows
 
 
+def epilogue_table(calls: int = 50):
+    """Cost of the zero-point epilogue: per call, the fp16 scale epilogue
+    (apt_gemm) against the zero-point epilogue (apt_gemm_affine) on the same
+    operands and selected config, fp16 output only; HIP events around `calls`
+    back-to-back calls after 3 warm-up calls, median of 3."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    import synth
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+    probs = [synth.layer_w2a4_affine("gate", 1), synth.layer_w2a4_affine("gate", 1024),
+             synth.affine_problem("w4a4_affine_2048x11008x4096", 2048, synth.MLP, synth.HIDDEN, 4, 4,
+                                  synth.rng(7))]
+    rows = []
+    for prob in probs:
+        M, N, K, p, q = prob.M, prob.N, prob.K, prob.p, prob.q
+        a = apt.pack(dev(prob.a_codes), q, activations=True)
+        w = apt.pack(dev(prob.w_codes), p)
+        sa, sw, za, zw = dev(prob.a_scale), dev(prob.w_scale), dev(prob.a_zero), dev(prob.w_zero)
+        c16 = torch.empty((M, N), dtype=torch.float16, device="cuda")
+        wsb = apt.apt_gemm_workspace_bytes(M, N, K, p, q, None)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        sp = torch.cuda.current_stream().cuda_stream
+
+        def plain():
+            apt.check(apt.apt_gemm(M, N, K, p, q, a.data.data_ptr(), w.data.data_ptr(),
+                                   a.rowsum.data_ptr(), w.rowsum.data_ptr(), None, sa.data_ptr(),
+                                   sw.data_ptr(), c16.data_ptr(), None, ws.data_ptr(), wsb, sp),
+                      "apt_gemm")
+
+        def affine():
+            apt.check(apt.apt_gemm_affine(M, N, K, p, q, a.data.data_ptr(), w.data.data_ptr(),
+                                          a.rowsum.data_ptr(), w.rowsum.data_ptr(), sa.data_ptr(),
+                                          za.data_ptr(), sw.data_ptr(), zw.data_ptr(),
+                                          c16.data_ptr(), None, None, ws.data_ptr(), wsb, sp),
+                      "apt_gemm_affine")
+        res = {}
+        for name, fn in (("scale_us", plain), ("zero_point_us", affine)):
+            ts = []
+            for _ in range(3):
+                for _ in range(3):
+                    fn()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record()
+                for _ in range(calls):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3 / calls)
+            res[name] = round(sorted(ts)[1], 2)
+        cfg = apt.select_config(M, N, K, p, q)
+        rows.append({"problem": prob.name, "route": apt.ROUTE_NAMES[cfg.route], **res,
+                     "extra": round(res["zero_point_us"] / res["scale_us"] - 1, 3)})
+        log("bench: epilogues %s %s" % (prob.name, res))
+    return rows
+
+
 def stored_traffic():
     """HBM traffic of the prefill GEMM from the committed rocprofv3 counter
     summary, if it was taken on the current kernel sources."""
@@ -693,6 +752,8 @@ def main():
     ap.add_argument("--search", action="store_true",
                     help="print the model's and the search module's config for every workload "
                          "shape, with their times, and exit")
+    ap.add_argument("--epilogues", action="store_true",
+                    help="print the cost of the zero-point epilogue against the scale epilogue and exit")
     ap.add_argument("--decode-sweep", action="store_true",
                     help="print the cold-weight time of one M=1 W2A4 GEMM against N and exit")
     ap.add_argument("--traffic-commands", default="",
@@ -720,6 +781,9 @@ def main():
         return
     if args.decode_sweep:
         print(json.dumps(decode_sweep(), indent=1), flush=True)
+        return
+    if args.epilogues:
+        print(json.dumps(epilogue_table(), indent=1), flush=True)
         return
     log("bench: building workload")
     wl = Workload()
