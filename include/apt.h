@@ -167,11 +167,13 @@ apt_status_t apt_quantize_pack_activations_fp16(const uint16_t* a_fp16, int M, i
 
 /* Host-only.  Chooses the route and tile shape for (M, N, K, p, q) (Sec. V-B:
  * lookup table, approximate matching): the config apt_search_config recorded
- * for exactly this problem, if any; otherwise a model of the MI355X kernels
- * (rounds of resident tiles per compute unit, measured cycles per chunk pair
- * of each tile shape, stream-K partial traffic; the FP4 route only with FP4
- * activations, q <= 2), which stands in for the approximate match.  The
- * choice never changes results.
+ * for exactly this problem, if any; otherwise the XOR route for M <= 8, and
+ * above that a model of the MI355X kernels (rounds of resident tiles per
+ * compute unit, measured cycles per chunk pair of each tile shape, stream-K
+ * partial traffic; the FP4 route only with FP4 activations, q <= 2; the XOR
+ * route when its cost per word pair and p*q beats them on small problems),
+ * which stands in for the approximate match.  The choice never changes
+ * results.
  * Errors: APT_ERR_INVALID_ARG for sizes < 1, bits outside [1, 8] or out == NULL. */
 apt_status_t apt_select_config(int M, int N, int K, int p, int q, apt_config_t* out);
 

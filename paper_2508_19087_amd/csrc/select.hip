@@ -17,6 +17,7 @@
 #include <algorithm>
 #include <array>
 #include <map>
+#include <cmath>
 #include <mutex>
 
 #include "apt_internal.h"
@@ -125,6 +126,18 @@ double model_us(const Int8Shape& s, int f, int M, int N, int K, int grid, int cu
 // The tail shape a split config with main shape i and tail size of shape t
 // runs: of the shapes of that size, the one with the main shape's wave count
 // (the library's rule), else t itself.
+// Modelled microseconds of the XOR route with 8 activation rows per
+// workgroup: a fixed part and a cost per 32-bit word pair of one activation
+// row and one weight row, rising with the p*q plane products per pair; when K
+// has fewer chunks than a workgroup's 32 chunk slots, part of every workgroup
+// idles (factor 1/sqrt(used share)).  Fitted to MI355X timings for M = 16 to
+// 256, N and K from 1024 to 14336 and p*q from 2 to 16.
+double model_xor_us(int M, int N, int K, int p, int q) {
+  const double used = std::min(1.0, (double)num_chunks(K) / 32.0);
+  const double words = (double)M * N * K / 32.0 / std::sqrt(used);
+  return 3.16 + words * (0.134 + 0.0624 * p * q) * 1e-6;
+}
+
 bool tail_runs_as(int i, int t) {
   const Int8Shape &m = kInt8Shapes[i], &ts = kInt8Shapes[t];
   for (int u = 0; u < kNumInt8Shapes; ++u) {
@@ -289,6 +302,15 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
                  i, 0, split, t);
       }
     }
+  }
+  // small problems: the XOR route's single launch against the MFMA routes'
+  // fixed costs.  The MFMA figures were measured with every compute unit
+  // busy and overstate grids of a few tiles by 10-40%, so they count at 90%
+  // here (measured over M = 16..256, N, K = 1024..14336, p*q = 2..16).
+  if (model_xor_us(M, N, K, p, q) < 0.9 * best) {
+    apt_config_t c = base_config(APT_ROUTE_XOR);
+    c.mt = 8;
+    return c;
   }
   const Int8Shape& s = kInt8Shapes[best_i];
   apt_config_t c = base_config(best_fp4 ? APT_ROUTE_FP4_MFMA : APT_ROUTE_INT8_MFMA);
