@@ -642,6 +642,71 @@ def paper_shapes(calls: int = 100, reps: int = 3):
     return rows
 
 
+def xor_crossover(calls: int = 50):
+    """Where the XOR route beats the MFMA routes: for M = 16..256 and a few
+    (N, K, p, q), the forced XOR route (8 activation rows per workgroup) and
+    the best of the 128x128 MFMA configs the model takes at such sizes (int8,
+    and FP4 where it applies; one workgroup per tile and 512 workgroups), each
+    as one HIP graph of `calls` calls (warm, int32 output), plus the selected
+    config; then the least-squares fit of the XOR model the selector uses."""
+    import math
+
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    C = apt.apt_config_t.make
+    g = np.random.default_rng(5)
+
+    def timed(M, N, K, p, q, cfg, a, w, c32):
+        wsb = apt.apt_gemm_workspace_bytes(M, N, K, p, q, cfg)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+
+        def launch(sp):
+            for _ in range(calls):
+                apt.check(apt.apt_gemm(M, N, K, p, q, a.data.data_ptr(), w.data.data_ptr(),
+                                       a.rowsum.data_ptr(), w.rowsum.data_ptr(), c32.data_ptr(), None,
+                                       None, None, cfg, ws.data_ptr(), wsb, sp), "apt_gemm")
+        gr = graph_of(torch, launch)
+        ts = []
+        for r in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            gr.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            if r > 0:
+                ts.append(e0.elapsed_time(e1) * 1e3 / calls)
+        return sorted(ts)[1]
+    rows = []
+    for N, K in [(1024, 1024), (4096, 4096), (14336, 4096), (4096, 14336)]:
+        for p, q in [(1, 2), (2, 2), (3, 4), (4, 4), (2, 8)]:
+            for M in (16, 32, 64, 128, 256):
+                ac = torch.from_numpy(g.integers(-(1 << (q - 1)), 1 << (q - 1), (M, K), dtype=np.int8)).cuda()
+                wc = torch.from_numpy(g.integers(-(1 << (p - 1)), 1 << (p - 1), (N, K), dtype=np.int8)).cuda()
+                a = apt.pack(ac, q, activations=True)
+                w = apt.pack(wc, p)
+                c32 = torch.empty((M, N), dtype=torch.int32, device="cuda")
+                routes = [apt.APT_ROUTE_INT8_MFMA] + ([apt.APT_ROUTE_FP4_MFMA] if p <= 2 and q <= 2 else [])
+                mfma = min(timed(M, N, K, p, q, C(r, 128, 128, 128, 2, 2, grid, 3), a, w, c32)
+                           for r in routes for grid in (0, 512))
+                xor = timed(M, N, K, p, q, C(apt.APT_ROUTE_XOR, mt=8), a, w, c32)
+                sel = apt.select_config(M, N, K, p, q)
+                selected = timed(M, N, K, p, q, sel, a, w, c32)
+                rows.append({"M": M, "N": N, "K": K, "p": p, "q": q, "xor_us": round(xor, 2),
+                             "mfma_128x128_us": round(mfma, 2), "selected": apt.ROUTE_NAMES[sel.route],
+                             "selected_us": round(selected, 2)})
+            log("bench: xor crossover N=%d K=%d W%dA%d done" % (N, K, p, q))
+    # the selector's XOR model: t = t0 + (M N K / 32) / sqrt(u) (a + b p q), u = min(1, chunks / 32)
+    words = np.array([r["M"] * r["N"] * r["K"] / 32 / math.sqrt(min(1.0, math.ceil(r["K"] / 128) / 32))
+                      for r in rows])
+    pq = np.array([r["p"] * r["q"] for r in rows], dtype=float)
+    t = np.array([r["xor_us"] for r in rows])
+    coef = np.linalg.lstsq(np.vstack([np.ones_like(words), words, words * pq]).T, t, rcond=None)[0]
+    return {"rows": rows, "xor_fit": {"t0_us": round(coef[0], 3), "a_ps_per_word": round(coef[1] * 1e6, 4),
+                                      "b_ps_per_word_per_pq": round(coef[2] * 1e6, 4)}}
+
+
 def stored_traffic():
     """HBM traffic of the prefill GEMM from the committed rocprofv3 counter
     summary, if it was taken on the current kernel sources."""
@@ -816,6 +881,8 @@ def main():
     ap.add_argument("--search", action="store_true",
                     help="print the model's and the search module's config for every workload "
                          "shape, with their times, and exit")
+    ap.add_argument("--xor-crossover", action="store_true",
+                    help="print the XOR route against the MFMA routes for small M, with the XOR model fit, and exit")
     ap.add_argument("--paper-shapes", action="store_true",
                     help="print this library's times at the shapes of the paper's kernel tables and exit")
     ap.add_argument("--epilogues", action="store_true",
@@ -853,6 +920,9 @@ def main():
         return
     if args.paper_shapes:
         print(json.dumps(paper_shapes(), indent=1), flush=True)
+        return
+    if args.xor_crossover:
+        print(json.dumps(xor_crossover(), indent=1), flush=True)
         return
     log("bench: building workload")
     wl = Workload()
