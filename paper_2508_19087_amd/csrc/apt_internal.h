@@ -97,7 +97,7 @@ void table_store(int M, int N, int K, int p, int q, const apt_config_t& c);
 void table_clear();
 int table_size();
 // Configs the search module times for a problem (at most max_out of them).
-constexpr int kMaxCandidates = 32;
+constexpr int kMaxCandidates = 64;  // bound checked in select.hip
 int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int max_out);
 
 }  // namespace apt

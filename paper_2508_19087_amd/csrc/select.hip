@@ -198,6 +198,12 @@ int table_size() {
 // workgroups, and the split launches the model considers (a main shape over
 // whole rounds of columns, a smaller shape on the rest); each of these again
 // on the FP4 route where it applies (FP4 or FP8 activations).
+// The most configs candidate_configs can list: XOR, +-1 planes, then for each
+// operand format every shape twice and every main shape with every tail.
+static_assert(2 + 2 * (2 * kNumInt8Shapes + kNumMainShapes * (kNumInt8Shapes - kFirstTail)) <=
+                  kMaxCandidates,
+              "the search module's candidate list must hold every config");
+
 int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int max_out) {
   int n = 0;
   auto add = [&](const apt_config_t& c) {
