@@ -53,6 +53,7 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
     case APT_ROUTE_PM1_MFMA:
       if (p > 7 || q > 7) return APT_ERR_UNSUPPORTED;
       if (!apt::pm1_config_ok(c, p, q)) return APT_ERR_INVALID_ARG;
+      if (!apt::pm1_sizes_ok(M, N)) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     default:
       return APT_ERR_INVALID_ARG;

@@ -88,6 +88,7 @@ size_t int8_workspace_bytes(int M, int N, int K, int q, const apt_config_t& cfg)
 // Plane-pair +-1 MFMA route (gemm_pm1.hip).
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
 bool pm1_config_ok(const apt_config_t& cfg, int p, int q);
+bool pm1_sizes_ok(int M, int N);
 
 // Host-side selector (select.hip): the search module's table first, then the
 // model.

@@ -206,6 +206,11 @@ bool pm1_config_ok(const apt_config_t& cfg, int p, int q) {
   return p <= 7 && q <= 7 && (cfg.bm == 0 || cfg.bm == kBM) && (cfg.bn == 0 || cfg.bn == kBN);
 }
 
+// The launch's one-dimensional grid holds one workgroup per tile.
+bool pm1_sizes_ok(int M, int N) {
+  return (int64_t)((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN) < ((int64_t)1 << 31);
+}
+
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t&, hipStream_t stream) {
   Pm1Params prm;
   prm.g = g;

@@ -194,6 +194,9 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
     (dict(M=64, N=1 << 20, K=1 << 16, p=1, q=1,
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_UNSUPPORTED),
+    # the +-1 plane route's grid holds one workgroup per tile
+    (dict(M=1 << 24, N=1 << 24, K=128, p=1, q=1, cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)),
+     apt.APT_ERR_UNSUPPORTED),
     # tile counts past 2^31 do not fit the plans' 32-bit counts (operands within 4 GiB)
     (dict(M=1 << 24, N=1 << 24, K=128, p=1, q=1,
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
