@@ -41,14 +41,19 @@ __global__ __launch_bounds__(kWave* kWaves) void gemm_xor_kernel(XorParams prm) 
   const int n0 = blockIdx.x * kRowGroup;
 
   // The activation rows m0 .. m0+7 are one row group: NC * Q * 8 uint4,
-  // ordered (chunk, plane, row).
-  const uint4* a_src = reinterpret_cast<const uint4*>(g.a_packed) + (int64_t)(m0 / kRowGroup) * NC * Q * kRowGroup;
+  // ordered (chunk, plane, row).  In LDS each chunk's Q * 8 vectors are
+  // followed by one pad vector: the 8 chunks a wave reads at once then start
+  // 32 Q + 4 dwords apart and fall in different banks (without the pad, every
+  // even Q puts them in the same ones).
+  constexpr int kChunkVecs = Q * kRowGroup;
+  const uint4* a_src = reinterpret_cast<const uint4*>(g.a_packed) + (int64_t)(m0 / kRowGroup) * NC * kChunkVecs;
   if (kALds) {
-    const int n_vec = NC * Q * kRowGroup;
-    for (int t = threadIdx.x; t < n_vec; t += blockDim.x) a_lds[t] = a_src[t];
+    const int n_vec = NC * kChunkVecs;
+    for (int t = threadIdx.x; t < n_vec; t += blockDim.x) a_lds[t + t / kChunkVecs] = a_src[t];
     __syncthreads();
   }
   const uint4* a_base = kALds ? a_lds : a_src;
+  const int a_chunk_stride = kALds ? kChunkVecs + 1 : kChunkVecs;
 
   const int lane = threadIdx.x % kWave;
   const int wave = threadIdx.x / kWave;
@@ -69,7 +74,7 @@ __global__ __launch_bounds__(kWave* kWaves) void gemm_xor_kernel(XorParams prm) 
         uint32_t s = 0u;
 #pragma unroll
         for (int j = 0; j < Q; ++j) {
-          const uint4 av = a_base[(c * Q + j) * kRowGroup + m];
+          const uint4 av = a_base[c * a_chunk_stride + j * kRowGroup + m];
 #pragma unroll
           for (int i = 0; i < P; ++i) {
             uint32_t cnt = __builtin_popcount(wv[i].x ^ av.x);

@@ -15,7 +15,8 @@ hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t&, hipStream_t s
   prm.nchunks = num_chunks(g.K);
   const int grid_x = padded_rows(g.N) / kRowGroup;
   const int grid_y = (g.M + kMT - 1) / kMT;
-  size_t lds = (size_t)prm.nchunks * g.q * kRowGroup * 16;
+  // staged activations: Q * 8 vectors of 16 bytes per chunk plus one pad vector
+  size_t lds = (size_t)prm.nchunks * (g.q * kRowGroup + 1) * 16;
   // Read the activation chunks from global memory instead of staging them
   // when they do not fit, or when only one activation row is real: staging
   // would copy 8 rows and put a barrier between the two memory latencies.

@@ -135,7 +135,7 @@ double model_us(const Int8Shape& s, int f, int M, int N, int K, int grid, int cu
 double model_xor_us(int M, int N, int K, int p, int q) {
   const double used = std::min(1.0, (double)num_chunks(K) / 32.0);
   const double words = (double)M * N * K / 32.0 / std::sqrt(used);
-  return 3.16 + words * (0.134 + 0.0624 * p * q) * 1e-6;
+  return 3.29 + words * (0.0508 + 0.0672 * p * q) * 1e-6;
 }
 
 bool tail_runs_as(int i, int t) {
