@@ -831,6 +831,30 @@ def counters_run(reps: int = 3):
     log("bench: counters run done (%d prefill GEMMs, copy of %d bytes)" % (reps + 1, COPY_BYTES))
 
 
+def counters_xor(M: int, N: int, K: int, p: int, q: int, reps: int = 3):
+    """For rocprofv3 --pmc on the XOR + popcount route: one M x N x K WpAq
+    problem on seeded random codes, forced onto the XOR route (8 activation
+    rows per workgroup), `reps` times after one warm-up call."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    g = np.random.default_rng(5)
+    ac = torch.from_numpy(g.integers(-(1 << (q - 1)), 1 << (q - 1), (M, K), dtype=np.int8)).cuda()
+    wc = torch.from_numpy(g.integers(-(1 << (p - 1)), 1 << (p - 1), (N, K), dtype=np.int8)).cuda()
+    a = apt.pack(ac, q, activations=True)
+    w = apt.pack(wc, p)
+    c32 = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    cfg = apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=8)
+    sp = torch.cuda.current_stream().cuda_stream
+    for _ in range(reps + 1):
+        apt.check(apt.apt_gemm(M, N, K, p, q, a.data.data_ptr(), w.data.data_ptr(), a.rowsum.data_ptr(),
+                               w.rowsum.data_ptr(), c32.data_ptr(), None, None, None, cfg, None, 0, sp),
+                  "apt_gemm")
+    torch.cuda.synchronize()
+    log("bench: counters run done (%d XOR GEMMs, %dx%dx%d W%dA%d)" % (reps + 1, M, N, K, p, q))
+
+
 def write_traffic(fetch_dir: str, write_dir: str, commands: str):
     """HBM bytes per prefill apt_gemm call from two rocprofv3 --pmc runs of
     counters_run (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch): the GEMM's
@@ -882,6 +906,8 @@ def main():
                     help="back-to-back prefill GEMM calls timed for the roofline")
     ap.add_argument("--counters-run", action="store_true",
                     help="run the prefill GEMM and a calibration copy for rocprofv3 --pmc, then exit")
+    ap.add_argument("--counters-xor", nargs=5, type=int, metavar=("M", "N", "K", "P", "Q"),
+                    help="run one problem on the XOR route for rocprofv3 --pmc, then exit")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs of --counters-run into profiles/")
     ap.add_argument("--routes", action="store_true",
@@ -913,6 +939,9 @@ def main():
     torch.cuda.set_device(0)
     if args.counters_run:
         counters_run()
+        return
+    if args.counters_xor:
+        counters_xor(*args.counters_xor)
         return
     if args.routes:
         print(json.dumps(route_table(), indent=1), flush=True)
