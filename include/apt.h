@@ -284,6 +284,13 @@ void apt_config_table_clear(void);
 /* Number of problems in the configuration table. */
 int apt_config_table_size(void);
 
+/* The hipError_t code (as an int) of the HIP runtime call that made the most
+ * recent call of this thread return APT_ERR_HIP; 0 if none has.  Each launch
+ * is checked through its own return status, so an error an unrelated runtime
+ * call left behind is never reported as the library's.  Host-only, no
+ * arguments, cannot fail. */
+int apt_last_hip_error(void);
+
 /* Static, NUL-terminated description of a status code. */
 const char* apt_status_string(apt_status_t status);
 

@@ -55,7 +55,9 @@ class apt_config_t(ctypes.Structure):
 class AptError(RuntimeError):
     def __init__(self, status, where):
         self.status = status
-        super().__init__("%s: %s (status %d)" % (where, status_string(status), status))
+        self.hip_error = apt_last_hip_error() if status == APT_ERR_HIP else 0
+        extra = ", hipError_t %d" % self.hip_error if status == APT_ERR_HIP else ""
+        super().__init__("%s: %s (status %d%s)" % (where, status_string(status), status, extra))
 
 
 _vp = ctypes.c_void_p
@@ -101,6 +103,8 @@ def lib() -> ctypes.CDLL:
         L.apt_config_table_clear.restype = None
         L.apt_config_table_size.argtypes = []
         L.apt_config_table_size.restype = ctypes.c_int
+        L.apt_last_hip_error.argtypes = []
+        L.apt_last_hip_error.restype = ctypes.c_int
         L.apt_status_string.argtypes = [ctypes.c_int]
         L.apt_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -184,6 +188,10 @@ def apt_config_table_size() -> int:
     return int(lib().apt_config_table_size())
 
 
+def apt_last_hip_error() -> int:
+    return int(lib().apt_last_hip_error())
+
+
 def status_string(status: int) -> str:
     return lib().apt_status_string(status).decode()
 
@@ -204,6 +212,17 @@ def _stream_ptr(stream=None):
     torch = _torch()
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream
+
+
+def _on_stream(stream):
+    """Context in which torch allocations belong to `stream` (the stream the
+    library's kernels use): the caching allocator then does not hand a block
+    to other work while those kernels may still use it."""
+    import contextlib
+    torch = _torch()
+    if stream is None:
+        return contextlib.nullcontext()
+    return torch.cuda.stream(stream)
 
 
 def _ptr(t):
@@ -229,8 +248,9 @@ def pack(codes, bits: int, activations: bool = False, stream=None) -> Packed:
     nbytes = apt_packed_bytes(rows, K, bits)
     if nbytes == 0:
         raise AptError(APT_ERR_INVALID_ARG, "apt_packed_bytes")
-    buf = torch.empty(nbytes, dtype=torch.uint8, device=codes.device)
-    rs = torch.empty(rows, dtype=torch.int32, device=codes.device)
+    with _on_stream(stream):
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=codes.device)
+        rs = torch.empty(rows, dtype=torch.int32, device=codes.device)
     fn = apt_quantize_pack_activations if activations else apt_pack_weights
     check(fn(codes.data_ptr(), rows, K, bits, buf.data_ptr(), rs.data_ptr(), _stream_ptr(stream)),
           fn.__name__)
@@ -247,9 +267,10 @@ def quantize_pack(x, bits: int, stream=None):
     nbytes = apt_packed_bytes(rows, K, bits)
     if nbytes == 0:
         raise AptError(APT_ERR_INVALID_ARG, "apt_packed_bytes")
-    buf = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
-    rs = torch.empty(rows, dtype=torch.int32, device=x.device)
-    scale = torch.empty(rows, dtype=torch.float16, device=x.device)
+    with _on_stream(stream):
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+        rs = torch.empty(rows, dtype=torch.int32, device=x.device)
+        scale = torch.empty(rows, dtype=torch.float16, device=x.device)
     check(apt_quantize_pack_activations_fp16(x.data_ptr(), rows, K, bits, buf.data_ptr(),
                                              rs.data_ptr(), scale.data_ptr(), _stream_ptr(stream)),
           "apt_quantize_pack_activations_fp16")
@@ -265,11 +286,12 @@ def gemm(a: Packed, w: Packed, out_int32: bool = True, a_scale=None, w_scale=Non
     assert a.K == w.K
     M, N, K = a.rows, w.rows, a.K
     dev = a.data.device
-    c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
-    c16 = torch.empty((M, N), dtype=torch.float16, device=dev) if out_fp16 else None
     ws_bytes = apt_gemm_workspace_bytes(M, N, K, w.bits, a.bits, cfg)
-    if workspace is None and ws_bytes > 0:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    with _on_stream(stream):
+        c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
+        c16 = torch.empty((M, N), dtype=torch.float16, device=dev) if out_fp16 else None
+        if workspace is None and ws_bytes > 0:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(apt_gemm(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
@@ -286,11 +308,12 @@ def gemm_affine(a: Packed, w: Packed, a_scale, a_zero, w_scale, w_zero, out_int3
     assert a.K == w.K
     M, N, K = a.rows, w.rows, a.K
     dev = a.data.device
-    c16 = torch.empty((M, N), dtype=torch.float16, device=dev)
-    c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
     ws_bytes = apt_gemm_workspace_bytes(M, N, K, w.bits, a.bits, cfg)
-    if workspace is None and ws_bytes > 0:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    with _on_stream(stream):
+        c16 = torch.empty((M, N), dtype=torch.float16, device=dev)
+        c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
+        if workspace is None and ws_bytes > 0:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(apt_gemm_affine(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
@@ -308,9 +331,10 @@ def search_config(a: Packed, w: Packed, stream=None):
     assert a.K == w.K
     M, N, K = a.rows, w.rows, a.K
     dev = a.data.device
-    c32 = torch.empty((M, N), dtype=torch.int32, device=dev)
     ws_bytes = apt_search_workspace_bytes(M, N, K, w.bits, a.bits)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes > 0 else None
+    with _on_stream(stream):
+        c32 = torch.empty((M, N), dtype=torch.int32, device=dev)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes > 0 else None
     st, c, us = apt_search_config(M, N, K, w.bits, a.bits, a.data.data_ptr(), w.data.data_ptr(),
                                   a.rowsum.data_ptr(), w.rowsum.data_ptr(), c32.data_ptr(),
                                   ws.data_ptr() if ws is not None else None, ws_bytes,

@@ -8,7 +8,22 @@
 
 #include "apt_internal.h"
 
+namespace apt {
+
+// hipError_t of the last call of this thread that returned APT_ERR_HIP.
+thread_local int t_last_hip_error = 0;
+
+apt_status_t hip_status(hipError_t e) {
+  if (e == hipSuccess) return APT_OK;
+  t_last_hip_error = (int)e;
+  return APT_ERR_HIP;
+}
+
+}  // namespace apt
+
 namespace {
+
+using apt::hip_status;
 
 bool bits_ok(int b) { return b >= 1 && b <= 8; }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -19,7 +34,6 @@ bool fits_int32(int K, int p, int q) {
   return bound < ((int64_t)1 << 31);
 }
 
-apt_status_t hip_status(hipError_t e) { return e == hipSuccess ? APT_OK : APT_ERR_HIP; }
 
 // The packers index a row's elements with 32-bit ints.
 constexpr int kMaxPackK = 1 << 30;
@@ -110,38 +124,47 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
 
 }  // extern "C"
 
-namespace {
+namespace apt {
 
-// Shared by apt_gemm and apt_gemm_affine once their own arguments are
-// checked: the common validation, config resolution and launch.
-apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed,
-                         const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
-                         int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
-                         uint16_t* c_fp16, const uint16_t* a_zero, const uint16_t* w_zero,
-                         const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
-                         void* stream) {
+apt_status_t gemm_check(int M, int N, int K, int p, int q, const void* a_packed,
+                        const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                        const int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                        const uint16_t* c_fp16, const apt_config_t* cfg, apt_config_t* resolved) {
   if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return APT_ERR_INVALID_ARG;
   if (a_packed == nullptr || w_packed == nullptr || !aligned16(a_packed) || !aligned16(w_packed))
     return APT_ERR_INVALID_ARG;
   if (c_int32 == nullptr && c_fp16 == nullptr) return APT_ERR_INVALID_ARG;
   if (c_fp16 != nullptr && (a_scale == nullptr || w_scale == nullptr)) return APT_ERR_INVALID_ARG;
   if (!fits_int32(K, p, q)) return APT_ERR_UNSUPPORTED;
-
   apt_config_t c;
   if (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
-    c = apt::select_config(M, N, K, p, q);
+    c = select_config(M, N, K, p, q);
   else
     c = *cfg;
   const bool have_rowsums = a_rowsum != nullptr && w_rowsum != nullptr;
-  apt_status_t st = check_config(c, M, N, K, p, q, have_rowsums);
+  const apt_status_t st = check_config(c, M, N, K, p, q, have_rowsums);
   if (st != APT_OK) return st;
-  if (c.route == APT_ROUTE_INT8_MFMA || c.route == APT_ROUTE_FP4_MFMA) {
-    if (workspace == nullptr || workspace_bytes < apt::int8_workspace_bytes(M, N, K, q, c))
-      return APT_ERR_WORKSPACE;
+  *resolved = c;
+  return APT_OK;
+}
+
+size_t gemm_workspace_need(int M, int N, int K, int q, const apt_config_t& c) {
+  if (c.route != APT_ROUTE_INT8_MFMA && c.route != APT_ROUTE_FP4_MFMA) return 0;
+  return int8_workspace_bytes(M, N, K, q, c);
+}
+
+apt_status_t gemm_launch(int M, int N, int K, int p, int q, const void* a_packed,
+                         const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                         int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                         uint16_t* c_fp16, const uint16_t* a_zero, const uint16_t* w_zero,
+                         const apt_config_t& c, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  const size_t need = gemm_workspace_need(M, N, K, q, c);
+  if (need > 0) {
+    if (workspace == nullptr || workspace_bytes < need) return APT_ERR_WORKSPACE;
     if (!aligned16(workspace)) return APT_ERR_INVALID_ARG;
   }
-
-  apt::GemmArgs g;
+  GemmArgs g;
   g.M = M; g.N = N; g.K = K; g.p = p; g.q = q;
   g.a_packed = static_cast<const uint32_t*>(a_packed);
   g.w_packed = static_cast<const uint32_t*>(w_packed);
@@ -155,15 +178,31 @@ apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed
   g.w_zero = reinterpret_cast<const __half*>(w_zero);
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (c.route) {
-    case APT_ROUTE_XOR: return hip_status(apt::launch_gemm_xor(g, c, s));
+    case APT_ROUTE_XOR: return hip_status(launch_gemm_xor(g, c, s));
     case APT_ROUTE_INT8_MFMA:
-    case APT_ROUTE_FP4_MFMA: return hip_status(apt::launch_gemm_int8(g, c, workspace, s));
-    case APT_ROUTE_PM1_MFMA: return hip_status(apt::launch_gemm_pm1(g, c, s));
+    case APT_ROUTE_FP4_MFMA: return hip_status(launch_gemm_int8(g, c, workspace, s));
+    case APT_ROUTE_PM1_MFMA: return hip_status(launch_gemm_pm1(g, c, s));
   }
   return APT_ERR_INVALID_ARG;
 }
 
-}  // namespace
+apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed,
+                         const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                         int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                         uint16_t* c_fp16, const uint16_t* a_zero, const uint16_t* w_zero,
+                         const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  apt_config_t c;
+  const apt_status_t st = gemm_check(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum,
+                                     c_int32, a_scale, w_scale, c_fp16, cfg, &c);
+  if (st != APT_OK) return st;
+  return gemm_launch(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale,
+                     w_scale, c_fp16, a_zero, w_zero, c, workspace, workspace_bytes, stream);
+}
+
+}  // namespace apt
+
+using apt::gemm_common;
 
 extern "C" {
 
@@ -220,10 +259,12 @@ apt_status_t apt_search_config(int M, int N, int K, int p, int q, const void* a_
   const int n = apt::candidate_configs(M, N, K, p, q, cand, apt::kMaxCandidates);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (hipEventCreate(&e0) != hipSuccess) return APT_ERR_HIP;
-  if (hipEventCreate(&e1) != hipSuccess) {
+  hipError_t he = hipEventCreate(&e0);
+  if (he != hipSuccess) return hip_status(he);
+  he = hipEventCreate(&e1);
+  if (he != hipSuccess) {
     (void)hipEventDestroy(e0);
-    return APT_ERR_HIP;
+    return hip_status(he);
   }
   constexpr int kWarm = 2, kTimed = 5;
   apt_status_t st = APT_OK;
@@ -241,15 +282,17 @@ apt_status_t apt_search_config(int M, int N, int K, int p, int q, const void* a_
     }
     if (r != APT_OK) continue;  // a candidate this problem cannot take
     for (int w = 1; w < kWarm && st == APT_OK; ++w) st = call(cand[i]);
-    if (st != APT_OK || hipEventRecord(e0, s) != hipSuccess) {
-      st = APT_ERR_HIP;
+    if (st != APT_OK) break;
+    if ((he = hipEventRecord(e0, s)) != hipSuccess) {
+      st = hip_status(he);
       break;
     }
     for (int t = 0; t < kTimed && st == APT_OK; ++t) st = call(cand[i]);
     float ms = 0.f;
-    if (st != APT_OK || hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
-        hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
-      st = APT_ERR_HIP;
+    if (st != APT_OK) break;
+    if ((he = hipEventRecord(e1, s)) != hipSuccess || (he = hipEventSynchronize(e1)) != hipSuccess ||
+        (he = hipEventElapsedTime(&ms, e0, e1)) != hipSuccess) {
+      st = hip_status(he);
       break;
     }
     const float us = ms * 1000.f / kTimed;
@@ -271,6 +314,8 @@ apt_status_t apt_search_config(int M, int N, int K, int p, int q, const void* a_
 void apt_config_table_clear(void) { apt::table_clear(); }
 
 int apt_config_table_size(void) { return apt::table_size(); }
+
+int apt_last_hip_error(void) { return apt::t_last_hip_error; }
 
 const char* apt_status_string(apt_status_t status) {
   switch (status) {

@@ -6,6 +6,9 @@
 #include <hip/hip_fp16.h>
 #include <stdint.h>
 
+#include <tuple>
+#include <utility>
+
 #include "../../include/apt.h"
 
 namespace apt {
@@ -19,6 +22,23 @@ constexpr int kRowGroup = 8;
 constexpr int kPlaneStride = kRowGroup * kWordsPerPlane;  // words from plane i to plane i+1
 
 inline int num_chunks(int K) { return (K + kChunk - 1) / kChunk; }
+
+// Launches kernel k on `stream` and returns the status of this launch alone.
+// (A launch followed by hipGetLastError would also report an error that an
+// earlier, unrelated runtime call of the thread left behind.)  The arguments
+// are converted to the kernel's parameter types and passed by address.
+template <typename... P, typename... A>
+inline hipError_t launch_kernel(void (*k)(P...), dim3 grid, dim3 block, size_t lds,
+                                hipStream_t stream, A&&... args) {
+  static_assert(sizeof...(P) == sizeof...(A), "one argument per kernel parameter");
+  std::tuple<P...> vals(std::forward<A>(args)...);
+  void* ptrs[sizeof...(P) > 0 ? sizeof...(P) : 1];
+  std::apply([&ptrs](auto&... v) {
+    int i = 0;
+    ((ptrs[i++] = static_cast<void*>(&v)), ...);
+  }, vals);
+  return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, ptrs, lds, stream);
+}
 
 // The FP4 MFMA route applies to (p, q) over K: E2M1 holds bipolar weights of
 // at most 2 bits, E2M1 (q <= 2) or E4M3 (q <= 4) the activations, and the
@@ -89,6 +109,35 @@ size_t int8_workspace_bytes(int M, int N, int K, int q, const apt_config_t& cfg)
 hipError_t launch_gemm_pm1(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
 bool pm1_config_ok(const apt_config_t& cfg, int p, int q);
 bool pm1_sizes_ok(int M, int N);
+
+// Maps a runtime status to the library's (APT_OK or APT_ERR_HIP, recording
+// the code for apt_last_hip_error) (api.hip).
+apt_status_t hip_status(hipError_t e);
+
+// The GEMM entry points' common steps (api.hip).  gemm_check validates
+// everything but the workspace (sizes, bit widths, pointers, outputs, the
+// int32 bound, the config) and resolves the config (cfg NULL or AUTO: the
+// selected one); gemm_workspace_need gives the workspace bytes of a
+// resolved config; gemm_launch checks the workspace and launches;
+// gemm_common is the three in a row.  a_zero / w_zero NULL for the scale
+// epilogue.
+apt_status_t gemm_check(int M, int N, int K, int p, int q, const void* a_packed,
+                        const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                        const int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                        const uint16_t* c_fp16, const apt_config_t* cfg, apt_config_t* resolved);
+size_t gemm_workspace_need(int M, int N, int K, int q, const apt_config_t& c);
+apt_status_t gemm_launch(int M, int N, int K, int p, int q, const void* a_packed,
+                         const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                         int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                         uint16_t* c_fp16, const uint16_t* a_zero, const uint16_t* w_zero,
+                         const apt_config_t& c, void* workspace, size_t workspace_bytes,
+                         void* stream);
+apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed,
+                         const void* w_packed, const int32_t* a_rowsum, const int32_t* w_rowsum,
+                         int32_t* c_int32, const uint16_t* a_scale, const uint16_t* w_scale,
+                         uint16_t* c_fp16, const uint16_t* a_zero, const uint16_t* w_zero,
+                         const apt_config_t* cfg, void* workspace, size_t workspace_bytes,
+                         void* stream);
 
 // Host-side selector (select.hip): the search module's table first, then the
 // model.

@@ -245,7 +245,7 @@ struct Stage {
 
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rsrc, const uint32_t* voff,
                                        int nchunks, int chunk) {
-    const int soff = min(chunk, nchunks - 1) * B * kPlaneStride * 4;
+    const uint32_t soff = (uint32_t)min(chunk, nchunks - 1) * (uint32_t)(B * kPlaneStride * 4);
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
 #pragma unroll
@@ -484,14 +484,17 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   const __amdgpu_buffer_rsrc_t w_rsrc = make_rsrc(g.w_packed, prm.w_bytes);
   const __amdgpu_buffer_rsrc_t a_rsrc = make_rsrc(prm.a_frag, prm.a_bytes);
   // Uniform byte offset of this wave's 32-row fragment block a of a tile.
-  auto a_block = [&](int m0, int a) __attribute__((always_inline)) {
+  // Offsets are unsigned 32-bit: the host admits fragment buffers below 4 GiB.
+  auto a_block = [&](int m0, int a) __attribute__((always_inline)) -> uint32_t {
     const int mb = min((m0 + wm * WTM) / 32 + a, prm.mblocks - 1);
-    return mb * prm.nsteps * kAVecs * kFragVecs * 16;
+    return (uint32_t)mb * (uint32_t)prm.nsteps * (uint32_t)(kAVecs * kFragVecs * 16);
   };
   const uint32_t a_lane = lane * 16;
   // vector x (F = 2: 0 or 1) of k-step ks of the fragment block
   auto load_a = [&](int m0, int chunk, int ks, int a, int x = 0) __attribute__((always_inline)) -> v4i {
-    const int soff = a_block(m0, a) + ((min(chunk, NCE - 1) * kSteps + ks) * kAVecs + x) * kFragVecs * 16;
+    const uint32_t soff =
+        a_block(m0, a) +
+        ((uint32_t)(min(chunk, NCE - 1) * kSteps + ks) * kAVecs + x) * (uint32_t)(kFragVecs * 16);
     return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_lane, soff, 0));
   };
   auto w_offsets = [&](int n0, uint32_t* voff) __attribute__((always_inline)) {
@@ -938,8 +941,7 @@ hipError_t launch_shape(const Int8Params& prm, int grid, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(sh.wm * sh.wn * kWave), lds, stream, prm);
-  return hipGetLastError();
+  return launch_kernel(kern, dim3(grid), dim3(sh.wm * sh.wn * kWave), lds, stream, prm);
 }
 
 template <int P, int F>
@@ -966,8 +968,7 @@ hipError_t launch_pair_shapes(const Int8Params& pa, int ga, const Int8Params& pb
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(ga + gb), dim3(a.wm * a.wn * kWave), lds, stream, pa, pb, ga);
-  return hipGetLastError();
+  return launch_kernel(kern, dim3(ga + gb), dim3(a.wm * a.wn * kWave), lds, stream, pa, pb, ga);
 }
 
 // The shape pairs built as one launch (same wave count): 256x256 or 512x128

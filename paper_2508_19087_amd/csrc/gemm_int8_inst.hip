@@ -35,9 +35,8 @@ hipError_t launch_expand(const uint32_t* a_packed, int M, int nchunks, int nstep
   int64_t threads = (int64_t)mblocks * 32 * (nsteps / Fmt<F>::kSteps) * kWordsPerPlane;
   if (threads < ncounters) threads = ncounters;
   const int blocks = (int)((threads + 255) / 256);
-  hipLaunchKernelGGL((expand_a_kernel<Q, F>), dim3(blocks), dim3(256), 0, stream, a_packed, M,
-                     nchunks, nsteps, mblocks, out, counters, ncounters);
-  return hipGetLastError();
+  return launch_kernel(expand_a_kernel<Q, F>, dim3(blocks), dim3(256), 0, stream, a_packed, M,
+                       nchunks, nsteps, mblocks, out, counters, ncounters);
 }
 
 template <int Q>

@@ -182,8 +182,7 @@ hipError_t launch_pq(const Pm1Params& prm0, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(tiles_m * prm.tiles_n), dim3(kThreads), lds, stream, prm);
-  return hipGetLastError();
+  return launch_kernel(kern, dim3(tiles_m * prm.tiles_n), dim3(kThreads), lds, stream, prm);
 }
 
 template <int P>

@@ -132,11 +132,8 @@ __global__ __launch_bounds__(kWave* kWaves) void gemm_xor_kernel(XorParams prm) 
 template <int P, int Q>
 inline hipError_t launch_pq(const XorParams& prm, int grid_x, int grid_y, size_t lds, hipStream_t s) {
   dim3 grid(grid_x, grid_y), block(kWave * kWaves);
-  if (lds > 0)
-    hipLaunchKernelGGL((gemm_xor_kernel<P, Q, true>), grid, block, lds, s, prm);
-  else
-    hipLaunchKernelGGL((gemm_xor_kernel<P, Q, false>), grid, block, 0, s, prm);
-  return hipGetLastError();
+  if (lds > 0) return launch_kernel(gemm_xor_kernel<P, Q, true>, grid, block, lds, s, prm);
+  return launch_kernel(gemm_xor_kernel<P, Q, false>, grid, block, 0, s, prm);
 }
 
 // Launch for weight bits P and any activation bits; one explicit

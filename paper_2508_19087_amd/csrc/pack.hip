@@ -338,19 +338,12 @@ hipError_t launch_rows(const void* src, int rows, int K, uint32_t* packed, int32
   const int groups = rows % kRowGroup == 0 ? rows / kRowGroup : 0;
   const dim3 block(kWave * nw), grid(rows);
   const uint8_t* s = static_cast<const uint8_t*>(src);
-  if (per_wave == 1)
-    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 1>), grid, block, 0, stream, s, rows, K, nchunks,
-                       groups, packed, rowsum, scale);
-  else if (per_wave == 2)
-    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 2>), grid, block, 0, stream, s, rows, K, nchunks,
-                       groups, packed, rowsum, scale);
-  else if (per_wave <= kMaxCachedSteps)
-    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 4>), grid, block, 0, stream, s, rows, K, nchunks,
-                       groups, packed, rowsum, scale);
-  else
-    hipLaunchKernelGGL((pack_rows_kernel<Src, B, 0>), grid, block, 0, stream, s, rows, K, nchunks,
-                       groups, packed, rowsum, scale);
-  return hipGetLastError();
+  auto kern = per_wave == 1                   ? pack_rows_kernel<Src, B, 1>
+              : per_wave == 2                 ? pack_rows_kernel<Src, B, 2>
+              : per_wave <= kMaxCachedSteps   ? pack_rows_kernel<Src, B, 4>
+                                              : pack_rows_kernel<Src, B, 0>;
+  return launch_kernel(kern, grid, block, 0, stream, s, rows, K, nchunks, groups, packed, rowsum,
+                       scale);
 }
 
 // The 16-byte load path needs whole 16-element groups and a 16-byte aligned base.

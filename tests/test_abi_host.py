@@ -14,7 +14,8 @@ def test_exports_every_declared_symbol():
     assert set(names) == {"apt_packed_bytes", "apt_pack_weights", "apt_quantize_pack_activations",
                           "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
                           "apt_gemm_affine", "apt_search_workspace_bytes", "apt_search_config",
-                          "apt_config_table_clear", "apt_config_table_size", "apt_status_string"}
+                          "apt_config_table_clear", "apt_config_table_size", "apt_last_hip_error",
+                          "apt_status_string"}
     L = apt.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -33,6 +34,13 @@ def test_status_strings():
     for s in range(5):
         assert apt.status_string(s)
     assert apt.status_string(99) == "unknown status"
+
+
+def test_last_hip_error_starts_clear():
+    # validation failures never touch the runtime, so they leave it at 0
+    assert apt.apt_gemm(0, 1, 1, 1, 1, None, None, None, None, None, None, None, None, None, None,
+                        0, None) == apt.APT_ERR_INVALID_ARG
+    assert apt.apt_last_hip_error() == 0
 
 
 def _shapes():

@@ -1,14 +1,11 @@
 """GPU parity on the five benchmark workloads at their full sizes, in the
-configuration the library selects (the one the benchmark times): int32
-bit-exact against the oracle (full outputs where the oracle is quick, sampled
-rows / columns / entries otherwise) and fp16 within 1e-3 relative of the exact
-value."""
-import numpy as np
+configuration the library selects (the one the benchmark times): every int32
+output bit-exact against the oracle and every fp16 output within 1e-3 relative
+of the exact value (Sec. III-B: the exact product is sum_ij 2^(i+j) Y(i,j))."""
 import pytest
 
 import synth
-from gpu_util import (assert_fp16_ok, assert_int32_equal, check_sampled, oracle_full, run)
-from oracle import oracle as ref
+from gpu_util import assert_fp16_ok, assert_int32_equal, oracle_full, run
 
 pytestmark = pytest.mark.gpu
 
@@ -32,14 +29,14 @@ def test_w2a2_decode(M, N):
 def test_w4a4_prefill_2048x11008x4096():
     prob = synth.w4a4_prefill()
     got, _ = run(prob)
-    check_sampled(prob, got, seed=3, what=prob.name)
+    assert_int32_equal(got, oracle_full(prob), prob.name)
 
 
 @pytest.mark.parametrize("index", range(len(synth.SWEEP_BITS)))
 def test_sweep_down_projection(index):
     prob = synth.sweep_down(index)
     got, _ = run(prob)
-    check_sampled(prob, got, seed=40 + index, n_entries=50000, what=prob.name)
+    assert_int32_equal(got, oracle_full(prob), prob.name)
 
 
 @pytest.mark.parametrize("layer", list(synth.LAYER_SHAPES))
@@ -47,13 +44,6 @@ def test_sweep_down_projection(index):
 def test_w2a4_layer(layer, M):
     prob = synth.layer_w2a4(layer, M)
     c32, c16 = run(prob, fp16=True)
-    if M == 1:
-        want = oracle_full(prob)
-        assert_int32_equal(c32, want, prob.name)
-        assert_fp16_ok(c16, want, prob, prob.name)
-    else:
-        va, vw, rows = check_sampled(prob, c32, seed=5, n_entries=30000, what=prob.name)
-        want_rows = ref.matmul(va[rows], vw)
-        sub = synth.Problem(prob.name, len(rows), prob.N, prob.K, prob.p, prob.q, prob.w_codes,
-                            prob.a_codes[rows], prob.w_scale, prob.a_scale[rows])
-        assert_fp16_ok(c16[rows], want_rows, sub, prob.name)
+    want = oracle_full(prob)
+    assert_int32_equal(c32, want, prob.name)
+    assert_fp16_ok(c16, want, prob, prob.name)
