@@ -245,6 +245,34 @@ apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q,
                              const apt_config_t* cfg,
                              void* workspace, size_t workspace_bytes, void* stream);
 
+/* Size of the device array apt_gemm_noalloc uses as its workspace (64 MiB). */
+#define APT_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* apt_gemm without a caller workspace and without any device allocation, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops, harnesses that forbid hipMalloc).  The workspace is a device
+ * array inside the library of APT_NOALLOC_SCRATCH_BYTES bytes; each GPU the
+ * library runs on holds its own copy until the process ends (the first call
+ * on a device looks up its address).  Every call on one GPU shares that GPU's
+ * copy, so calls that overlap in time on one GPU (concurrent streams, or
+ * several host threads) race and must be serialised by the caller; calls in
+ * stream order are safe (the kernels rewrite or clear what they read).
+ * Arguments, results and errors as apt_gemm without workspace and
+ * workspace_bytes; the outputs are caller buffers as there.  With cfg NULL or
+ * route AUTO the selected config is used, and if its stream-K partial tiles
+ * do not fit, the same tiles with one workgroup per tile (the result is the
+ * same).  Errors: as apt_gemm, and APT_ERR_WORKSPACE when the resolved
+ * config needs more than APT_NOALLOC_SCRATCH_BYTES (activation fragments of
+ * about M * K bytes on the MFMA routes, plus stream-K partial tiles of a
+ * forced persistent grid); APT_ERR_UNSUPPORTED for a device ordinal of 64 or
+ * more; nothing is launched in either case. */
+apt_status_t apt_gemm_noalloc(int M, int N, int K, int p, int q,
+                              const void* a_packed, const void* w_packed,
+                              const int32_t* a_rowsum, const int32_t* w_rowsum,
+                              int32_t* c_int32,
+                              const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
+                              const apt_config_t* cfg, void* stream);
+
 /* Device workspace bytes apt_search_config needs for this problem: the most
  * that any config it times needs (apt_gemm_workspace_bytes).  Returns 0 for
  * invalid sizes or bit widths. */

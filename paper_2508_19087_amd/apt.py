@@ -91,6 +91,9 @@ def lib() -> ctypes.CDLL:
         L.apt_gemm.argtypes = ([ctypes.c_int] * 5 + [_vp] * 8 + [ctypes.POINTER(apt_config_t)] +
                                [_vp, ctypes.c_size_t, _vp])
         L.apt_gemm.restype = ctypes.c_int
+        L.apt_gemm_noalloc.argtypes = ([ctypes.c_int] * 5 + [_vp] * 8 +
+                                       [ctypes.POINTER(apt_config_t), _vp])
+        L.apt_gemm_noalloc.restype = ctypes.c_int
         L.apt_gemm_affine.argtypes = ([ctypes.c_int] * 5 + [_vp] * 10 +
                                       [ctypes.POINTER(apt_config_t)] + [_vp, ctypes.c_size_t, _vp])
         L.apt_gemm_affine.restype = ctypes.c_int
@@ -154,6 +157,13 @@ def apt_gemm(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_s
     return lib().apt_gemm(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32,
                           a_scale, w_scale, c_fp16, ctypes.byref(cfg) if cfg is not None else None,
                           workspace, workspace_bytes, stream)
+
+
+def apt_gemm_noalloc(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale,
+                     w_scale, c_fp16, cfg, stream) -> int:
+    return lib().apt_gemm_noalloc(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32,
+                                  a_scale, w_scale, c_fp16,
+                                  ctypes.byref(cfg) if cfg is not None else None, stream)
 
 
 def apt_gemm_affine(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, a_scale, a_zero,

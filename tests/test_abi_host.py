@@ -15,6 +15,7 @@ def test_exports_every_declared_symbol():
                           "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
                           "apt_gemm_affine", "apt_search_workspace_bytes", "apt_search_config",
                           "apt_config_table_clear", "apt_config_table_size", "apt_last_hip_error",
+                          "apt_gemm_noalloc",
                           "apt_status_string"}
     L = apt.lib()
     for n in names:
@@ -327,3 +328,31 @@ def test_fp4_workspace_is_half_the_int8_fragments():
             assert apt.apt_gemm_workspace_bytes(M, 512, K, 2, q, f4) == a
     assert apt.apt_gemm_workspace_bytes(64, 512, 1000, 3, 2, f4) == 0  # p = 3: not runnable
     assert apt.apt_gemm_workspace_bytes(64, 512, 1000, 2, 5, f4) == 0  # q = 5: not runnable
+
+
+def test_noalloc_rejects_before_any_launch():
+    """apt_gemm_noalloc validates like apt_gemm and refuses a config whose
+    workspace exceeds its fixed array, before it touches the runtime."""
+    f = apt.apt_gemm_noalloc
+    fake = 1 << 12  # aligned, never dereferenced: every case below fails validation
+    assert f(0, 1, 1, 1, 1, fake, fake, fake, fake, fake, None, None, None, None,
+             None) == apt.APT_ERR_INVALID_ARG
+    assert f(4, 4, 4, 2, 2, fake, fake, fake, fake, None, None, None, None, None,
+             None) == apt.APT_ERR_INVALID_ARG
+    assert f(4, 4, 4, 2, 2, fake + 4, fake, fake, fake, fake, None, None, None, None,
+             None) == apt.APT_ERR_INVALID_ARG
+    assert f(4, 4, 40000, 8, 8, fake, fake, fake, fake, fake, None, None, None, None,
+             None) == apt.APT_ERR_UNSUPPORTED
+    # activation fragments of 65536 x 4096 bytes (256 MiB) exceed the 64 MiB array
+    cfg = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 128, 128, 4, 1, 0, 3)
+    assert apt.apt_gemm_workspace_bytes(65536, 4096, 4096, 4, 4, cfg) > 64 << 20
+    assert f(65536, 4096, 4096, 4, 4, fake, fake, fake, fake, fake, None, None, None, cfg,
+             None) == apt.APT_ERR_WORKSPACE
+    assert f(65536, 4096, 4096, 4, 4, fake, fake, fake, fake, fake, None, None, None, None,
+             None) == apt.APT_ERR_WORKSPACE
+    # a forced persistent grid whose partial tiles do not fit is refused, not changed
+    cfg = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 300, 3)
+    assert apt.apt_gemm_workspace_bytes(1000, 1000, 4096, 4, 4, cfg) > 64 << 20
+    assert f(1000, 1000, 4096, 4, 4, fake, fake, fake, fake, fake, None, None, None, cfg,
+             None) == apt.APT_ERR_WORKSPACE
+    assert apt.apt_last_hip_error() == 0
