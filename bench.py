@@ -236,7 +236,8 @@ def search_table(calls: int = 20):
     import paper_2508_19087_amd as apt
     import synth
     dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
-    probs = [synth.w2a2_decode(M, N) for M in (1, 4, 8) for N in (4096, synth.MLP)]
+    probs = [synth.w1a2_small()]
+    probs += [synth.w2a2_decode(M, N) for M in (1, 4, 8) for N in (4096, synth.MLP)]
     probs += [synth.w4a4_prefill()] + [synth.sweep_down(i) for i in range(len(synth.SWEEP_BITS))]
     probs += [synth.layer_w2a4(name, M) for M in (1, 1024) for name in ("q", "gate", "down")]
 
@@ -283,14 +284,93 @@ def search_table(calls: int = 20):
         t_model = timed(model)
         best, t_search = apt.search_config(a, w)
         t_best = timed(best)
-        rows.append({"problem": prob.name, "model": short(model), "model_us": round(t_model, 2),
+        rows.append({"problem": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
+                     "q": prob.q, "model": short(model), "model_us": round(t_model, 2),
                      "searched": short(best), "searched_us": round(t_best, 2),
-                     "search_timing_us": round(t_search, 2)})
+                     "search_timing_us": round(t_search, 2), "searched_config": best.as_dict()})
         log("bench: search %s: model %s %.2f us, searched %s %.2f us"
             % (prob.name, short(model), t_model, short(best), t_best))
         del a, w, c32
     apt.apt_config_table_clear()
     return rows
+
+
+def calibrate(calls: int = 20):
+    """Calibration of the selector's MFMA model (csrc/select.hip): for each
+    model tile shape and operand class (int8 operands at weight widths 2, 4 and
+    8 with 4-bit activations; FP4 operands at W2A2), apt_gemm call times with
+    M = 2048 at K = 2048 and 6144 (8 and 24 chunk pairs), over one full round
+    of tiles (N chosen so), and for shapes with two workgroups per compute unit
+    also over half a round (one per compute unit).  The K slope gives the
+    microseconds per chunk pair, its intercept the fixed time."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    shapes = [(256, 256, 4, 2, 1), (512, 128, 8, 1, 1), (256, 128, 4, 1, 2), (256, 128, 4, 2, 1),
+              (128, 128, 2, 2, 2)]
+    classes = [("int8_w2", apt.APT_ROUTE_INT8_MFMA, 2, 4), ("int8_w4", apt.APT_ROUTE_INT8_MFMA, 4, 4),
+               ("int8_w8", apt.APT_ROUTE_INT8_MFMA, 8, 4), ("fp4_w2a2", apt.APT_ROUTE_FP4_MFMA, 2, 2)]
+    M, Ks = 2048, (2048, 6144)
+    g = np.random.default_rng(11)
+    sp = torch.cuda.current_stream().cuda_stream
+    out = []
+    for cname, route, p, q in classes:
+        ops = {}
+        for K in Ks:
+            ac = torch.from_numpy(g.integers(-(1 << (q - 1)), 1 << (q - 1), (M, K), dtype=np.int8)).cuda()
+            a = apt.pack(ac, q, activations=True)
+            for bm, bn, wm, wn, per_cu in shapes:
+                for label, tiles in (("full", cus * per_cu), ("alone", cus)):
+                    if label == "alone" and per_cu == 1:
+                        continue
+                    N = tiles // (M // bm) * bn
+                    key = (N, K)
+                    if key not in ops:
+                        wc = torch.from_numpy(g.integers(-(1 << (p - 1)), 1 << (p - 1), (N, K),
+                                                         dtype=np.int8)).cuda()
+                        ops[key] = apt.pack(wc, p)
+                    w = ops[key]
+                    cfg = apt.apt_config_t.make(route, bm, bn, 128, wm, wn, 0, 3)
+                    wsb = apt.apt_gemm_workspace_bytes(M, N, K, p, q, cfg)
+                    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+                    c32 = torch.empty((M, N), dtype=torch.int32, device="cuda")
+
+                    def call():
+                        apt.check(apt.apt_gemm(M, N, K, p, q, a.data.data_ptr(), w.data.data_ptr(),
+                                               a.rowsum.data_ptr(), w.rowsum.data_ptr(), c32.data_ptr(),
+                                               None, None, None, cfg, ws.data_ptr(), wsb, sp), "apt_gemm")
+                    for _ in range(3):
+                        call()
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    torch.cuda.synchronize()
+                    e0.record()
+                    for _ in range(calls):
+                        call()
+                    e1.record()
+                    torch.cuda.synchronize()
+                    us = e0.elapsed_time(e1) * 1e3 / calls
+                    out.append({"class": cname, "shape": [bm, bn, wm, wn], "round": label, "M": M, "N": N,
+                                "K": K, "us": round(us, 2)})
+                    log("bench: calibrate %s %dx%d/%dx%d %s K=%d: %.2f us" % (cname, bm, bn, wm, wn, label,
+                                                                              K, us))
+                    del ws, c32
+        del ops
+    # the model's figures: pair time (slope over the 16 extra pairs), fixed time (intercept)
+    fits = []
+    for cname, _, _, _ in classes:
+        for bm, bn, wm, wn, per_cu in shapes:
+            def t(label, K):
+                return [r["us"] for r in out if r["class"] == cname and r["shape"] == [bm, bn, wm, wn]
+                        and r["round"] == label and r["K"] == K][0]
+            pair = (t("full", 6144) - t("full", 2048)) / 16.0
+            fixed = t("full", 2048) - 8 * pair
+            alone = (t("alone", 6144) - t("alone", 2048)) / 16.0 if per_cu > 1 else pair
+            fits.append({"class": cname, "shape": [bm, bn, wm, wn], "per_cu": per_cu,
+                         "pair_us": round(pair, 3), "pair_alone_us": round(alone, 3),
+                         "fixed_us": round(fixed, 2)})
+    return {"cus": cus, "timings": out, "model": fits}
 
 
 def graph_of(torch, launch):
@@ -355,31 +435,45 @@ def decode_cold(wl, reps: int = 4):
             "effective_TOPS": round(p.ops / t / 1e12, 4),
             "method": "HIP graph of %d back-to-back GEMMs, one per cold weight copy" % copies}
         del ws, g
-    # practical ceiling: plain device copies of the larger weight matrix, cold, the same way
-    big = wl.items[1]["w"].data
-    n = big.numel()
-    copies = max(8, int(2 * MALL_BYTES // n) + 1)
-    srcs = [big.clone() for _ in range(copies)]
-    dst = torch.empty_like(big)
+    out["read_ceiling_same_bytes"] = read_ceiling(torch, wl.items[1]["w"].data, reps)
+    return out
 
-    def launch_copies(sp):
-        for src in srcs:
-            dst.copy_(src)
-    g = graph_of(torch, launch_copies)
+
+def read_ceiling(torch, buf, reps: int = 4):
+    """A read-only cold reference for a decode GEMM's weight bytes: a row-wise
+    maximum (torch.amax over rows of 4 KB, one int32 per row written) of each
+    of enough copies of the buffer (> 2x the Infinity Cache) that every read
+    comes from HBM, replayed as one HIP graph like the GEMM rotation and
+    checked on every replay.  It reads each byte once, as the GEMM does."""
+    n = buf.numel()
+    assert n % 4096 == 0
+    copies = max(8, int(2 * MALL_BYTES // n) + 1)
+    srcs = [buf.clone().view(torch.int32).view(-1, 1024) for _ in range(copies)]
+    outs = [torch.empty(x.shape[0], dtype=torch.int32, device="cuda") for x in srcs]
+
+    def launch(sp):
+        for x, o in zip(srcs, outs):
+            torch.amax(x, dim=1, out=o)
+    g = graph_of(torch, launch)
+    want = torch.amax(srcs[0], dim=1)
     times = []
     for r in range(reps):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         g.replay()
         e1.record()
         torch.cuda.synchronize()
+        assert all(torch.equal(o, want) for o in outs), "read ceiling replay"
         if r > 0:
             times.append(e0.elapsed_time(e1) / copies)
-    assert torch.equal(dst, srcs[-1])
     t = sorted(times)[len(times) // 2] * 1e-3
-    out["copy_ceiling_same_bytes"] = {"bytes_read": n, "us_per_copy": round(t * 1e6, 3),
-                                      "read_GBs": round(n / t / 1e9, 1)}
-    return out
+    return {"bytes_read": n, "us": round(t * 1e6, 3), "read_GBs": round(n / t / 1e9, 1),
+            "frac_hbm": round(n / t / 1e9 / PEAK_HBM_GBS, 4), "copies": copies,
+            "method": "HIP graph of torch.amax over 4 KB rows of each cold copy (reads every "
+                      "byte once; one int32 written per 4 KB)"}
 
 
 def decode_layer_cold(wl, reps: int = 4):
@@ -493,9 +587,11 @@ def decode_sweep(reps: int = 4):
                 ts.append(e0.elapsed_time(e1) * 1e3 / copies)
         t = sorted(ts)[len(ts) // 2]
         bytes_alg = (N * K * p + K * q) / 8 + 4 * N
+        ceil = read_ceiling(torch, w.data, reps)
         rows.append({"N": N, "K": K, "weight_bytes": nb, "copies": copies, "us": round(t, 3),
                      "GB/s": round(bytes_alg / t / 1e3, 1),
-                     "frac_hbm": round(bytes_alg / t / 1e3 / PEAK_HBM_GBS, 4)})
+                     "frac_hbm": round(bytes_alg / t / 1e3 / PEAK_HBM_GBS, 4),
+                     "read_ceiling_us": ceil["us"], "read_ceiling_frac_hbm": ceil["frac_hbm"]})
         log("bench: decode sweep N=%d %.2f us" % (N, t))
         del ws, gr
     # the launch floor in the same setting: a graph of one-element kernels
@@ -855,6 +951,114 @@ def counters_xor(M: int, N: int, K: int, p: int, q: int, reps: int = 3):
     log("bench: counters run done (%d XOR GEMMs, %dx%dx%d W%dA%d)" % (reps + 1, M, N, K, p, q))
 
 
+def workload_problems():
+    """Every workload configuration: the W1A2 16x512x512 GEMM, the W2A2 decode
+    GEMMs (M = 1, 4, 8; N = 4096, 11008), the W4A4 prefill GEMM, the (p, q)
+    sweep on the down projection and the W2A4 layer set at 1 and 1024 tokens."""
+    import synth
+    probs = [synth.w1a2_small()]
+    probs += [synth.w2a2_decode(M, N) for M in (1, 4, 8) for N in (4096, synth.MLP)]
+    probs += [synth.w4a4_prefill()]
+    probs += [synth.sweep_down(i) for i in range(len(synth.SWEEP_BITS))]
+    probs += [synth.layer_w2a4(name, M) for M in (1, 1024) for name in synth.LAYER_SHAPES]
+    return probs
+
+
+def workloads_run(calls: int = 20):
+    """For rocprofv3 --kernel-trace: every workload configuration packed
+    first, then, workload by workload, one torch fill of a marker buffer (a
+    kernel that separates the workloads in the trace) and `calls` back-to-back
+    apt_gemm calls in the selected config (int32 output, plus the fp16
+    epilogue where the workload has scales).  Prints the plan as JSON."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+    items = []
+    for prob in workload_problems():
+        a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
+        w = apt.pack(dev(prob.w_codes), prob.p)
+        fp16 = prob.a_scale is not None
+        items.append((prob, a, w, dev(prob.a_scale) if fp16 else None,
+                      dev(prob.w_scale) if fp16 else None))
+    marker = torch.empty(1, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    plan = []
+    for i, (prob, a, w, sa, sw) in enumerate(items):
+        cfg = apt.select_config(prob.M, prob.N, prob.K, prob.p, prob.q)
+        ws_bytes = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
+        ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+        c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+        c16 = torch.empty((prob.M, prob.N), dtype=torch.float16, device="cuda") if sa is not None else None
+        marker.fill_(i)
+        sp = torch.cuda.current_stream().cuda_stream
+        for _ in range(calls):
+            apt.check(apt.apt_gemm(prob.M, prob.N, prob.K, prob.p, prob.q, a.data.data_ptr(),
+                                   w.data.data_ptr(), a.rowsum.data_ptr(), w.rowsum.data_ptr(),
+                                   c32.data_ptr(), sa.data_ptr() if sa is not None else None,
+                                   sw.data_ptr() if sw is not None else None,
+                                   c16.data_ptr() if c16 is not None else None, cfg,
+                                   ws.data_ptr(), ws_bytes, sp), "apt_gemm")
+        torch.cuda.synchronize()
+        plan.append({"workload": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
+                     "q": prob.q, "ops": prob.ops, "fp16": c16 is not None, "calls": calls,
+                     "config": cfg.as_dict()})
+        del ws, c32, c16
+    print(json.dumps(plan), flush=True)
+
+
+def write_workload_stats(trace_csv: str, plan_json: str, command: str):
+    """Per-workload kernel durations from the rocprofv3 kernel trace of
+    workloads_run: the dispatches between consecutive marker fills belong to
+    one workload; the first call of each is a warm-up and is left out."""
+    import csv
+    import statistics
+    plan = json.load(open(plan_json))
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Start_Timestamp"]))
+    segs, cur = [], None
+    for r in rows:
+        name = r["Kernel_Name"]
+        if "FillFunctor" in name or "fill" in name.lower():
+            cur = []
+            segs.append(cur)
+        elif cur is not None:
+            cur.append((name, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0))
+    assert len(segs) == len(plan), (len(segs), len(plan))
+    lines = ["# Kernel durations of every workload configuration in its selected config (rocprofv3",
+             "# kernel trace; per kernel: median and mean duration over the calls after the first,",
+             "# in microseconds; 'per call' sums the kernels one apt_gemm call launches, 'TOPS' is",
+             "# 2 M N K over that sum).  Weights and activations are packed before the timed calls.",
+             "# command (repository root on the MI355X box): " + command,
+             ""]
+    for pl, seg in zip(plan, segs):
+        per_call = len(seg) // pl["calls"]
+        assert per_call * pl["calls"] == len(seg), (pl["workload"], len(seg))
+        body = seg[per_call:]  # skip the first call
+        names = []
+        for n, _ in body:
+            if n not in names:
+                names.append(n)
+        total = 0.0
+        parts = []
+        for n in names:
+            ts = [t for k, t in body if k == n]
+            med = statistics.median(ts)
+            total += med * len(ts) / (pl["calls"] - 1)
+            short = n.split("(")[0].replace("void ", "").replace("apt::", "")
+            parts.append("%s median %.2f mean %.2f" % (short, med, statistics.mean(ts)))
+        c = pl["config"]
+        route = {1: "xor", 2: "pm1", 3: "int8", 4: "fp4"}[c["route"]]
+        cfg = route if route == "xor" else "%s %dx%d/%dx%d g%d%s" % (
+            route, c["bm"], c["bn"], c["waves_m"], c["waves_n"], c["grid"],
+            " split %d" % c["split_n"] if c["split_n"] else "")
+        lines.append("%-32s %-28s per call %8.2f us  %8.1f TOPS" % (
+            pl["workload"], cfg, total, pl["ops"] / total / 1e6))
+        for ptxt in parts:
+            lines.append("    " + ptxt)
+    print("\n".join(lines))
+
+
 def write_traffic(fetch_dir: str, write_dir: str, commands: str):
     """HBM bytes per prefill apt_gemm call from two rocprofv3 --pmc runs of
     counters_run (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch): the GEMM's
@@ -923,11 +1127,22 @@ def main():
                     help="print the cost of the zero-point epilogue against the scale epilogue and exit")
     ap.add_argument("--decode-sweep", action="store_true",
                     help="print the cold-weight time of one M=1 W2A4 GEMM against N and exit")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="print the selector model's calibration (pair and fixed times per tile "
+                         "shape and operand class) and exit")
+    ap.add_argument("--workloads", action="store_true",
+                    help="for a rocprofv3 kernel trace: every workload configuration's selected "
+                         "apt_gemm, 20 calls each, separated by marker fills; prints the plan")
+    ap.add_argument("--write-workload-stats", nargs=3, metavar=("TRACE_CSV", "PLAN_JSON", "COMMAND"),
+                    help="print the per-workload kernel durations of a --workloads trace and exit")
     ap.add_argument("--traffic-commands", default="",
                     help="the commands that produced the --write-traffic directories")
     args = ap.parse_args()
     if args.write_traffic:
         write_traffic(args.write_traffic[0], args.write_traffic[1], args.traffic_commands)
+        return
+    if args.write_workload_stats:
+        write_workload_stats(*args.write_workload_stats)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
@@ -939,6 +1154,12 @@ def main():
     torch.cuda.set_device(0)
     if args.counters_run:
         counters_run()
+        return
+    if args.workloads:
+        workloads_run()
+        return
+    if args.calibrate:
+        print(json.dumps(calibrate(), indent=1), flush=True)
         return
     if args.counters_xor:
         counters_xor(*args.counters_xor)

@@ -143,6 +143,9 @@ apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed
 // model.
 apt_config_t select_config(int M, int N, int K, int p, int q);
 bool table_lookup(int M, int N, int K, int p, int q, apt_config_t* out);
+// The shipped table of searched configs with approximate matching.
+bool shipped_lookup(int M, int N, int K, int p, int q, apt_config_t* out);
+int shipped_table_size();
 void table_store(int M, int N, int K, int p, int q, const apt_config_t& c);
 void table_clear();
 int table_size();

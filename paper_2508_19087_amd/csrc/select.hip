@@ -1,10 +1,12 @@
 // select.hip - host-side kernel-config selector (APT-LLM, arXiv 2508.19087,
 // Sec. V: tunable hyperparameters, lookup table, approximate matching).
 //
-// Lookup table: configs found by the search module (apt_search_config, Sec.
-// V-B "best kernel search") are kept per (M, N, K, p, q) and win over the
-// model below for exactly that problem; every other problem takes the model,
-// which plays the part of the paper's approximate matching.
+// Lookup tables: configs found by the search module (apt_search_config, Sec.
+// V-B "best kernel search") are kept per (M, N, K, p, q) and win over
+// everything else for exactly that problem; next comes the shipped table of
+// searched configs for the workload shapes, matched approximately (same p, q
+// and M bucket, nearest N and K within a radius); every other problem takes
+// the model.
 //
 // The paper searches, per (M, N, K, bits), the block/warp shapes that satisfy
 // its tile constraint and stores the fastest in a table.  Here the
@@ -34,21 +36,27 @@ struct ShapeTimes {
 struct Int8Shape {
   int bm, bn, wm, wn;
   int per_cu;            // workgroups resident per compute unit (registers and LDS)
-  ShapeTimes t[2];       // int8 operands, FP4 operands
+  ShapeTimes t[4];       // operand classes: int8 with weights of <= 2, <= 4 and <= 8 bits; FP4
 };
 
-// Measured on MI355X with M = 2048, K = 2048 and 6144 (the K slope gives the
-// pair time, its intercept the fixed time), with one full round of tiles and,
-// for the 4-wave shapes, half a round (one workgroup per compute unit): int8
-// operands at W4A4, FP4 operands at W2A2 (their only use in the model: FP4
+// Operand class of the model's figures: the loop's cost grows with the weight
+// planes reassembled per chunk (p), while the activations reach it as int8
+// (or FP4) fragments whatever q is.
+inline int time_class(bool fp4, int p) { return fp4 ? 3 : p <= 2 ? 0 : p <= 4 ? 1 : 2; }
+
+// Measured on MI355X by bench.py --calibrate: apt_gemm call times with
+// M = 2048 at K = 2048 and 6144 (the K slope gives the pair time, its
+// intercept the fixed time), with one full round of tiles and, for the 4-wave
+// shapes, half a round (one workgroup per compute unit); int8 operands at
+// W2A4, W4A4 and W8A4, FP4 operands at W2A2 (the model's only FP4 use: FP4
 // weights with FP8 activations measured no faster than int8 operands, so that
 // form is left to the search module).
 constexpr Int8Shape kInt8Shapes[] = {
-    {256, 256, 4, 2, 1, {{3.74, 3.74, 19.6}, {1.87, 1.87, 19.7}}},
-    {512, 128, 8, 1, 1, {{2.81, 2.81, 21.4}, {1.71, 1.71, 20.1}}},
-    {256, 128, 4, 1, 2, {{3.39, 1.81, 12.9}, {1.70, 1.01, 14.0}}},
-    {256, 128, 4, 2, 1, {{2.04, 2.04, 12.3}, {1.14, 1.14, 11.8}}},
-    {128, 128, 2, 2, 2, {{1.88, 1.17, 12.2}, {1.17, 0.90, 9.0}}},
+    {256, 256, 4, 2, 1, {{2.91, 2.91, 19.5}, {3.19, 3.19, 20.2}, {4.75, 4.75, 24.0}, {1.87, 1.87, 19.2}}},
+    {512, 128, 8, 1, 1, {{3.41, 3.41, 14.9}, {3.79, 3.79, 15.3}, {4.62, 4.62, 21.3}, {2.17, 2.17, 16.4}}},
+    {256, 128, 4, 1, 2, {{3.43, 1.76, 12.4}, {3.51, 1.76, 17.5}, {4.04, 2.19, 32.8}, {2.24, 1.19, 13.1}}},
+    {256, 128, 4, 2, 1, {{1.82, 1.82, 11.5}, {2.45, 2.45, 10.3}, {3.81, 3.81, 8.8}, {1.30, 1.30, 10.9}}},
+    {128, 128, 2, 2, 2, {{2.13, 1.26, 7.8}, {2.41, 1.29, 7.9}, {3.13, 1.73, 10.7}, {1.61, 0.98, 7.2}}},
 };
 constexpr int kNumInt8Shapes = (int)(sizeof(kInt8Shapes) / sizeof(kInt8Shapes[0]));
 // Main shapes of a split launch (the first three above) and their tails (the
@@ -85,7 +93,7 @@ apt_config_t base_config(int route) {
   return c;
 }
 
-// Modelled microseconds of shape s with operand format f (0 int8, 1 FP4) and
+// Modelled microseconds of shape s with operand class f (time_class) and
 // `grid` workgroups (0 = one per tile), without the fixed time.  Workgroups
 // run in rounds of cus * per_cu; a last partial round of at most one
 // workgroup per compute unit runs at the alone rate.
@@ -158,7 +166,65 @@ int split_columns(const Int8Shape& s, int M, int N, int cus) {
   return split < N ? split : 0;
 }
 
+// The shipped lookup table (Sec. V-B keeps the search results for common LLM
+// shapes): the configs the best-kernel search module picked on MI355X for the
+// workload shapes with M > 8 (bench.py --search), keyed by the M bucket
+// ceil(log2 M), N, K, p and q.  Smaller M always takes the XOR route.
+struct ShippedEntry {
+  int mlog, N, K, p, q;
+  apt_config_t cfg;
+};
+constexpr ShippedEntry kShipped[] = {
+    { 4,   512,   512, 1, 2, {1, 0, 0, 0, 0, 0, 0, 0, 8, 0, 0, 0, 0, {0, 0, 0}}},  // w1a2_16x512x512
+    {11, 11008,  4096, 4, 4, {3, 256, 128, 128, 4, 1, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w4a4_prefill_2048x11008x4096
+    { 9,  4096, 11008, 1, 1, {4, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w1a1_512x4096x11008
+    { 9,  4096, 11008, 1, 4, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w1a4_512x4096x11008
+    { 9,  4096, 11008, 2, 8, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w2a8_512x4096x11008
+    { 9,  4096, 11008, 3, 3, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w3a3_512x4096x11008
+    { 9,  4096, 11008, 3, 8, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w3a8_512x4096x11008
+    { 9,  4096, 11008, 4, 8, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w4a8_512x4096x11008
+    {10,  4096,  4096, 2, 4, {3, 128, 128, 128, 2, 2, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_q_m1024
+    {10, 11008,  4096, 2, 4, {3, 128, 128, 128, 2, 2, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_gate_m1024
+    {10,  4096, 11008, 2, 4, {3, 128, 128, 128, 2, 2, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_down_m1024
+};
+
+// Approximate matching (Sec. V-B; the paper gives no distance): an entry
+// matches a problem with the same p, q and M bucket when
+// |log2(N / N_e)| + |log2(K / K_e)| <= kMatchRadius; the nearest such entry
+// whose config is valid for the problem wins, and a problem no entry matches
+// takes the model.  The radius admits shapes within about 1.4x of a tabled one
+// in one dimension (a TP shard of a tabled layer, a neighbouring hidden size).
+constexpr double kMatchRadius = 0.5;
+
+int mlog_of(int M) {
+  int l = 0;
+  while ((1 << l) < M) ++l;
+  return l;
+}
+
 }  // namespace
+
+bool shipped_lookup(int M, int N, int K, int p, int q, apt_config_t* out) {
+  const int ml = mlog_of(M);
+  double best = kMatchRadius + 1e-9;
+  const ShippedEntry* hit = nullptr;
+  for (const ShippedEntry& e : kShipped) {
+    if (e.mlog != ml || e.p != p || e.q != q) continue;
+    const double d = std::fabs(std::log2((double)N / e.N)) + std::fabs(std::log2((double)K / e.K));
+    if (d > best) continue;
+    const apt_config_t& c = e.cfg;
+    const bool mfma = c.route == APT_ROUTE_INT8_MFMA || c.route == APT_ROUTE_FP4_MFMA;
+    if (mfma && (!int8_config_ok(c, N) || !int8_sizes_ok(M, N, K, p, q, c))) continue;
+    if (c.route == APT_ROUTE_FP4_MFMA && !fp4_route_ok(K, p, q)) continue;
+    best = d;
+    hit = &e;
+  }
+  if (hit == nullptr) return false;
+  *out = hit->cfg;
+  return true;
+}
+
+int shipped_table_size() { return (int)(sizeof(kShipped) / sizeof(kShipped[0])); }
 
 namespace {
 
@@ -259,6 +325,7 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
 apt_config_t select_config(int M, int N, int K, int p, int q) {
   apt_config_t hit;
   if (table_lookup(M, N, K, p, q, &hit)) return hit;
+  if (M > 8 && shipped_lookup(M, N, K, p, q, &hit)) return hit;
   if (M <= 8) {
     apt_config_t c = base_config(APT_ROUTE_XOR);
     c.mt = 8;
@@ -284,8 +351,9 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
     }
   };
   // int8 operands, then (where they apply) FP4 operands for both sides
-  for (int f = 0; f < (fp4_route_ok(K, p, q) && q <= 2 ? 2 : 1); ++f) {
-    fp4 = f == 1;
+  for (int fi = 0; fi < (fp4_route_ok(K, p, q) && q <= 2 ? 2 : 1); ++fi) {
+    fp4 = fi == 1;
+    const int f = time_class(fp4, p);
     for (int i = 0; i < kNumInt8Shapes; ++i) {
       const Int8Shape& s = kInt8Shapes[i];
       const int round = std::min(cus * s.per_cu, kMaxGrid);

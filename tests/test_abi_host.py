@@ -356,3 +356,23 @@ def test_noalloc_rejects_before_any_launch():
     assert f(1000, 1000, 4096, 4, 4, fake, fake, fake, fake, fake, None, None, None, cfg,
              None) == apt.APT_ERR_WORKSPACE
     assert apt.apt_last_hip_error() == 0
+
+
+def test_shipped_table_configs_and_approximate_match():
+    """The shipped table (searched configs of the workload shapes, Sec. V-B)
+    answers the workload shapes and shapes near them (same p, q and M bucket,
+    N and K within the matching radius); every config it gives is valid for its
+    problem (it has a workspace size)."""
+    import bench
+    for prob in bench.workload_problems():
+        st, c = apt.apt_select_config(prob.M, prob.N, prob.K, prob.p, prob.q)
+        assert st == apt.APT_OK
+        if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA):
+            assert apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, c) > 0
+    prefill = apt.select_config(2048, 11008, 4096, 4, 4)
+    assert (prefill.route, prefill.bm, prefill.bn, prefill.waves_m, prefill.waves_n, prefill.grid) == \
+        (apt.APT_ROUTE_INT8_MFMA, 256, 128, 4, 1, 0)
+    near = apt.select_config(1900, 11000, 4200, 4, 4)
+    assert near.as_dict() == prefill.as_dict()
+    down = apt.select_config(512, 4096, 11008, 3, 3)
+    assert apt.select_config(500, 4000, 11000, 3, 3).as_dict() == down.as_dict()
