@@ -373,6 +373,61 @@ def calibrate(calls: int = 20):
     return {"cus": cus, "timings": out, "model": fits}
 
 
+def format_sweep(calls: int = 20):
+    """The operand formats of the reassembled MFMA route against each other:
+    int8 and FP6 (E2M3) operands on every tile shape, with one workgroup per
+    tile and with one persistent round, on the W3A3 down projection
+    (512x4096x11008) and W3A3 2048x11008x4096 and 1024x4096x4096; HIP events
+    around `calls` back-to-back apt_gemm calls (warm weights, int32 output)."""
+    import numpy as np
+    import torch
+
+    import paper_2508_19087_amd as apt
+    import synth
+    dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
+    shapes = [(256, 256, 4, 2, 1), (512, 128, 8, 1, 1), (256, 128, 4, 1, 2), (256, 128, 4, 2, 1),
+              (128, 128, 2, 2, 2)]
+    probs = [synth.sweep_down(3), synth.random_problem(synth.rng(9), 2048, 11008, 4096, 3, 3),
+             synth.random_problem(synth.rng(10), 1024, 4096, 4096, 3, 3)]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    sp = torch.cuda.current_stream().cuda_stream
+    rows = []
+    for prob in probs:
+        a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
+        w = apt.pack(dev(prob.w_codes), prob.p)
+        c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+        for bm, bn, wm, wn, per_cu in shapes:
+            for grid in (0, cus * per_cu):
+                row = {"problem": "%dx%dx%d W%dA%d" % (prob.M, prob.N, prob.K, prob.p, prob.q),
+                       "shape": "%dx%d/%dx%d g%d" % (bm, bn, wm, wn, grid)}
+                for name, route in (("int8_us", apt.APT_ROUTE_INT8_MFMA), ("fp6_us", apt.APT_ROUTE_FP6_MFMA)):
+                    cfg = apt.apt_config_t.make(route, bm, bn, 128, wm, wn, grid, 3)
+                    wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
+                    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+
+                    def call():
+                        apt.check(apt.apt_gemm(prob.M, prob.N, prob.K, prob.p, prob.q, a.data.data_ptr(),
+                                               w.data.data_ptr(), a.rowsum.data_ptr(), w.rowsum.data_ptr(),
+                                               c32.data_ptr(), None, None, None, cfg, ws.data_ptr(), wsb, sp),
+                                  "apt_gemm")
+                    for _ in range(3):
+                        call()
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    torch.cuda.synchronize()
+                    e0.record()
+                    for _ in range(calls):
+                        call()
+                    e1.record()
+                    torch.cuda.synchronize()
+                    row[name] = round(e0.elapsed_time(e1) * 1e3 / calls, 2)
+                    del ws
+                rows.append(row)
+                log("bench: formats %s %s int8 %.2f fp6 %.2f us" % (row["problem"], row["shape"],
+                                                                     row["int8_us"], row["fp6_us"]))
+        del a, w, c32
+    return rows
+
+
 def graph_of(torch, launch):
     """A HIP graph (torch.cuda.CUDAGraph) of launch(stream_ptr), captured on a
     side stream after one eager warm-up there."""
@@ -1130,6 +1185,8 @@ def main():
     ap.add_argument("--calibrate", action="store_true",
                     help="print the selector model's calibration (pair and fixed times per tile "
                          "shape and operand class) and exit")
+    ap.add_argument("--format-sweep", action="store_true",
+                    help="print int8 against FP6 operands on every tile shape for W3A3 shapes and exit")
     ap.add_argument("--workloads", action="store_true",
                     help="for a rocprofv3 kernel trace: every workload configuration's selected "
                          "apt_gemm, 20 calls each, separated by marker fills; prints the plan")
@@ -1157,6 +1214,9 @@ def main():
         return
     if args.workloads:
         workloads_run()
+        return
+    if args.format_sweep:
+        print(json.dumps(format_sweep(), indent=1), flush=True)
         return
     if args.calibrate:
         print(json.dumps(calibrate(), indent=1), flush=True)

@@ -73,10 +73,12 @@ enum {
   APT_ROUTE_XOR = 1,        /* XOR + popcount on packed words, cross-lane reduction (Sec. III-B, 1-bit XOR form) */
   APT_ROUTE_PM1_MFMA = 2,   /* every (i, j) plane pair as +-1 int8 operands on the int8 matrix cores */
   APT_ROUTE_INT8_MFMA = 3,  /* planes reassembled in LDS into one int8 operand, one int8 MFMA per element pair */
-  APT_ROUTE_FP4_MFMA = 4    /* as APT_ROUTE_INT8_MFMA with the bipolar values as operands of the
+  APT_ROUTE_FP4_MFMA = 4,   /* as APT_ROUTE_INT8_MFMA with the bipolar values as operands of the
                                block-scaled MFMA: FP4 (E2M1) weights, p <= 2, and FP4 (q <= 2) or
                                FP8 E4M3 (q <= 4) activations; K_pad (2^p-1)(2^q-1) < 2^24,
                                K_pad = K rounded up to a multiple of 128 */
+  APT_ROUTE_FP6_MFMA = 5    /* as APT_ROUTE_FP4_MFMA with FP6 (E2M3) weights and activations,
+                               p, q <= 3; K_pad (2^p-1)(2^q-1) < 2^24 */
 };
 
 /* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950

@@ -59,6 +59,9 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
     case APT_ROUTE_FP4_MFMA:
       if (!apt::fp4_route_ok(K, p, q)) return APT_ERR_UNSUPPORTED;
       [[fallthrough]];
+    case APT_ROUTE_FP6_MFMA:
+      if (c.route == APT_ROUTE_FP6_MFMA && !apt::fp6_route_ok(K, p, q)) return APT_ERR_UNSUPPORTED;
+      [[fallthrough]];
     case APT_ROUTE_INT8_MFMA:
       if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
@@ -117,7 +120,7 @@ size_t apt_gemm_workspace_bytes(int M, int N, int K, int p, int q, const apt_con
   const apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
                              ? apt::select_config(M, N, K, p, q)
                              : *cfg;
-  if (c.route != APT_ROUTE_INT8_MFMA && c.route != APT_ROUTE_FP4_MFMA) return 0;
+  if (!apt::mfma_route(c.route)) return 0;
   if (check_config(c, M, N, K, p, q, true) != APT_OK) return 0;
   return apt::int8_workspace_bytes(M, N, K, q, c);
 }
@@ -149,7 +152,7 @@ apt_status_t gemm_check(int M, int N, int K, int p, int q, const void* a_packed,
 }
 
 size_t gemm_workspace_need(int M, int N, int K, int q, const apt_config_t& c) {
-  if (c.route != APT_ROUTE_INT8_MFMA && c.route != APT_ROUTE_FP4_MFMA) return 0;
+  if (!mfma_route(c.route)) return 0;
   return int8_workspace_bytes(M, N, K, q, c);
 }
 
@@ -180,7 +183,8 @@ apt_status_t gemm_launch(int M, int N, int K, int p, int q, const void* a_packed
   switch (c.route) {
     case APT_ROUTE_XOR: return hip_status(launch_gemm_xor(g, c, s));
     case APT_ROUTE_INT8_MFMA:
-    case APT_ROUTE_FP4_MFMA: return hip_status(launch_gemm_int8(g, c, workspace, s));
+    case APT_ROUTE_FP4_MFMA:
+    case APT_ROUTE_FP6_MFMA: return hip_status(launch_gemm_int8(g, c, workspace, s));
     case APT_ROUTE_PM1_MFMA: return hip_status(launch_gemm_pm1(g, c, s));
   }
   return APT_ERR_INVALID_ARG;
@@ -235,7 +239,7 @@ size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q) {
   const int n = apt::candidate_configs(M, N, K, p, q, cand, apt::kMaxCandidates);
   size_t most = 0;
   for (int i = 0; i < n; ++i)
-    if ((cand[i].route == APT_ROUTE_INT8_MFMA || cand[i].route == APT_ROUTE_FP4_MFMA) &&
+    if (apt::mfma_route(cand[i].route) &&
         apt::int8_config_ok(cand[i], N))
       most = std::max(most, apt::int8_workspace_bytes(M, N, K, q, cand[i]));
   return most;

@@ -49,6 +49,16 @@ inline bool fp4_route_ok(int K, int p, int q) {
   return p <= 2 && q <= 4 &&
          (int64_t)num_chunks(K) * kChunk * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
 }
+// The FP6 MFMA route applies to (p, q) over K: E2M3 holds bipolar values of
+// at most 3 bits, and the fp32 sums stay exact as for the FP4 route.
+inline bool fp6_route_ok(int K, int p, int q) {
+  return p <= 3 && q <= 3 &&
+         (int64_t)num_chunks(K) * kChunk * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
+}
+// Routes that run the reassembled MFMA kernels (operand formats int8, FP4, FP6).
+inline bool mfma_route(int route) {
+  return route == APT_ROUTE_INT8_MFMA || route == APT_ROUTE_FP4_MFMA || route == APT_ROUTE_FP6_MFMA;
+}
 inline int padded_rows(int R) { return (R + kRowGroup - 1) / kRowGroup * kRowGroup; }
 
 // Word offset of the 4 words of plane i, chunk c, row r.

@@ -68,18 +68,26 @@ constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes
 // holds elements 16 h .. 16 h + 15 of the k-step's first 32 in bytes 0..15
 // and of its second 32 in bytes 16..31, which puts nibble n of word 2 ks + x
 // (n = 16 h + j) against byte 16 x + j of lane half h.
+//   F = 3: FP6 (E2M3) weights and activations of at most 3 bits, the same
+//          MFMA with both operands in the six-bit format (24 operand bytes per
+//          lane and k-step, 64 elements of k per MFMA).  Each lane half's 24
+//          bytes sit in a 32-byte slot of the LDS row and in two 16-byte
+//          fragment vectors (the second half-used).
 template <int F>
 struct Fmt {
   static constexpr int kStepK = F ? 64 : 32;                   // k per MFMA
   static constexpr int kSteps = kChunk / kStepK;               // k-steps per chunk
-  static constexpr int kRowBytes = kSteps * kStepBytes + 16;   // padded LDS row of a chunk
-  static constexpr int kAVecs = F == 2 ? 2 : 1;                // 16-byte activation vectors per lane and k-step
+  static constexpr int kStepRowBytes = F == 3 ? 2 * kStepBytes : kStepBytes;  // LDS row bytes per k-step
+  static constexpr int kHalfBytes = kStepRowBytes / 2;         // per lane half
+  static constexpr int kRowBytes = kSteps * kStepRowBytes + 16;  // padded LDS row of a chunk
+  static constexpr int kAVecs = F >= 2 ? 2 : 1;                // 16-byte activation vectors per lane and k-step
 };
 constexpr int kStages = 3;                      // weight LDS ring depth
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 typedef uint32_t v2u __attribute__((ext_vector_type(2)));
@@ -180,7 +188,15 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
     for (int j = 0; j < Q; ++j) pw[j] = 0u;
   }
   const int mb = row / 32, l = row % 32;
-  if (F == 2) {
+  if (F == 3) {
+    // word w -> k-step w / 2, lane half w mod 2; vector 0 holds operand dwords
+    // 0..3, vector 1 dwords 4..5
+    uint32_t o[6] = {0u, 0u, 0u, 0u, 0u, 0u};
+    if (chunk < nchunks) fp6_word<(Q <= 3 ? Q : 3)>(pw, o);
+    v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w / 2) * 2 * kFragVecs;
+    f[(w % 2) * 32 + l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    f[kFragVecs + (w % 2) * 32 + l] = v4i{(int)o[4], (int)o[5], 0, 0};
+  } else if (F == 2) {
     // word w -> k-step w / 2, vector w mod 2; byte j of lane half h is element
     // 4 (j mod 8) + 2 h + j / 8 of the word
     uint32_t o[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
@@ -275,6 +291,18 @@ struct Stage {
     const int r = item % ROWS;
     const int sub = item / ROWS;
     uint32_t o[4];
+    if (F == 3) {
+      if (h != 0) return;
+      uint32_t pw[B], o6[6];
+#pragma unroll
+      for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
+      fp6_word<(B <= 3 ? B : 3)>(pw, o6);
+      const int wc = sub * kWpi + w;  // word of the chunk -> k-step wc / 2, lane half wc mod 2
+      uint8_t* d = lds_tile + r * kRowBytes + (wc / 2) * Fmt<F>::kStepRowBytes + (wc % 2) * Fmt<F>::kHalfBytes;
+      *reinterpret_cast<uint4*>(d) = make_uint4(o6[0], o6[1], o6[2], o6[3]);
+      *reinterpret_cast<uint2*>(d + 16) = make_uint2(o6[4], o6[5]);
+      return;
+    }
     if (F) {
       if (h != 0) return;
       uint32_t pw[B];
@@ -420,7 +448,8 @@ struct Stream {
 // call it; `lds` is the dynamic LDS of the launch).
 template <int P, int F, int BM, int BN, int WM, int WN, int SPLIT>
 __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* lds, int w, int G) {
-  static_assert(F == 0 || P <= 2, "FP4 operands hold weights of at most 2 bits");
+  static_assert(F == 0 || P <= (F == 3 ? 3 : 2),
+                "FP4 operands hold weights of at most 2 bits, FP6 operands at most 3");
   constexpr int kSteps = Fmt<F>::kSteps;
   constexpr int kAVecs = Fmt<F>::kAVecs;
   constexpr int kRowBytes = Fmt<F>::kRowBytes;
@@ -515,13 +544,17 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   v4i afr[kSteps * kAVecs][FM];  // vector x of k-step ks at ks * kAVecs + x
 
   const int lrow = lane % 32;
-  const int lk = (lane / 32) * 16;
+  const int lk = (lane / 32) * Fmt<F>::kHalfBytes;
   const int w_lane = (wn * WTN + lrow) * kRowBytes + lk;
   v4i wf[2][FN];
-  auto read_wf = [&](const uint8_t* stage, int ks, v4i* dst) __attribute__((always_inline)) {
+  v2i wf6[2][F == 3 ? FN : 1];  // FP6: operand dwords 4..5
+  auto read_wf = [&](const uint8_t* stage, int ks, int sl) __attribute__((always_inline)) {
 #pragma unroll
-    for (int b = 0; b < FN; ++b)
-      dst[b] = *reinterpret_cast<const v4i*>(stage + w_lane + b * 32 * kRowBytes + ks * kStepBytes);
+    for (int b = 0; b < FN; ++b) {
+      const uint8_t* src = stage + w_lane + b * 32 * kRowBytes + ks * Fmt<F>::kStepRowBytes;
+      wf[sl][b] = *reinterpret_cast<const v4i*>(src);
+      if constexpr (F == 3) wf6[sl][b] = *reinterpret_cast<const v2i*>(src + 16);
+    }
   };
 
   // One pipeline step: the MFMAs of one chunk from stage `cst`.  During
@@ -539,9 +572,9 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     for (int ks = 0; ks < kSteps; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
       if (ks + 1 < kSteps)
-        read_wf(cst, ks + 1, wf[nxt]);
+        read_wf(cst, ks + 1, nxt);
       else
-        read_wf(nst, 0, wf[nxt]);
+        read_wf(nst, 0, nxt);
 #pragma unroll
       for (int hu = 0; hu < kHalves; ++hu)
         if (hu * kSteps / kHalves == ks) rw.store_half(sst, tid, hu / 2, hu % 2, mid);
@@ -549,7 +582,16 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
       for (int b = 0; b < FN; ++b)
 #pragma unroll
         for (int a = 0; a < FM; ++a)
-          if (F == 2) {
+          if constexpr (F == 3) {
+            // E2M3 weights and activations (format code 2), unit E8M0 scales (127)
+            const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3],
+                            wf6[cur][b][0], wf6[cur][b][1], 0, 0};
+            const v4i a0 = afr[2 * ks][a], a1 = afr[2 * ks + 1][a];
+            const v8i ab = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], 0, 0};
+            acc[b][a] = __builtin_bit_cast(
+                v16i, __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                          wa, ab, __builtin_bit_cast(v16f, acc[b][a]), 2, 2, 0, 127, 0, 127));
+          } else if constexpr (F == 2) {
             // E2M1 weights (format code 4) x E4M3 activations (code 0), unit E8M0 scales (127)
             const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3], 0, 0, 0, 0};
             const v4i a0 = afr[2 * ks][a], a1 = afr[2 * ks + 1][a];
@@ -557,7 +599,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
             acc[b][a] = __builtin_bit_cast(
                 v16i, __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                           wa, ab, __builtin_bit_cast(v16f, acc[b][a]), 4, 0, 0, 127, 0, 127));
-          } else if (F) {
+          } else if constexpr (F == 1) {
             // E2M1 x E2M1 (format code 4 for both), unit E8M0 scales (127)
             const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3], 0, 0, 0, 0};
             const v8i ab = {afr[ks][a][0], afr[ks][a][1], afr[ks][a][2], afr[ks][a][3], 0, 0, 0, 0};
@@ -847,7 +889,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
 #pragma unroll
       for (int x = 0; x < kAVecs; ++x) afr[ks * kAVecs + x][a] = load_a(cp.m0, 2 * cp.pair, ks, a, x);
   __syncthreads();
-  read_wf(lds, 0, wf[0]);
+  read_wf(lds, 0, 0);
 
   int s0 = 0;  // stage of the current pair's first chunk
   while (cp.tile < prm.tiles) {

@@ -15,6 +15,9 @@ hipError_t launch_for_p(int fmt, int shape, const Int8Params& prm, int grid, hip
     if (fmt == 1) return launch_p_shape<P, 1>(shape, prm, grid, stream);
     if (fmt == 2) return launch_p_shape<P, 2>(shape, prm, grid, stream);
   }
+  if constexpr (P <= 3) {
+    if (fmt == 3) return launch_p_shape<P, 3>(shape, prm, grid, stream);
+  }
   return hipErrorInvalidValue;
 }
 
@@ -25,6 +28,9 @@ hipError_t launch_pair_for_p(int fmt, int sa, const Int8Params& pa, int ga, int 
   if constexpr (P <= 2) {
     if (fmt == 1) return launch_p_pair<P, 1>(sa, pa, ga, sb, pb, gb, stream);
     if (fmt == 2) return launch_p_pair<P, 2>(sa, pa, ga, sb, pb, gb, stream);
+  }
+  if constexpr (P <= 3) {
+    if (fmt == 3) return launch_p_pair<P, 3>(sa, pa, ga, sb, pb, gb, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -54,6 +60,11 @@ hipError_t launch_expand_for_q(int fmt, const uint32_t* a_packed, int M, int nch
   if constexpr (Q >= 3 && Q <= 4) {
     if (fmt == 2)
       return launch_expand<Q, 2>(a_packed, M, nchunks, nsteps, mblocks, out, counters, ncounters,
+                                 stream);
+  }
+  if constexpr (Q <= 3) {
+    if (fmt == 3)
+      return launch_expand<Q, 3>(a_packed, M, nchunks, nsteps, mblocks, out, counters, ncounters,
                                  stream);
   }
   return hipErrorInvalidValue;

@@ -138,6 +138,59 @@ __device__ __forceinline__ void fp4_word(const uint32_t* pw, uint32_t out[4]) {
   out[3] = bsel(m2, o01 >> 2, o23);  // elements 4f + 3
 }
 
+// FP6 operand fields (OCP E2M3: sign bit 5, exponent bits 4..3 with bias 1,
+// mantissa bits 2..0) of the 32 elements of plane words pw[0..B-1], B <= 3.
+// Every bipolar value of up to 3 bits is exact in E2M3: +-1 = e 01 m 000,
+// +-3 = e 10 m 100, +-5 = e 11 m 010, +-7 = e 11 m 110.  The words u are
+// rebuilt as bytes (the int8 tree), mapped to their E2M3 codes with one byte
+// permute per dword (the 8-entry table of v = 2u - (2^B - 1)), and the 32
+// six-bit codes are packed without gaps into out[0..5] (a 192-bit operand):
+// field s (bits 6s .. 6s+5) holds element 8 (s mod 4) + s / 4.  Weights and
+// activations use the same order, and a dot product is unchanged by a common
+// permutation of k, so the order never shows in the result.
+template <int B>
+__host__ __device__ constexpr uint32_t e2m3_of_word(uint32_t u) {
+  // |v| = 1, 3, 5, 7 -> 8, 20, 26, 30; sign bit 32
+  const int v = 2 * (int)u - ((1 << B) - 1);
+  const int a = v < 0 ? -v : v;
+  const uint32_t mag = a == 1 ? 8u : a == 3 ? 20u : a == 5 ? 26u : 30u;
+  return v < 0 ? mag | 32u : mag;
+}
+
+template <int B>
+__host__ __device__ constexpr uint32_t e2m3_table(int half) {
+  // bytes 4 half .. 4 half + 3 of the table indexed by u (entries past 2^B unused)
+  uint32_t t = 0u;
+  for (int j = 0; j < 4; ++j) {
+    const int u = 4 * half + j;
+    t |= (u < (1 << B) ? e2m3_of_word<B>((uint32_t)u) : 0u) << (8 * j);
+  }
+  return t;
+}
+
+template <int B>
+__device__ __forceinline__ void fp6_word(const uint32_t* pw, uint32_t out[6]) {
+  static_assert(B >= 1 && B <= 3, "E2M3 holds bipolar values of up to 3 bits");
+  uint32_t by[8];
+  reassemble_word<B>(pw, by);  // byte j of by[t]: u of element 8 j + t
+  constexpr uint32_t lo = e2m3_table<B>(0), hi = e2m3_table<B>(1);
+  uint32_t y[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const uint32_t c = __builtin_amdgcn_perm(hi, lo, by[t]);  // byte j <- table[u_j]
+    // four 6-bit codes (one per byte) -> 24 contiguous bits
+    const uint32_t c01 = bsel(0x3Fu, c, c >> 2);      // bits 0..11: codes 0, 1
+    const uint32_t c012 = bsel(0xFFFu, c01, c >> 4);  // bits 0..17: codes 0..2
+    y[t] = bsel(0x3FFFFu, c012, c >> 6);               // bits 0..23: codes 0..3
+  }
+  out[0] = y[0] | (y[1] << 24);
+  out[1] = (y[1] >> 8) | (y[2] << 16);
+  out[2] = (y[2] >> 16) | (y[3] << 8);
+  out[3] = y[4] | (y[5] << 24);
+  out[4] = (y[5] >> 8) | (y[6] << 16);
+  out[5] = (y[6] >> 16) | (y[7] << 8);
+}
+
 // Operand offset of the reassembled byte y: bipolar value v = 2 y + c.
 //   B <= 7: y = u,        v = 2u - (2^B - 1)  ->  c = 1 - 2^B
 //   B == 8: y = u - 128,  v = 2u - 255        ->  c = 1

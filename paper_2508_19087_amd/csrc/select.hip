@@ -213,9 +213,9 @@ bool shipped_lookup(int M, int N, int K, int p, int q, apt_config_t* out) {
     const double d = std::fabs(std::log2((double)N / e.N)) + std::fabs(std::log2((double)K / e.K));
     if (d > best) continue;
     const apt_config_t& c = e.cfg;
-    const bool mfma = c.route == APT_ROUTE_INT8_MFMA || c.route == APT_ROUTE_FP4_MFMA;
-    if (mfma && (!int8_config_ok(c, N) || !int8_sizes_ok(M, N, K, p, q, c))) continue;
+    if (mfma_route(c.route) && (!int8_config_ok(c, N) || !int8_sizes_ok(M, N, K, p, q, c))) continue;
     if (c.route == APT_ROUTE_FP4_MFMA && !fp4_route_ok(K, p, q)) continue;
+    if (c.route == APT_ROUTE_FP6_MFMA && !fp6_route_ok(K, p, q)) continue;
     best = d;
     hit = &e;
   }
@@ -310,12 +310,15 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
       add(c);
     }
   }
-  // the same tile configs with FP4 operands where they apply
-  if (fp4_route_ok(K, p, q)) {
-    const int end = n;
+  // the same tile configs with FP4 operands where they apply, and with FP6
+  // operands where those apply and FP4 does not (p or q = 3)
+  const int end = n;
+  const int route = fp4_route_ok(K, p, q) ? APT_ROUTE_FP4_MFMA
+                    : fp6_route_ok(K, p, q) ? APT_ROUTE_FP6_MFMA : 0;
+  if (route != 0) {
     for (int j = n_int8_single - 2 * kNumInt8Shapes; j < end; ++j) {
       apt_config_t c = out[j];
-      c.route = APT_ROUTE_FP4_MFMA;
+      c.route = route;
       add(c);
     }
   }

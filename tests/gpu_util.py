@@ -34,15 +34,18 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
                                               split, tbm, tbn, tg)
                     out.append(("int8_%dx%d_w%dx%d_tail%dx%d@%d_g%d" % (bm, bn, wm, wn, tbm, tbn, split,
                                                                         tg), c))
-    if p <= 2 and q <= 4:  # the same tile configs with FP4 weights (FP4 or FP8 activations)
-        fp4 = []
+    floats = []
+    for route, tag, ok in ((apt.APT_ROUTE_FP4_MFMA, "fp4", p <= 2 and q <= 4),
+                           (apt.APT_ROUTE_FP6_MFMA, "fp6", p <= 3 and q <= 3)):
+        if not ok:  # the same tile configs with FP4 weights (FP4 or FP8 activations) / FP6 operands
+            continue
         for name, c in out:
             if c.route == apt.APT_ROUTE_INT8_MFMA:
-                f = apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, c.bm, c.bn, c.bk, c.waves_m,
-                                          c.waves_n, c.grid, c.lds_stages, c.mt, c.split_n, c.tail_bm,
-                                          c.tail_bn, c.tail_grid)
-                fp4.append(("fp4" + name[4:], f))
-        out += fp4
+                f = apt.apt_config_t.make(route, c.bm, c.bn, c.bk, c.waves_m, c.waves_n, c.grid,
+                                          c.lds_stages, c.mt, c.split_n, c.tail_bm, c.tail_bn,
+                                          c.tail_grid)
+                floats.append((tag + name[4:], f))
+    out += floats
     if p <= 7 and q <= 7:
         out.append(("pm1", apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)))
     return out

@@ -62,7 +62,8 @@ def _int8_workspace(M, N, K, c, q=4):
     256 bytes."""
     up = lambda x: (x + 255) // 256 * 256
     nce = ((K + 127) // 128 + 1) // 2 * 2
-    # int8 or FP8 bytes, or FP4 nibbles (half as many bytes: FP4 route with q <= 2)
+    # int8 or FP8 bytes, FP6 fields in 32 bytes per 32 elements, or FP4 nibbles (half as
+    # many bytes: FP4 route with q <= 2)
     nib = c.route == apt.APT_ROUTE_FP4_MFMA and q <= 2
     ws = up((M + 31) // 32 * 32 * nce * (64 if nib else 128))
     launches = [(c.bm, c.bn, N, c.grid)]
@@ -98,7 +99,7 @@ def test_select_config_valid(shape):
     st, c = apt.apt_select_config(*shape)
     assert st == apt.APT_OK
     assert c.route in (apt.APT_ROUTE_XOR, apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_PM1_MFMA,
-                       apt.APT_ROUTE_FP4_MFMA)
+                       apt.APT_ROUTE_FP4_MFMA, apt.APT_ROUTE_FP6_MFMA)
     if c.route == apt.APT_ROUTE_FP4_MFMA:
         M, N, K, p, q = shape
         k_pad = (K + 127) // 128 * 128
@@ -107,7 +108,7 @@ def test_select_config_valid(shape):
         assert c.route == apt.APT_ROUTE_XOR
     M, N, K, p, q = shape
     ws = apt.apt_gemm_workspace_bytes(*shape, c)
-    if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA):
+    if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA, apt.APT_ROUTE_FP6_MFMA):
         assert ws == _int8_workspace(M, N, K, c, q)
     else:
         assert ws == 0
@@ -199,6 +200,16 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
      apt.APT_ERR_WORKSPACE),
     (dict(M=64, p=1, q=2, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 96, 128, 128, 2, 2)),
      apt.APT_ERR_INVALID_ARG),
+    # FP6 route: weights and activations of at most 3 bits, fp32 sums below 2^24
+    (dict(p=4, q=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(p=3, q=4, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(K=(1 << 24) // 49 // 128 * 128 + 1, p=3, q=3,
+          cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(M=64, p=3, q=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_WORKSPACE),
     # packed weights past 4 GiB do not fit the int8 kernels' 32-bit offsets
     (dict(M=64, N=1 << 20, K=1 << 16, p=1, q=1,
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
@@ -376,3 +387,15 @@ def test_shipped_table_configs_and_approximate_match():
     assert near.as_dict() == prefill.as_dict()
     down = apt.select_config(512, 4096, 11008, 3, 3)
     assert apt.select_config(500, 4000, 11000, 3, 3).as_dict() == down.as_dict()
+
+
+def test_fp6_workspace_and_bound():
+    """FP6 activations take 32 bytes of fragment per 32 elements (as int8), and the
+    route admits W3A3 up to K_pad * 49 < 2^24."""
+    f6 = apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)
+    i8 = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)
+    assert apt.apt_gemm_workspace_bytes(100, 300, 1000, 3, 3, f6) == \
+        apt.apt_gemm_workspace_bytes(100, 300, 1000, 3, 3, i8) > 0
+    k_ok = ((1 << 24) - 1) // 49 // 128 * 128
+    assert apt.apt_gemm_workspace_bytes(64, 64, k_ok, 3, 3, f6) > 0
+    assert apt.apt_gemm_workspace_bytes(64, 64, k_ok + 128, 3, 3, f6) == 0

@@ -74,6 +74,32 @@ def test_fp4_exact_at_its_bound(q):
             assert_int32_equal(got, want, "%s K=%d" % (name, K))
 
 
+def test_fp6_exact_at_its_bound():
+    """The FP6 route sums in fp32 and takes W3A3 while K_pad * 49 < 2^24 (the padding
+    products count too).  At the largest such K_pad with every product +49 the running
+    sum climbs to within one product of 2^24; rows with mixed signs, uniform codes and
+    a K whose last chunk is padded go through every FP6 config."""
+    p = q = 3
+    k_pad = ((1 << 24) - 1) // 49 // 128 * 128
+    fp6 = [(n, c) for n, c in forced_configs(p, q, 10, k_pad) if c.route == apt.APT_ROUTE_FP6_MFMA]
+    assert fp6
+    for K in (k_pad, k_pad - 57):
+        g = synth.rng(2600, K)
+        M, N = 3, 10
+        a = np.full((M, K), 3, np.int8)   # code 3: value +7
+        w = np.full((N, K), 3, np.int8)
+        w[1::2] = -4                      # code -4: value -7
+        a[2] = synth.uniform_codes(g, 1, K, q)[0]
+        w[2] = synth.uniform_codes(g, 1, K, p)[0]
+        prob = synth.Problem("fp6 bound", M, N, K, p, q, w, a)
+        want = oracle_full(prob)
+        assert want[0, 0] == 49 * K and want[0, 1] == -49 * K
+        packed = pack_problem(prob)
+        for name, cfg in fp6:
+            got, _ = run(prob, cfg=cfg, packed=packed)
+            assert_int32_equal(got, want, "%s K=%d" % (name, K))
+
+
 def test_extreme_values_all_ones_and_zeros():
     """Worst-case magnitudes: all-ones / all-zeros bipolar words at p = q = 8."""
     for M, N, K in [(3, 5, 1000), (70, 80, 4100)]:

@@ -203,3 +203,43 @@ def test_fp32_sums_exact_with_fp8_activations():
     assert float(np.cumsum(prod, dtype=np.float32)[-1]) == 45.0 * k_pad
     over = np.full((1 << 24) // 45 + 2, 45.0, np.float32)
     assert float(np.cumsum(over, dtype=np.float32)[-1]) != 45.0 * over.size
+
+
+# ---- FP6 (E2M3) operands of the FP6 route (p, q <= 3) ----------------------------
+
+def e2m3_value(code: int) -> float:
+    """OCP E2M3 decoding: sign bit 5, exponent bits 4..3 (bias 1), mantissa
+    bits 2..0; exponent 0 is subnormal (mantissa / 8)."""
+    s = -1.0 if code & 32 else 1.0
+    e = (code >> 3) & 3
+    m = code & 7
+    return s * (m / 8 if e == 0 else 2.0 ** (e - 1) * (1.0 + m / 8))
+
+
+def test_e2m3_codes_of_bipolar_values():
+    """Every bipolar value of up to 3 bits (odd, |v| <= 7) is exact in E2M3 with
+    exactly one code (the table the FP6 route maps words through), and 9, the
+    first odd value past 3 bits, is not an E2M3 value."""
+    table = {}
+    for c in range(64):
+        table.setdefault(e2m3_value(c), []).append(c)
+    for b in range(1, 4):
+        for u in range(1 << b):
+            v = int(ref.decode(np.array([u], np.uint8), b)[0])
+            assert v == 2 * u - ((1 << b) - 1)
+            codes = table[float(v)]
+            assert len(codes) == 1
+            # sign bit set exactly for negative values; exponent 1..3 (normal numbers)
+            assert (codes[0] >> 5) == (1 if v < 0 else 0) and 1 <= (codes[0] >> 3) & 3 <= 3
+    assert 9.0 not in table and -9.0 not in table
+
+
+def test_fp32_sums_exact_with_fp6_operands():
+    """W3A3 through the FP6 route: products up to 7 * 7 = 49; with
+    K_pad * 49 < 2^24 every fp32 partial sum is an exact integer, and just past
+    the bound an fp32 running sum loses a unit."""
+    k_pad = ((1 << 24) - 1) // 49 // 128 * 128
+    prod = np.full(k_pad, 49.0, np.float32)
+    assert float(np.cumsum(prod, dtype=np.float32)[-1]) == 49.0 * k_pad
+    over = np.full((1 << 24) // 49 + 2, 49.0, np.float32)
+    assert float(np.cumsum(over, dtype=np.float32)[-1]) != 49.0 * over.size
