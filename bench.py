@@ -428,6 +428,41 @@ def format_sweep(calls: int = 20):
     return rows
 
 
+MFMA_ISSUE_MODES = [
+    (0, "16 MFMAs per k-step, registers only (one wave per SIMD)"),
+    (1, "+ 4 LDS reads of the next k-step's A fragments"),
+    (2, "+ one workgroup barrier per chunk of 4 k-steps"),
+    (3, "+ 4 buffer loads x 16 B per lane per k-step (B fragments, a chunk ahead)"),
+    (4, "mode 2 + 4 buffer loads x 4 B per lane per k-step"),
+    (5, "mode 2 + 2 buffer loads x 16 B per lane per k-step"),
+    (6, "mode 2 + 4 x 16 B loads per k-step straight into LDS, read back a k-step ahead"),
+    (7, "mode 3's per-SIMD pattern on two waves per SIMD (8 MFMAs + 2 loads per wave and k-step)"),
+]
+
+
+def mfma_issue(blocks: int = 256, chunks: int = 4000):
+    """The MFMA-issue probe (probes/mfma_issue.hip, libapt_probe.so): cycles
+    per v_mfma_i32_32x32x32_i8 per SIMD for each part of the GEMM loop's
+    instruction pattern, with the shader clock read from s_memtime against
+    s_memrealtime."""
+    import ctypes
+
+    import torch  # noqa: F401  (the HIP runtime torch loaded serves the probe library too)
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2508_19087_amd", "libapt_probe.so"))
+    lib.apt_probe_mfma_issue.argtypes = [ctypes.c_int] * 3 + [ctypes.POINTER(ctypes.c_double)]
+    lib.apt_probe_mfma_issue.restype = ctypes.c_int
+    rows = []
+    for mode, what in MFMA_ISSUE_MODES:
+        res = (ctypes.c_double * 3)()
+        rc = lib.apt_probe_mfma_issue(mode, blocks, chunks, res)
+        if rc != 0:
+            raise RuntimeError("mfma issue probe mode %d failed at step %d" % (mode, rc))
+        rows.append({"mode": mode, "pattern": what, "cycles_per_mfma": round(res[0], 1),
+                     "clock_GHz": round(res[1], 3), "us_per_chunk": round(res[2], 3)})
+        log("bench: mfma issue mode %d: %.1f cycles per MFMA at %.2f GHz" % (mode, res[0], res[1]))
+    return rows
+
+
 def graph_of(torch, launch):
     """A HIP graph (torch.cuda.CUDAGraph) of launch(stream_ptr), captured on a
     side stream after one eager warm-up there."""
@@ -1185,6 +1220,9 @@ def main():
     ap.add_argument("--calibrate", action="store_true",
                     help="print the selector model's calibration (pair and fixed times per tile "
                          "shape and operand class) and exit")
+    ap.add_argument("--mfma-issue", action="store_true",
+                    help="print the MFMA-issue probe's cycles per MFMA for each part of the GEMM "
+                         "loop's instruction pattern and exit")
     ap.add_argument("--format-sweep", action="store_true",
                     help="print int8 against FP6 operands on every tile shape for W3A3 shapes and exit")
     ap.add_argument("--workloads", action="store_true",
@@ -1214,6 +1252,9 @@ def main():
         return
     if args.workloads:
         workloads_run()
+        return
+    if args.mfma_issue:
+        print(json.dumps(mfma_issue(), indent=1), flush=True)
         return
     if args.format_sweep:
         print(json.dumps(format_sweep(), indent=1), flush=True)

@@ -3,7 +3,9 @@
 Each source in csrc/ is compiled to an object with hipcc in parallel, then the
 objects are linked into paper_2508_19087_amd/libapt.so.  A source named
 *_inst.hip instantiates kernels for one weight bit width and is compiled once
-per width with -DAPT_INST_P=1..8.
+per width with -DAPT_INST_P=1..8.  The measurement probes in probes/ (not part
+of the library) are linked into a library of their own, libapt_probe.so, which
+only bench.py loads.
 """
 from __future__ import annotations
 
@@ -15,6 +17,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
+PROBES = os.path.join(HERE, "probes")
+PROBE_LIB = os.path.join(HERE, "libapt_probe.so")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libapt.so")
 ARCH = "gfx950"
@@ -27,13 +31,13 @@ CFLAGS = [
 ]
 
 
-def units():
+def units(directory=CSRC):
     """(source, extra flags, object name) of every compilation unit."""
     out = []
-    for f in sorted(os.listdir(CSRC)):
+    for f in sorted(os.listdir(directory)):
         if not f.endswith(".hip"):
             continue
-        src = os.path.join(CSRC, f)
+        src = os.path.join(directory, f)
         if f.endswith("_inst.hip"):
             for p in range(1, 9):
                 out.append((src, ["-DAPT_INST_P=%d" % p], f[:-4] + "_p%d.o" % p))
@@ -52,29 +56,37 @@ def _compile(unit) -> str:
     return obj
 
 
-def build(jobs: int | None = None, verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    todo = units()
-    jobs = jobs or min(len(todo), max(1, min(16, os.cpu_count() or 1)))
-    # longest units first
-    todo.sort(key=lambda u: -os.path.getsize(u[0]) - (10 ** 6 if u[1] else 0))
-    with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(_compile, todo))
-    tmp = LIB + ".tmp%d" % os.getpid()
+def _link(objs, lib):
+    tmp = lib + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC"] + objs + ["-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (r.stdout, r.stderr))
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(jobs: int | None = None, verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    todo = units()
+    probes = [(src, extra, "probe_" + name) for src, extra, name in units(PROBES)]
+    jobs = jobs or min(len(todo), max(1, min(16, os.cpu_count() or 1)))
+    # longest units first
+    todo.sort(key=lambda u: -os.path.getsize(u[0]) - (10 ** 6 if u[1] else 0))
+    with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(_compile, todo + probes))
+    _link(objs[:len(todo)], LIB)
+    if probes:
+        _link(objs[len(todo):], PROBE_LIB)
     if verbose:
-        print("built", LIB)
+        print("built", LIB, "and", PROBE_LIB if probes else "")
     return LIB
 
 
 def clean():
     shutil.rmtree(BUILD, ignore_errors=True)
-    if os.path.exists(LIB):
-        os.remove(LIB)
+    for lib in (LIB, PROBE_LIB):
+        if os.path.exists(lib):
+            os.remove(lib)
 
 
 if __name__ == "__main__":
