@@ -62,6 +62,13 @@ class Workload:
         self.apt, self.torch, self.np = apt, torch, np
         self.stream = torch.cuda.current_stream()
         self.sp = self.stream.cuda_stream
+        # The decode GEMMs and the prefill GEMM are independent problems (other
+        # tokens, other sequences), so a step issues the decode chain on a second
+        # stream of default priority, where its kernels run beside the prefill
+        # GEMM on the compute units its last partial round of tiles leaves idle.
+        self.side = torch.cuda.Stream()
+        self.side_sp = self.side.cuda_stream
+        self.overlap = True
         self.dec = [synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]
         self.pre = synth.w4a4_prefill()
         dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
@@ -85,11 +92,12 @@ class Workload:
         self.ops = sum(it["prob"].ops for it in self.items)
         torch.cuda.synchronize()
 
-    def pack_act(self, it):
+    def pack_act(self, it, sp=None):
         p = it["prob"]
+        sp = sp if sp is not None else self.sp
         st = self.apt.apt_quantize_pack_activations(it["a_codes"].data_ptr(), p.M, p.K, p.q,
                                                     it["a_buf"].data_ptr(), it["a_rs"].data_ptr(),
-                                                    self.sp)
+                                                    sp)
         self.apt.check(st, "apt_quantize_pack_activations")
 
     def gemm(self, it, w=None, sp=None):
@@ -106,9 +114,15 @@ class Workload:
         self.apt.check(st, "apt_gemm")
 
     def step(self):
-        for it in self.items:
-            self.pack_act(it)
-            self.gemm(it)
+        """One pass of the path: each problem's activations packed, then its GEMM.
+        With `overlap`, the two decode problems run on the side stream and the
+        prefill on the main one; a device-wide synchronize closes the step."""
+        sp = self.side_sp if self.overlap else self.sp
+        for it in self.items[:2]:
+            self.pack_act(it, sp)
+            self.gemm(it, sp=sp)
+        self.pack_act(self.items[2])
+        self.gemm(self.items[2])
 
 
 def prefill_call_time(wl, calls: int) -> float:
@@ -425,6 +439,44 @@ def format_sweep(calls: int = 20):
                 log("bench: formats %s %s int8 %.2f fp6 %.2f us" % (row["problem"], row["shape"],
                                                                      row["int8_us"], row["fp6_us"]))
         del a, w, c32
+    return rows
+
+
+def vendor_int8(calls: int = 50):
+    """Context for the prefill GEMM: the vendor library's dense int8 GEMM
+    (torch._int_mm, int32 result) on M=2048, N=11008, K=4096 with operands
+    already int8 in memory (no bit-planes, no reassembly), the weight as an
+    [N][K] row-major matrix (passed transposed) and as a [K][N] one; HIP events
+    around `calls` back-to-back calls after 3 warm-up calls."""
+    import torch
+    g = torch.Generator().manual_seed(12)
+    M, N, K = 2048, 11008, 4096
+    a = torch.randint(-8, 8, (M, K), dtype=torch.int8, generator=g).cuda()
+    w = torch.randint(-8, 8, (N, K), dtype=torch.int8, generator=g).cuda()
+    wkn = w.t().contiguous()
+    rows = []
+    for name, b in (("weight [N][K] (transposed view)", w.t()), ("weight [K][N]", wkn)):
+        out = torch._int_mm(a, b)
+        ref = torch._int_mm(a, wkn) if name != "weight [K][N]" else out
+        assert torch.equal(out, ref)
+        for _ in range(3):
+            torch._int_mm(a, b)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(calls):
+            torch._int_mm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / calls
+        rows.append({"gemm": "torch._int_mm %dx%dx%d int8, %s" % (M, N, K, name), "us": round(us, 2),
+                     "TOPS": round(2.0 * M * N * K / us / 1e6, 1)})
+        log("bench: vendor int8 %s: %.2f us" % (name, us))
+    # the library's own call on the same shape at W4A4, for the same timing method
+    wl = Workload()
+    us = prefill_call_time(wl, calls) * 1e6
+    rows.append({"gemm": "apt_gemm W4A4 2048x11008x4096 (bit-planes, selected config)", "us": round(us, 2),
+                 "TOPS": round(2.0 * M * N * K / us / 1e6, 1)})
     return rows
 
 
@@ -1220,6 +1272,12 @@ def main():
     ap.add_argument("--calibrate", action="store_true",
                     help="print the selector model's calibration (pair and fixed times per tile "
                          "shape and operand class) and exit")
+    ap.add_argument("--serial-step", action="store_true",
+                    help="run the whole step on one stream (the decode GEMMs before the prefill) "
+                         "instead of the decode chain on a second stream beside the prefill")
+    ap.add_argument("--vendor-int8", action="store_true",
+                    help="print the vendor library's dense int8 GEMM (torch._int_mm) on the prefill "
+                         "shape with int8 operands, as context, and exit")
     ap.add_argument("--mfma-issue", action="store_true",
                     help="print the MFMA-issue probe's cycles per MFMA for each part of the GEMM "
                          "loop's instruction pattern and exit")
@@ -1253,6 +1311,9 @@ def main():
     if args.workloads:
         workloads_run()
         return
+    if args.vendor_int8:
+        print(json.dumps(vendor_int8(), indent=1), flush=True)
+        return
     if args.mfma_issue:
         print(json.dumps(mfma_issue(), indent=1), flush=True)
         return
@@ -1285,6 +1346,7 @@ def main():
         return
     log("bench: building workload")
     wl = Workload()
+    wl.overlap = not args.serial_step
     for _ in range(args.warmup):
         wl.step()
     torch.cuda.synchronize()
@@ -1323,6 +1385,8 @@ def main():
         "config": {"workload": "W2A2 decode M=1 (N=4096 and N=11008, K=4096, int32 + fp16 epilogue) "
                                "+ W4A4 prefill M=2048 N=11008 K=4096 (int32); activations packed "
                                "every step, weights packed once",
+                   "schedule": ("decode chain on a second stream beside the prefill chain"
+                                if wl.overlap else "one stream"),
                    "prefill_config": cfg},
         "roofline": roofline,
     }
