@@ -496,21 +496,30 @@ def mfma_issue(blocks: int = 256, chunks: int = 4000):
     """The MFMA-issue probe (probes/mfma_issue.hip, libapt_probe.so): cycles
     per v_mfma_i32_32x32x32_i8 per SIMD for each part of the GEMM loop's
     instruction pattern, with the shader clock read from s_memtime against
-    s_memrealtime."""
+    s_memrealtime, on pseudo-random operand bytes, then modes 0, 3 and 7 on
+    sparse bytes (one small nonzero byte per dword) and on 4-bit bipolar values
+    (random odd bytes in [-15, 15]); mode 0's accumulators are checked against
+    a closed form (result_checked)."""
     import ctypes
 
     import torch  # noqa: F401  (the HIP runtime torch loaded serves the probe library too)
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2508_19087_amd", "libapt_probe.so"))
-    lib.apt_probe_mfma_issue.argtypes = [ctypes.c_int] * 3 + [ctypes.POINTER(ctypes.c_double)]
+    lib.apt_probe_mfma_issue.argtypes = [ctypes.c_int] * 4 + [ctypes.POINTER(ctypes.c_double)]
     lib.apt_probe_mfma_issue.restype = ctypes.c_int
     rows = []
-    for mode, what in MFMA_ISSUE_MODES:
-        res = (ctypes.c_double * 3)()
-        rc = lib.apt_probe_mfma_issue(mode, blocks, chunks, res)
+    kinds = ["random", "sparse", "bipolar4"]
+    runs = [(mode, what, 0) for mode, what in MFMA_ISSUE_MODES]
+    runs += [(m, MFMA_ISSUE_MODES[m][1], d) for d in (1, 2) for m in (0, 3, 7)]
+    for mode, what, data in runs:
+        res = (ctypes.c_double * 4)()
+        rc = lib.apt_probe_mfma_issue(mode, blocks, chunks, data, res)
         if rc != 0:
-            raise RuntimeError("mfma issue probe mode %d failed at step %d" % (mode, rc))
-        rows.append({"mode": mode, "pattern": what, "cycles_per_mfma": round(res[0], 1),
-                     "clock_GHz": round(res[1], 3), "us_per_chunk": round(res[2], 3)})
+            raise RuntimeError("mfma issue probe mode %d failed at step %d%s" %
+                               (mode, rc, " (accumulator sums differ from the closed form)" if rc == 5 else ""))
+        rows.append({"mode": mode, "operands": kinds[data], "pattern": what,
+                     "cycles_per_mfma": round(res[0], 1),
+                     "clock_GHz": round(res[1], 3), "us_per_chunk": round(res[2], 3),
+                     "result_checked": bool(res[3])})
         log("bench: mfma issue mode %d: %.1f cycles per MFMA at %.2f GHz" % (mode, res[0], res[1]))
     return rows
 
