@@ -497,9 +497,10 @@ def mfma_issue(blocks: int = 256, chunks: int = 4000):
     per v_mfma_i32_32x32x32_i8 per SIMD for each part of the GEMM loop's
     instruction pattern, with the shader clock read from s_memtime against
     s_memrealtime, on pseudo-random operand bytes, then modes 0, 3 and 7 on
-    sparse bytes (one small nonzero byte per dword) and on 4-bit bipolar values
-    (random odd bytes in [-15, 15]); mode 0's accumulators are checked against
-    a closed form (result_checked)."""
+    sparse bytes (one small nonzero byte per dword), on 4-bit bipolar values
+    (random odd bytes in [-15, 15]) and on 4-bit codes (random bytes in
+    [0, 15], what the reassembled int8 route multiplies at W4A4); mode 0's
+    accumulators are checked against a closed form (result_checked)."""
     import ctypes
 
     import torch  # noqa: F401  (the HIP runtime torch loaded serves the probe library too)
@@ -507,9 +508,9 @@ def mfma_issue(blocks: int = 256, chunks: int = 4000):
     lib.apt_probe_mfma_issue.argtypes = [ctypes.c_int] * 4 + [ctypes.POINTER(ctypes.c_double)]
     lib.apt_probe_mfma_issue.restype = ctypes.c_int
     rows = []
-    kinds = ["random", "sparse", "bipolar4"]
+    kinds = ["random", "sparse", "bipolar4", "code4"]
     runs = [(mode, what, 0) for mode, what in MFMA_ISSUE_MODES]
-    runs += [(m, MFMA_ISSUE_MODES[m][1], d) for d in (1, 2) for m in (0, 3, 7)]
+    runs += [(m, MFMA_ISSUE_MODES[m][1], d) for d in (1, 2, 3) for m in (0, 3, 7)]
     for mode, what, data in runs:
         res = (ctypes.c_double * 4)()
         rc = lib.apt_probe_mfma_issue(mode, blocks, chunks, data, res)

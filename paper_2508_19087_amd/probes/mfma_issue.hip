@@ -19,9 +19,9 @@
 // 100 MHz constant counter (s_memrealtime) around its loop; the host averages
 // them into cycles per MFMA per SIMD and the shader clock.
 // Operands come from one host-generated buffer (registers, LDS and the load
-// buffer), of pseudo-random bytes, of sparse bytes or of 4-bit bipolar values:
-// the shader clock under dense MFMA work depends on how many operand bits
-// switch.  Each wave ends by summing every element of each
+// buffer) of pseudo-random bytes, sparse bytes, 4-bit bipolar values or 4-bit
+// codes: the shader clock under dense MFMA work depends on how many operand
+// bits switch.  Each wave ends by summing every element of each
 // accumulator over its lanes; for mode 0, whose operands never change, the
 // host checks every wave's sums against a closed form: the sum of all
 // elements of A.B is sum_k colsum_A(k) * rowsum_B(k), and in the operand
@@ -175,9 +175,11 @@ int run(int blocks, int chunks, int data, double* res) {
     x ^= x >> 7;
     x ^= x << 17;
     // 1: one small byte per dword, the rest zero (few bits switch); 2: odd values in
-    // [-15, 15], the int8 operand bytes of 4-bit bipolar values; 0: any byte
+    // [-15, 15], 4-bit bipolar values as int8; 3: bytes in [0, 15], the 4-bit
+    // codes the reassembled int8 route multiplies; 0: any byte
     bytes[i] = data == 1   ? (int8_t)(i % 4 == 0 ? (x >> 58) : 0)
                : data == 2 ? (int8_t)(2 * (int)(x >> 60) - 15)
+               : data == 3 ? (int8_t)(x >> 60)
                            : (int8_t)(x >> 56);
   }
   int rc = 0;
@@ -230,8 +232,9 @@ int run(int blocks, int chunks, int data, double* res) {
 
 // Runs probe mode `mode` (0-7) for `chunks` chunks on `blocks` workgroups,
 // on pseudo-random operand bytes (data = 0), on bytes of which only the low
-// byte of each dword is nonzero and small (data = 1), or on random odd bytes
-// in [-15, 15] (data = 2: the operand bytes of 4-bit bipolar values), and writes cycles
+// byte of each dword is nonzero and small (data = 1), on random odd bytes in
+// [-15, 15] (data = 2: 4-bit bipolar values) or on random bytes in [0, 15]
+// (data = 3: the 4-bit codes the reassembled int8 route multiplies), and writes cycles
 // per MFMA per SIMD, the shader clock (GHz) and microseconds per chunk to
 // res[0..2], and to res[3] 1 if the accumulators were checked (mode 0) and 0
 // otherwise.  Returns 0, a nonzero step number on a HIP error, or 5 if mode
