@@ -90,7 +90,9 @@ enum {
  *              2x4 waves, 512x128 with 8x1, 256x128 with 4x2 or 4x1, 128x128
  *              with 2x2; the 4-wave shapes run two workgroups per compute unit)
  *   bk         K elements staged per pipeline step (MFMA routes: 0 or 128)
- *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route)
+ *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route); XOR
+ *              route: waves_m = waves per workgroup, each owning one 8-row
+ *              group of weight rows (0 = chosen by the library, or 1, 2, 4)
  *   grid       int8 MFMA route: persistent workgroups, 0..4096.  0 = one
  *              workgroup per tile.  Otherwise each workgroup takes
  *              floor(T / grid) whole tiles (T tiles in all) and the K chunks of
@@ -99,7 +101,8 @@ enum {
  *              sums through the workspace.  The result does not depend on it.
  *   lds_stages depth of the weight LDS ring (int8 MFMA route: 0 or 3; the
  *              +-1 plane route ignores it)
- *   mt         XOR route: activation rows per workgroup (0 or 8)
+ *   mt         XOR route: activation rows per block row: 1, 8, or 0 = 1
+ *              when M = 1 and 8 otherwise
  *   split_n    int8 MFMA route: 0, or a multiple of bn with 0 < split_n < N
  *              and of 8: columns [0, split_n) use the tile above and columns
  *              [split_n, N) a second launch with tile tail_bm x tail_bn (of

@@ -54,7 +54,7 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
   switch (c.route) {
     case APT_ROUTE_XOR:
       if (!apt::xor_config_ok(c)) return APT_ERR_INVALID_ARG;
-      if ((M + 7) / 8 > 65535) return APT_ERR_UNSUPPORTED;
+      if (!apt::xor_sizes_ok(M, N, K, p, q, c)) return APT_ERR_UNSUPPORTED;
       return APT_OK;
     case APT_ROUTE_FP4_MFMA:
       if (!apt::fp4_route_ok(K, p, q)) return APT_ERR_UNSUPPORTED;

@@ -105,6 +105,7 @@ __device__ __forceinline__ float affine_value(int32_t c, float sa, float sw, flo
 // XOR + popcount route (gemm_xor.hip).  Any shape.
 hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
 bool xor_config_ok(const apt_config_t& cfg);
+bool xor_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg);
 
 // Reassembled int8 MFMA route (gemm_int8.hip).  The workspace holds the
 // activations expanded into MFMA fragments (int8_workspace_bytes).

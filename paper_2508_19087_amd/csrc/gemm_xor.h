@@ -8,138 +8,267 @@
 // Padding bits are zero in both operands, so they XOR to zero and the true K
 // enters the constant term.
 //
-// Work split: a workgroup owns one 8-row group of weight rows and up to 8
-// activation rows (staged in LDS when they fit).  Lane l of wave v takes weight
-// row slot l mod 8 and the chunks c = (l / 8) + 8 v + 32 t, so the 8 lanes that
-// share a chunk read one 128-byte line per plane.  All 1-bit products of an
-// output stay in registers (the register analogue of the paper's fragment-level
-// recovery, Sec. IV-B); partial sums meet through lane shuffles and one LDS
-// exchange, and nothing intermediate goes to global memory.
+// This route streams the weight planes once, so it is the decode route
+// (M <= 8, bound by HBM) and the route of small problems.
+//
+// Work split: every wave owns one whole 8-row group of weight rows and its
+// whole K, for MT activation rows (MT = 1: one row, MT = 8: the 8 rows of an
+// activation row group).  Lane l takes weight row slot l mod 8 and the chunks
+// c = l / 8 + 8 t, so the 8 lanes that share a chunk read one 128-byte line
+// per plane.  The chunks are walked in batches of kB per lane with two batches
+// of weight words in flight: the loads of batch t + 2 are issued before batch
+// t + 1 is used, so a lane keeps up to 2 kB P 16-byte loads outstanding
+// (with one activation row, every load of a lane up to K = 16384 is issued
+// before the first is used) and the latency of HBM is paid about once per
+// wave, not once per batch; the popcounts consume the loads in the order
+// they complete.  The weight loads carry the non-temporal hint: each weight byte is
+// read once per call, and the hint measured 10-15% faster cold streaming
+// than plain loads.  All 1-bit products of an output stay in
+// registers (the register analogue of the paper's fragment-level recovery,
+// Sec. IV-B); the 8 chunk lanes of a row meet through three lane shuffles, and
+// nothing intermediate goes to memory.  A workgroup is W such waves side by
+// side (W = 1, 2 or 4); they share only the copy of the activation chunks in LDS, so no wave
+// waits for another after that copy.
 #include "apt_internal.h"
 
 namespace apt {
 namespace xorpop {
 
 constexpr int kWave = 64;
-constexpr int kWaves = 4;
-constexpr int kMT = 8;                       // activation rows per workgroup
-constexpr int kSlots = kWaves * kWave / kRowGroup;  // chunk slots per workgroup (32)
+constexpr int kMaxWaves = 4;                 // waves per workgroup, at most
+constexpr int kChunkLanes = kWave / kRowGroup;  // lanes per row slot (8)
+// LDS of the staged activation chunks, at most (bytes).
+constexpr size_t kMaxActLds = 64 * 1024;
 
 struct XorParams {
   GemmArgs g;
-  int nchunks;
+  int nchunks;   // NC, chunks of K
+  int groups;    // row groups of the packed weights (padded N / 8)
 };
 
-template <int P, int Q, bool kALds>
-__global__ __launch_bounds__(kWave* kWaves) void gemm_xor_kernel(XorParams prm) {
+// Activation chunk vectors per chunk in LDS: MT = 8 stages all 8 rows of each
+// plane plus one pad vector (so that the 8 chunk lanes of a wave, which read
+// 8 consecutive chunks at once, start 32 Q + 4 dwords apart and fall in
+// different banks); MT = 1 stages the one row's Q vectors.  The copy covers
+// the chunks rounded up to a multiple of 8 (one chunk per lane and round),
+// the chunks past K as zeros.
+template <int Q, int MT>
+__host__ __device__ constexpr int act_chunk_vecs() { return MT == 8 ? Q * kRowGroup + 1 : Q; }
+__host__ __device__ constexpr int staged_chunks(int nchunks) {
+  return (nchunks + kChunkLanes - 1) / kChunkLanes * kChunkLanes;
+}
+
+// Chunks per lane per batch: about 8 16-byte weight loads per batch, or 16
+// in the deep form (one activation row and K past one plain batch per lane:
+// with two batches in flight every load of a lane up to K = 16384 at p = 2
+// is issued before the first is used).
+template <int P, bool DEEP>
+__host__ __device__ constexpr int batch_chunks() {
+  return DEEP ? (P >= 16 ? 1 : 16 / P) : (P >= 8 ? 1 : 8 / P);
+}
+// Activation vectors each thread loads into registers before the weight
+// loads are issued (the rest of a larger copy is loaded after them).
+constexpr int kStagePre = 4;
+// Cache policy of the weight loads: non-temporal.
+constexpr int kNT = 2;
+
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t xor_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+
+// Every load below is a buffer load whose offset is past the resource's end
+// when its element does not exist (a chunk past K, a row group past N, a
+// vector past the copy): such loads return zeros without touching memory.
+// The loads are therefore unconditional (no branch) and their waits count
+// exactly; a zero weight word meets a zero activation word in the chunks
+// between K and the end of the last round, which adds nothing to any
+// popcount.
+template <int P, int Q, int MT, bool DEEP, bool kALds>
+__global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams prm) {
   extern __shared__ uint4 a_lds[];
-  __shared__ uint32_t red[kWaves][kMT][kRowGroup];
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
-  const int m0 = blockIdx.y * kMT;
-  const int mrows = min(kMT, g.M - m0);
-  const int n0 = blockIdx.x * kRowGroup;
-
-  // The activation rows m0 .. m0+7 are one row group: NC * Q * 8 uint4,
-  // ordered (chunk, plane, row).  In LDS each chunk's Q * 8 vectors are
-  // followed by one pad vector: the 8 chunks a wave reads at once then start
-  // 32 Q + 4 dwords apart and fall in different banks (without the pad, every
-  // even Q puts them in the same ones).
-  constexpr int kChunkVecs = Q * kRowGroup;
-  const uint4* a_src = reinterpret_cast<const uint4*>(g.a_packed) + (int64_t)(m0 / kRowGroup) * NC * kChunkVecs;
-  if (kALds) {
-    const int n_vec = NC * kChunkVecs;
-    for (int t = threadIdx.x; t < n_vec; t += blockDim.x) a_lds[t + t / kChunkVecs] = a_src[t];
-    __syncthreads();
-  }
-  const uint4* a_base = kALds ? a_lds : a_src;
-  const int a_chunk_stride = kALds ? kChunkVecs + 1 : kChunkVecs;
-
+  const int m0 = blockIdx.y * MT;
+  const int mrows = min(MT, g.M - m0);
   const int lane = threadIdx.x % kWave;
   const int wave = threadIdx.x / kWave;
   const int slot = lane % kRowGroup;
-  const int cs = lane / kRowGroup + (kWave / kRowGroup) * wave;
-  const uint4* w_grp = reinterpret_cast<const uint4*>(g.w_packed) + (int64_t)blockIdx.x * NC * P * kRowGroup;
+  const int cl = lane / kRowGroup;
+  const int rg = __builtin_amdgcn_readfirstlane(blockIdx.x * (int)(blockDim.x / kWave) + wave);
+  const bool rv = rg < prm.groups;
 
-  uint32_t S[kMT];
+  // ---- activation chunks: rows m0 .. m0 + MT - 1 (all in the row group
+  // m0 / 8), ordered (chunk, plane, row) in the packed buffer.  The first
+  // vectors of the LDS copy are requested before the weight loads: loads
+  // complete in order, so a copy requested after them would wait for the
+  // whole weight stream before the first popcount could start.
+  constexpr int kAV = act_chunk_vecs<Q, MT>();
+  const uint4* a_src = reinterpret_cast<const uint4*>(g.a_packed) +
+                       (int64_t)(m0 / kRowGroup) * NC * Q * kRowGroup;
+  const __amdgpu_buffer_rsrc_t a_rsrc = xor_rsrc(a_src, (uint32_t)NC * Q * kRowGroup * 16u);
+  const int a_row = MT == 1 ? m0 % kRowGroup : 0;
+  const int NS = staged_chunks(NC);
+  const int n_vec = MT == 8 ? NS * Q * kRowGroup : NS * Q;  // staged vectors
+  // vector t of the copy (zeros past chunk NC)
+  auto a_at = [&](int t) __attribute__((always_inline)) -> uint4 {
+    const uint32_t v = MT == 8 ? (uint32_t)t : (uint32_t)t * kRowGroup + a_row;
+    const uint32_t off = t < n_vec ? v * 16u : 0xFFFFFFF0u;
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, off, 0, 0));
+  };
+  auto lds_at = [&](int t) __attribute__((always_inline)) -> int {
+    return MT == 8 ? t + t / (Q * kRowGroup) : t;
+  };
+  uint4 pre[kStagePre];
+  if (kALds) {
 #pragma unroll
-  for (int m = 0; m < kMT; ++m) S[m] = 0u;
-  for (int c = cs; c < NC; c += kSlots) {
-    uint4 wv[P];
+    for (int k = 0; k < kStagePre; ++k) pre[k] = a_at(threadIdx.x + k * (int)blockDim.x);
+  }
+
+  // ---- weight batches
+  constexpr int kB = batch_chunks<P, DEEP>();
+  const int T = NS / kChunkLanes;  // chunk rounds
+  const uint32_t w_bytes = rv ? (uint32_t)NC * P * kRowGroup * 16u : 0u;
+  const __amdgpu_buffer_rsrc_t w_rsrc =
+      xor_rsrc(reinterpret_cast<const uint4*>(g.w_packed) + (int64_t)(rv ? rg : 0) * NC * P * kRowGroup,
+               w_bytes);
+  v4u wcur[kB][P], wnxt[kB][P];
+  auto load = [&](v4u (&wv)[kB][P], int t0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < P; ++i) wv[i] = w_grp[(c * P + i) * kRowGroup + slot];
+    for (int b = 0; b < kB; ++b) {
+      const int c = cl + kChunkLanes * (t0 + b);
+      // (the plane offset is added to it, so the offset of a missing chunk
+      // stays below 2^32 - 2^12; a row group holds at most 2^31 bytes)
+      const uint32_t off = c < NC ? (uint32_t)((c * P) * kRowGroup + slot) * 16u : 0x80000000u;
 #pragma unroll
-    for (int m = 0; m < kMT; ++m) {
-      if (m < mrows) {
-        uint32_t s = 0u;
+      for (int i = 0; i < P; ++i)
+        wv[b][i] = __builtin_amdgcn_raw_buffer_load_b128(w_rsrc, off, i * kRowGroup * 16, kNT);
+    }
+  };
+  load(wcur, 0);
+  if (kB < T) load(wnxt, kB);
+
+  if (kALds) {
+#pragma unroll
+    for (int k = 0; k < kStagePre; ++k) {
+      const int t = threadIdx.x + k * (int)blockDim.x;
+      if (t < n_vec) a_lds[lds_at(t)] = pre[k];
+    }
+    for (int t = threadIdx.x + kStagePre * (int)blockDim.x; t < n_vec; t += blockDim.x)
+      a_lds[lds_at(t)] = a_at(t);
+    __syncthreads();
+  }
+  // vector of chunk c, plane j, row m (zeros for c >= NC)
+  auto act = [&](int c, int j, int m) __attribute__((always_inline)) -> uint4 {
+    if (kALds) return MT == 8 ? a_lds[c * kAV + j * kRowGroup + m] : a_lds[c * kAV + j];
+    const uint32_t v = (uint32_t)(c * Q + j) * kRowGroup + (MT == 8 ? m : a_row);
+    return __builtin_bit_cast(
+        uint4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, c < NC ? v * 16u : 0xFFFFFFF0u, 0, 0));
+  };
+
+  uint32_t S[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) S[m] = 0u;
+  auto compute = [&](const v4u (&wv)[kB][P], int t0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < kB; ++b) {
+      if (t0 + b >= T) break;  // uniform: past the last round
+      const int c = cl + kChunkLanes * (t0 + b);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        if (m >= mrows) break;  // uniform
 #pragma unroll
         for (int j = 0; j < Q; ++j) {
-          const uint4 av = a_base[c * a_chunk_stride + j * kRowGroup + m];
+          const uint4 av = act(c, j, m);
+          uint32_t s = 0u;
 #pragma unroll
           for (int i = 0; i < P; ++i) {
-            uint32_t cnt = __builtin_popcount(wv[i].x ^ av.x);
-            cnt += __builtin_popcount(wv[i].y ^ av.y);
-            cnt += __builtin_popcount(wv[i].z ^ av.z);
-            cnt += __builtin_popcount(wv[i].w ^ av.w);
-            s += cnt << (i + j);
+            uint32_t cnt = __builtin_popcount(wv[b][i][0] ^ av.x);
+            cnt += __builtin_popcount(wv[b][i][1] ^ av.y);
+            cnt += __builtin_popcount(wv[b][i][2] ^ av.z);
+            cnt += __builtin_popcount(wv[b][i][3] ^ av.w);
+            s += cnt << i;
           }
+          S[m] += s << j;
         }
-        S[m] += s;
       }
     }
-  }
-  // Sum over the 8 chunk slots of the wave (lanes with equal slot), then over
-  // the 4 waves through LDS.
+  };
+  for (int t0 = 0; t0 < T; t0 += kB) {
+    compute(wcur, t0);
+    if (t0 + kB < T) {
 #pragma unroll
-  for (int m = 0; m < kMT; ++m) {
+      for (int b = 0; b < kB; ++b)
+#pragma unroll
+        for (int i = 0; i < P; ++i) wcur[b][i] = wnxt[b][i];
+      if (t0 + 2 * kB < T) load(wnxt, t0 + 2 * kB);
+    }
+  }
+
+  // ---- sum over the 8 chunk lanes of each row slot
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
     S[m] += __shfl_xor(S[m], 8);
     S[m] += __shfl_xor(S[m], 16);
     S[m] += __shfl_xor(S[m], 32);
   }
-  if (lane < kRowGroup) {
+
+  // ---- outputs: lane (cl, slot) writes activation row m0 + cl (MT = 8) or
+  // m0 (MT = 1, lanes with cl = 0) of weight row 8 rg + slot
+  const int m = MT == 8 ? cl : 0;
+  const int n = rg * kRowGroup + slot;
+  if (m >= mrows || (MT == 1 && cl != 0) || !rv || n >= g.N) return;
+  const int mg = m0 + m;
+  const uint32_t kabq = (uint32_t)g.K * ((1u << P) - 1u) * ((1u << Q) - 1u);
+  uint32_t tot = S[0];
 #pragma unroll
-    for (int m = 0; m < kMT; ++m) red[wave][m][slot] = S[m];
-  }
-  __syncthreads();
-  if (threadIdx.x < kMT * kRowGroup) {
-    const int m = threadIdx.x / kRowGroup, sl = threadIdx.x % kRowGroup;
-    const int mg = m0 + m, n = n0 + sl;
-    if (m < mrows && n < g.N) {
-      uint32_t tot = 0u;
-#pragma unroll
-      for (int v = 0; v < kWaves; ++v) tot += red[v][m][sl];
-      const uint32_t kabq = (uint32_t)g.K * ((1u << P) - 1u) * ((1u << Q) - 1u);
-      const int32_t c = (int32_t)(kabq - 2u * tot);
-      const int64_t o = (int64_t)mg * g.N + n;
-      if (g.c_int32) g.c_int32[o] = c;
-      if (g.c_fp16) {
-        float f;
-        if (g.a_zero) {
-          const float sw = __half2float(g.w_scale[n]), zw = __half2float(g.w_zero[n]);
-          f = affine_value(c, __half2float(g.a_scale[mg]), sw, zw, (float)g.a_rowsum[mg],
-                           __half2float(g.a_zero[mg]),
-                           sw * (float)g.w_rowsum[n] + (float)g.K * zw);
-        } else {
-          f = (float)c * __half2float(g.a_scale[mg]);
-          f = f * __half2float(g.w_scale[n]);
-        }
-        g.c_fp16[o] = __float2half_rn(f);
-      }
+  for (int mm = 1; mm < MT; ++mm)
+    if (m == mm) tot = S[mm];
+  const int32_t c = (int32_t)(kabq - 2u * tot);
+  const int64_t o = (int64_t)mg * g.N + n;
+  if (g.c_int32) g.c_int32[o] = c;
+  if (g.c_fp16) {
+    float f;
+    if (g.a_zero) {
+      const float sw = __half2float(g.w_scale[n]), zw = __half2float(g.w_zero[n]);
+      f = affine_value(c, __half2float(g.a_scale[mg]), sw, zw, (float)g.a_rowsum[mg],
+                       __half2float(g.a_zero[mg]), sw * (float)g.w_rowsum[n] + (float)g.K * zw);
+    } else {
+      f = (float)c * __half2float(g.a_scale[mg]);
+      f = f * __half2float(g.w_scale[n]);
     }
+    g.c_fp16[o] = __float2half_rn(f);
   }
 }
 
+// Launch shape of one XOR-route call (resolved from the config by the host).
+struct XorLaunch {
+  bool deep;   // deep batches (batch_chunks)
+  int mt;      // activation rows per block row (1 or 8)
+  int waves;   // waves per workgroup (1, 2 or 4)
+  bool lds;    // activation chunks staged in LDS
+  size_t lds_bytes;
+  dim3 grid;
+};
+
+template <int P, int Q, int MT, bool DEEP>
+inline hipError_t launch_mt(const XorParams& prm, const XorLaunch& L, hipStream_t s) {
+  const dim3 block(kWave * L.waves);
+  if (L.lds) return launch_kernel(gemm_xor_kernel<P, Q, MT, DEEP, true>, L.grid, block, L.lds_bytes, s, prm);
+  return launch_kernel(gemm_xor_kernel<P, Q, MT, DEEP, false>, L.grid, block, 0, s, prm);
+}
+
 template <int P, int Q>
-inline hipError_t launch_pq(const XorParams& prm, int grid_x, int grid_y, size_t lds, hipStream_t s) {
-  dim3 grid(grid_x, grid_y), block(kWave * kWaves);
-  if (lds > 0) return launch_kernel(gemm_xor_kernel<P, Q, true>, grid, block, lds, s, prm);
-  return launch_kernel(gemm_xor_kernel<P, Q, false>, grid, block, 0, s, prm);
+inline hipError_t launch_pq(const XorParams& prm, const XorLaunch& L, hipStream_t s) {
+  if (L.mt == 1) return L.deep ? launch_mt<P, Q, 1, true>(prm, L, s) : launch_mt<P, Q, 1, false>(prm, L, s);
+  return launch_mt<P, Q, 8, false>(prm, L, s);
 }
 
 // Launch for weight bits P and any activation bits; one explicit
 // instantiation per P lives in gemm_xor_inst.hip (built once per P).
 template <int P>
-hipError_t launch_for_p(int q, const XorParams& prm, int gx, int gy, size_t lds, hipStream_t s);
+hipError_t launch_for_p(int q, const XorParams& prm, const XorLaunch& L, hipStream_t s);
 
 }  // namespace xorpop
 }  // namespace apt

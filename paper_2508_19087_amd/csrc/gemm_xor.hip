@@ -1,35 +1,70 @@
 // gemm_xor.hip - launch geometry and dispatch of the XOR + popcount route;
 // the kernel is in gemm_xor.h.
+#include <algorithm>
+
 #include "gemm_xor.h"
 
 namespace apt {
 
-using xorpop::kMT;
+using xorpop::XorLaunch;
 using xorpop::XorParams;
 
-bool xor_config_ok(const apt_config_t& cfg) { return cfg.mt == 0 || cfg.mt == kMT; }
+// Config fields of the XOR route: mt = activation rows per block row (0:
+// 1 when M = 1, else 8), waves_m = waves per workgroup, each owning one
+// 8-row group of weight rows (0: chosen below, or 1, 2 or 4).
+bool xor_config_ok(const apt_config_t& cfg) {
+  return (cfg.mt == 0 || cfg.mt == 1 || cfg.mt == 8) &&
+         (cfg.waves_m == 0 || cfg.waves_m == 1 || cfg.waves_m == 2 || cfg.waves_m == 4);
+}
 
-hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t&, hipStream_t stream) {
+namespace {
+
+size_t act_lds_bytes_q(int q, int mt, int nchunks) {
+  const int per = mt == 8 ? q * kRowGroup + 1 : q;
+  return (size_t)xorpop::staged_chunks(nchunks) * per * 16;
+}
+
+}  // namespace
+
+XorLaunch xor_launch_shape(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
+  XorLaunch L;
+  L.mt = cfg.mt != 0 ? cfg.mt : (M == 1 ? 1 : 8);
+  // one activation row: deep batches once a lane has more than one batch of
+  // the plain form (8 / p chunks)
+  const int rounds = xorpop::staged_chunks(num_chunks(K)) / xorpop::kChunkLanes;
+  L.deep = L.mt == 1 && rounds > std::max(1, 8 / p);
+  // four waves per workgroup, two in the deep form (cold weights on MI355X:
+  // four equal within noise at 4 MB and 4-10% faster from 22 MB up and with
+  // eight activation rows; two 4% faster at K = 11008)
+  L.waves = cfg.waves_m != 0 ? cfg.waves_m : (L.deep ? 2 : 4);
+  const int groups = padded_rows(N) / kRowGroup;
+  L.grid = dim3((groups + L.waves - 1) / L.waves, (M + L.mt - 1) / L.mt);
+  L.lds_bytes = act_lds_bytes_q(q, L.mt, num_chunks(K));
+  L.lds = L.lds_bytes <= xorpop::kMaxActLds;
+  if (!L.lds) L.lds_bytes = 0;
+  return L;
+}
+
+bool xor_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
+  const XorLaunch L = xor_launch_shape(M, N, K, p, q, cfg);
+  return L.grid.x <= 0x7fffffffu && L.grid.y <= 65535u;
+}
+
+hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream) {
   XorParams prm;
   prm.g = g;
   prm.nchunks = num_chunks(g.K);
-  const int grid_x = padded_rows(g.N) / kRowGroup;
-  const int grid_y = (g.M + kMT - 1) / kMT;
-  // staged activations: Q * 8 vectors of 16 bytes per chunk plus one pad vector
-  size_t lds = (size_t)prm.nchunks * (g.q * kRowGroup + 1) * 16;
-  // Read the activation chunks from global memory instead of staging them
-  // when they do not fit, or when only one activation row is real: staging
-  // would copy 8 rows and put a barrier between the two memory latencies.
-  if (lds > 64 * 1024 || g.M == 1) lds = 0;
+  prm.groups = padded_rows(g.N) / kRowGroup;
+  const XorLaunch L = xor_launch_shape(g.M, g.N, g.K, g.p, g.q, cfg);
   switch (g.p) {
-    case 1: return xorpop::launch_for_p<1>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 2: return xorpop::launch_for_p<2>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 3: return xorpop::launch_for_p<3>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 4: return xorpop::launch_for_p<4>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 5: return xorpop::launch_for_p<5>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 6: return xorpop::launch_for_p<6>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 7: return xorpop::launch_for_p<7>(g.q, prm, grid_x, grid_y, lds, stream);
-    case 8: return xorpop::launch_for_p<8>(g.q, prm, grid_x, grid_y, lds, stream);
+    case 1: return xorpop::launch_for_p<1>(g.q, prm, L, stream);
+    case 2: return xorpop::launch_for_p<2>(g.q, prm, L, stream);
+    case 3: return xorpop::launch_for_p<3>(g.q, prm, L, stream);
+    case 4: return xorpop::launch_for_p<4>(g.q, prm, L, stream);
+    case 5: return xorpop::launch_for_p<5>(g.q, prm, L, stream);
+    case 6: return xorpop::launch_for_p<6>(g.q, prm, L, stream);
+    case 7: return xorpop::launch_for_p<7>(g.q, prm, L, stream);
+    case 8: return xorpop::launch_for_p<8>(g.q, prm, L, stream);
   }
   return hipErrorInvalidValue;
 }

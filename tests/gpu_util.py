@@ -13,12 +13,18 @@ INT8_SHAPES = [(256, 256, 4, 2), (256, 256, 2, 4), (256, 128, 4, 2), (128, 128, 
 
 def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
     """(name, config) of every route and tile shape the library can be forced
-    to; the int8 shapes with one workgroup per tile (grid 0) and with
+    to; the XOR route with every launch shape; the int8 shapes with one workgroup per tile (grid 0) and with
     persistent stream-K grids: 256 workgroups, 7 (many workgroups share each
     tile) and 300; with N, also split launches (main tiles, then 128x128 tail
     tiles, one per workgroup and stream-K)."""
     del K
     out = [("xor", apt.apt_config_t.make(apt.APT_ROUTE_XOR))]
+    # XOR route launch shapes: activation rows per block row (1 or 8), waves per
+    # workgroup
+    for mt in (1, 8):
+        for waves in (1, 2, 4):
+            c = apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_m=waves, mt=mt)
+            out.append(("xor_mt%d_w%d" % (mt, waves), c))
     for bm, bn, wm, wn in INT8_SHAPES:
         for grid in (0, 256, 7, 300):
             c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, grid, 3)
