@@ -502,11 +502,7 @@ def mfma_issue(blocks: int = 256, chunks: int = 4000):
     [0, 15], what the reassembled int8 route multiplies at W4A4); mode 0's
     accumulators are checked against a closed form (result_checked)."""
     import ctypes
-
-    import torch  # noqa: F401  (the HIP runtime torch loaded serves the probe library too)
-    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2508_19087_amd", "libapt_probe.so"))
-    lib.apt_probe_mfma_issue.argtypes = [ctypes.c_int] * 4 + [ctypes.POINTER(ctypes.c_double)]
-    lib.apt_probe_mfma_issue.restype = ctypes.c_int
+    lib = probe_lib()
     rows = []
     kinds = ["random", "sparse", "bipolar4", "code4"]
     runs = [(mode, what, 0) for mode, what in MFMA_ISSUE_MODES]
@@ -591,23 +587,48 @@ def decode_cold(wl, reps: int = 4):
     return out
 
 
+def probe_lib():
+    """The measurement probes (probes/*.hip, libapt_probe.so; not part of
+    libapt.so)."""
+    import ctypes
+
+    import torch  # noqa: F401  (the HIP runtime torch loaded serves the probe library too)
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2508_19087_amd", "libapt_probe.so"))
+    lib.apt_probe_mfma_issue.argtypes = [ctypes.c_int] * 4 + [ctypes.POINTER(ctypes.c_double)]
+    lib.apt_probe_mfma_issue.restype = ctypes.c_int
+    lib.apt_probe_read_blocks.argtypes = [ctypes.c_int64, ctypes.c_int]
+    lib.apt_probe_read_blocks.restype = ctypes.c_int64
+    lib.apt_probe_read_xor.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                       ctypes.c_void_p, ctypes.c_void_p]
+    lib.apt_probe_read_xor.restype = ctypes.c_int
+    return lib
+
+
+READ_VECS, READ_NT = 2, 1  # read probe: 16-byte vectors per lane, non-temporal loads
+
+
 def read_ceiling(torch, buf, reps: int = 4):
-    """A read-only cold reference for a decode GEMM's weight bytes: a row-wise
-    maximum (torch.amax over rows of 4 KB, one int32 per row written) of each
-    of enough copies of the buffer (> 2x the Infinity Cache) that every read
-    comes from HBM, replayed as one HIP graph like the GEMM rotation and
-    checked on every replay.  It reads each byte once, as the GEMM does."""
-    n = buf.numel()
-    assert n % 4096 == 0
+    """A read-only cold reference for a decode GEMM's weight bytes: the read
+    probe (probes/read_stream.hip) reads every byte of each of enough copies of
+    the buffer (> 2x the Infinity Cache) that every read comes from HBM, with
+    16-byte non-temporal loads, two per lane, folded by XOR to one word per
+    workgroup; replayed as one HIP graph like the GEMM rotation, and every
+    replay's words are checked against the XOR of the buffer's words."""
+    import numpy as np
+    lib = probe_lib()
+    n = buf.numel() * buf.element_size()
     copies = max(8, int(2 * MALL_BYTES // n) + 1)
-    srcs = [buf.clone().view(torch.int32).view(-1, 1024) for _ in range(copies)]
-    outs = [torch.empty(x.shape[0], dtype=torch.int32, device="cuda") for x in srcs]
+    srcs = [buf.clone() for _ in range(copies)]
+    nb = lib.apt_probe_read_blocks(n, READ_VECS)
+    outs = [torch.empty(nb, dtype=torch.int32, device="cuda") for _ in srcs]
 
     def launch(sp):
         for x, o in zip(srcs, outs):
-            torch.amax(x, dim=1, out=o)
+            rc = lib.apt_probe_read_xor(x.data_ptr(), n, READ_VECS, READ_NT, o.data_ptr(), sp)
+            if rc != 0:
+                raise RuntimeError("read probe launch failed (%d)" % rc)
     g = graph_of(torch, launch)
-    want = torch.amax(srcs[0], dim=1)
+    want = np.bitwise_xor.reduce(buf.cpu().numpy().view(np.uint32))
     times = []
     for r in range(reps):
         for o in outs:
@@ -618,14 +639,16 @@ def read_ceiling(torch, buf, reps: int = 4):
         g.replay()
         e1.record()
         torch.cuda.synchronize()
-        assert all(torch.equal(o, want) for o in outs), "read ceiling replay"
+        got = np.bitwise_xor.reduce(torch.stack(outs).cpu().numpy().view(np.uint32), axis=1)
+        assert (got == want).all(), "read probe replay"
         if r > 0:
             times.append(e0.elapsed_time(e1) / copies)
     t = sorted(times)[len(times) // 2] * 1e-3
     return {"bytes_read": n, "us": round(t * 1e6, 3), "read_GBs": round(n / t / 1e9, 1),
             "frac_hbm": round(n / t / 1e9 / PEAK_HBM_GBS, 4), "copies": copies,
-            "method": "HIP graph of torch.amax over 4 KB rows of each cold copy (reads every "
-                      "byte once; one int32 written per 4 KB)"}
+            "method": "HIP graph of the read probe over each cold copy (16-byte non-temporal "
+                      "loads, %d per lane; every byte read once, XOR-folded to one checked word "
+                      "per workgroup)" % READ_VECS}
 
 
 def decode_layer_cold(wl, reps: int = 4):

@@ -92,7 +92,9 @@ enum {
  *   bk         K elements staged per pipeline step (MFMA routes: 0 or 128)
  *   waves_m, waves_n   wave grid inside a workgroup (int8 MFMA route); XOR
  *              route: waves_m = waves per workgroup, each owning one 8-row
- *              group of weight rows (0 = chosen by the library, or 1, 2, 4)
+ *              group of weight rows (0 = chosen by the library, or 1, 2, 4),
+ *              waves_n = K split: 2 or 4 waves of a workgroup share one row
+ *              group and divide its K (1 = none, 0 = chosen by the library)
  *   grid       int8 MFMA route: persistent workgroups, 0..4096.  0 = one
  *              workgroup per tile.  Otherwise each workgroup takes
  *              floor(T / grid) whole tiles (T tiles in all) and the K chunks of

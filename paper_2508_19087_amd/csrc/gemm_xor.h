@@ -27,8 +27,11 @@
 // registers (the register analogue of the paper's fragment-level recovery,
 // Sec. IV-B); the 8 chunk lanes of a row meet through three lane shuffles, and
 // nothing intermediate goes to memory.  A workgroup is W such waves side by
-// side (W = 1, 2 or 4); they share only the copy of the activation chunks in LDS, so no wave
-// waits for another after that copy.
+// side (W = 1, 2 or 4); they share only the copy of the activation chunks in
+// LDS, so no wave waits for another after that copy.  With few row groups
+// (short N, long K) the W waves of a workgroup instead share one row group
+// and take every W-th chunk round (K split), so that more waves share the
+// popcount work; their sums meet through LDS at the end.
 #include "apt_internal.h"
 
 namespace apt {
@@ -44,6 +47,8 @@ struct XorParams {
   GemmArgs g;
   int nchunks;   // NC, chunks of K
   int groups;    // row groups of the packed weights (padded N / 8)
+  int ksplit;    // 1: each wave owns a row group; W > 1: the W waves of a
+                 // workgroup share one and take every W-th chunk round
 };
 
 // Activation chunk vectors per chunk in LDS: MT = 8 stages all 8 rows of each
@@ -96,7 +101,10 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
   const int wave = threadIdx.x / kWave;
   const int slot = lane % kRowGroup;
   const int cl = lane / kRowGroup;
-  const int rg = __builtin_amdgcn_readfirstlane(blockIdx.x * (int)(blockDim.x / kWave) + wave);
+  const int KW = prm.ksplit;
+  const int kv = KW > 1 ? wave : 0;  // this wave's share of the chunk rounds
+  const int rg = __builtin_amdgcn_readfirstlane(KW > 1 ? (int)blockIdx.x
+                                                       : blockIdx.x * (int)(blockDim.x / kWave) + wave);
   const bool rv = rg < prm.groups;
 
   // ---- activation chunks: rows m0 .. m0 + MT - 1 (all in the row group
@@ -128,7 +136,9 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
 
   // ---- weight batches
   constexpr int kB = batch_chunks<P, DEEP>();
-  const int T = NS / kChunkLanes;  // chunk rounds
+  // chunk rounds of this wave: t = kv + KW u, u < T (round t holds chunks
+  // 8 t .. 8 t + 7, one per chunk lane)
+  const int T = (NS / kChunkLanes - kv + KW - 1) / KW;
   const uint32_t w_bytes = rv ? (uint32_t)NC * P * kRowGroup * 16u : 0u;
   const __amdgpu_buffer_rsrc_t w_rsrc =
       xor_rsrc(reinterpret_cast<const uint4*>(g.w_packed) + (int64_t)(rv ? rg : 0) * NC * P * kRowGroup,
@@ -137,7 +147,7 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
   auto load = [&](v4u (&wv)[kB][P], int t0) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < kB; ++b) {
-      const int c = cl + kChunkLanes * (t0 + b);
+      const int c = cl + kChunkLanes * (kv + KW * (t0 + b));
       // (the plane offset is added to it, so the offset of a missing chunk
       // stays below 2^32 - 2^12; a row group holds at most 2^31 bytes)
       const uint32_t off = c < NC ? (uint32_t)((c * P) * kRowGroup + slot) * 16u : 0x80000000u;
@@ -174,7 +184,7 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
 #pragma unroll
     for (int b = 0; b < kB; ++b) {
       if (t0 + b >= T) break;  // uniform: past the last round
-      const int c = cl + kChunkLanes * (t0 + b);
+      const int c = cl + kChunkLanes * (kv + KW * (t0 + b));
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
         if (m >= mrows) break;  // uniform
@@ -214,6 +224,23 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
     S[m] += __shfl_xor(S[m], 32);
   }
 
+  // ---- K split: the waves' sums meet in LDS, wave 0 finishes
+  if (KW > 1) {
+    __shared__ uint32_t red[kMaxWaves][MT][kRowGroup];
+    if (cl == 0) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m) red[wave][m][slot] = S[m];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      uint32_t tot = 0u;
+      for (int v = 0; v < KW; ++v) tot += red[v][m][slot];
+      S[m] = tot;
+    }
+  }
+
   // ---- outputs: lane (cl, slot) writes activation row m0 + cl (MT = 8) or
   // m0 (MT = 1, lanes with cl = 0) of weight row 8 rg + slot
   const int m = MT == 8 ? cl : 0;
@@ -245,6 +272,7 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
 // Launch shape of one XOR-route call (resolved from the config by the host).
 struct XorLaunch {
   bool deep;   // deep batches (batch_chunks)
+  int ksplit;  // waves sharing one row group (1 = none)
   int mt;      // activation rows per block row (1 or 8)
   int waves;   // waves per workgroup (1, 2 or 4)
   bool lds;    // activation chunks staged in LDS

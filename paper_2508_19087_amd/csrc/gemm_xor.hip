@@ -10,11 +10,13 @@ using xorpop::XorLaunch;
 using xorpop::XorParams;
 
 // Config fields of the XOR route: mt = activation rows per block row (0:
-// 1 when M = 1, else 8), waves_m = waves per workgroup, each owning one
-// 8-row group of weight rows (0: chosen below, or 1, 2 or 4).
+// 1 when M = 1, else 8); waves_m = waves per workgroup, each owning one 8-row
+// group of weight rows (0: chosen below, or 1, 2 or 4); waves_n = K split, the
+// waves of a workgroup sharing one row group (0: chosen below, 1 = none, or 2
+// or 4; with 2 or 4, waves_m is ignored).
 bool xor_config_ok(const apt_config_t& cfg) {
-  return (cfg.mt == 0 || cfg.mt == 1 || cfg.mt == 8) &&
-         (cfg.waves_m == 0 || cfg.waves_m == 1 || cfg.waves_m == 2 || cfg.waves_m == 4);
+  auto w_ok = [](int w) { return w == 0 || w == 1 || w == 2 || w == 4; };
+  return (cfg.mt == 0 || cfg.mt == 1 || cfg.mt == 8) && w_ok(cfg.waves_m) && w_ok(cfg.waves_n);
 }
 
 namespace {
@@ -29,16 +31,26 @@ size_t act_lds_bytes_q(int q, int mt, int nchunks) {
 XorLaunch xor_launch_shape(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
   XorLaunch L;
   L.mt = cfg.mt != 0 ? cfg.mt : (M == 1 ? 1 : 8);
-  // one activation row: deep batches once a lane has more than one batch of
-  // the plain form (8 / p chunks)
+  const int groups = padded_rows(N) / kRowGroup;
   const int rounds = xorpop::staged_chunks(num_chunks(K)) / xorpop::kChunkLanes;
-  L.deep = L.mt == 1 && rounds > std::max(1, 8 / p);
+  // K split over four waves when one wave per row group would leave most
+  // SIMDs without a wave (fewer than 1024 row groups) and a wave would walk
+  // 8 or more chunk rounds (K > 7168); measured on MI355X with cold weights:
+  // 4096 x 11008 at W2A4 5.0 against 7.1 us (one token) and 14.5 against
+  // 22.3 us (8 tokens), while at K = 4096 the split is 3-8% slower
+  L.ksplit = cfg.waves_n != 0 ? cfg.waves_n : (groups < 1024 && rounds >= 8 ? 4 : 1);
+  // one activation row: deep batches once a wave has more than one batch of
+  // the plain form (8 / p chunks per lane)
+  const int wave_rounds = (rounds + L.ksplit - 1) / L.ksplit;
+  L.deep = L.mt == 1 && wave_rounds > std::max(1, 8 / p);
   // four waves per workgroup, two in the deep form (cold weights on MI355X:
   // four equal within noise at 4 MB and 4-10% faster from 22 MB up and with
   // eight activation rows; two 4% faster at K = 11008)
-  L.waves = cfg.waves_m != 0 ? cfg.waves_m : (L.deep ? 2 : 4);
-  const int groups = padded_rows(N) / kRowGroup;
-  L.grid = dim3((groups + L.waves - 1) / L.waves, (M + L.mt - 1) / L.mt);
+  if (L.ksplit > 1)
+    L.waves = L.ksplit;
+  else
+    L.waves = cfg.waves_m != 0 ? cfg.waves_m : (L.deep ? 2 : 4);
+  L.grid = dim3(L.ksplit > 1 ? groups : (groups + L.waves - 1) / L.waves, (M + L.mt - 1) / L.mt);
   L.lds_bytes = act_lds_bytes_q(q, L.mt, num_chunks(K));
   L.lds = L.lds_bytes <= xorpop::kMaxActLds;
   if (!L.lds) L.lds_bytes = 0;
@@ -56,6 +68,7 @@ hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream
   prm.nchunks = num_chunks(g.K);
   prm.groups = padded_rows(g.N) / kRowGroup;
   const XorLaunch L = xor_launch_shape(g.M, g.N, g.K, g.p, g.q, cfg);
+  prm.ksplit = L.ksplit;
   switch (g.p) {
     case 1: return xorpop::launch_for_p<1>(g.q, prm, L, stream);
     case 2: return xorpop::launch_for_p<2>(g.q, prm, L, stream);

@@ -264,9 +264,10 @@ int table_size() {
 // workgroups, and the split launches the model considers (a main shape over
 // whole rounds of columns, a smaller shape on the rest); each of these again
 // on the FP4 route where it applies (FP4 or FP8 activations).
-// The most configs candidate_configs can list: XOR, +-1 planes, then for each
+// The most configs candidate_configs can list: XOR (three launch shapes),
+// +-1 planes, then for each
 // operand format every shape twice and every main shape with every tail.
-static_assert(2 + 2 * (2 * kNumInt8Shapes + kNumMainShapes * (kNumInt8Shapes - kFirstTail)) <=
+static_assert(4 + 2 * (2 * kNumInt8Shapes + kNumMainShapes * (kNumInt8Shapes - kFirstTail)) <=
                   kMaxCandidates,
               "the search module's candidate list must hold every config");
 
@@ -275,9 +276,17 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
   auto add = [&](const apt_config_t& c) {
     if (n < max_out) out[n++] = c;
   };
-  apt_config_t x = base_config(APT_ROUTE_XOR);
-  x.mt = 8;
-  add(x);
+  // the XOR route with the library's launch shape, and with the K split
+  // forced off and on
+  for (int ks = 0; ks <= 4; ks += 4) {
+    apt_config_t x = base_config(APT_ROUTE_XOR);
+    x.waves_n = ks;
+    add(x);
+    if (ks == 0) {
+      x.waves_n = 1;
+      add(x);
+    }
+  }
   if (p <= 7 && q <= 7) add(base_config(APT_ROUTE_PM1_MFMA));
   const int cus = compute_units();
   auto int8_cfg = [&](const Int8Shape& s, int grid) {
@@ -329,11 +338,7 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
   apt_config_t hit;
   if (table_lookup(M, N, K, p, q, &hit)) return hit;
   if (M > 8 && shipped_lookup(M, N, K, p, q, &hit)) return hit;
-  if (M <= 8) {
-    apt_config_t c = base_config(APT_ROUTE_XOR);
-    c.mt = 8;
-    return c;
-  }
+  if (M <= 8) return base_config(APT_ROUTE_XOR);  // launch shape chosen by the route
   const int cus = compute_units();
   // Candidates: each shape alone, with one workgroup per tile or a
   // persistent grid of one round; and each main shape over the columns that
@@ -384,11 +389,7 @@ apt_config_t select_config(int M, int N, int K, int p, int q) {
   // fixed costs.  The MFMA figures were measured with every compute unit
   // busy and overstate grids of a few tiles by 10-40%, so they count at 90%
   // here (measured over M = 16..256, N, K = 1024..14336, p*q = 2..16).
-  if (model_xor_us(M, N, K, p, q) < 0.9 * best) {
-    apt_config_t c = base_config(APT_ROUTE_XOR);
-    c.mt = 8;
-    return c;
-  }
+  if (model_xor_us(M, N, K, p, q) < 0.9 * best) return base_config(APT_ROUTE_XOR);
   const Int8Shape& s = kInt8Shapes[best_i];
   apt_config_t c = base_config(best_fp4 ? APT_ROUTE_FP4_MFMA : APT_ROUTE_INT8_MFMA);
   c.bm = s.bm;

@@ -20,11 +20,14 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
     del K
     out = [("xor", apt.apt_config_t.make(apt.APT_ROUTE_XOR))]
     # XOR route launch shapes: activation rows per block row (1 or 8), waves per
-    # workgroup
+    # workgroup (one row group each), or the K split over 2 or 4 waves
     for mt in (1, 8):
         for waves in (1, 2, 4):
-            c = apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_m=waves, mt=mt)
+            c = apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_m=waves, waves_n=1, mt=mt)
             out.append(("xor_mt%d_w%d" % (mt, waves), c))
+        for ks in (2, 4):
+            c = apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_n=ks, mt=mt)
+            out.append(("xor_mt%d_ks%d" % (mt, ks), c))
     for bm, bn, wm, wn in INT8_SHAPES:
         for grid in (0, 256, 7, 300):
             c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, bm, bn, 128, wm, wn, grid, 3)

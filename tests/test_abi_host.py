@@ -151,6 +151,10 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
      apt.APT_ERR_INVALID_ARG),
     (dict(p=8, cfg=apt.apt_config_t.make(apt.APT_ROUTE_PM1_MFMA)), apt.APT_ERR_UNSUPPORTED),
     (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=3)), apt.APT_ERR_INVALID_ARG),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_m=3)), apt.APT_ERR_INVALID_ARG),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_n=8)), apt.APT_ERR_INVALID_ARG),
+    # one activation row per block row: M block rows, at most 65535
+    (dict(M=65536, cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=1)), apt.APT_ERR_UNSUPPORTED),
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_WORKSPACE),
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2), ws=WS,
