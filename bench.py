@@ -21,6 +21,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import subprocess
 import sys
 import time
@@ -1144,7 +1145,9 @@ def workloads_run(calls: int = 20):
     first, then, workload by workload, one torch fill of a marker buffer (a
     kernel that separates the workloads in the trace) and `calls` back-to-back
     apt_gemm calls in the selected config (int32 output, plus the fp16
-    epilogue where the workload has scales).  Prints the plan as JSON."""
+    epilogue where the workload has scales); then the same for the activation
+    packers of the decode workloads (code and fp16 sources).  Prints the plan
+    as JSON."""
     import numpy as np
     import torch
 
@@ -1180,6 +1183,36 @@ def workloads_run(calls: int = 20):
                      "q": prob.q, "ops": prob.ops, "fp16": c16 is not None, "calls": calls,
                      "config": cfg.as_dict()})
         del ws, c32, c16
+    # the activation packers of the decode workloads (M <= 8, K = 4096): the
+    # code source and the fp16 quantizer, `calls` back-to-back calls each
+    seen = set()
+    for prob, a, w, sa, sw in items:
+        if prob.M > 8 or (prob.M, prob.K, prob.q) in seen:
+            continue
+        seen.add((prob.M, prob.K, prob.q))
+        codes = dev(prob.a_codes)
+        x16 = torch.from_numpy(np.ascontiguousarray(
+            (prob.a_codes.astype(np.float32) * 0.37).astype(np.float16))).cuda()
+        buf = torch.empty(apt.apt_packed_bytes(prob.M, prob.K, prob.q), dtype=torch.uint8, device="cuda")
+        rs = torch.empty(prob.M, dtype=torch.int32, device="cuda")
+        sc = torch.empty(prob.M, dtype=torch.float16, device="cuda")
+        sp = torch.cuda.current_stream().cuda_stream
+        for kind in ("codes", "fp16"):
+            marker.fill_(len(plan))
+            for _ in range(calls):
+                if kind == "codes":
+                    st = apt.apt_quantize_pack_activations(codes.data_ptr(), prob.M, prob.K, prob.q,
+                                                           buf.data_ptr(), rs.data_ptr(), sp)
+                else:
+                    st = apt.apt_quantize_pack_activations_fp16(x16.data_ptr(), prob.M, prob.K, prob.q,
+                                                                buf.data_ptr(), rs.data_ptr(),
+                                                                sc.data_ptr(), sp)
+                apt.check(st, "pack")
+            torch.cuda.synchronize()
+            plan.append({"workload": "pack_%s_m%d_k%d_q%d" % (kind, prob.M, prob.K, prob.q),
+                         "M": prob.M, "K": prob.K, "q": prob.q, "calls": calls, "pack": kind,
+                         "bytes": prob.M * prob.K * (1 if kind == "codes" else 2)
+                         + apt.apt_packed_bytes(prob.M, prob.K, prob.q) + 4 * prob.M})
     print(json.dumps(plan), flush=True)
 
 
@@ -1197,7 +1230,7 @@ def write_workload_stats(trace_csv: str, plan_json: str, command: str):
         if "FillFunctor" in name or "fill" in name.lower():
             cur = []
             segs.append(cur)
-        elif cur is not None:
+        elif cur is not None and "rocclr" not in name:  # (host-to-device copies are not timed)
             cur.append((name, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0))
     assert len(segs) == len(plan), (len(segs), len(plan))
     lines = ["# Kernel durations of every workload configuration in its selected config (rocprofv3",
@@ -1220,10 +1253,17 @@ def write_workload_stats(trace_csv: str, plan_json: str, command: str):
             ts = [t for k, t in body if k == n]
             med = statistics.median(ts)
             total += med * len(ts) / (pl["calls"] - 1)
-            short = n.split("(")[0].replace("void ", "").replace("apt::", "")
+            short = re.sub(r"\(anonymous namespace\)::", "", n)
+            short = short.split("(")[0].replace("void ", "").replace("apt::", "")
             parts.append("%s median %.2f mean %.2f" % (short, med, statistics.mean(ts)))
+        if "pack" in pl:
+            lines.append("%-32s %-28s per call %8.2f us  %8.1f GB/s" % (
+                pl["workload"], "packer (%s source)" % pl["pack"], total, pl["bytes"] / total / 1e3))
+            for ptxt in parts:
+                lines.append("    " + ptxt)
+            continue
         c = pl["config"]
-        route = {1: "xor", 2: "pm1", 3: "int8", 4: "fp4"}[c["route"]]
+        route = {1: "xor", 2: "pm1", 3: "int8", 4: "fp4", 5: "fp6"}[c["route"]]
         cfg = route if route == "xor" else "%s %dx%d/%dx%d g%d%s" % (
             route, c["bm"], c["bn"], c["waves_m"], c["waves_n"], c["grid"],
             " split %d" % c["split_n"] if c["split_n"] else "")

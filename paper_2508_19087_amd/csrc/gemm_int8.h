@@ -165,24 +165,26 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
                                                        int nchunks, int nsteps, int mblocks,
                                                        v4i* __restrict__ out, int* __restrict__ counters,
                                                        int ncounters) {
-  // One thread per (word w, row, chunk), w fastest: 4 threads read one row's
-  // 16 contiguous bytes of a plane, so a wave reads whole 128-byte lines.
+  // One thread per (word w, row) of chunk blockIdx.y, w fastest: 4 threads
+  // read one row's 16 contiguous bytes of a plane, so a wave reads whole
+  // 128-byte lines.  (A two-dimensional grid keeps the index arithmetic in
+  // 32 bits: no division by the row count per thread.)
   const int rows = mblocks * 32;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int t = blockIdx.x * (int)blockDim.x + threadIdx.x;
   // The stream-K arrival counters of this call start cleared (the GEMM
   // launch follows in stream order).
-  if (t < ncounters) counters[t] = 0;
+  if (blockIdx.y == 0)
+    for (int i = t; i < ncounters; i += gridDim.x * blockDim.x) counters[i] = 0;
+  if (t >= rows * kWordsPerPlane) return;
+  const int w = t % kWordsPerPlane;
+  const int row = t / kWordsPerPlane;
+  const int chunk = blockIdx.y;
   constexpr int kSteps = Fmt<F>::kSteps;
-  if (t >= (int64_t)rows * (nsteps / kSteps) * kWordsPerPlane) return;
-  const int w = (int)(t % kWordsPerPlane);
-  const int64_t rc = t / kWordsPerPlane;
-  const int row = (int)(rc % rows);
-  const int chunk = (int)(rc / rows);
   uint32_t pw[Q];
   if (row < M && chunk < nchunks) {
     const uint32_t* src = a_packed + plane_words(row, chunk, 0, nchunks, Q) + w;
 #pragma unroll
-    for (int j = 0; j < Q; ++j) pw[j] = src[j * kPlaneStride];
+    for (int j = 0; j < Q; ++j) pw[j] = __builtin_nontemporal_load(src + j * kPlaneStride);
   } else {
 #pragma unroll
     for (int j = 0; j < Q; ++j) pw[j] = 0u;

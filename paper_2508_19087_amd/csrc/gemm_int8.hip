@@ -132,6 +132,8 @@ bool int8_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
   // tile and chunk-pair counts are 32-bit in the plans and kernels (smallest tile 128x128)
   const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + 127) / 128);
   if (tiles * (((int64_t)num_chunks(K) + 1) / 2) >= ((int64_t)1 << 31)) return false;
+  // the activation expansion runs one grid row per chunk (an even count)
+  if (((num_chunks(K) + 1) & ~1) > 65535) return false;
   int8::Plan pl[2];
   const int n = int8::make_plans(M, N, K, cfg, pl);
   for (int i = 0; i < n; ++i)

@@ -38,11 +38,10 @@ hipError_t launch_pair_for_p(int fmt, int sa, const Int8Params& pa, int ga, int 
 template <int Q, int F>
 hipError_t launch_expand(const uint32_t* a_packed, int M, int nchunks, int nsteps, int mblocks,
                          v4i* out, int* counters, int ncounters, hipStream_t stream) {
-  int64_t threads = (int64_t)mblocks * 32 * (nsteps / Fmt<F>::kSteps) * kWordsPerPlane;
-  if (threads < ncounters) threads = ncounters;
-  const int blocks = (int)((threads + 255) / 256);
-  return launch_kernel(expand_a_kernel<Q, F>, dim3(blocks), dim3(256), 0, stream, a_packed, M,
-                       nchunks, nsteps, mblocks, out, counters, ncounters);
+  // x: (row, word) pairs of one chunk; y: the chunks (an even count)
+  const int blocks = (mblocks * 32 * kWordsPerPlane + 255) / 256;
+  return launch_kernel(expand_a_kernel<Q, F>, dim3(blocks, nsteps / Fmt<F>::kSteps), dim3(256), 0,
+                       stream, a_packed, M, nchunks, nsteps, mblocks, out, counters, ncounters);
 }
 
 template <int Q>

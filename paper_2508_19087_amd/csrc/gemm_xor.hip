@@ -43,13 +43,15 @@ XorLaunch xor_launch_shape(int M, int N, int K, int p, int q, const apt_config_t
   // the plain form (8 / p chunks per lane)
   const int wave_rounds = (rounds + L.ksplit - 1) / L.ksplit;
   L.deep = L.mt == 1 && wave_rounds > std::max(1, 8 / p);
-  // four waves per workgroup, two in the deep form (cold weights on MI355X:
-  // four equal within noise at 4 MB and 4-10% faster from 22 MB up and with
-  // eight activation rows; two 4% faster at K = 11008)
+  // waves per workgroup: one while the row groups alone would not give every
+  // compute unit a workgroup of four (so that they spread over all compute
+  // units), two in the deep form, else four (cold weights on MI355X: equal
+  // within noise at 4 MB, four 4-10% faster from 22 MB up and with eight
+  // activation rows, two 4% faster at K = 11008)
   if (L.ksplit > 1)
     L.waves = L.ksplit;
   else
-    L.waves = cfg.waves_m != 0 ? cfg.waves_m : (L.deep ? 2 : 4);
+    L.waves = cfg.waves_m != 0 ? cfg.waves_m : groups < 1024 ? 1 : (L.deep ? 2 : 4);
   L.grid = dim3(L.ksplit > 1 ? groups : (groups + L.waves - 1) / L.waves, (M + L.mt - 1) / L.mt);
   L.lds_bytes = act_lds_bytes_q(q, L.mt, num_chunks(K));
   L.lds = L.lds_bytes <= xorpop::kMaxActLds;
