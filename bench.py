@@ -390,10 +390,12 @@ def calibrate(calls: int = 20):
 
 def format_sweep(calls: int = 20):
     """The operand formats of the reassembled MFMA route against each other:
-    int8 and FP6 (E2M3) operands on every tile shape, with one workgroup per
-    tile and with one persistent round, on the W3A3 down projection
-    (512x4096x11008) and W3A3 2048x11008x4096 and 1024x4096x4096; HIP events
-    around `calls` back-to-back apt_gemm calls (warm weights, int32 output)."""
+    int8 against FP6 (E2M3) operands on W3A3 problems (the W3A3 down
+    projection 512x4096x11008, 2048x11008x4096 and 1024x4096x4096) and int8
+    against FP8 (E4M3) operands on W4A4 problems (2048x11008x4096, the prefill
+    workload, and 512x4096x11008), on every tile shape with one workgroup per
+    tile and with one persistent round; HIP events around `calls`
+    back-to-back apt_gemm calls (warm weights, int32 output)."""
     import numpy as np
     import torch
 
@@ -403,7 +405,8 @@ def format_sweep(calls: int = 20):
     shapes = [(256, 256, 4, 2, 1), (512, 128, 8, 1, 1), (256, 128, 4, 1, 2), (256, 128, 4, 2, 1),
               (128, 128, 2, 2, 2)]
     probs = [synth.sweep_down(3), synth.random_problem(synth.rng(9), 2048, 11008, 4096, 3, 3),
-             synth.random_problem(synth.rng(10), 1024, 4096, 4096, 3, 3)]
+             synth.random_problem(synth.rng(10), 1024, 4096, 4096, 3, 3), synth.w4a4_prefill(),
+             synth.random_problem(synth.rng(11), 512, 4096, 11008, 4, 4)]
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     sp = torch.cuda.current_stream().cuda_stream
     rows = []
@@ -411,11 +414,13 @@ def format_sweep(calls: int = 20):
         a = apt.pack(dev(prob.a_codes), prob.q, activations=True)
         w = apt.pack(dev(prob.w_codes), prob.p)
         c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+        fl_name, fl_route = (("fp6_us", apt.APT_ROUTE_FP6_MFMA) if max(prob.p, prob.q) <= 3
+                             else ("fp8_us", apt.APT_ROUTE_FP8_MFMA))
         for bm, bn, wm, wn, per_cu in shapes:
             for grid in (0, cus * per_cu):
                 row = {"problem": "%dx%dx%d W%dA%d" % (prob.M, prob.N, prob.K, prob.p, prob.q),
                        "shape": "%dx%d/%dx%d g%d" % (bm, bn, wm, wn, grid)}
-                for name, route in (("int8_us", apt.APT_ROUTE_INT8_MFMA), ("fp6_us", apt.APT_ROUTE_FP6_MFMA)):
+                for name, route in (("int8_us", apt.APT_ROUTE_INT8_MFMA), (fl_name, fl_route)):
                     cfg = apt.apt_config_t.make(route, bm, bn, 128, wm, wn, grid, 3)
                     wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
                     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
@@ -437,8 +442,9 @@ def format_sweep(calls: int = 20):
                     row[name] = round(e0.elapsed_time(e1) * 1e3 / calls, 2)
                     del ws
                 rows.append(row)
-                log("bench: formats %s %s int8 %.2f fp6 %.2f us" % (row["problem"], row["shape"],
-                                                                     row["int8_us"], row["fp6_us"]))
+                log("bench: formats %s %s int8 %.2f %s %.2f us" % (row["problem"], row["shape"],
+                                                                    row["int8_us"], fl_name[:3],
+                                                                    row[fl_name]))
         del a, w, c32
     return rows
 
@@ -1355,7 +1361,7 @@ def main():
                     help="print the MFMA-issue probe's cycles per MFMA for each part of the GEMM "
                          "loop's instruction pattern and exit")
     ap.add_argument("--format-sweep", action="store_true",
-                    help="print int8 against FP6 operands on every tile shape for W3A3 shapes and exit")
+                    help="print int8 against FP6 (W3A3) and FP8 (W4A4) operands on every tile shape and exit")
     ap.add_argument("--workloads", action="store_true",
                     help="for a rocprofv3 kernel trace: every workload configuration's selected "
                          "apt_gemm, 20 calls each, separated by marker fills; prints the plan")

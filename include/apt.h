@@ -77,8 +77,10 @@ enum {
                                block-scaled MFMA: FP4 (E2M1) weights, p <= 2, and FP4 (q <= 2) or
                                FP8 E4M3 (q <= 4) activations; K_pad (2^p-1)(2^q-1) < 2^24,
                                K_pad = K rounded up to a multiple of 128 */
-  APT_ROUTE_FP6_MFMA = 5    /* as APT_ROUTE_FP4_MFMA with FP6 (E2M3) weights and activations,
+  APT_ROUTE_FP6_MFMA = 5,   /* as APT_ROUTE_FP4_MFMA with FP6 (E2M3) weights and activations,
                                p, q <= 3; K_pad (2^p-1)(2^q-1) < 2^24 */
+  APT_ROUTE_FP8_MFMA = 6    /* as APT_ROUTE_FP4_MFMA with FP8 (E4M3) weights and activations,
+                               p, q <= 4; K_pad (2^p-1)(2^q-1) < 2^24 */
 };
 
 /* Kernel configuration (the tunable hyperparameters of Sec. V-A in gfx950

@@ -8,7 +8,7 @@ hand-written HIP kernels behind the C ABI of include/apt.h (libapt.so); this
 package is its Python binding.
 """
 from .apt import (APT_ERR_HIP, APT_ERR_INVALID_ARG, APT_ERR_UNSUPPORTED, APT_ERR_WORKSPACE,  # noqa: F401
-                  APT_OK, APT_ROUTE_AUTO, APT_ROUTE_FP4_MFMA, APT_ROUTE_FP6_MFMA, APT_ROUTE_INT8_MFMA, APT_ROUTE_PM1_MFMA, APT_ROUTE_XOR,
+                  APT_OK, APT_ROUTE_AUTO, APT_ROUTE_FP4_MFMA, APT_ROUTE_FP6_MFMA, APT_ROUTE_FP8_MFMA, APT_ROUTE_INT8_MFMA, APT_ROUTE_PM1_MFMA, APT_ROUTE_XOR,
                   ROUTE_NAMES, AptError, Packed, apt_config_t, apt_gemm, apt_gemm_affine,
                   apt_gemm_workspace_bytes, apt_config_table_clear, apt_config_table_size,
                   apt_last_hip_error, apt_gemm_noalloc,

@@ -29,9 +29,10 @@ APT_ROUTE_PM1_MFMA = 2
 APT_ROUTE_INT8_MFMA = 3
 APT_ROUTE_FP4_MFMA = 4
 APT_ROUTE_FP6_MFMA = 5
+APT_ROUTE_FP8_MFMA = 6
 ROUTE_NAMES = {APT_ROUTE_XOR: "xor_popcount", APT_ROUTE_PM1_MFMA: "pm1_planes_mfma",
                APT_ROUTE_INT8_MFMA: "reassembled_int8_mfma", APT_ROUTE_FP4_MFMA: "reassembled_fp4_mfma",
-               APT_ROUTE_FP6_MFMA: "reassembled_fp6_mfma"}
+               APT_ROUTE_FP6_MFMA: "reassembled_fp6_mfma", APT_ROUTE_FP8_MFMA: "reassembled_fp8_mfma"}
 
 
 class apt_config_t(ctypes.Structure):

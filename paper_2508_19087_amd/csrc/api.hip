@@ -62,6 +62,9 @@ apt_status_t check_config(const apt_config_t& c, int M, int N, int K, int p, int
     case APT_ROUTE_FP6_MFMA:
       if (c.route == APT_ROUTE_FP6_MFMA && !apt::fp6_route_ok(K, p, q)) return APT_ERR_UNSUPPORTED;
       [[fallthrough]];
+    case APT_ROUTE_FP8_MFMA:
+      if (c.route == APT_ROUTE_FP8_MFMA && !apt::fp8_route_ok(K, p, q)) return APT_ERR_UNSUPPORTED;
+      [[fallthrough]];
     case APT_ROUTE_INT8_MFMA:
       if (!apt::int8_config_ok(c, N)) return APT_ERR_INVALID_ARG;
       if (!have_rowsums) return APT_ERR_INVALID_ARG;
@@ -184,7 +187,8 @@ apt_status_t gemm_launch(int M, int N, int K, int p, int q, const void* a_packed
     case APT_ROUTE_XOR: return hip_status(launch_gemm_xor(g, c, s));
     case APT_ROUTE_INT8_MFMA:
     case APT_ROUTE_FP4_MFMA:
-    case APT_ROUTE_FP6_MFMA: return hip_status(launch_gemm_int8(g, c, workspace, s));
+    case APT_ROUTE_FP6_MFMA:
+    case APT_ROUTE_FP8_MFMA: return hip_status(launch_gemm_int8(g, c, workspace, s));
     case APT_ROUTE_PM1_MFMA: return hip_status(launch_gemm_pm1(g, c, s));
   }
   return APT_ERR_INVALID_ARG;

@@ -55,9 +55,16 @@ inline bool fp6_route_ok(int K, int p, int q) {
   return p <= 3 && q <= 3 &&
          (int64_t)num_chunks(K) * kChunk * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
 }
-// Routes that run the reassembled MFMA kernels (operand formats int8, FP4, FP6).
+// The FP8 MFMA route applies to (p, q) over K: E4M3 holds bipolar values of
+// at most 4 bits, and the fp32 sums stay exact as for the FP4 route.
+inline bool fp8_route_ok(int K, int p, int q) {
+  return p <= 4 && q <= 4 &&
+         (int64_t)num_chunks(K) * kChunk * ((1 << p) - 1) * ((1 << q) - 1) < ((int64_t)1 << 24);
+}
+// Routes that run the reassembled MFMA kernels (operand formats int8, FP4, FP6, FP8).
 inline bool mfma_route(int route) {
-  return route == APT_ROUTE_INT8_MFMA || route == APT_ROUTE_FP4_MFMA || route == APT_ROUTE_FP6_MFMA;
+  return route == APT_ROUTE_INT8_MFMA || route == APT_ROUTE_FP4_MFMA || route == APT_ROUTE_FP6_MFMA ||
+         route == APT_ROUTE_FP8_MFMA;
 }
 inline int padded_rows(int R) { return (R + kRowGroup - 1) / kRowGroup * kRowGroup; }
 

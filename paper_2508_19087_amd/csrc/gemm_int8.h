@@ -73,11 +73,16 @@ constexpr int kFragVecs = kWave;                // one 32x32 fragment = 64 lanes
 //          lane and k-step, 64 elements of k per MFMA).  Each lane half's 24
 //          bytes sit in a 32-byte slot of the LDS row and in two 16-byte
 //          fragment vectors (the second half-used).
+//   F = 4: FP8 (E4M3) weights and activations of at most 4 bits, the same
+//          MFMA with both operands in E4M3 (32 operand bytes per lane and
+//          k-step, 64 elements of k per MFMA, the int8 multiply-add rate):
+//          lane half h of k-step ks holds the 32 bytes of word 2 ks + h in the
+//          order of the int8 byte tree, on both sides, so equal elements meet.
 template <int F>
 struct Fmt {
   static constexpr int kStepK = F ? 64 : 32;                   // k per MFMA
   static constexpr int kSteps = kChunk / kStepK;               // k-steps per chunk
-  static constexpr int kStepRowBytes = F == 3 ? 2 * kStepBytes : kStepBytes;  // LDS row bytes per k-step
+  static constexpr int kStepRowBytes = F >= 3 ? 2 * kStepBytes : kStepBytes;  // LDS row bytes per k-step
   static constexpr int kHalfBytes = kStepRowBytes / 2;         // per lane half
   static constexpr int kRowBytes = kSteps * kStepRowBytes + 16;  // padded LDS row of a chunk
   static constexpr int kAVecs = F >= 2 ? 2 : 1;                // 16-byte activation vectors per lane and k-step
@@ -190,7 +195,15 @@ __global__ __launch_bounds__(256) void expand_a_kernel(const uint32_t* __restric
     for (int j = 0; j < Q; ++j) pw[j] = 0u;
   }
   const int mb = row / 32, l = row % 32;
-  if (F == 3) {
+  if (F == 4) {
+    // word w -> k-step w / 2, lane half w mod 2; vector 0 holds operand dwords
+    // 0..3, vector 1 dwords 4..7
+    uint32_t o[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (chunk < nchunks) fp8_word<(Q <= 4 ? Q : 4)>(pw, o);
+    v4i* f = out + ((int64_t)mb * nsteps + chunk * kSteps + w / 2) * 2 * kFragVecs;
+    f[(w % 2) * 32 + l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    f[kFragVecs + (w % 2) * 32 + l] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+  } else if (F == 3) {
     // word w -> k-step w / 2, lane half w mod 2; vector 0 holds operand dwords
     // 0..3, vector 1 dwords 4..5
     uint32_t o[6] = {0u, 0u, 0u, 0u, 0u, 0u};
@@ -293,6 +306,18 @@ struct Stage {
     const int r = item % ROWS;
     const int sub = item / ROWS;
     uint32_t o[4];
+    if (F == 4) {
+      if (h != 0) return;
+      uint32_t pw[B], o8[8];
+#pragma unroll
+      for (int i = 0; i < B; ++i) pw[i] = raw[it][i][w];
+      fp8_word<(B <= 4 ? B : 4)>(pw, o8);
+      const int wc = sub * kWpi + w;  // word of the chunk -> k-step wc / 2, lane half wc mod 2
+      uint8_t* d = lds_tile + r * kRowBytes + (wc / 2) * Fmt<F>::kStepRowBytes + (wc % 2) * Fmt<F>::kHalfBytes;
+      *reinterpret_cast<uint4*>(d) = make_uint4(o8[0], o8[1], o8[2], o8[3]);
+      *reinterpret_cast<uint4*>(d + 16) = make_uint4(o8[4], o8[5], o8[6], o8[7]);
+      return;
+    }
     if (F == 3) {
       if (h != 0) return;
       uint32_t pw[B], o6[6];
@@ -450,8 +475,8 @@ struct Stream {
 // call it; `lds` is the dynamic LDS of the launch).
 template <int P, int F, int BM, int BN, int WM, int WN, int SPLIT>
 __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* lds, int w, int G) {
-  static_assert(F == 0 || P <= (F == 3 ? 3 : 2),
-                "FP4 operands hold weights of at most 2 bits, FP6 operands at most 3");
+  static_assert(F == 0 || P <= (F == 4 ? 4 : F == 3 ? 3 : 2),
+                "FP4 operands hold weights of at most 2 bits, FP6 at most 3, FP8 at most 4");
   constexpr int kSteps = Fmt<F>::kSteps;
   constexpr int kAVecs = Fmt<F>::kAVecs;
   constexpr int kRowBytes = Fmt<F>::kRowBytes;
@@ -550,12 +575,14 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
   const int w_lane = (wn * WTN + lrow) * kRowBytes + lk;
   v4i wf[2][FN];
   v2i wf6[2][F == 3 ? FN : 1];  // FP6: operand dwords 4..5
+  v4i wf8[2][F == 4 ? FN : 1];  // FP8: operand dwords 4..7
   auto read_wf = [&](const uint8_t* stage, int ks, int sl) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < FN; ++b) {
       const uint8_t* src = stage + w_lane + b * 32 * kRowBytes + ks * Fmt<F>::kStepRowBytes;
       wf[sl][b] = *reinterpret_cast<const v4i*>(src);
       if constexpr (F == 3) wf6[sl][b] = *reinterpret_cast<const v2i*>(src + 16);
+      if constexpr (F == 4) wf8[sl][b] = *reinterpret_cast<const v4i*>(src + 16);
     }
   };
 
@@ -584,7 +611,16 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
       for (int b = 0; b < FN; ++b)
 #pragma unroll
         for (int a = 0; a < FM; ++a)
-          if constexpr (F == 3) {
+          if constexpr (F == 4) {
+            // E4M3 weights and activations (format code 0), unit E8M0 scales (127)
+            const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3],
+                            wf8[cur][b][0], wf8[cur][b][1], wf8[cur][b][2], wf8[cur][b][3]};
+            const v4i a0 = afr[2 * ks][a], a1 = afr[2 * ks + 1][a];
+            const v8i ab = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+            acc[b][a] = __builtin_bit_cast(
+                v16i, __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                          wa, ab, __builtin_bit_cast(v16f, acc[b][a]), 0, 0, 0, 127, 0, 127));
+          } else if constexpr (F == 3) {
             // E2M3 weights and activations (format code 2), unit E8M0 scales (127)
             const v8i wa = {wf[cur][b][0], wf[cur][b][1], wf[cur][b][2], wf[cur][b][3],
                             wf6[cur][b][0], wf6[cur][b][1], 0, 0};

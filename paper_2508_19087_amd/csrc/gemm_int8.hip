@@ -50,8 +50,10 @@ hipError_t launch_pair(int p, int fmt, int sa, const Int8Params& pa, int ga, int
 }
 
 // Operand format of a config (the F of the kernels): int8 for the int8 route;
-// for the FP4 route FP4 activations when q <= 2, FP8 activations otherwise.
+// for the FP4 route FP4 activations when q <= 2, FP8 activations otherwise;
+// FP6 and FP8 operands for the FP6 and FP8 routes.
 int operand_format(const apt_config_t& cfg, int q) {
+  if (cfg.route == APT_ROUTE_FP8_MFMA) return 4;
   if (cfg.route == APT_ROUTE_FP6_MFMA) return 3;
   if (cfg.route != APT_ROUTE_FP4_MFMA) return 0;
   return q <= 2 ? 1 : 2;

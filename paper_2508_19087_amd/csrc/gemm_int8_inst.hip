@@ -1,8 +1,8 @@
 // gemm_int8_inst.hip - instantiates the reassembled MFMA kernels for one bit
 // width, APT_INST_P: the main kernel for weight width APT_INST_P and the
 // activation expansion for activation width APT_INST_P, with int8 operands
-// and, where the widths allow, FP4 weights with FP4 or FP8 activations (the
-// build compiles this file once per width).
+// and, where the widths allow, FP4 weights with FP4 or FP8 activations, FP6
+// operands and FP8 operands (the build compiles this file once per width).
 #include "gemm_int8.h"
 
 namespace apt {
@@ -18,6 +18,9 @@ hipError_t launch_for_p(int fmt, int shape, const Int8Params& prm, int grid, hip
   if constexpr (P <= 3) {
     if (fmt == 3) return launch_p_shape<P, 3>(shape, prm, grid, stream);
   }
+  if constexpr (P <= 4) {
+    if (fmt == 4) return launch_p_shape<P, 4>(shape, prm, grid, stream);
+  }
   return hipErrorInvalidValue;
 }
 
@@ -31,6 +34,9 @@ hipError_t launch_pair_for_p(int fmt, int sa, const Int8Params& pa, int ga, int 
   }
   if constexpr (P <= 3) {
     if (fmt == 3) return launch_p_pair<P, 3>(sa, pa, ga, sb, pb, gb, stream);
+  }
+  if constexpr (P <= 4) {
+    if (fmt == 4) return launch_p_pair<P, 4>(sa, pa, ga, sb, pb, gb, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -64,6 +70,11 @@ hipError_t launch_expand_for_q(int fmt, const uint32_t* a_packed, int M, int nch
   if constexpr (Q <= 3) {
     if (fmt == 3)
       return launch_expand<Q, 3>(a_packed, M, nchunks, nsteps, mblocks, out, counters, ncounters,
+                                 stream);
+  }
+  if constexpr (Q <= 4) {
+    if (fmt == 4)
+      return launch_expand<Q, 4>(a_packed, M, nchunks, nsteps, mblocks, out, counters, ncounters,
                                  stream);
   }
   return hipErrorInvalidValue;

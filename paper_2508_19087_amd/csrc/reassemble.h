@@ -191,6 +191,52 @@ __device__ __forceinline__ void fp6_word(const uint32_t* pw, uint32_t out[6]) {
   out[5] = (y[6] >> 16) | (y[7] << 8);
 }
 
+// FP8 operand bytes (OCP E4M3: sign bit 7, exponent bits 6..3 with bias 7,
+// mantissa bits 2..0) of the 32 elements of plane words pw[0..B-1], B <= 4.
+// Every bipolar value of up to 4 bits (odd, |v| <= 15) is exact in E4M3.  The
+// words u are rebuilt as bytes (the int8 tree, same element order) and each
+// byte becomes the E4M3 code of v = 2u - (2^B - 1) through a byte permute over
+// the 8-entry table of u mod 8, plus, for B = 4, a second table for u >= 8
+// chosen by bit 3 of the byte.
+template <int B>
+__host__ __device__ constexpr uint32_t e4m3_of_word(uint32_t u) {
+  const int v = 2 * (int)u - ((1 << B) - 1);
+  const int a = v < 0 ? -v : v;
+  // |v| = 1, 3, ..., 15: exponent field 7 + floor(log2 |v|), 3 mantissa bits
+  const int e = a >= 8 ? 3 : a >= 4 ? 2 : a >= 2 ? 1 : 0;
+  const uint32_t bits = (uint32_t)(((e + 7) << 3) | (((a << 3) >> e) & 7));
+  return v < 0 ? bits | 0x80u : bits;
+}
+
+template <int B>
+__host__ __device__ constexpr uint32_t e4m3_table(int quarter) {
+  // bytes 4 quarter .. 4 quarter + 3 of the table indexed by u (entries past 2^B unused)
+  uint32_t t = 0u;
+  for (int j = 0; j < 4; ++j) {
+    const int u = 4 * quarter + j;
+    t |= (u < (1 << B) ? e4m3_of_word<B>((uint32_t)u) : 0u) << (8 * j);
+  }
+  return t;
+}
+
+template <int B>
+__device__ __forceinline__ uint32_t e4m3_dword(uint32_t by) {
+  static_assert(B >= 1 && B <= 4, "E4M3 holds bipolar values of up to 4 bits");
+  if (B <= 3) return __builtin_amdgcn_perm(e4m3_table<B>(1), e4m3_table<B>(0), by);
+  const uint32_t lo = by & 0x07070707u;
+  const uint32_t c0 = __builtin_amdgcn_perm(e4m3_table<B>(1), e4m3_table<B>(0), lo);
+  const uint32_t c1 = __builtin_amdgcn_perm(e4m3_table<B>(3), e4m3_table<B>(2), lo);
+  const uint32_t hi = ((by >> 3) & 0x01010101u) * 0xFFu;  // 0xFF in the bytes with u >= 8
+  return (c1 & hi) | (c0 & ~hi);  // (a per-lane mask: one v_bfi_b32)
+}
+
+template <int B>
+__device__ __forceinline__ void fp8_word(const uint32_t* pw, uint32_t out[8]) {
+  reassemble_word<B>(pw, out);  // byte j of out[t]: u of element 8 j + t
+#pragma unroll
+  for (int t = 0; t < 8; ++t) out[t] = e4m3_dword<B>(out[t]);
+}
+
 // Operand offset of the reassembled byte y: bipolar value v = 2 y + c.
 //   B <= 7: y = u,        v = 2u - (2^B - 1)  ->  c = 1 - 2^B
 //   B == 8: y = u - 128,  v = 2u - 255        ->  c = 1

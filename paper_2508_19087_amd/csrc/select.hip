@@ -216,6 +216,7 @@ bool shipped_lookup(int M, int N, int K, int p, int q, apt_config_t* out) {
     if (mfma_route(c.route) && (!int8_config_ok(c, N) || !int8_sizes_ok(M, N, K, p, q, c))) continue;
     if (c.route == APT_ROUTE_FP4_MFMA && !fp4_route_ok(K, p, q)) continue;
     if (c.route == APT_ROUTE_FP6_MFMA && !fp6_route_ok(K, p, q)) continue;
+    if (c.route == APT_ROUTE_FP8_MFMA && !fp8_route_ok(K, p, q)) continue;
     best = d;
     hit = &e;
   }
@@ -319,11 +320,13 @@ int candidate_configs(int M, int N, int K, int p, int q, apt_config_t* out, int 
       add(c);
     }
   }
-  // the same tile configs with FP4 operands where they apply, and with FP6
-  // operands where those apply and FP4 does not (p or q = 3)
+  // the same tile configs with FP4 operands where they apply, with FP6
+  // operands where those apply and FP4 does not (p or q = 3), and with FP8
+  // operands where neither applies (p or q = 4)
   const int end = n;
-  const int route = fp4_route_ok(K, p, q) ? APT_ROUTE_FP4_MFMA
-                    : fp6_route_ok(K, p, q) ? APT_ROUTE_FP6_MFMA : 0;
+  const int route = fp4_route_ok(K, p, q)   ? APT_ROUTE_FP4_MFMA
+                    : fp6_route_ok(K, p, q) ? APT_ROUTE_FP6_MFMA
+                    : fp8_route_ok(K, p, q) ? APT_ROUTE_FP8_MFMA : 0;
   if (route != 0) {
     for (int j = n_int8_single - 2 * kNumInt8Shapes; j < end; ++j) {
       apt_config_t c = out[j];

@@ -45,8 +45,9 @@ def forced_configs(p: int, q: int, N: int = 0, K: int = 0):
                                                                         tg), c))
     floats = []
     for route, tag, ok in ((apt.APT_ROUTE_FP4_MFMA, "fp4", p <= 2 and q <= 4),
-                           (apt.APT_ROUTE_FP6_MFMA, "fp6", p <= 3 and q <= 3)):
-        if not ok:  # the same tile configs with FP4 weights (FP4 or FP8 activations) / FP6 operands
+                           (apt.APT_ROUTE_FP6_MFMA, "fp6", p <= 3 and q <= 3),
+                           (apt.APT_ROUTE_FP8_MFMA, "fp8", p <= 4 and q <= 4)):
+        if not ok:  # the same tile configs with FP4 weights (FP4 or FP8 activations) / FP6 / FP8 operands
             continue
         for name, c in out:
             if c.route == apt.APT_ROUTE_INT8_MFMA:

@@ -99,7 +99,7 @@ def test_select_config_valid(shape):
     st, c = apt.apt_select_config(*shape)
     assert st == apt.APT_OK
     assert c.route in (apt.APT_ROUTE_XOR, apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_PM1_MFMA,
-                       apt.APT_ROUTE_FP4_MFMA, apt.APT_ROUTE_FP6_MFMA)
+                       apt.APT_ROUTE_FP4_MFMA, apt.APT_ROUTE_FP6_MFMA, apt.APT_ROUTE_FP8_MFMA)
     if c.route == apt.APT_ROUTE_FP4_MFMA:
         M, N, K, p, q = shape
         k_pad = (K + 127) // 128 * 128
@@ -108,7 +108,8 @@ def test_select_config_valid(shape):
         assert c.route == apt.APT_ROUTE_XOR
     M, N, K, p, q = shape
     ws = apt.apt_gemm_workspace_bytes(*shape, c)
-    if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA, apt.APT_ROUTE_FP6_MFMA):
+    if c.route in (apt.APT_ROUTE_INT8_MFMA, apt.APT_ROUTE_FP4_MFMA, apt.APT_ROUTE_FP6_MFMA,
+                   apt.APT_ROUTE_FP8_MFMA):
         assert ws == _int8_workspace(M, N, K, c, q)
     else:
         assert ws == 0
@@ -213,6 +214,16 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
           cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_UNSUPPORTED),
     (dict(M=64, p=3, q=3, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP6_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_WORKSPACE),
+    # FP8 route: weights and activations of at most 4 bits, fp32 sums below 2^24
+    (dict(p=5, q=4, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(p=4, q=5, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(K=(1 << 24) // 225 // 128 * 128 + 1, p=4, q=4,
+          cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_UNSUPPORTED),
+    (dict(M=64, p=4, q=4, cfg=apt.apt_config_t.make(apt.APT_ROUTE_FP8_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_WORKSPACE),
     # packed weights past 4 GiB do not fit the int8 kernels' 32-bit offsets
     (dict(M=64, N=1 << 20, K=1 << 16, p=1, q=1,
@@ -403,3 +414,15 @@ def test_fp6_workspace_and_bound():
     k_ok = ((1 << 24) - 1) // 49 // 128 * 128
     assert apt.apt_gemm_workspace_bytes(64, 64, k_ok, 3, 3, f6) > 0
     assert apt.apt_gemm_workspace_bytes(64, 64, k_ok + 128, 3, 3, f6) == 0
+
+
+def test_fp8_workspace_and_bound():
+    """FP8 activations take one byte of fragment per element (as int8), and the
+    route admits W4A4 up to K_pad * 225 < 2^24."""
+    f8 = apt.apt_config_t.make(apt.APT_ROUTE_FP8_MFMA, 128, 128, 128, 2, 2)
+    i8 = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)
+    assert apt.apt_gemm_workspace_bytes(100, 300, 1000, 4, 4, f8) == \
+        apt.apt_gemm_workspace_bytes(100, 300, 1000, 4, 4, i8) > 0
+    k_ok = ((1 << 24) - 1) // 225 // 128 * 128
+    assert apt.apt_gemm_workspace_bytes(64, 64, k_ok, 4, 4, f8) > 0
+    assert apt.apt_gemm_workspace_bytes(64, 64, k_ok + 128, 4, 4, f8) == 0

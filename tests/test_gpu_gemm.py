@@ -100,6 +100,33 @@ def test_fp6_exact_at_its_bound():
             assert_int32_equal(got, want, "%s K=%d" % (name, K))
 
 
+def test_fp8_exact_at_its_bound():
+    """The FP8 route sums in fp32 and takes W4A4 while K_pad * 225 < 2^24 (the
+    padding products count too).  At the largest such K_pad with every product
+    +225 the running sum climbs to within one product of 2^24; rows with mixed
+    signs, uniform codes and a K whose last chunk is padded go through every FP8
+    config."""
+    p = q = 4
+    k_pad = ((1 << 24) - 1) // 225 // 128 * 128
+    fp8 = [(n, c) for n, c in forced_configs(p, q, 10, k_pad) if c.route == apt.APT_ROUTE_FP8_MFMA]
+    assert fp8
+    for K in (k_pad, k_pad - 57):
+        g = synth.rng(2700, K)
+        M, N = 3, 10
+        a = np.full((M, K), 7, np.int8)   # code 7: value +15
+        w = np.full((N, K), 7, np.int8)
+        w[1::2] = -8                      # code -8: value -15
+        a[2] = synth.uniform_codes(g, 1, K, q)[0]
+        w[2] = synth.uniform_codes(g, 1, K, p)[0]
+        prob = synth.Problem("fp8 bound", M, N, K, p, q, w, a)
+        want = oracle_full(prob)
+        assert want[0, 0] == 225 * K and want[0, 1] == -225 * K
+        packed = pack_problem(prob)
+        for name, cfg in fp8:
+            got, _ = run(prob, cfg=cfg, packed=packed)
+            assert_int32_equal(got, want, "%s K=%d" % (name, K))
+
+
 def test_extreme_values_all_ones_and_zeros():
     """Worst-case magnitudes: all-ones / all-zeros bipolar words at p = q = 8."""
     for M, N, K in [(3, 5, 1000), (70, 80, 4100)]:

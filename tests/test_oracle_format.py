@@ -243,3 +243,23 @@ def test_fp32_sums_exact_with_fp6_operands():
     assert float(np.cumsum(prod, dtype=np.float32)[-1]) == 49.0 * k_pad
     over = np.full((1 << 24) // 49 + 2, 49.0, np.float32)
     assert float(np.cumsum(over, dtype=np.float32)[-1]) != 49.0 * over.size
+
+
+# ---- FP8 (E4M3) operands of the FP8 route (p, q <= 4) ----------------------------
+
+def test_fp32_sums_exact_with_fp8_operands():
+    """W4A4 through the FP8 route (both operands E4M3, whose codes of the bipolar
+    values up to 4 bits are pinned above): products up to 15 * 15 = 225; with
+    K_pad * 225 < 2^24 every fp32 partial sum is an exact integer, and just past
+    the bound an fp32 running sum loses a unit."""
+    k_pad = ((1 << 24) - 1) // 225 // 128 * 128
+    prod = np.full(k_pad, 225.0, np.float32)
+    assert float(np.cumsum(prod, dtype=np.float32)[-1]) == 225.0 * k_pad
+    over = np.full((1 << 24) // 225 + 2, 225.0, np.float32)
+    assert float(np.cumsum(over, dtype=np.float32)[-1]) != 225.0 * over.size
+    # every product of two 4-bit bipolar values is an integer that fp32 and
+    # E4M3 x E4M3 hold exactly
+    vals = [2 * u - 15 for u in range(16)]
+    for a in vals:
+        for b in vals:
+            assert float(np.float32(a) * np.float32(b)) == a * b
