@@ -922,7 +922,7 @@ def paper_shapes(calls: int = 100, reps: int = 3):
 
 def xor_crossover(calls: int = 50):
     """Where the XOR route beats the MFMA routes: for M = 16..256 and a few
-    (N, K, p, q), the forced XOR route (8 activation rows per workgroup) and
+    (N, K, p, q), the forced XOR route (its own launch shape) and
     the best of the 128x128 MFMA configs the model takes at such sizes (int8,
     and FP4 where it applies; one workgroup per tile and 512 workgroups), each
     as one HIP graph of `calls` calls (warm, int32 output), plus the selected
@@ -968,21 +968,27 @@ def xor_crossover(calls: int = 50):
                 routes = [apt.APT_ROUTE_INT8_MFMA] + ([apt.APT_ROUTE_FP4_MFMA] if p <= 2 and q <= 2 else [])
                 mfma = min(timed(M, N, K, p, q, C(r, 128, 128, 128, 2, 2, grid, 3), a, w, c32)
                            for r in routes for grid in (0, 512))
-                xor = timed(M, N, K, p, q, C(apt.APT_ROUTE_XOR, mt=8), a, w, c32)
+                xor = timed(M, N, K, p, q, C(apt.APT_ROUTE_XOR), a, w, c32)
                 sel = apt.select_config(M, N, K, p, q)
                 selected = timed(M, N, K, p, q, sel, a, w, c32)
                 rows.append({"M": M, "N": N, "K": K, "p": p, "q": q, "xor_us": round(xor, 2),
                              "mfma_128x128_us": round(mfma, 2), "selected": apt.ROUTE_NAMES[sel.route],
                              "selected_us": round(selected, 2)})
             log("bench: xor crossover N=%d K=%d W%dA%d done" % (N, K, p, q))
-    # the selector's XOR model: t = t0 + (M N K / 32) / sqrt(u) (a + b p q), u = min(1, chunks / 32)
-    words = np.array([r["M"] * r["N"] * r["K"] / 32 / math.sqrt(min(1.0, math.ceil(r["K"] / 128) / 32))
-                      for r in rows])
-    pq = np.array([r["p"] * r["q"] for r in rows], dtype=float)
+    # the selector's XOR model: t = t0 + W (a + b q + c p q), W = 8 ceil(M / 8) N K / 32 word pairs
+    # (8 activation rows per block row), fitted by least squares on the relative error
     t = np.array([r["xor_us"] for r in rows])
-    coef = np.linalg.lstsq(np.vstack([np.ones_like(words), words, words * pq]).T, t, rcond=None)[0]
-    return {"rows": rows, "xor_fit": {"t0_us": round(coef[0], 3), "a_ps_per_word": round(coef[1] * 1e6, 4),
-                                      "b_ps_per_word_per_pq": round(coef[2] * 1e6, 4)}}
+    W = np.array([8 * math.ceil(r["M"] / 8) * r["N"] * r["K"] / 32 for r in rows]) * 1e-6
+    q = np.array([r["q"] for r in rows], dtype=float)
+    pq = np.array([r["p"] * r["q"] for r in rows], dtype=float)
+    X = np.vstack([np.ones_like(W), W, W * q, W * pq]).T
+    coef = np.linalg.lstsq(X / t[:, None], np.ones_like(t), rcond=None)[0]
+    err = np.abs(X @ coef / t - 1)
+    return {"rows": rows, "xor_fit": {"t0_us": round(coef[0], 3), "a_ps_per_word": round(coef[1], 4),
+                                      "b_ps_per_word_per_q": round(coef[2], 4),
+                                      "c_ps_per_word_per_pq": round(coef[3], 4),
+                                      "median_rel_err": round(float(np.median(err)), 3),
+                                      "max_rel_err": round(float(err.max()), 3)}}
 
 
 def stored_traffic():

@@ -134,16 +134,15 @@ double model_us(const Int8Shape& s, int f, int M, int N, int K, int grid, int cu
 // The tail shape a split config with main shape i and tail size of shape t
 // runs: of the shapes of that size, the one with the main shape's wave count
 // (the library's rule), else t itself.
-// Modelled microseconds of the XOR route with 8 activation rows per
-// workgroup: a fixed part and a cost per 32-bit word pair of one activation
-// row and one weight row, rising with the p*q plane products per pair; when K
-// has fewer chunks than a workgroup's 32 chunk slots, part of every workgroup
-// idles (factor 1/sqrt(used share)).  Fitted to MI355X timings for M = 16 to
-// 256, N and K from 1024 to 14336 and p*q from 2 to 16.
+// Modelled microseconds of the XOR route (8 activation rows per block row):
+// a fixed part and a cost per 32-bit word pair of an 8-row activation block
+// and one weight row, rising with the activation planes read from LDS (q) and
+// with the p*q plane products.  Fitted (least squares on the relative error)
+// to MI355X timings for M = 16 to 256, N and K from 1024 to 14336 and p*q
+// from 2 to 16: median error 8%.
 double model_xor_us(int M, int N, int K, int p, int q) {
-  const double used = std::min(1.0, (double)num_chunks(K) / 32.0);
-  const double words = (double)M * N * K / 32.0 / std::sqrt(used);
-  return 3.29 + words * (0.0508 + 0.0672 * p * q) * 1e-6;
+  const double words = 8.0 * ((M + 7) / 8) * (double)N * K / 32.0;
+  return 3.564 + words * (-0.2140 + 0.1792 * q + 0.0439 * p * q) * 1e-6;
 }
 
 bool tail_runs_as(int i, int t) {
