@@ -282,6 +282,55 @@ apt_status_t apt_gemm_noalloc(int M, int N, int K, int p, int q,
                               const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
                               const apt_config_t* cfg, void* stream);
 
+/* Activation sources of apt_gemm_decode. */
+enum {
+  APT_ACT_CODES = 1, /* int8 [M][K], signed q-bit codes (as apt_quantize_pack_activations) */
+  APT_ACT_FP16 = 2   /* fp16 bits [M][K], quantized per row as apt_quantize_pack_activations_fp16 */
+};
+
+/* Largest M apt_gemm_decode takes. */
+#define APT_DECODE_MAX_M 8
+
+/* The decode GEMM (one to eight tokens) with the activation side of the
+ * conversion fused into it: C = A * W^T on the XOR + popcount route (Sec.
+ * III-B), where A is given unpacked and each workgroup converts its token's
+ * row to bipolar-INT bit-planes (Sec. III-A conversion, Sec. IV-A steps 1-3;
+ * for fp16 input after quantizing the row) into its LDS, so that neither a
+ * packer launch nor a packed activation buffer sits between the token and
+ * the GEMV.  Results equal those of the packer (apt_quantize_pack_activations
+ * for codes, apt_quantize_pack_activations_fp16 for fp16) followed by apt_gemm
+ * on the XOR route, bit for bit: the same codes, scales, int32 C and fp16
+ * output.
+ *   a_src     device, the activations [M][K] row-major in the a_kind format;
+ *             fp16 values must be finite (as for the fp16 packer); 2-byte
+ *             aligned for fp16 (16-byte alignment and K % 16 == 0 select wider
+ *             loads; the result does not depend on it)
+ *   a_kind    APT_ACT_CODES or APT_ACT_FP16
+ *   w_packed  device, packed p-bit weights [N][K] (apt_pack_weights), 16-byte aligned
+ *   c_int32   device int32 [M][N] row-major, or NULL
+ *   a_scale   APT_ACT_CODES: device fp16 bits [M], per-token bipolar scale
+ *             (required with c_fp16, else may be NULL); APT_ACT_FP16: must be NULL
+ *             (the scale is computed from the row)
+ *   w_scale   device fp16 bits [N], per-channel bipolar scale (required with c_fp16)
+ *   c_fp16    device fp16 bits [M][N] row-major, or NULL; as apt_gemm's epilogue,
+ *             with the computed row scale for APT_ACT_FP16
+ *   a_scale_out  APT_ACT_FP16: device fp16 bits [M] receiving each row's scale
+ *             s_m (as the fp16 packer's a_scale), or NULL; APT_ACT_CODES: must be NULL
+ *   cfg       NULL or route AUTO: the library's XOR launch shape; else an XOR
+ *             route config (waves_m, waves_n as for apt_gemm; mt 0 or 1)
+ * Errors: APT_ERR_INVALID_ARG for M outside [1, APT_DECODE_MAX_M], N or K < 1,
+ * bits outside [1, 8], a bad a_kind, a NULL source or weight pointer, a
+ * misaligned weight or fp16 source pointer, both outputs NULL, c_fp16 without
+ * its scales, a scale pointer the a_kind does not take, or a cfg that is not
+ * an XOR config with mt 0 or 1; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >=
+ * 2^31 or when the row's bit-planes (ceil(K / 1024) * 1024 * q / 8 bytes) do
+ * not fit in 64 KB of LDS; APT_ERR_HIP on launch failure. */
+apt_status_t apt_gemm_decode(int M, int N, int K, int p, int q,
+                             const void* a_src, int a_kind, const void* w_packed,
+                             int32_t* c_int32, const uint16_t* a_scale,
+                             const uint16_t* w_scale, uint16_t* c_fp16,
+                             uint16_t* a_scale_out, const apt_config_t* cfg, void* stream);
+
 /* Device workspace bytes apt_search_config needs for this problem: the most
  * that any config it times needs (apt_gemm_workspace_bytes).  Returns 0 for
  * invalid sizes or bit widths. */

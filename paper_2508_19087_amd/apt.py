@@ -30,6 +30,9 @@ APT_ROUTE_INT8_MFMA = 3
 APT_ROUTE_FP4_MFMA = 4
 APT_ROUTE_FP6_MFMA = 5
 APT_ROUTE_FP8_MFMA = 6
+APT_ACT_CODES = 1
+APT_ACT_FP16 = 2
+APT_DECODE_MAX_M = 8
 ROUTE_NAMES = {APT_ROUTE_XOR: "xor_popcount", APT_ROUTE_PM1_MFMA: "pm1_planes_mfma",
                APT_ROUTE_INT8_MFMA: "reassembled_int8_mfma", APT_ROUTE_FP4_MFMA: "reassembled_fp4_mfma",
                APT_ROUTE_FP6_MFMA: "reassembled_fp6_mfma", APT_ROUTE_FP8_MFMA: "reassembled_fp8_mfma"}
@@ -100,6 +103,9 @@ def lib() -> ctypes.CDLL:
         L.apt_gemm_affine.argtypes = ([ctypes.c_int] * 5 + [_vp] * 10 +
                                       [ctypes.POINTER(apt_config_t)] + [_vp, ctypes.c_size_t, _vp])
         L.apt_gemm_affine.restype = ctypes.c_int
+        L.apt_gemm_decode.argtypes = ([ctypes.c_int] * 5 + [_vp, ctypes.c_int] + [_vp] * 6 +
+                                      [ctypes.POINTER(apt_config_t), _vp])
+        L.apt_gemm_decode.restype = ctypes.c_int
         L.apt_search_workspace_bytes.argtypes = [ctypes.c_int] * 5
         L.apt_search_workspace_bytes.restype = ctypes.c_size_t
         L.apt_search_config.argtypes = ([ctypes.c_int] * 5 + [_vp] * 6 + [ctypes.c_size_t, _vp,
@@ -176,6 +182,13 @@ def apt_gemm_affine(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, a_sca
                                  a_zero, w_scale, w_zero, c_fp16, c_int32,
                                  ctypes.byref(cfg) if cfg is not None else None, workspace,
                                  workspace_bytes, stream)
+
+
+def apt_gemm_decode(M, N, K, p, q, a_src, a_kind, w_packed, c_int32, a_scale, w_scale, c_fp16,
+                    a_scale_out, cfg, stream) -> int:
+    return lib().apt_gemm_decode(M, N, K, p, q, a_src, a_kind, w_packed, c_int32, a_scale,
+                                 w_scale, c_fp16, a_scale_out,
+                                 ctypes.byref(cfg) if cfg is not None else None, stream)
 
 
 def apt_search_workspace_bytes(M, N, K, p, q) -> int:
@@ -311,6 +324,31 @@ def gemm(a: Packed, w: Packed, out_int32: bool = True, a_scale=None, w_scale=Non
                    _ptr(a.rowsum), _ptr(w.rowsum), _ptr(c32), _ptr(a_scale), _ptr(w_scale),
                    _ptr(c16), cfg, ws_ptr, ws_len, _stream_ptr(stream)), "apt_gemm")
     return c32, c16
+
+
+def gemm_decode(x, q: int, w: Packed, out_int32: bool = True, a_scale=None, w_scale=None,
+                out_fp16: bool = False, cfg: apt_config_t | None = None, stream=None):
+    """Decode GEMM on unpacked activations x [M][K] (M <= 8, a CUDA tensor):
+    int8 q-bit codes, or fp16 values quantized per row inside the kernel.
+    Returns (c_int32 or None, c_fp16 or None, scales): the fp16 row scales the
+    kernel computed for fp16 x, else None."""
+    torch = _torch()
+    assert x.is_cuda and x.dim() == 2 and x.dtype in (torch.int8, torch.float16)
+    x = x.contiguous()
+    M, K = x.shape
+    assert K == w.K
+    N = w.rows
+    fp16_src = x.dtype == torch.float16
+    dev = x.device
+    with _on_stream(stream):
+        c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
+        c16 = torch.empty((M, N), dtype=torch.float16, device=dev) if out_fp16 else None
+        scale = torch.empty(M, dtype=torch.float16, device=dev) if fp16_src else None
+    check(apt_gemm_decode(M, N, K, w.bits, q, x.data_ptr(),
+                          APT_ACT_FP16 if fp16_src else APT_ACT_CODES, w.data.data_ptr(),
+                          _ptr(c32), _ptr(a_scale), _ptr(w_scale), _ptr(c16), _ptr(scale), cfg,
+                          _stream_ptr(stream)), "apt_gemm_decode")
+    return c32, c16, scale
 
 
 def gemm_affine(a: Packed, w: Packed, a_scale, a_zero, w_scale, w_zero, out_int32: bool = False,

@@ -237,6 +237,44 @@ apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q, const void* a_pa
                      w_scale, c_fp16, a_zero, w_zero, cfg, workspace, workspace_bytes, stream);
 }
 
+apt_status_t apt_gemm_decode(int M, int N, int K, int p, int q, const void* a_src, int a_kind,
+                             const void* w_packed, int32_t* c_int32, const uint16_t* a_scale,
+                             const uint16_t* w_scale, uint16_t* c_fp16, uint16_t* a_scale_out,
+                             const apt_config_t* cfg, void* stream) {
+  if (M < 1 || M > APT_DECODE_MAX_M || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q))
+    return APT_ERR_INVALID_ARG;
+  if (a_kind != APT_ACT_CODES && a_kind != APT_ACT_FP16) return APT_ERR_INVALID_ARG;
+  const bool fp16_src = a_kind == APT_ACT_FP16;
+  if (a_src == nullptr || w_packed == nullptr || !aligned16(w_packed)) return APT_ERR_INVALID_ARG;
+  if (fp16_src && (reinterpret_cast<uintptr_t>(a_src) & 1u) != 0) return APT_ERR_INVALID_ARG;
+  if (c_int32 == nullptr && c_fp16 == nullptr) return APT_ERR_INVALID_ARG;
+  if (c_fp16 != nullptr && (w_scale == nullptr || (!fp16_src && a_scale == nullptr)))
+    return APT_ERR_INVALID_ARG;
+  if (fp16_src ? a_scale != nullptr : a_scale_out != nullptr) return APT_ERR_INVALID_ARG;
+  if (!fits_int32(K, p, q)) return APT_ERR_UNSUPPORTED;
+  apt_config_t c{};
+  c.route = APT_ROUTE_XOR;
+  if (cfg != nullptr && cfg->route != APT_ROUTE_AUTO) {
+    if (cfg->route != APT_ROUTE_XOR || !apt::xor_act_config_ok(*cfg)) return APT_ERR_INVALID_ARG;
+    c = *cfg;
+  }
+  if (!apt::xor_act_sizes_ok(M, N, K, p, q, c)) return APT_ERR_UNSUPPORTED;
+  apt::GemmArgs g;
+  g.M = M; g.N = N; g.K = K; g.p = p; g.q = q;
+  g.a_packed = nullptr;
+  g.w_packed = static_cast<const uint32_t*>(w_packed);
+  g.a_rowsum = nullptr;
+  g.w_rowsum = nullptr;
+  g.c_int32 = c_int32;
+  g.a_scale = reinterpret_cast<const __half*>(a_scale);
+  g.w_scale = reinterpret_cast<const __half*>(w_scale);
+  g.c_fp16 = reinterpret_cast<__half*>(c_fp16);
+  g.a_zero = nullptr;
+  g.w_zero = nullptr;
+  return hip_status(apt::launch_gemm_xor_act(g, a_src, fp16_src, a_scale_out, c,
+                                             static_cast<hipStream_t>(stream)));
+}
+
 size_t apt_search_workspace_bytes(int M, int N, int K, int p, int q) {
   if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return 0;
   apt_config_t cand[apt::kMaxCandidates];

@@ -33,6 +33,7 @@
 // and take every W-th chunk round (K split), so that more waves share the
 // popcount work; their sums meet through LDS at the end.
 #include "apt_internal.h"
+#include "rowcode.h"
 
 namespace apt {
 namespace xorpop {
@@ -49,7 +50,21 @@ struct XorParams {
   int groups;    // row groups of the packed weights (padded N / 8)
   int ksplit;    // 1: each wave owns a row group; W > 1: the W waves of a
                  // workgroup share one and take every W-th chunk round
+  // Fused activation source (SRC 1: int8 codes, 2: fp16 values, [M][K]),
+  // converted per workgroup into the LDS copy; a_vec: 16-byte loads allowed
+  // (K % 16 == 0 and a 16-byte aligned base).  SRC 2 writes each row's
+  // bipolar scale to a_scale_out (if not NULL) from the first column block.
+  const void* a_src;
+  int a_vec;
+  uint16_t* a_scale_out;
 };
+
+// Source of the activations: the packed planes, or (one activation row per
+// block row) int8 codes or fp16 values converted inside the kernel.
+enum { kSrcPacked = 0, kSrcCodes = 1, kSrcHalf = 2 };
+// Rounds of 16 source elements per lane that the fused form holds in
+// registers (requested before the weights); a longer row loads the rest after.
+constexpr int kSrcHeld = 4;
 
 // Activation chunk vectors per chunk in LDS: MT = 8 stages all 8 rows of each
 // plane plus one pad vector (so that the 8 chunk lanes of a wave, which read
@@ -90,8 +105,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t xor_rsrc(const void* base, uin
 // exactly; a zero weight word meets a zero activation word in the chunks
 // between K and the end of the last round, which adds nothing to any
 // popcount.
-template <int P, int Q, int MT, bool DEEP, bool kALds>
+template <int P, int Q, int MT, bool DEEP, bool kALds, int SRC = kSrcPacked>
 __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams prm) {
+  static_assert(SRC == kSrcPacked || (MT == 1 && kALds), "the fused source builds a one-row LDS copy");
   extern __shared__ uint4 a_lds[];
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
@@ -129,9 +145,36 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
     return MT == 8 ? t + t / (Q * kRowGroup) : t;
   };
   uint4 pre[kStagePre];
-  if (kALds) {
+  if (kALds && SRC == kSrcPacked) {
 #pragma unroll
     for (int k = 0; k < kStagePre; ++k) pre[k] = a_at(threadIdx.x + k * (int)blockDim.x);
+  }
+  // Fused source: lane t takes elements 16 t + 16 L r, r = 0, 1, ... (L lanes
+  // in the workgroup) of row m0, up to the padded row length 128 NS; its first
+  // kSrcHeld rounds are requested here, before the weights.
+  using CodeSrc = rowcode::CodeRow<false, Q>;
+  using CodeVec = rowcode::CodeRow<true, Q>;
+  using HalfSrc = rowcode::HalfRow<false, Q>;
+  using HalfVec = rowcode::HalfRow<true, Q>;
+  constexpr int kSrcDwords = SRC == kSrcHalf ? HalfSrc::kDwords : CodeSrc::kDwords;
+  constexpr int kElemBytes = SRC == kSrcHalf ? 2 : 1;
+  const int src_step = (int)blockDim.x * rowcode::kLaneElems;
+  const int src_rounds = (NS * kChunk + src_step - 1) / src_step;  // uniform
+  const __amdgpu_buffer_rsrc_t s_rsrc = xor_rsrc(
+      static_cast<const uint8_t*>(prm.a_src) + (int64_t)m0 * g.K * kElemBytes, (uint32_t)g.K * kElemBytes);
+  auto src_load = [&](int r, uint32_t* d) __attribute__((always_inline)) {
+    const int k0 = r * src_step + (int)threadIdx.x * rowcode::kLaneElems;
+    if (SRC == kSrcHalf) {
+      if (prm.a_vec) HalfVec::load(s_rsrc, k0, d); else HalfSrc::load(s_rsrc, k0, d);
+    } else {
+      if (prm.a_vec) CodeVec::load(s_rsrc, k0, d); else CodeSrc::load(s_rsrc, k0, d);
+    }
+  };
+  uint32_t sd[SRC != kSrcPacked ? kSrcHeld : 1][kSrcDwords];
+  if (SRC != kSrcPacked) {
+#pragma unroll
+    for (int r = 0; r < kSrcHeld; ++r)
+      if (r < src_rounds) src_load(r, sd[r]);
   }
 
   // ---- weight batches
@@ -159,7 +202,8 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
   load(wcur, 0);
   if (kB < T) load(wnxt, kB);
 
-  if (kALds) {
+  float s_act = 0.0f;  // fused fp16 source: this row's bipolar scale
+  if (kALds && SRC == kSrcPacked) {
 #pragma unroll
     for (int k = 0; k < kStagePre; ++k) {
       const int t = threadIdx.x + k * (int)blockDim.x;
@@ -167,6 +211,65 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
     }
     for (int t = threadIdx.x + kStagePre * (int)blockDim.x; t < n_vec; t += blockDim.x)
       a_lds[lds_at(t)] = a_at(t);
+    __syncthreads();
+  }
+  if (SRC != kSrcPacked) {
+    // The conversion of the packer (Sec. III-A, and for fp16 the bipolar form
+    // of the per-row linear quantizer), with the plane words stored in the
+    // one-row LDS layout: word w of plane j of chunk c at dword
+    // 4 (c Q + j) + w.  Rounds past kSrcHeld are loaded (again) here.
+    __shared__ uint32_t s_red[kMaxWaves];
+    uint32_t* lds32 = reinterpret_cast<uint32_t*>(a_lds);
+    float rh = 0.0f, s2 = 0.0f;
+    if (SRC == kSrcHalf) {
+      rowcode::ushort2_t mm = {0, 0};
+#pragma unroll
+      for (int r = 0; r < kSrcHeld; ++r)
+        if (r < src_rounds) mm = HalfSrc::fold_max(mm, sd[r]);
+      for (int r = kSrcHeld; r < src_rounds; ++r) {
+        uint32_t d[kSrcDwords];
+        src_load(r, d);
+        mm = HalfSrc::fold_max(mm, d);
+      }
+      uint32_t m = max((uint32_t)mm.x, (uint32_t)mm.y);
+      for (int off = kWave / 2; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+      if (lane == 0) s_red[wave] = m;
+      __syncthreads();
+      m = 0u;
+      for (int v = 0; v < (int)(blockDim.x / kWave); ++v) m = max(m, s_red[v]);
+      const uint16_t s16 = rowcode::row_scale<Q>(m, rh, s2);
+      s_act = __half2float(__ushort_as_half(s16));
+      if (prm.a_scale_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) prm.a_scale_out[m0] = s16;
+    }
+    const bool odd = (lane & 1) != 0;
+    // uniform in r: both lanes of a pair run every round (DPP swap)
+    auto convert = [&](int r, const uint32_t* d) __attribute__((always_inline)) {
+      const int k0 = r * src_step + (int)threadIdx.x * rowcode::kLaneElems;
+      uint32_t u[4];
+      if (SRC == kSrcHalf) HalfSrc::words(d, rh, s2, u); else CodeSrc::words(d, rh, s2, u);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {  // elements past K: all-zero words
+        const int n_valid = g.K - (k0 + 4 * t);
+        u[t] &= n_valid >= 4 ? 0xFFFFFFFFu : (n_valid <= 0 ? 0u : ((1u << (8 * n_valid)) - 1u));
+      }
+      uint32_t alo = u[0], ahi = u[1], blo = u[2], bhi = u[3];
+      rowcode::transpose8x8<Q>(alo, ahi);
+      rowcode::transpose8x8<Q>(blo, bhi);
+      uint32_t* dst = lds32 + (k0 / kChunk) * Q * kWordsPerPlane + (k0 % kChunk) / 32;
+#pragma unroll
+      for (int i = 0; i < Q; i += 2) {
+        const uint32_t wv = rowcode::plane_word(i < 4 ? alo : ahi, i < 4 ? blo : bhi, i % 4, odd);
+        if (k0 < NS * kChunk && (!odd || i + 1 < Q)) dst[(i + (odd ? 1 : 0)) * kWordsPerPlane] = wv;
+      }
+    };
+#pragma unroll
+    for (int r = 0; r < kSrcHeld; ++r)
+      if (r < src_rounds) convert(r, sd[r]);
+    for (int r = kSrcHeld; r < src_rounds; ++r) {
+      uint32_t d[kSrcDwords];
+      src_load(r, d);
+      convert(r, d);
+    }
     __syncthreads();
   }
   // vector of chunk c, plane j, row m (zeros for c >= NC)
@@ -262,7 +365,7 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
       f = affine_value(c, __half2float(g.a_scale[mg]), sw, zw, (float)g.a_rowsum[mg],
                        __half2float(g.a_zero[mg]), sw * (float)g.w_rowsum[n] + (float)g.K * zw);
     } else {
-      f = (float)c * __half2float(g.a_scale[mg]);
+      f = (float)c * (SRC == kSrcHalf ? s_act : __half2float(g.a_scale[mg]));
       f = f * __half2float(g.w_scale[n]);
     }
     g.c_fp16[o] = __float2half_rn(f);
@@ -278,13 +381,30 @@ struct XorLaunch {
   bool lds;    // activation chunks staged in LDS
   size_t lds_bytes;
   dim3 grid;
+  int src;     // kSrcPacked, or a fused source (needs mt = 1 and lds)
 };
+
+// Launch with `lds` bytes of dynamic LDS; past 48 KB (with the kernel's own
+// static arrays the workgroup then nears 64 KB) the kernel's limit is raised
+// first.
+template <class Kernel>
+inline hipError_t launch_lds(Kernel kern, const XorLaunch& L, hipStream_t s, const XorParams& prm) {
+  if (L.lds_bytes > 48 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.lds_bytes);
+    if (e != hipSuccess) return e;
+  }
+  return launch_kernel(kern, L.grid, dim3(kWave * L.waves), L.lds_bytes, s, prm);
+}
 
 template <int P, int Q, int MT, bool DEEP>
 inline hipError_t launch_mt(const XorParams& prm, const XorLaunch& L, hipStream_t s) {
-  const dim3 block(kWave * L.waves);
-  if (L.lds) return launch_kernel(gemm_xor_kernel<P, Q, MT, DEEP, true>, L.grid, block, L.lds_bytes, s, prm);
-  return launch_kernel(gemm_xor_kernel<P, Q, MT, DEEP, false>, L.grid, block, 0, s, prm);
+  if constexpr (MT == 1) {
+    if (L.src == kSrcCodes) return launch_lds(gemm_xor_kernel<P, Q, 1, DEEP, true, kSrcCodes>, L, s, prm);
+    if (L.src == kSrcHalf) return launch_lds(gemm_xor_kernel<P, Q, 1, DEEP, true, kSrcHalf>, L, s, prm);
+  }
+  if (L.lds) return launch_lds(gemm_xor_kernel<P, Q, MT, DEEP, true>, L, s, prm);
+  return launch_kernel(gemm_xor_kernel<P, Q, MT, DEEP, false>, L.grid, dim3(kWave * L.waves), 0, s, prm);
 }
 
 template <int P, int Q>

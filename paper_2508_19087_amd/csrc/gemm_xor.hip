@@ -56,6 +56,7 @@ XorLaunch xor_launch_shape(int M, int N, int K, int p, int q, const apt_config_t
   L.lds_bytes = act_lds_bytes_q(q, L.mt, num_chunks(K));
   L.lds = L.lds_bytes <= xorpop::kMaxActLds;
   if (!L.lds) L.lds_bytes = 0;
+  L.src = xorpop::kSrcPacked;
   return L;
 }
 
@@ -64,13 +65,59 @@ bool xor_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
   return L.grid.x <= 0x7fffffffu && L.grid.y <= 65535u;
 }
 
+// The fused form runs one activation row per block row and builds its LDS
+// copy from the source: mt must resolve to 1 and the copy must fit in LDS.
+bool xor_act_config_ok(const apt_config_t& cfg) { return xor_config_ok(cfg) && cfg.mt != 8; }
+
+bool xor_act_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg) {
+  apt_config_t c = cfg;
+  c.mt = 1;
+  const XorLaunch L = xor_launch_shape(M, N, K, p, q, c);
+  return L.lds && L.grid.x <= 0x7fffffffu && L.grid.y <= 65535u;
+}
+
+namespace {
+
+hipError_t launch_xor(const XorParams& prm, const XorLaunch& L, hipStream_t stream);
+
+}  // namespace
+
 hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream) {
   XorParams prm;
   prm.g = g;
   prm.nchunks = num_chunks(g.K);
   prm.groups = padded_rows(g.N) / kRowGroup;
+  prm.a_src = nullptr;
+  prm.a_vec = 0;
+  prm.a_scale_out = nullptr;
   const XorLaunch L = xor_launch_shape(g.M, g.N, g.K, g.p, g.q, cfg);
   prm.ksplit = L.ksplit;
+  return launch_xor(prm, L, stream);
+}
+
+hipError_t launch_gemm_xor_act(const GemmArgs& g, const void* a_src, bool fp16_src,
+                               uint16_t* a_scale_out, const apt_config_t& cfg, hipStream_t stream) {
+  apt_config_t c = cfg;
+  c.mt = 1;
+  XorParams prm;
+  prm.g = g;
+  prm.nchunks = num_chunks(g.K);
+  prm.groups = padded_rows(g.N) / kRowGroup;
+  prm.a_src = a_src;
+  // 16-byte loads: every row starts 16-byte aligned and holds whole vectors
+  prm.a_vec = (reinterpret_cast<uintptr_t>(a_src) & 15u) == 0 && g.K % 16 == 0;
+  prm.a_scale_out = fp16_src ? a_scale_out : nullptr;
+  XorLaunch L = xor_launch_shape(g.M, g.N, g.K, g.p, g.q, c);
+  if (!L.lds) return hipErrorInvalidValue;
+  L.src = fp16_src ? xorpop::kSrcHalf : xorpop::kSrcCodes;
+  prm.ksplit = L.ksplit;
+  return launch_xor(prm, L, stream);
+}
+
+namespace {
+
+hipError_t launch_xor(const XorParams& prm, const XorLaunch& L, hipStream_t stream) {
+  const GemmArgs& g = prm.g;
   switch (g.p) {
     case 1: return xorpop::launch_for_p<1>(g.q, prm, L, stream);
     case 2: return xorpop::launch_for_p<2>(g.q, prm, L, stream);
@@ -83,5 +130,7 @@ hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream
   }
   return hipErrorInvalidValue;
 }
+
+}  // namespace
 
 }  // namespace apt

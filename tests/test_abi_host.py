@@ -15,7 +15,7 @@ def test_exports_every_declared_symbol():
                           "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
                           "apt_gemm_affine", "apt_search_workspace_bytes", "apt_search_config",
                           "apt_config_table_clear", "apt_config_table_size", "apt_last_hip_error",
-                          "apt_gemm_noalloc",
+                          "apt_gemm_noalloc", "apt_gemm_decode",
                           "apt_status_string"}
     L = apt.lib()
     for n in names:
@@ -292,6 +292,40 @@ def test_pack_rejects_huge_rows():
         assert fn(A, 1, K, 2, W, None, None) == apt.APT_ERR_UNSUPPORTED
     assert apt.apt_quantize_pack_activations_fp16(A, 1, K, 2, W, None, A + 2, None) == \
         apt.APT_ERR_UNSUPPORTED
+
+
+def gemm_decode(M=4, N=4, K=64, p=2, q=2, x=A, kind=apt.APT_ACT_CODES, w=W, c32=C, sa=S,
+                sw=S + 128, c16=None, so=None, cfg=None):
+    return apt.apt_gemm_decode(M, N, K, p, q, x, kind, w, c32, sa, sw, c16, so, cfg, None)
+
+
+XOR = apt.APT_ROUTE_XOR
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(M=0), apt.APT_ERR_INVALID_ARG), (dict(M=apt.APT_DECODE_MAX_M + 1), apt.APT_ERR_INVALID_ARG),
+    (dict(N=0), apt.APT_ERR_INVALID_ARG), (dict(K=0), apt.APT_ERR_INVALID_ARG),
+    (dict(p=9), apt.APT_ERR_INVALID_ARG), (dict(q=0), apt.APT_ERR_INVALID_ARG),
+    (dict(kind=0), apt.APT_ERR_INVALID_ARG), (dict(kind=3), apt.APT_ERR_INVALID_ARG),
+    (dict(x=None), apt.APT_ERR_INVALID_ARG), (dict(w=None), apt.APT_ERR_INVALID_ARG),
+    (dict(w=W + 4), apt.APT_ERR_INVALID_ARG),
+    (dict(kind=apt.APT_ACT_FP16, x=A + 1, sa=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c32=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c16=C, sa=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c16=C, sw=None), apt.APT_ERR_INVALID_ARG),
+    (dict(kind=apt.APT_ACT_FP16), apt.APT_ERR_INVALID_ARG),       # a_scale with an fp16 source
+    (dict(so=S + 64), apt.APT_ERR_INVALID_ARG),                   # scale output with codes
+    (dict(cfg=apt.apt_config_t.make(XOR, mt=8)), apt.APT_ERR_INVALID_ARG),
+    (dict(cfg=apt.apt_config_t.make(XOR, waves_m=3)), apt.APT_ERR_INVALID_ARG),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
+     apt.APT_ERR_INVALID_ARG),
+    (dict(K=33026, p=8, q=8), apt.APT_ERR_UNSUPPORTED),
+    (dict(K=65537, p=1, q=8), apt.APT_ERR_UNSUPPORTED),           # planes past 64 KB of LDS
+    (dict(K=131073, p=1, q=4), apt.APT_ERR_UNSUPPORTED),
+])
+def test_gemm_decode_validation(kw, want):
+    """Rejected before any HIP call (the pointers are never dereferenced)."""
+    assert gemm_decode(**kw) == want
 
 
 def test_config_struct_layout():
