@@ -594,6 +594,110 @@ def decode_cold(wl, reps: int = 4):
     return out
 
 
+def replay_us(torch, g, n, reps: int = 4, before=None, check=None) -> float:
+    """Median microseconds per launch group of graph g (n groups per replay),
+    replay 0 untimed; before() runs ahead of and check() after each replay."""
+    times = []
+    for r in range(reps):
+        if before is not None:
+            before()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if check is not None:
+            check()
+        if r > 0:
+            times.append(e0.elapsed_time(e1) * 1e3 / n)
+    return sorted(times)[len(times) // 2]
+
+
+def decode_token_cold(wl, reps: int = 4):
+    """One token's decode GEMM as a whole, with cold weights: from the token's
+    activations (int8 codes, or fp16 values quantized per row) to the int32
+    and fp16 outputs.  Unfused = the packer (or the fp16 quantizer-packer)
+    then apt_gemm, two launches; fused = apt_gemm_decode, one launch that
+    converts the row inside the GEMV.  Each variant is one HIP graph over the
+    cold weight copies; every replay's outputs are checked, and the fused
+    outputs must equal the unfused ones bit for bit."""
+    torch, apt, np = wl.torch, wl.apt, wl.np
+    import synth
+    out = {}
+    for it in wl.items[:2]:
+        p = it["prob"]
+        wbytes = it["w"].data.numel()
+        copies = max(8, int(2 * MALL_BYTES // wbytes) + 1)
+        ws = [it["w"].data.clone() for _ in range(copies)]
+        x16 = torch.from_numpy(synth.fp16_activations(synth.rng(81, p.N, p.K), p.M, p.K)).cuda()
+        sa_q = torch.empty(p.M, dtype=torch.float16, device="cuda")
+        c32 = torch.empty((p.M, p.N), dtype=torch.int32, device="cuda")
+        c16 = torch.empty((p.M, p.N), dtype=torch.float16, device="cuda")
+        rowsum = it["w"].rowsum
+
+        def gemm(w, sp, sa):
+            apt.check(apt.apt_gemm(p.M, p.N, p.K, p.p, p.q, it["a_buf"].data_ptr(), w.data_ptr(),
+                                   it["a_rs"].data_ptr(), rowsum.data_ptr(), c32.data_ptr(),
+                                   sa.data_ptr(), it["sw"].data_ptr(), c16.data_ptr(), None,
+                                   it["ws"].data_ptr(), it["ws_bytes"], sp), "apt_gemm")
+
+        def unfused_codes(sp):
+            for w in ws:
+                wl.pack_act(it, sp)
+                gemm(w, sp, it["sa"])
+
+        def fused_codes(sp):
+            for w in ws:
+                apt.check(apt.apt_gemm_decode(p.M, p.N, p.K, p.p, p.q, it["a_codes"].data_ptr(),
+                                              apt.APT_ACT_CODES, w.data_ptr(), c32.data_ptr(),
+                                              it["sa"].data_ptr(), it["sw"].data_ptr(),
+                                              c16.data_ptr(), None, None, sp), "apt_gemm_decode")
+
+        def unfused_fp16(sp):
+            for w in ws:
+                apt.check(apt.apt_quantize_pack_activations_fp16(
+                    x16.data_ptr(), p.M, p.K, p.q, it["a_buf"].data_ptr(), it["a_rs"].data_ptr(),
+                    sa_q.data_ptr(), sp), "apt_quantize_pack_activations_fp16")
+                gemm(w, sp, sa_q)
+
+        def fused_fp16(sp):
+            for w in ws:
+                apt.check(apt.apt_gemm_decode(p.M, p.N, p.K, p.p, p.q, x16.data_ptr(),
+                                              apt.APT_ACT_FP16, w.data_ptr(), c32.data_ptr(), None,
+                                              it["sw"].data_ptr(), c16.data_ptr(), sa_q.data_ptr(),
+                                              None, sp), "apt_gemm_decode")
+        row = {}
+        for src, pair in (("codes", (unfused_codes, fused_codes)), ("fp16", (unfused_fp16, fused_fp16))):
+            refs = None
+            for name, fn in zip(("unfused", "fused"), pair):
+                fn(wl.sp)
+                torch.cuda.synchronize()
+                got = (c32.clone(), c16.clone(), sa_q.clone())
+                if refs is None:
+                    refs = got
+                else:
+                    assert all(torch.equal(a, b) for a, b in zip(got[:2], refs[:2])), \
+                        "fused %s output differs from the unfused path" % src
+                    if src == "fp16":
+                        assert torch.equal(got[2], refs[2]), "fused fp16 scales differ"
+                g = graph_of(torch, fn)
+
+                def zero():
+                    c32.zero_()
+                    c16.zero_()
+
+                def check():
+                    assert torch.equal(c32, refs[0]) and torch.equal(c16, refs[1]), "graph replay"
+                row["%s_%s_us" % (src, name)] = round(replay_us(torch, g, copies, reps, zero, check), 3)
+                del g
+        row["launches"] = {"unfused": 2, "fused": 1}
+        row["weight_copies"] = copies
+        out["m1_n%d_k%d" % (p.N, p.K)] = row
+        del ws
+    return out
+
+
 def probe_lib():
     """The measurement probes (probes/*.hip, libapt_probe.so; not part of
     libapt.so)."""
@@ -661,10 +765,14 @@ def read_ceiling(torch, buf, reps: int = 4):
 def decode_layer_cold(wl, reps: int = 4):
     """One token through the linears of the W2A4 7B-class decoder layer with
     cold weights: q/k/v fused along N (one packed [3*4096][4096] matrix against
-    their shared input), o, gate/up fused (N = 2*11008) and down, four apt_gemm
-    launches with fp16 output per layer.  Enough layer copies (> 2x the
-    Infinity Cache) are rotated in one HIP graph that every launch reads HBM;
-    every replay's outputs are checked against the eager result."""
+    their shared input), o, gate/up fused (N = 2*11008) and down, four GEMMs
+    with fp16 output per layer.  Three forms: the GEMMs alone on activations
+    packed beforehand (four apt_gemm launches), and from each GEMM's fp16
+    input: the fp16 quantizer-packer then apt_gemm (eight launches), or
+    apt_gemm_decode (four launches, the row quantized inside each).  Enough
+    layer copies (> 2x the Infinity Cache) are rotated in one HIP graph that
+    every launch reads HBM; every replay's outputs are checked against the
+    eager result, and the two fp16-input forms must agree bit for bit."""
     torch, apt, np = wl.torch, wl.apt, wl.np
     import synth
     dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
@@ -672,7 +780,7 @@ def decode_layer_cold(wl, reps: int = 4):
     gemms = []
     bytes_alg = 0.0
     ops = 0
-    for parts in groups:
+    for gi, parts in enumerate(groups):
         probs = [synth.layer_w2a4(name, 1) for name in parts]
         p0 = probs[0]
         w_codes = np.concatenate([pr.w_codes for pr in probs], 0)
@@ -683,6 +791,10 @@ def decode_layer_cold(wl, reps: int = 4):
         g["sa"] = dev(p0.a_scale)
         g["sw"] = dev(np.concatenate([pr.w_scale for pr in probs]))
         g["c16"] = torch.empty((M, N), dtype=torch.float16, device="cuda")
+        g["x16"] = dev(synth.fp16_activations(synth.rng(82, gi), M, K))
+        g["xq"] = torch.empty_like(g["a"].data)
+        g["xq_rs"] = torch.empty(M, dtype=torch.int32, device="cuda")
+        g["xq_s"] = torch.empty(M, dtype=torch.float16, device="cuda")
         wsb = apt.apt_gemm_workspace_bytes(M, N, K, p0.p, p0.q, None)
         g["ws"], g["ws_bytes"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda"), wsb
         gemms.append(g)
@@ -693,41 +805,64 @@ def decode_layer_cold(wl, reps: int = 4):
     wcopies = [[apt.Packed(g["w"].data.clone(), g["w"].rowsum.clone(), g["N"], g["K"], g["p"])
                 for g in gemms] for _ in range(copies)]
 
-    def run(ws_list, sp):
-        for g, w in zip(gemms, ws_list):
-            st = apt.apt_gemm(1, g["N"], g["K"], g["p"], g["q"], g["a"].data.data_ptr(),
-                              w.data.data_ptr(), g["a"].rowsum.data_ptr(), w.rowsum.data_ptr(), None,
-                              g["sa"].data_ptr(), g["sw"].data_ptr(), g["c16"].data_ptr(), None,
-                              g["ws"].data_ptr(), g["ws_bytes"], sp)
-            apt.check(st, "apt_gemm")
-    run([g["w"] for g in gemms], wl.sp)
-    torch.cuda.synchronize()
-    refs = [g["c16"].clone() for g in gemms]
+    def gemm(g, w, sp, a, a_rs, sa):
+        apt.check(apt.apt_gemm(1, g["N"], g["K"], g["p"], g["q"], a.data_ptr(), w.data.data_ptr(),
+                               a_rs.data_ptr(), w.rowsum.data_ptr(), None, sa.data_ptr(),
+                               g["sw"].data_ptr(), g["c16"].data_ptr(), None, g["ws"].data_ptr(),
+                               g["ws_bytes"], sp), "apt_gemm")
 
-    def launch(sp):
-        for ws_list in wcopies:
-            run(ws_list, sp)
-    graph = graph_of(torch, launch)
-    times = []
-    for r in range(reps):
-        for g in gemms:
-            g["c16"].zero_()
+    def gemms_only(ws_list, sp):
+        for g, w in zip(gemms, ws_list):
+            gemm(g, w, sp, g["a"].data, g["a"].rowsum, g["sa"])
+
+    def unfused_fp16(ws_list, sp):
+        for g, w in zip(gemms, ws_list):
+            apt.check(apt.apt_quantize_pack_activations_fp16(
+                g["x16"].data_ptr(), 1, g["K"], g["q"], g["xq"].data_ptr(), g["xq_rs"].data_ptr(),
+                g["xq_s"].data_ptr(), sp), "apt_quantize_pack_activations_fp16")
+            gemm(g, w, sp, g["xq"], g["xq_rs"], g["xq_s"])
+
+    def fused_fp16(ws_list, sp):
+        for g, w in zip(gemms, ws_list):
+            apt.check(apt.apt_gemm_decode(1, g["N"], g["K"], g["p"], g["q"], g["x16"].data_ptr(),
+                                          apt.APT_ACT_FP16, w.data.data_ptr(), None, None,
+                                          g["sw"].data_ptr(), g["c16"].data_ptr(), None, None, sp),
+                      "apt_gemm_decode")
+    res = {}
+    fp16_ref = None
+    for name, run, launches in (("gemms_only", gemms_only, 4), ("unfused_fp16", unfused_fp16, 8),
+                                ("fused_fp16", fused_fp16, 4)):
+        run([g["w"] for g in gemms], wl.sp)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        graph.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        assert all(torch.equal(g["c16"], ref) for g, ref in zip(gemms, refs)), "layer graph replay"
-        if r > 0:
-            times.append(e0.elapsed_time(e1) / copies)
-    t = sorted(times)[len(times) // 2] * 1e-3
-    return {"us_per_layer": round(t * 1e6, 3), "launches_per_layer": len(gemms),
+        refs = [g["c16"].clone() for g in gemms]
+        if name == "unfused_fp16":
+            fp16_ref = refs
+        elif name == "fused_fp16":
+            assert all(torch.equal(a, b) for a, b in zip(refs, fp16_ref)), "fused layer differs"
+
+        def launch(sp, run=run):
+            for ws_list in wcopies:
+                run(ws_list, sp)
+        graph = graph_of(torch, launch)
+
+        def zero():
+            for g in gemms:
+                g["c16"].zero_()
+
+        def check(refs=refs):
+            assert all(torch.equal(g["c16"], r) for g, r in zip(gemms, refs)), "layer graph replay"
+        res[name] = (replay_us(torch, graph, copies, reps, zero, check), launches)
+        del graph
+    t = res["gemms_only"][0] * 1e-6
+    return {"us_per_layer": round(t * 1e6, 3), "launches_per_layer": 4,
             "algorithmic_bytes": int(bytes_alg), "achieved_GBs": round(bytes_alg / t / 1e9, 1),
             "peak_GBs": PEAK_HBM_GBS, "frac": round(bytes_alg / t / 1e9 / PEAK_HBM_GBS, 4),
             "layer_copies": copies, "effective_TOPS": round(ops / t / 1e12, 4),
+            "from_fp16_inputs": {k: {"us_per_layer": round(v[0], 3), "launches_per_layer": v[1]}
+                                 for k, v in res.items() if k != "gemms_only"},
             "method": "HIP graph of %d layers (q/k/v fused, o, gate/up fused, down), one per cold "
-                      "copy of the layer's weights; fp16 output" % copies}
+                      "copy of the layer's weights; fp16 output; us_per_layer, frac: the GEMMs "
+                      "on activations packed beforehand" % copies}
 
 
 def decode_sweep(reps: int = 4):
@@ -795,6 +930,81 @@ def decode_sweep(reps: int = 4):
     rows.append({"launch_floor_us": round(sorted(ts)[len(ts) // 2], 3),
                  "method": "HIP graph of 200 one-element kernels (torch add_), us per kernel"})
     return rows
+
+
+DECODE_SHAPES = [(0, 0, 0), (8, 4, 1), (8, 0, 4), (1, 4, 1), (1, 2, 1), (1, 0, 4), (1, 0, 2)]
+
+
+def decode_shapes(reps: int = 4):
+    """XOR-route launch shapes for decode batches (M = 2, 4, 8) with cold
+    weights: for each problem, the packed-activation GEMM (apt_gemm) and the
+    fused forms (apt_gemm_decode from int8 codes and from fp16) in every
+    (mt, waves_m, waves_n) of DECODE_SHAPES, (0, 0, 0) being the library's
+    own choice.  Each entry is one HIP graph over enough weight copies
+    (> 2x the Infinity Cache) that every launch reads HBM; every shape's
+    int32 output must equal the first one's.  Prints a text table."""
+    import torch
+
+    import paper_2508_19087_amd as apt
+    import synth
+    sp0 = torch.cuda.current_stream().cuda_stream
+    lines = []
+    hdr = "%6s %6s %5s %2s %-7s" % ("N", "K", "WpAq", "M", "source") + "".join(
+        "%9s" % ("auto" if s == (0, 0, 0) else "%d/%d/%d" % s) for s in DECODE_SHAPES) + "  best"
+    lines.append(hdr)
+    for (N, K, p, q) in [(4096, 4096, 2, 2), (11008, 4096, 2, 2), (4096, 4096, 2, 4), (11008, 4096, 2, 4),
+                         (4096, 11008, 2, 4), (16384, 4096, 2, 4), (22016, 4096, 2, 4)]:
+        g = synth.rng(83, N, K)
+        w = apt.pack(torch.from_numpy(synth.uniform_codes(g, N, K, p)).cuda(), p)
+        copies = max(8, int(2 * MALL_BYTES // w.data.numel()) + 1)
+        ws = [w.data.clone() for _ in range(copies)]
+        sw = torch.from_numpy(synth.scales(g, N, *synth.W_SCALE_RANGE)).cuda()
+        for M in (2, 4, 8):
+            xc = torch.from_numpy(synth.uniform_codes(g, M, K, q)).cuda()
+            x16 = torch.from_numpy(synth.fp16_activations(g, M, K)).cuda()
+            sa = torch.from_numpy(synth.scales(g, M, *synth.A_SCALE_RANGE)).cuda()
+            a = apt.pack(xc, q, activations=True)
+            c32 = torch.empty((M, N), dtype=torch.int32, device="cuda")
+            c16 = torch.empty((M, N), dtype=torch.float16, device="cuda")
+            so = torch.empty(M, dtype=torch.float16, device="cuda")
+            for src in ("packed", "codes", "fp16"):
+                ref, ts = None, []
+                for mt, wm, wn in DECODE_SHAPES:
+                    cfg = apt.apt_config_t.make(apt.APT_ROUTE_XOR, waves_m=wm, waves_n=wn, mt=mt)
+
+                    def launch(sp, cfg=cfg, src=src):
+                        for wi in ws:
+                            if src == "packed":
+                                st = apt.apt_gemm(M, N, K, p, q, a.data.data_ptr(), wi.data_ptr(), None,
+                                                  None, c32.data_ptr(), sa.data_ptr(), sw.data_ptr(),
+                                                  c16.data_ptr(), cfg, None, 0, sp)
+                            elif src == "codes":
+                                st = apt.apt_gemm_decode(M, N, K, p, q, xc.data_ptr(), apt.APT_ACT_CODES,
+                                                         wi.data_ptr(), c32.data_ptr(), sa.data_ptr(),
+                                                         sw.data_ptr(), c16.data_ptr(), None, cfg, sp)
+                            else:
+                                st = apt.apt_gemm_decode(M, N, K, p, q, x16.data_ptr(), apt.APT_ACT_FP16,
+                                                         wi.data_ptr(), c32.data_ptr(), None,
+                                                         sw.data_ptr(), c16.data_ptr(), so.data_ptr(),
+                                                         cfg, sp)
+                            apt.check(st, src)
+                    launch(sp0)
+                    torch.cuda.synchronize()
+                    if ref is None:
+                        ref = c32.clone()
+                    assert torch.equal(c32, ref), "launch shapes disagree"
+                    gr = graph_of(torch, launch)
+                    ts.append(replay_us(torch, gr, copies, reps))
+                    del gr
+                best = min(range(len(ts)), key=lambda i: ts[i])
+                bs = DECODE_SHAPES[best]
+                lines.append("%6d %6d  W%dA%d %2d %-7s" % (N, K, p, q, M, src) +
+                             "".join("%9.2f" % t for t in ts) +
+                             "  %s" % ("auto" if bs == (0, 0, 0) else "%d/%d/%d" % bs))
+                log("bench: decode shapes %s" % lines[-1])
+        del ws
+        torch.cuda.empty_cache()
+    return "\n".join(lines)
 
 
 def epilogue_table(calls: int = 50):
@@ -1373,6 +1583,12 @@ def main():
                          "apt_gemm, 20 calls each, separated by marker fills; prints the plan")
     ap.add_argument("--write-workload-stats", nargs=3, metavar=("TRACE_CSV", "PLAN_JSON", "COMMAND"),
                     help="print the per-workload kernel durations of a --workloads trace and exit")
+    ap.add_argument("--decode-shapes", action="store_true",
+                    help="print the XOR launch shapes for 2-8 tokens (packed and fused activations) "
+                         "with cold weights and exit")
+    ap.add_argument("--decode-chain", action="store_true",
+                    help="print one token's decode GEMMs and decoder layer from their activations, "
+                         "unfused and fused, with cold weights, and exit")
     ap.add_argument("--traffic-commands", default="",
                     help="the commands that produced the --write-traffic directories")
     args = ap.parse_args()
@@ -1417,6 +1633,9 @@ def main():
     if args.search:
         print(json.dumps(search_table(), indent=1), flush=True)
         return
+    if args.decode_shapes:
+        print(decode_shapes(), flush=True)
+        return
     if args.decode_sweep:
         print(json.dumps(decode_sweep(), indent=1), flush=True)
         return
@@ -1431,6 +1650,12 @@ def main():
         return
     log("bench: building workload")
     wl = Workload()
+    if args.decode_chain:
+        res = {"token_chain": decode_token_cold(wl)}
+        log("bench: one-token W2A4 decoder layer with cold weights")
+        res["w2a4_layer_m1"] = decode_layer_cold(wl)
+        print(json.dumps(res, indent=1), flush=True)
+        return
     wl.overlap = not args.serial_step
     for _ in range(args.warmup):
         wl.step()
@@ -1480,6 +1705,8 @@ def main():
     if not args.no_decode_cold:
         log("bench: decode GEMMs with cold weights")
         result["decode_cold"] = decode_cold(wl)
+        log("bench: one token's decode GEMM from its activations, unfused and fused")
+        result["decode_cold"]["token_chain"] = decode_token_cold(wl)
         log("bench: one-token W2A4 decoder layer with cold weights")
         result["decode_cold"]["w2a4_layer_m1"] = decode_layer_cold(wl)
     if not args.no_cpu_baseline:

@@ -105,8 +105,10 @@ enum {
  *              sums through the workspace.  The result does not depend on it.
  *   lds_stages depth of the weight LDS ring (int8 MFMA route: 0 or 3; the
  *              +-1 plane route ignores it)
- *   mt         XOR route: activation rows per block row: 1, 8, or 0 = 1
- *              when M = 1 and 8 otherwise
+ *   mt         XOR route: activation rows per block row: 1, 8, or 0 =
+ *              chosen by the library (1 for M = 1, for M <= 2 below 2048
+ *              row groups of 8 weight rows, and below 1024 row groups unless
+ *              K > 7168 and M > 2; else 8)
  *   split_n    int8 MFMA route: 0, or a multiple of bn with 0 < split_n < N
  *              and of 8: columns [0, split_n) use the tile above and columns
  *              [split_n, N) a second launch with tile tail_bm x tail_bn (of
@@ -293,8 +295,8 @@ enum {
 
 /* The decode GEMM (one to eight tokens) with the activation side of the
  * conversion fused into it: C = A * W^T on the XOR + popcount route (Sec.
- * III-B), where A is given unpacked and each workgroup converts its token's
- * row to bipolar-INT bit-planes (Sec. III-A conversion, Sec. IV-A steps 1-3;
+ * III-B), where A is given unpacked and each workgroup converts its tokens'
+ * rows to bipolar-INT bit-planes (Sec. III-A conversion, Sec. IV-A steps 1-3;
  * for fp16 input after quantizing the row) into its LDS, so that neither a
  * packer launch nor a packed activation buffer sits between the token and
  * the GEMV.  Results equal those of the packer (apt_quantize_pack_activations
@@ -317,14 +319,19 @@ enum {
  *   a_scale_out  APT_ACT_FP16: device fp16 bits [M] receiving each row's scale
  *             s_m (as the fp16 packer's a_scale), or NULL; APT_ACT_CODES: must be NULL
  *   cfg       NULL or route AUTO: the library's XOR launch shape; else an XOR
- *             route config (waves_m, waves_n as for apt_gemm; mt 0 or 1)
+ *             route config (mt, waves_m, waves_n as for apt_gemm)
+ * Each workgroup keeps the bit-planes of its activation rows in LDS: with mt
+ * = 1 one row, ceil(K / 1024) * 1024 * q / 8 bytes; with mt = 8 eight rows,
+ * ceil(K / 1024) * 16 * (8 q + 1) bytes; at most 64 KB.  mt = 0 takes 1 for
+ * M = 1, below 1024 row groups of 8 weight rows, and below 2048 row groups
+ * for M <= 2 or an fp16 source; else 8 if that fits, else 1.
  * Errors: APT_ERR_INVALID_ARG for M outside [1, APT_DECODE_MAX_M], N or K < 1,
  * bits outside [1, 8], a bad a_kind, a NULL source or weight pointer, a
  * misaligned weight or fp16 source pointer, both outputs NULL, c_fp16 without
  * its scales, a scale pointer the a_kind does not take, or a cfg that is not
- * an XOR config with mt 0 or 1; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >=
- * 2^31 or when the row's bit-planes (ceil(K / 1024) * 1024 * q / 8 bytes) do
- * not fit in 64 KB of LDS; APT_ERR_HIP on launch failure. */
+ * a valid XOR config; APT_ERR_UNSUPPORTED when K (2^p-1)(2^q-1) >= 2^31 or
+ * when the rows' bit-planes do not fit in 64 KB of LDS; APT_ERR_HIP on launch
+ * failure. */
 apt_status_t apt_gemm_decode(int M, int N, int K, int p, int q,
                              const void* a_src, int a_kind, const void* w_packed,
                              int32_t* c_int32, const uint16_t* a_scale,

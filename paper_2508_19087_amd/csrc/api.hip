@@ -255,10 +255,10 @@ apt_status_t apt_gemm_decode(int M, int N, int K, int p, int q, const void* a_sr
   apt_config_t c{};
   c.route = APT_ROUTE_XOR;
   if (cfg != nullptr && cfg->route != APT_ROUTE_AUTO) {
-    if (cfg->route != APT_ROUTE_XOR || !apt::xor_act_config_ok(*cfg)) return APT_ERR_INVALID_ARG;
+    if (cfg->route != APT_ROUTE_XOR || !apt::xor_config_ok(*cfg)) return APT_ERR_INVALID_ARG;
     c = *cfg;
   }
-  if (!apt::xor_act_sizes_ok(M, N, K, p, q, c)) return APT_ERR_UNSUPPORTED;
+  if (!apt::xor_act_sizes_ok(M, N, K, p, q, c, fp16_src)) return APT_ERR_UNSUPPORTED;
   apt::GemmArgs g;
   g.M = M; g.N = N; g.K = K; g.p = p; g.q = q;
   g.a_packed = nullptr;

@@ -113,14 +113,12 @@ __device__ __forceinline__ float affine_value(int32_t c, float sa, float sw, flo
 hipError_t launch_gemm_xor(const GemmArgs& g, const apt_config_t& cfg, hipStream_t stream);
 bool xor_config_ok(const apt_config_t& cfg);
 bool xor_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg);
-// XOR route with the activation row converted inside the kernel from int8
+// XOR route with the activation rows converted inside the kernel from int8
 // codes or (fp16_src) fp16 values; a_scale_out receives the fp16 source's
-// per-row scales (or NULL).  mt is forced to 1 (cfg.mt must not be 8) and the
-// row's LDS copy must fit (xor_act_sizes_ok).
+// per-row scales (or NULL).  The rows' LDS copy must fit (xor_act_sizes_ok).
 hipError_t launch_gemm_xor_act(const GemmArgs& g, const void* a_src, bool fp16_src,
                                uint16_t* a_scale_out, const apt_config_t& cfg, hipStream_t stream);
-bool xor_act_config_ok(const apt_config_t& cfg);
-bool xor_act_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg);
+bool xor_act_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg, bool fp16_src);
 
 // Reassembled int8 MFMA route (gemm_int8.hip).  The workspace holds the
 // activations expanded into MFMA fragments (int8_workspace_bytes).

@@ -107,7 +107,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t xor_rsrc(const void* base, uin
 // popcount.
 template <int P, int Q, int MT, bool DEEP, bool kALds, int SRC = kSrcPacked>
 __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams prm) {
-  static_assert(SRC == kSrcPacked || (MT == 1 && kALds), "the fused source builds a one-row LDS copy");
+  static_assert(SRC == kSrcPacked || kALds, "the fused source builds the LDS copy");
   extern __shared__ uint4 a_lds[];
   const GemmArgs& g = prm.g;
   const int NC = prm.nchunks;
@@ -149,32 +149,43 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
 #pragma unroll
     for (int k = 0; k < kStagePre; ++k) pre[k] = a_at(threadIdx.x + k * (int)blockDim.x);
   }
-  // Fused source: lane t takes elements 16 t + 16 L r, r = 0, 1, ... (L lanes
-  // in the workgroup) of row m0, up to the padded row length 128 NS; its first
-  // kSrcHeld rounds are requested here, before the weights.
+  // Fused source: for each of the block row's activation rows, lane t takes
+  // elements 16 t + 16 L r, r = 0, 1, ... (L lanes in the workgroup) up to the
+  // padded row length 128 NS.  The first kHeld rounds of every row are
+  // requested here, before the weights.
   using CodeSrc = rowcode::CodeRow<false, Q>;
   using CodeVec = rowcode::CodeRow<true, Q>;
   using HalfSrc = rowcode::HalfRow<false, Q>;
   using HalfVec = rowcode::HalfRow<true, Q>;
   constexpr int kSrcDwords = SRC == kSrcHalf ? HalfSrc::kDwords : CodeSrc::kDwords;
   constexpr int kElemBytes = SRC == kSrcHalf ? 2 : 1;
+  constexpr int kSrcRows = SRC != kSrcPacked ? MT : 1;
+  constexpr int kHeld = MT == 1 ? kSrcHeld : 1;
   const int src_step = (int)blockDim.x * rowcode::kLaneElems;
-  const int src_rounds = (NS * kChunk + src_step - 1) / src_step;  // uniform
-  const __amdgpu_buffer_rsrc_t s_rsrc = xor_rsrc(
-      static_cast<const uint8_t*>(prm.a_src) + (int64_t)m0 * g.K * kElemBytes, (uint32_t)g.K * kElemBytes);
-  auto src_load = [&](int r, uint32_t* d) __attribute__((always_inline)) {
+  const int src_rounds = (NS * kChunk + src_step - 1) / src_step;  // per row, uniform
+  // row m of the block row: its K elements (reads past them return zeros)
+  auto s_rsrc = [&](int m) __attribute__((always_inline)) {
+    return xor_rsrc(static_cast<const uint8_t*>(prm.a_src) + (int64_t)(m0 + m) * g.K * kElemBytes,
+                    (uint32_t)g.K * kElemBytes);
+  };
+  auto src_load = [&](__amdgpu_buffer_rsrc_t rs, int r, uint32_t* d) __attribute__((always_inline)) {
     const int k0 = r * src_step + (int)threadIdx.x * rowcode::kLaneElems;
     if (SRC == kSrcHalf) {
-      if (prm.a_vec) HalfVec::load(s_rsrc, k0, d); else HalfSrc::load(s_rsrc, k0, d);
+      if (prm.a_vec) HalfVec::load(rs, k0, d); else HalfSrc::load(rs, k0, d);
     } else {
-      if (prm.a_vec) CodeVec::load(s_rsrc, k0, d); else CodeSrc::load(s_rsrc, k0, d);
+      if (prm.a_vec) CodeVec::load(rs, k0, d); else CodeSrc::load(rs, k0, d);
     }
   };
-  uint32_t sd[SRC != kSrcPacked ? kSrcHeld : 1][kSrcDwords];
+  uint32_t sd[kSrcRows][kHeld][kSrcDwords];
   if (SRC != kSrcPacked) {
 #pragma unroll
-    for (int r = 0; r < kSrcHeld; ++r)
-      if (r < src_rounds) src_load(r, sd[r]);
+    for (int m = 0; m < kSrcRows; ++m) {
+      if (m >= mrows) break;  // uniform
+      const __amdgpu_buffer_rsrc_t rs = s_rsrc(m);
+#pragma unroll
+      for (int r = 0; r < kHeld; ++r)
+        if (r < src_rounds) src_load(rs, r, sd[m][r]);
+    }
   }
 
   // ---- weight batches
@@ -202,7 +213,8 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
   load(wcur, 0);
   if (kB < T) load(wnxt, kB);
 
-  float s_act = 0.0f;  // fused fp16 source: this row's bipolar scale
+  // fused fp16 source: each row's bipolar scale, and the quotient constants
+  __shared__ float s_row[SRC == kSrcHalf ? 3 * MT : 1];
   if (kALds && SRC == kSrcPacked) {
 #pragma unroll
     for (int k = 0; k < kStagePre; ++k) {
@@ -216,34 +228,47 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
   if (SRC != kSrcPacked) {
     // The conversion of the packer (Sec. III-A, and for fp16 the bipolar form
     // of the per-row linear quantizer), with the plane words stored in the
-    // one-row LDS layout: word w of plane j of chunk c at dword
-    // 4 (c Q + j) + w.  Rounds past kSrcHeld are loaded (again) here.
-    __shared__ uint32_t s_red[kMaxWaves];
+    // LDS layout of act(): word w of plane j of chunk c of row m at dword
+    // 4 (c kAV + j) + w (MT = 1) or 4 (c kAV + 8 j + m) + w (MT = 8).  Rounds
+    // past kHeld are loaded (again) here.
     uint32_t* lds32 = reinterpret_cast<uint32_t*>(a_lds);
-    float rh = 0.0f, s2 = 0.0f;
     if (SRC == kSrcHalf) {
-      rowcode::ushort2_t mm = {0, 0};
+      __shared__ uint32_t s_red[MT][kMaxWaves];
+      const int nw = (int)(blockDim.x / kWave);
 #pragma unroll
-      for (int r = 0; r < kSrcHeld; ++r)
-        if (r < src_rounds) mm = HalfSrc::fold_max(mm, sd[r]);
-      for (int r = kSrcHeld; r < src_rounds; ++r) {
-        uint32_t d[kSrcDwords];
-        src_load(r, d);
-        mm = HalfSrc::fold_max(mm, d);
+      for (int m = 0; m < kSrcRows; ++m) {
+        if (m >= mrows) break;  // uniform
+        rowcode::ushort2_t mm = {0, 0};
+#pragma unroll
+        for (int r = 0; r < kHeld; ++r)
+          if (r < src_rounds) mm = HalfSrc::fold_max(mm, sd[m][r]);
+        const __amdgpu_buffer_rsrc_t rs = s_rsrc(m);
+        for (int r = kHeld; r < src_rounds; ++r) {
+          uint32_t d[kSrcDwords];
+          src_load(rs, r, d);
+          mm = HalfSrc::fold_max(mm, d);
+        }
+        uint32_t v = max((uint32_t)mm.x, (uint32_t)mm.y);
+        for (int off = kWave / 2; off > 0; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off));
+        if (lane == 0) s_red[m][wave] = v;
       }
-      uint32_t m = max((uint32_t)mm.x, (uint32_t)mm.y);
-      for (int off = kWave / 2; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
-      if (lane == 0) s_red[wave] = m;
       __syncthreads();
-      m = 0u;
-      for (int v = 0; v < (int)(blockDim.x / kWave); ++v) m = max(m, s_red[v]);
-      const uint16_t s16 = rowcode::row_scale<Q>(m, rh, s2);
-      s_act = __half2float(__ushort_as_half(s16));
-      if (prm.a_scale_out != nullptr && blockIdx.x == 0 && threadIdx.x == 0) prm.a_scale_out[m0] = s16;
+      if ((int)threadIdx.x < mrows) {
+        const int m = threadIdx.x;
+        uint32_t v = 0u;
+        for (int w = 0; w < nw; ++w) v = max(v, s_red[m][w]);
+        float rh, s2;
+        const uint16_t s16 = rowcode::row_scale<Q>(v, rh, s2);
+        s_row[3 * m] = __half2float(__ushort_as_half(s16));
+        s_row[3 * m + 1] = rh;
+        s_row[3 * m + 2] = s2;
+        if (prm.a_scale_out != nullptr && blockIdx.x == 0) prm.a_scale_out[m0 + m] = s16;
+      }
+      __syncthreads();
     }
     const bool odd = (lane & 1) != 0;
     // uniform in r: both lanes of a pair run every round (DPP swap)
-    auto convert = [&](int r, const uint32_t* d) __attribute__((always_inline)) {
+    auto convert = [&](int m, int r, const uint32_t* d, float rh, float s2) __attribute__((always_inline)) {
       const int k0 = r * src_step + (int)threadIdx.x * rowcode::kLaneElems;
       uint32_t u[4];
       if (SRC == kSrcHalf) HalfSrc::words(d, rh, s2, u); else CodeSrc::words(d, rh, s2, u);
@@ -255,20 +280,29 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
       uint32_t alo = u[0], ahi = u[1], blo = u[2], bhi = u[3];
       rowcode::transpose8x8<Q>(alo, ahi);
       rowcode::transpose8x8<Q>(blo, bhi);
-      uint32_t* dst = lds32 + (k0 / kChunk) * Q * kWordsPerPlane + (k0 % kChunk) / 32;
+      const int c = k0 / kChunk;
+      uint32_t* dst = lds32 + (c * kAV + (MT == 8 ? m : 0)) * kWordsPerPlane + (k0 % kChunk) / 32;
+      constexpr int kPlaneDwords = (MT == 8 ? kRowGroup : 1) * kWordsPerPlane;
 #pragma unroll
       for (int i = 0; i < Q; i += 2) {
         const uint32_t wv = rowcode::plane_word(i < 4 ? alo : ahi, i < 4 ? blo : bhi, i % 4, odd);
-        if (k0 < NS * kChunk && (!odd || i + 1 < Q)) dst[(i + (odd ? 1 : 0)) * kWordsPerPlane] = wv;
+        if (k0 < NS * kChunk && (!odd || i + 1 < Q)) dst[(i + (odd ? 1 : 0)) * kPlaneDwords] = wv;
       }
     };
 #pragma unroll
-    for (int r = 0; r < kSrcHeld; ++r)
-      if (r < src_rounds) convert(r, sd[r]);
-    for (int r = kSrcHeld; r < src_rounds; ++r) {
-      uint32_t d[kSrcDwords];
-      src_load(r, d);
-      convert(r, d);
+    for (int m = 0; m < kSrcRows; ++m) {
+      if (m >= mrows) break;  // uniform
+      const float rh = SRC == kSrcHalf ? s_row[3 * m + 1] : 0.0f;
+      const float s2 = SRC == kSrcHalf ? s_row[3 * m + 2] : 0.0f;
+#pragma unroll
+      for (int r = 0; r < kHeld; ++r)
+        if (r < src_rounds) convert(m, r, sd[m][r], rh, s2);
+      const __amdgpu_buffer_rsrc_t rs = s_rsrc(m);
+      for (int r = kHeld; r < src_rounds; ++r) {
+        uint32_t d[kSrcDwords];
+        src_load(rs, r, d);
+        convert(m, r, d, rh, s2);
+      }
     }
     __syncthreads();
   }
@@ -365,7 +399,7 @@ __global__ __launch_bounds__(kWave* kMaxWaves) void gemm_xor_kernel(XorParams pr
       f = affine_value(c, __half2float(g.a_scale[mg]), sw, zw, (float)g.a_rowsum[mg],
                        __half2float(g.a_zero[mg]), sw * (float)g.w_rowsum[n] + (float)g.K * zw);
     } else {
-      f = (float)c * (SRC == kSrcHalf ? s_act : __half2float(g.a_scale[mg]));
+      f = (float)c * (SRC == kSrcHalf ? s_row[3 * m] : __half2float(g.a_scale[mg]));
       f = f * __half2float(g.w_scale[n]);
     }
     g.c_fp16[o] = __float2half_rn(f);
@@ -399,10 +433,8 @@ inline hipError_t launch_lds(Kernel kern, const XorLaunch& L, hipStream_t s, con
 
 template <int P, int Q, int MT, bool DEEP>
 inline hipError_t launch_mt(const XorParams& prm, const XorLaunch& L, hipStream_t s) {
-  if constexpr (MT == 1) {
-    if (L.src == kSrcCodes) return launch_lds(gemm_xor_kernel<P, Q, 1, DEEP, true, kSrcCodes>, L, s, prm);
-    if (L.src == kSrcHalf) return launch_lds(gemm_xor_kernel<P, Q, 1, DEEP, true, kSrcHalf>, L, s, prm);
-  }
+  if (L.src == kSrcCodes) return launch_lds(gemm_xor_kernel<P, Q, MT, DEEP, true, kSrcCodes>, L, s, prm);
+  if (L.src == kSrcHalf) return launch_lds(gemm_xor_kernel<P, Q, MT, DEEP, true, kSrcHalf>, L, s, prm);
   if (L.lds) return launch_lds(gemm_xor_kernel<P, Q, MT, DEEP, true>, L, s, prm);
   return launch_kernel(gemm_xor_kernel<P, Q, MT, DEEP, false>, L.grid, dim3(kWave * L.waves), 0, s, prm);
 }

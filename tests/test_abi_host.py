@@ -315,7 +315,8 @@ XOR = apt.APT_ROUTE_XOR
     (dict(c16=C, sw=None), apt.APT_ERR_INVALID_ARG),
     (dict(kind=apt.APT_ACT_FP16), apt.APT_ERR_INVALID_ARG),       # a_scale with an fp16 source
     (dict(so=S + 64), apt.APT_ERR_INVALID_ARG),                   # scale output with codes
-    (dict(cfg=apt.apt_config_t.make(XOR, mt=8)), apt.APT_ERR_INVALID_ARG),
+    (dict(cfg=apt.apt_config_t.make(XOR, mt=5)), apt.APT_ERR_INVALID_ARG),
+    (dict(K=7169, p=1, q=8, cfg=apt.apt_config_t.make(XOR, mt=8)), apt.APT_ERR_UNSUPPORTED),
     (dict(cfg=apt.apt_config_t.make(XOR, waves_m=3)), apt.APT_ERR_INVALID_ARG),
     (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)),
      apt.APT_ERR_INVALID_ARG),

@@ -139,15 +139,18 @@ def test_decode_all_bit_pairs(p, q):
     check_fp16(2, 33, 777, p, q, seed=3)
 
 
-XOR_SHAPES = [dict(waves_m=w, waves_n=1) for w in (1, 2, 4)] + [dict(waves_n=b) for b in (2, 4)]
+XOR_SHAPES = ([dict(mt=mt, waves_m=w, waves_n=1) for mt in (1, 8) for w in (1, 2, 4)] +
+              [dict(mt=mt, waves_n=b) for mt in (1, 8) for b in (2, 4)])
 
 
 @pytest.mark.parametrize("shape", XOR_SHAPES, ids=lambda d: "-".join("%s%d" % kv for kv in d.items()))
 @pytest.mark.parametrize("K", [100, 4096, 7000, 11008])
-def test_decode_forced_shapes(shape, K):
-    cfg = apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=1, **shape)
-    check_codes(3, 200, K, 3, 3, cfg=cfg, seed=4)
-    check_fp16(3, 200, K, 3, 3, cfg=cfg, seed=4)
+@pytest.mark.parametrize("M", [3, 8])
+def test_decode_forced_shapes(shape, K, M):
+    """One or eight activation rows per block row (mt), each wave shape."""
+    cfg = apt.apt_config_t.make(apt.APT_ROUTE_XOR, **shape)
+    check_codes(M, 200, K, 3, 3, cfg=cfg, seed=4)
+    check_fp16(M, 200, K, 3, 3, cfg=cfg, seed=4)
 
 
 @pytest.mark.parametrize("offset", [1, 3, 8])
@@ -178,7 +181,7 @@ def test_decode_special_fp16_rows():
 
 def test_decode_matches_unfused_path():
     """Bit-identical to packer + apt_gemm (XOR route), codes and fp16."""
-    for M, K in [(1, 4096), (4, 11008), (8, 1000)]:
+    for M, K in [(1, 4096), (2, 4096), (4, 11008), (8, 1000), (8, 4096)]:
         check_codes(M, 1024, K, 2, 4, seed=6, against_unfused=True)
         check_fp16(M, 1024, K, 2, 4, seed=6, against_unfused=True)
 
@@ -194,6 +197,25 @@ def test_decode_largest_k_in_lds():
     c = torch.empty((1, 16), dtype=torch.int32, device="cuda")
     st = apt.apt_gemm_decode(1, 16, 65537, 1, 8, x.data_ptr(), apt.APT_ACT_CODES, w.data.data_ptr(),
                              c.data_ptr(), None, None, None, None, None, _stream())
+    assert st == apt.APT_ERR_UNSUPPORTED
+
+
+def test_decode_eight_rows_lds_limit():
+    """Eight rows at q = 8: K = 7168 is the longest whose eight-row copy fits
+    in LDS; past it the library converts one row per block row (mt = 0), and a
+    forced mt = 8 is refused."""
+    mt8 = apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=8)
+    check_codes(8, 64, 7168, 2, 8, cfg=mt8, seed=9, against_unfused=True)
+    check_fp16(8, 64, 7168, 2, 8, cfg=mt8, seed=9, against_unfused=True)
+    check_codes(8, 16384, 7169, 2, 8, seed=9)   # 2048 row groups: mt = 8 would be chosen
+    check_fp16(8, 64, 7169, 2, 8, seed=9)
+    import torch
+    x = torch.zeros((8, 7169), dtype=torch.int8, device="cuda")
+    w = apt.pack(dev(synth.uniform_codes(synth.rng(95), 64, 7169, 2)), 2)
+    c = torch.empty((8, 64), dtype=torch.int32, device="cuda")
+    st = apt.apt_gemm_decode(8, 64, 7169, 2, 8, x.data_ptr(), apt.APT_ACT_CODES, w.data.data_ptr(),
+                             c.data_ptr(), None, None, None, None,
+                             apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=8), _stream())
     assert st == apt.APT_ERR_UNSUPPORTED
 
 
