@@ -1,9 +1,11 @@
 """Benchmark of the WpAq bipolar-INT GEMM hot path on one MI355X.
 
 One step is one pass of the whole path over one batch of synthetic input:
-  decode  (M = 1):    pack the W2A2 token's activations, then the two 7B-class
-                      decode GEMMs (N=4096 and N=11008, K=4096) with int32 and
-                      fp16-epilogue outputs;
+  decode  (M = 1):    the two 7B-class W2A2 decode GEMMs (N=4096 and N=11008,
+                      K=4096) with int32 and fp16-epilogue outputs, each one
+                      apt_gemm_decode launch that converts the token's codes
+                      to bipolar planes inside the GEMV (--unfused-decode:
+                      the packer, then apt_gemm);
   prefill (M = 2048): pack the W4A4 activations, then the 2048 x 11008 x 4096
                       GEMM with int32 output.
 Weights are packed once before timing (they are static).  Every call goes
@@ -70,6 +72,7 @@ class Workload:
         self.side = torch.cuda.Stream()
         self.side_sp = self.side.cuda_stream
         self.overlap = True
+        self.unfused_decode = False
         self.dec = [synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]
         self.pre = synth.w4a4_prefill()
         dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
@@ -114,14 +117,32 @@ class Workload:
                                it["ws"].data_ptr(), it["ws_bytes"], sp)
         self.apt.check(st, "apt_gemm")
 
+    def decode(self, it, w=None, sp=None):
+        """The decode GEMM from the token's codes in one launch: apt_gemm_decode
+        converts the activation row inside the GEMV (same results as
+        pack_act + gemm on the XOR route)."""
+        p = it["prob"]
+        w = w if w is not None else it["w"]
+        sp = sp if sp is not None else self.sp
+        st = self.apt.apt_gemm_decode(p.M, p.N, p.K, p.p, p.q, it["a_codes"].data_ptr(),
+                                      self.apt.APT_ACT_CODES, w.data.data_ptr(), it["c32"].data_ptr(),
+                                      it["sa"].data_ptr(), it["sw"].data_ptr(), it["c16"].data_ptr(),
+                                      None, None, sp)
+        self.apt.check(st, "apt_gemm_decode")
+
     def step(self):
-        """One pass of the path: each problem's activations packed, then its GEMM.
-        With `overlap`, the two decode problems run on the side stream and the
-        prefill on the main one; a device-wide synchronize closes the step."""
+        """One pass of the path: the two decode GEMMs from their tokens' codes
+        (converted and decomposed into planes inside the GEMV, or with
+        `unfused_decode` packed by the packer first), then the prefill's
+        activations packed and its GEMM.  With `overlap`, the decode problems
+        run on the side stream and the prefill on the main one."""
         sp = self.side_sp if self.overlap else self.sp
         for it in self.items[:2]:
-            self.pack_act(it, sp)
-            self.gemm(it, sp=sp)
+            if self.unfused_decode:
+                self.pack_act(it, sp)
+                self.gemm(it, sp=sp)
+            else:
+                self.decode(it, sp=sp)
         self.pack_act(self.items[2])
         self.gemm(self.items[2])
 
@@ -1435,6 +1456,33 @@ def workloads_run(calls: int = 20):
                          "M": prob.M, "K": prob.K, "q": prob.q, "calls": calls, "pack": kind,
                          "bytes": prob.M * prob.K * (1 if kind == "codes" else 2)
                          + apt.apt_packed_bytes(prob.M, prob.K, prob.q) + 4 * prob.M})
+    # the decode workloads through apt_gemm_decode (one launch from the token's
+    # codes or fp16 values, int32 and fp16 outputs)
+    for i, (prob, a, w, sa, sw) in enumerate(items):
+        if prob.M > 8 or sa is None:
+            continue
+        codes = dev(prob.a_codes)
+        x16 = torch.from_numpy(np.ascontiguousarray(
+            (prob.a_codes.astype(np.float32) * 0.37).astype(np.float16))).cuda()
+        c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
+        c16 = torch.empty((prob.M, prob.N), dtype=torch.float16, device="cuda")
+        so = torch.empty(prob.M, dtype=torch.float16, device="cuda")
+        sp = torch.cuda.current_stream().cuda_stream
+        for kind in ("codes", "fp16"):
+            marker.fill_(len(plan))
+            for _ in range(calls):
+                if kind == "codes":
+                    st = apt.apt_gemm_decode(prob.M, prob.N, prob.K, prob.p, prob.q, codes.data_ptr(),
+                                             apt.APT_ACT_CODES, w.data.data_ptr(), c32.data_ptr(),
+                                             sa.data_ptr(), sw.data_ptr(), c16.data_ptr(), None, None, sp)
+                else:
+                    st = apt.apt_gemm_decode(prob.M, prob.N, prob.K, prob.p, prob.q, x16.data_ptr(),
+                                             apt.APT_ACT_FP16, w.data.data_ptr(), c32.data_ptr(), None,
+                                             sw.data_ptr(), c16.data_ptr(), so.data_ptr(), None, sp)
+                apt.check(st, "apt_gemm_decode")
+            torch.cuda.synchronize()
+            plan.append({"workload": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
+                         "q": prob.q, "ops": prob.ops, "calls": calls, "decode": kind})
     print(json.dumps(plan), flush=True)
 
 
@@ -1458,7 +1506,8 @@ def write_workload_stats(trace_csv: str, plan_json: str, command: str):
     lines = ["# Kernel durations of every workload configuration in its selected config (rocprofv3",
              "# kernel trace; per kernel: median and mean duration over the calls after the first,",
              "# in microseconds; 'per call' sums the kernels one apt_gemm call launches, 'TOPS' is",
-             "# 2 M N K over that sum).  Weights and activations are packed before the timed calls.",
+             "# 2 M N K over that sum).  Weights and activations are packed before the timed calls,",
+             "# except in the apt_gemm_decode lines, which take the tokens' codes or fp16 values.",
              "# command (repository root on the MI355X box): " + command,
              ""]
     for pl, seg in zip(plan, segs):
@@ -1484,8 +1533,14 @@ def write_workload_stats(trace_csv: str, plan_json: str, command: str):
             for ptxt in parts:
                 lines.append("    " + ptxt)
             continue
+        if "decode" in pl:
+            lines.append("%-32s %-28s per call %8.2f us  %8.1f TOPS" % (
+                pl["workload"], "apt_gemm_decode (%s)" % pl["decode"], total, pl["ops"] / total / 1e6))
+            for ptxt in parts:
+                lines.append("    " + ptxt)
+            continue
         c = pl["config"]
-        route = {1: "xor", 2: "pm1", 3: "int8", 4: "fp4", 5: "fp6"}[c["route"]]
+        route = {1: "xor", 2: "pm1", 3: "int8", 4: "fp4", 5: "fp6", 6: "fp8"}[c["route"]]
         cfg = route if route == "xor" else "%s %dx%d/%dx%d g%d%s" % (
             route, c["bm"], c["bn"], c["waves_m"], c["waves_n"], c["grid"],
             " split %d" % c["split_n"] if c["split_n"] else "")
@@ -1567,6 +1622,9 @@ def main():
     ap.add_argument("--calibrate", action="store_true",
                     help="print the selector model's calibration (pair and fixed times per tile "
                          "shape and operand class) and exit")
+    ap.add_argument("--unfused-decode", action="store_true",
+                    help="in the step, pack each decode token's activations with the packer and "
+                         "then run apt_gemm, instead of apt_gemm_decode's one launch")
     ap.add_argument("--serial-step", action="store_true",
                     help="run the whole step on one stream (the decode GEMMs before the prefill) "
                          "instead of the decode chain on a second stream beside the prefill")
@@ -1657,6 +1715,7 @@ def main():
         print(json.dumps(res, indent=1), flush=True)
         return
     wl.overlap = not args.serial_step
+    wl.unfused_decode = args.unfused_decode
     for _ in range(args.warmup):
         wl.step()
     torch.cuda.synchronize()
@@ -1693,10 +1752,12 @@ def main():
         "ms_per_step": round(step_s * 1e3, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int8", "data": "synthetic",
         "config": {"workload": "W2A2 decode M=1 (N=4096 and N=11008, K=4096, int32 + fp16 epilogue) "
-                               "+ W4A4 prefill M=2048 N=11008 K=4096 (int32); activations packed "
-                               "every step, weights packed once",
+                               "+ W4A4 prefill M=2048 N=11008 K=4096 (int32); activations converted "
+                               "and decomposed every step, weights packed once",
                    "schedule": ("decode chain on a second stream beside the prefill chain"
                                 if wl.overlap else "one stream"),
+                   "decode_activations": ("packer + apt_gemm" if wl.unfused_decode else
+                                          "apt_gemm_decode (converted inside the GEMV)"),
                    "prefill_config": cfg},
         "roofline": roofline,
     }
