@@ -6,8 +6,10 @@ One step is one pass of the whole path over one batch of synthetic input:
                       apt_gemm_decode launch that converts the token's codes
                       to bipolar planes inside the GEMV (--unfused-decode:
                       the packer, then apt_gemm);
-  prefill (M = 2048): pack the W4A4 activations, then the 2048 x 11008 x 4096
-                      GEMM with int32 output.
+  prefill (M = 2048): the W4A4 2048 x 11008 x 4096 GEMM with int32 output
+                      from the activation codes, one apt_gemm_act call that
+                      converts them straight into the int8 MFMA operand
+                      fragments (--packed-prefill: the packer, then apt_gemm).
 Weights are packed once before timing (they are static).  Every call goes
 through the C ABI with the config chosen by the library's selector.
 
@@ -39,7 +41,8 @@ MALL_BYTES = 256 << 20      # Infinity Cache; cold-weight runs rotate through > 
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2508_19087_amd/csrc/gemm_int8.h", "paper_2508_19087_amd/csrc/gemm_int8.hip",
                   "paper_2508_19087_amd/csrc/gemm_int8_inst.hip", "paper_2508_19087_amd/csrc/reassemble.h",
-                  "paper_2508_19087_amd/csrc/select.hip"]
+                  "paper_2508_19087_amd/csrc/select.hip", "paper_2508_19087_amd/csrc/act_frag.hip",
+                  "paper_2508_19087_amd/csrc/rowcode.h"]
 
 
 def kernel_hash() -> str:
@@ -73,6 +76,7 @@ class Workload:
         self.side_sp = self.side.cuda_stream
         self.overlap = True
         self.unfused_decode = False
+        self.packed_prefill = False
         self.dec = [synth.w2a2_decode(1, 4096), synth.w2a2_decode(1, synth.MLP)]
         self.pre = synth.w4a4_prefill()
         dev = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()  # noqa: E731
@@ -87,8 +91,11 @@ class Workload:
             it["a_rs"] = torch.empty(prob.M, dtype=torch.int32, device="cuda")
             it["c32"] = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
             wsb = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, None)
-            it["ws"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            wsa = apt.apt_gemm_act_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q,
+                                                   apt.APT_ACT_CODES, None)
+            it["ws"] = torch.empty(max(wsb, wsa, 16), dtype=torch.uint8, device="cuda")
             it["ws_bytes"] = wsb
+            it["ws_act_bytes"] = wsa
             if fp16:
                 it["sa"], it["sw"] = dev(prob.a_scale), dev(prob.w_scale)
                 it["c16"] = torch.empty((prob.M, prob.N), dtype=torch.float16, device="cuda")
@@ -130,12 +137,38 @@ class Workload:
                                       None, None, sp)
         self.apt.check(st, "apt_gemm_decode")
 
+    def gemm_act(self, it, sp=None):
+        """The GEMM from the activations' codes in one call (apt_gemm_act): on
+        the int8 MFMA route the codes go straight into the operand fragments
+        (same results as pack_act + gemm)."""
+        p = it["prob"]
+        sp = sp if sp is not None else self.sp
+        fp16 = it["fp16"]
+        st = self.apt.apt_gemm_act(p.M, p.N, p.K, p.p, p.q, it["a_codes"].data_ptr(),
+                                   self.apt.APT_ACT_CODES, it["w"].data.data_ptr(),
+                                   it["w"].rowsum.data_ptr(), it["c32"].data_ptr(),
+                                   it["sa"].data_ptr() if fp16 else None,
+                                   it["sw"].data_ptr() if fp16 else None,
+                                   it["c16"].data_ptr() if fp16 else None, None, None,
+                                   it["ws"].data_ptr(), it["ws_act_bytes"], sp)
+        self.apt.check(st, "apt_gemm_act")
+
+    def prefill(self, sp=None):
+        """The prefill problem as the step runs it: apt_gemm_act from the codes,
+        or with `packed_prefill` the packer and then apt_gemm."""
+        it = self.items[2]
+        if self.packed_prefill:
+            self.pack_act(it, sp)
+            self.gemm(it, sp=sp)
+        else:
+            self.gemm_act(it, sp)
+
     def step(self):
         """One pass of the path: the two decode GEMMs from their tokens' codes
         (converted and decomposed into planes inside the GEMV, or with
-        `unfused_decode` packed by the packer first), then the prefill's
-        activations packed and its GEMM.  With `overlap`, the decode problems
-        run on the side stream and the prefill on the main one."""
+        `unfused_decode` packed by the packer first), then the prefill GEMM
+        from its codes (see prefill).  With `overlap`, the decode problems run
+        on the side stream and the prefill on the main one."""
         sp = self.side_sp if self.overlap else self.sp
         for it in self.items[:2]:
             if self.unfused_decode:
@@ -143,24 +176,33 @@ class Workload:
                 self.gemm(it, sp=sp)
             else:
                 self.decode(it, sp=sp)
-        self.pack_act(self.items[2])
-        self.gemm(self.items[2])
+        self.prefill()
+
+
+def prefill_call(wl):
+    """The one call of the prefill GEMM the roofline describes (the step's
+    form): apt_gemm_act from the codes (fragment writer + GEMM kernel), or
+    with packed_prefill apt_gemm on activations packed beforehand (expansion
+    + GEMM kernel)."""
+    it = wl.items[2]
+    if wl.packed_prefill:
+        wl.pack_act(it)
+        return lambda: wl.gemm(it)
+    return lambda: wl.gemm_act(it)
 
 
 def prefill_call_time(wl, calls: int) -> float:
-    """Average seconds per prefill apt_gemm call (activation expansion plus
-    the GEMM kernel), timed with HIP events on the workload's stream around
-    `calls` back-to-back calls."""
+    """Average seconds per prefill call (prefill_call), timed with HIP events
+    on the workload's stream around `calls` back-to-back calls."""
     torch = wl.torch
-    it = wl.items[2]
-    wl.pack_act(it)
+    call = prefill_call(wl)
     for _ in range(3):
-        wl.gemm(it)
+        call()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(wl.stream)
     for _ in range(calls):
-        wl.gemm(it)
+        call()
     e1.record(wl.stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) * 1e-3 / calls
@@ -1328,16 +1370,16 @@ COPY_BYTES = 256 << 20  # calibration copy for the HBM byte counters
 TRAFFIC_JSON = "gemm_int8_w4a4_2048x11008x4096_traffic.json"
 
 
-def counters_run(reps: int = 3):
-    """For rocprofv3 --pmc: the prefill GEMM `reps` times after one warm-up
-    call, then a plain device copy of COPY_BYTES (read and written once),
+def counters_run(reps: int = 3, packed_prefill: bool = False):
+    """For rocprofv3 --pmc: the prefill call (prefill_call) `reps` times after
+    one warm-up call, then a plain device copy of COPY_BYTES (read and written once),
     whose counter readings calibrate the byte counters."""
     import torch
     wl = Workload()
-    it = wl.items[2]
-    wl.pack_act(it)
+    wl.packed_prefill = packed_prefill
+    call = prefill_call(wl)
     for _ in range(reps + 1):
-        wl.gemm(it)
+        call()
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
@@ -1575,7 +1617,8 @@ def write_traffic(fetch_dir: str, write_dir: str, commands: str):
         copy = [v for k, vs in vals.items() if "copyBuffer" in k for v in vs if v > COPY_BYTES / 4]
         factor = COPY_BYTES / statistics.median(copy)
         # the GEMM's kernels: every dispatch after the warm-up call
-        gemm = {k: vs for k, vs in vals.items() if "expand_a_kernel" in k or "gemm_int8_" in k}
+        gemm = {k: vs for k, vs in vals.items()
+                if "expand_a_kernel" in k or "act_frag_kernel" in k or "gemm_int8_" in k}
         per_call = 0.0
         kernels = {}
         for k, vs in gemm.items():
@@ -1622,6 +1665,9 @@ def main():
     ap.add_argument("--calibrate", action="store_true",
                     help="print the selector model's calibration (pair and fixed times per tile "
                          "shape and operand class) and exit")
+    ap.add_argument("--packed-prefill", action="store_true",
+                    help="in the step and the roofline, pack the prefill activations with the packer "
+                         "and run apt_gemm, instead of apt_gemm_act from the codes")
     ap.add_argument("--unfused-decode", action="store_true",
                     help="in the step, pack each decode token's activations with the packer and "
                          "then run apt_gemm, instead of apt_gemm_decode's one launch")
@@ -1665,7 +1711,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     if args.counters_run:
-        counters_run()
+        counters_run(packed_prefill=args.packed_prefill)
         return
     if args.workloads:
         workloads_run()
@@ -1716,6 +1762,7 @@ def main():
         return
     wl.overlap = not args.serial_step
     wl.unfused_decode = args.unfused_decode
+    wl.packed_prefill = args.packed_prefill
     for _ in range(args.warmup):
         wl.step()
     torch.cuda.synchronize()
@@ -1743,8 +1790,10 @@ def main():
     tiles += ", one workgroup per tile" if sel.grid == 0 else ", %d persistent workgroups" % sel.grid
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": traffic,
-                "kernel": "apt_gemm W4A4 M=2048 N=11008 K=4096: expand_a_kernel + gemm_int8 kernel "
-                          "(%s), %d back-to-back calls" % (tiles, args.roofline_calls),
+                "kernel": ("apt_gemm W4A4 M=2048 N=11008 K=4096 on packed activations: expand_a_kernel"
+                           if wl.packed_prefill else
+                           "apt_gemm_act W4A4 M=2048 N=11008 K=4096 from the int8 codes: act_frag_kernel")
+                          + " + gemm_int8 kernel (%s), %d back-to-back calls" % (tiles, args.roofline_calls),
                 "avg_launch_us": round(gemm_s * 1e6, 2)}
     result = {
         "metric": METRIC, "value": round(wl.ops / step_s / 1e12, 3), "unit": "TOPS",
@@ -1758,6 +1807,9 @@ def main():
                                 if wl.overlap else "one stream"),
                    "decode_activations": ("packer + apt_gemm" if wl.unfused_decode else
                                           "apt_gemm_decode (converted inside the GEMV)"),
+                   "prefill_activations": ("packer + apt_gemm" if wl.packed_prefill else
+                                           "apt_gemm_act (codes written straight into the int8 "
+                                           "MFMA fragments)"),
                    "prefill_config": cfg},
         "roofline": roofline,
     }

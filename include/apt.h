@@ -338,6 +338,51 @@ apt_status_t apt_gemm_decode(int M, int N, int K, int p, int q,
                              const uint16_t* w_scale, uint16_t* c_fp16,
                              uint16_t* a_scale_out, const apt_config_t* cfg, void* stream);
 
+/* Device workspace bytes apt_gemm_act needs for this problem, activation
+ * kind and config (cfg NULL or route AUTO = the selected one); 0 when the
+ * call needs none (the fused XOR form) or for invalid arguments. */
+size_t apt_gemm_act_workspace_bytes(int M, int N, int K, int p, int q, int a_kind,
+                                    const apt_config_t* cfg);
+
+/* C = A * W^T for any M with the activations given unpacked, as int8 codes
+ * or fp16 values (APT_ACT_CODES / APT_ACT_FP16, quantized per row as
+ * apt_quantize_pack_activations_fp16 does): the conversion to bipolar-INT
+ * (Sec. III-A) runs inside this call, in the form the route needs, and the
+ * results equal those of the matching packer followed by apt_gemm with the
+ * same config, bit for bit (codes, scales, int32 C and fp16 output).
+ *   - XOR route with M <= APT_DECODE_MAX_M whose rows fit in LDS: the rows are
+ *     converted to bit-planes inside the GEMV, as apt_gemm_decode does (no
+ *     workspace);
+ *   - int8 MFMA route: the rows are written straight into the route's int8
+ *     MFMA operand fragments, with their row sums (and fp16 scales), by one
+ *     kernel (Sec. III-B's plane sum rebuilt before the multiply, as apt_gemm
+ *     does from the planes), so no bit-planes are written or read;
+ *   - every other route: the packer writes the bit-planes (Sec. IV-A) into the
+ *     workspace, then the route runs as in apt_gemm.
+ *   a_src     device, [M][K] row-major: int8 codes, or fp16 bits (2-byte
+ *             aligned; values must be finite); 16-byte alignment and K % 16 == 0
+ *             select wider loads (the result does not depend on it)
+ *   w_packed  device, packed p-bit weights [N][K] (apt_pack_weights), 16-byte aligned
+ *   w_rowsum  device int32 [N] from apt_pack_weights; required by the MFMA
+ *             routes, may be NULL on the XOR and +-1 plane routes
+ *   c_int32, w_scale, c_fp16, cfg   as apt_gemm
+ *   a_scale   APT_ACT_CODES: per-token bipolar scale (fp16 bits [M]), required
+ *             with c_fp16; APT_ACT_FP16: must be NULL
+ *   a_scale_out  APT_ACT_FP16: device fp16 bits [M] receiving the row scales,
+ *             or NULL; APT_ACT_CODES: must be NULL
+ *   workspace, workspace_bytes  device scratch of at least
+ *             apt_gemm_act_workspace_bytes(...) bytes, 16-byte aligned (NULL
+ *             when 0); overwritten; calls sharing it must not overlap in time
+ * Errors: as apt_gemm (a_packed and a_rowsum replaced by a_src), and
+ * APT_ERR_INVALID_ARG for a bad a_kind, a misaligned fp16 source or a scale
+ * pointer the a_kind does not take; APT_ERR_UNSUPPORTED also for K > 2^30. */
+apt_status_t apt_gemm_act(int M, int N, int K, int p, int q,
+                          const void* a_src, int a_kind, const void* w_packed,
+                          const int32_t* w_rowsum, int32_t* c_int32,
+                          const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
+                          uint16_t* a_scale_out, const apt_config_t* cfg,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
 /* Device workspace bytes apt_search_config needs for this problem: the most
  * that any config it times needs (apt_gemm_workspace_bytes).  Returns 0 for
  * invalid sizes or bit widths. */

@@ -12,6 +12,7 @@ from .apt import (APT_ACT_CODES, APT_ACT_FP16, APT_DECODE_MAX_M, APT_ERR_HIP, AP
                   ROUTE_NAMES, AptError, Packed, apt_config_t, apt_gemm, apt_gemm_affine,
                   apt_gemm_workspace_bytes, apt_config_table_clear, apt_config_table_size,
                   apt_last_hip_error, apt_gemm_noalloc, apt_gemm_decode, gemm_decode,
+                  apt_gemm_act, apt_gemm_act_workspace_bytes, gemm_act,
                   apt_search_config, apt_search_workspace_bytes, check,
                   apt_pack_weights, apt_packed_bytes, apt_quantize_pack_activations,
                   apt_quantize_pack_activations_fp16, apt_select_config, gemm, header_functions,

@@ -106,6 +106,11 @@ def lib() -> ctypes.CDLL:
         L.apt_gemm_decode.argtypes = ([ctypes.c_int] * 5 + [_vp, ctypes.c_int] + [_vp] * 6 +
                                       [ctypes.POINTER(apt_config_t), _vp])
         L.apt_gemm_decode.restype = ctypes.c_int
+        L.apt_gemm_act_workspace_bytes.argtypes = [ctypes.c_int] * 6 + [ctypes.POINTER(apt_config_t)]
+        L.apt_gemm_act_workspace_bytes.restype = ctypes.c_size_t
+        L.apt_gemm_act.argtypes = ([ctypes.c_int] * 5 + [_vp, ctypes.c_int] + [_vp] * 7 +
+                                   [ctypes.POINTER(apt_config_t), _vp, ctypes.c_size_t, _vp])
+        L.apt_gemm_act.restype = ctypes.c_int
         L.apt_search_workspace_bytes.argtypes = [ctypes.c_int] * 5
         L.apt_search_workspace_bytes.restype = ctypes.c_size_t
         L.apt_search_config.argtypes = ([ctypes.c_int] * 5 + [_vp] * 6 + [ctypes.c_size_t, _vp,
@@ -189,6 +194,19 @@ def apt_gemm_decode(M, N, K, p, q, a_src, a_kind, w_packed, c_int32, a_scale, w_
     return lib().apt_gemm_decode(M, N, K, p, q, a_src, a_kind, w_packed, c_int32, a_scale,
                                  w_scale, c_fp16, a_scale_out,
                                  ctypes.byref(cfg) if cfg is not None else None, stream)
+
+
+def apt_gemm_act_workspace_bytes(M, N, K, p, q, a_kind, cfg=None) -> int:
+    return int(lib().apt_gemm_act_workspace_bytes(M, N, K, p, q, a_kind,
+                                                  ctypes.byref(cfg) if cfg else None))
+
+
+def apt_gemm_act(M, N, K, p, q, a_src, a_kind, w_packed, w_rowsum, c_int32, a_scale, w_scale,
+                 c_fp16, a_scale_out, cfg, workspace, workspace_bytes, stream) -> int:
+    return lib().apt_gemm_act(M, N, K, p, q, a_src, a_kind, w_packed, w_rowsum, c_int32, a_scale,
+                              w_scale, c_fp16, a_scale_out,
+                              ctypes.byref(cfg) if cfg is not None else None, workspace,
+                              workspace_bytes, stream)
 
 
 def apt_search_workspace_bytes(M, N, K, p, q) -> int:
@@ -348,6 +366,37 @@ def gemm_decode(x, q: int, w: Packed, out_int32: bool = True, a_scale=None, w_sc
                           APT_ACT_FP16 if fp16_src else APT_ACT_CODES, w.data.data_ptr(),
                           _ptr(c32), _ptr(a_scale), _ptr(w_scale), _ptr(c16), _ptr(scale), cfg,
                           _stream_ptr(stream)), "apt_gemm_decode")
+    return c32, c16, scale
+
+
+def gemm_act(x, q: int, w: Packed, out_int32: bool = True, a_scale=None, w_scale=None,
+             out_fp16: bool = False, cfg: apt_config_t | None = None, stream=None,
+             workspace=None):
+    """C = A W^T for unpacked activations x [M][K] (a CUDA tensor: int8 q-bit
+    codes, or fp16 values quantized per row inside the call), any M.  Returns
+    (c_int32 or None, c_fp16 or None, scales): the fp16 row scales for fp16 x,
+    else None.  A workspace of apt_gemm_act_workspace_bytes is allocated with
+    torch unless one is passed."""
+    torch = _torch()
+    assert x.is_cuda and x.dim() == 2 and x.dtype in (torch.int8, torch.float16)
+    x = x.contiguous()
+    M, K = x.shape
+    assert K == w.K
+    N = w.rows
+    kind = APT_ACT_FP16 if x.dtype == torch.float16 else APT_ACT_CODES
+    dev = x.device
+    ws_bytes = apt_gemm_act_workspace_bytes(M, N, K, w.bits, q, kind, cfg)
+    with _on_stream(stream):
+        c32 = torch.empty((M, N), dtype=torch.int32, device=dev) if out_int32 else None
+        c16 = torch.empty((M, N), dtype=torch.float16, device=dev) if out_fp16 else None
+        scale = torch.empty(M, dtype=torch.float16, device=dev) if kind == APT_ACT_FP16 else None
+        if workspace is None and ws_bytes > 0:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    check(apt_gemm_act(M, N, K, w.bits, q, x.data_ptr(), kind, w.data.data_ptr(), _ptr(w.rowsum),
+                       _ptr(c32), _ptr(a_scale), _ptr(w_scale), _ptr(c16), _ptr(scale), cfg,
+                       ws_ptr, ws_len, _stream_ptr(stream)), "apt_gemm_act")
     return c32, c16, scale
 
 

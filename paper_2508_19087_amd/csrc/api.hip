@@ -208,6 +208,74 @@ apt_status_t gemm_common(int M, int N, int K, int p, int q, const void* a_packed
                      w_scale, c_fp16, a_zero, w_zero, c, workspace, workspace_bytes, stream);
 }
 
+// ---- GEMM from unpacked activations (apt_gemm_act) ----------------------
+//
+// How a resolved config consumes the activations: the XOR route's fused form
+// (M <= 8, rows converted in the GEMV's LDS), the int8-format MFMA route's
+// fragments written straight from the source, or else the packer into the
+// workspace followed by the route as apt_gemm runs it.
+enum class ActPlan { kFusedXor, kFragments, kPack };
+
+struct ActLayout {
+  ActPlan plan;
+  size_t route_bytes;  // the route's own workspace, at offset 0
+  size_t planes_off;   // packed activations (kPack)
+  size_t rowsum_off;   // int32 [M] row sums (kFragments, kPack)
+  size_t scale_off;    // fp16 [M] scales of an fp16 source (kFragments, kPack)
+  size_t total;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+ActLayout act_layout(int M, int N, int K, int p, int q, bool fp16, const apt_config_t& c) {
+  ActLayout L{};
+  if (c.route == APT_ROUTE_XOR && M <= APT_DECODE_MAX_M &&
+      xor_act_sizes_ok(M, N, K, p, q, c, fp16)) {
+    L.plan = ActPlan::kFusedXor;
+    return L;
+  }
+  const bool frags = c.route == APT_ROUTE_INT8_MFMA && int8_operand_format(c, q) == 0;
+  L.plan = frags ? ActPlan::kFragments : ActPlan::kPack;
+  L.route_bytes = align256(gemm_workspace_need(M, N, K, q, c));
+  size_t off = L.route_bytes;
+  L.planes_off = off;
+  if (!frags) off += align256(apt_packed_bytes(M, K, q));
+  L.rowsum_off = off;
+  off += align256((size_t)M * 4);
+  L.scale_off = off;
+  off += align256((size_t)M * 2);
+  L.total = off;
+  return L;
+}
+
+// Validates an apt_gemm_act call and resolves its config; returns APT_OK or
+// the status to report.
+apt_status_t act_check(int M, int N, int K, int p, int q, const void* a_src, int a_kind,
+                       const void* w_packed, const int32_t* w_rowsum, const int32_t* c_int32,
+                       const uint16_t* a_scale, const uint16_t* w_scale, const uint16_t* c_fp16,
+                       const uint16_t* a_scale_out, const apt_config_t* cfg, apt_config_t* resolved,
+                       ActLayout* layout) {
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return APT_ERR_INVALID_ARG;
+  if (a_kind != APT_ACT_CODES && a_kind != APT_ACT_FP16) return APT_ERR_INVALID_ARG;
+  const bool fp16 = a_kind == APT_ACT_FP16;
+  if (a_src == nullptr || w_packed == nullptr || !aligned16(w_packed)) return APT_ERR_INVALID_ARG;
+  if (fp16 && (reinterpret_cast<uintptr_t>(a_src) & 1u) != 0) return APT_ERR_INVALID_ARG;
+  if (c_int32 == nullptr && c_fp16 == nullptr) return APT_ERR_INVALID_ARG;
+  if (c_fp16 != nullptr && (w_scale == nullptr || (!fp16 && a_scale == nullptr)))
+    return APT_ERR_INVALID_ARG;
+  if (fp16 ? a_scale != nullptr : a_scale_out != nullptr) return APT_ERR_INVALID_ARG;
+  if (!fits_int32(K, p, q)) return APT_ERR_UNSUPPORTED;
+  if (K > kMaxPackK) return APT_ERR_UNSUPPORTED;
+  apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO) ? select_config(M, N, K, p, q)
+                                                                      : *cfg;
+  // the activation row sums come from this call; the weights' from the caller
+  const apt_status_t st = check_config(c, M, N, K, p, q, w_rowsum != nullptr);
+  if (st != APT_OK) return st;
+  *resolved = c;
+  *layout = act_layout(M, N, K, p, q, fp16, c);
+  return APT_OK;
+}
+
 }  // namespace apt
 
 using apt::gemm_common;
@@ -235,6 +303,70 @@ apt_status_t apt_gemm_affine(int M, int N, int K, int p, int q, const void* a_pa
     return APT_ERR_INVALID_ARG;
   return gemm_common(M, N, K, p, q, a_packed, w_packed, a_rowsum, w_rowsum, c_int32, a_scale,
                      w_scale, c_fp16, a_zero, w_zero, cfg, workspace, workspace_bytes, stream);
+}
+
+size_t apt_gemm_act_workspace_bytes(int M, int N, int K, int p, int q, int a_kind,
+                                    const apt_config_t* cfg) {
+  if (M < 1 || N < 1 || K < 1 || !bits_ok(p) || !bits_ok(q)) return 0;
+  if (a_kind != APT_ACT_CODES && a_kind != APT_ACT_FP16) return 0;
+  const apt_config_t c = (cfg == nullptr || cfg->route == APT_ROUTE_AUTO)
+                             ? apt::select_config(M, N, K, p, q)
+                             : *cfg;
+  if (check_config(c, M, N, K, p, q, true) != APT_OK) return 0;
+  return apt::act_layout(M, N, K, p, q, a_kind == APT_ACT_FP16, c).total;
+}
+
+apt_status_t apt_gemm_act(int M, int N, int K, int p, int q, const void* a_src, int a_kind,
+                          const void* w_packed, const int32_t* w_rowsum, int32_t* c_int32,
+                          const uint16_t* a_scale, const uint16_t* w_scale, uint16_t* c_fp16,
+                          uint16_t* a_scale_out, const apt_config_t* cfg, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  apt_config_t c;
+  apt::ActLayout L;
+  const apt_status_t st = apt::act_check(M, N, K, p, q, a_src, a_kind, w_packed, w_rowsum, c_int32,
+                                         a_scale, w_scale, c_fp16, a_scale_out, cfg, &c, &L);
+  if (st != APT_OK) return st;
+  if (L.total > 0) {
+    if (workspace == nullptr || workspace_bytes < L.total) return APT_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return APT_ERR_INVALID_ARG;
+  }
+  const bool fp16 = a_kind == APT_ACT_FP16;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  apt::GemmArgs g;
+  g.M = M; g.N = N; g.K = K; g.p = p; g.q = q;
+  g.a_packed = nullptr;
+  g.w_packed = static_cast<const uint32_t*>(w_packed);
+  g.a_rowsum = nullptr;
+  g.w_rowsum = w_rowsum;
+  g.c_int32 = c_int32;
+  g.a_scale = reinterpret_cast<const __half*>(a_scale);
+  g.w_scale = reinterpret_cast<const __half*>(w_scale);
+  g.c_fp16 = reinterpret_cast<__half*>(c_fp16);
+  g.a_zero = nullptr;
+  g.w_zero = nullptr;
+  if (L.plan == apt::ActPlan::kFusedXor)
+    return hip_status(apt::launch_gemm_xor_act(g, a_src, fp16, a_scale_out, c, s));
+  int32_t* rowsum = reinterpret_cast<int32_t*>(ws + L.rowsum_off);
+  uint16_t* scale = reinterpret_cast<uint16_t*>(ws + L.scale_off);
+  g.a_rowsum = rowsum;
+  if (fp16) g.a_scale = reinterpret_cast<const __half*>(scale);
+  if (L.plan == apt::ActPlan::kFragments) {
+    const apt::ActSource src{a_src, fp16, rowsum, scale, a_scale_out};
+    return hip_status(apt::launch_gemm_int8(g, c, ws, s, &src));
+  }
+  // the packer into the workspace, then the route on the packed rows (an fp16
+  // source's scales go straight to the caller's array when there is one)
+  uint32_t* planes = reinterpret_cast<uint32_t*>(ws + L.planes_off);
+  if (a_scale_out != nullptr) scale = a_scale_out;
+  const hipError_t e =
+      fp16 ? apt::launch_quantize_pack(static_cast<const uint16_t*>(a_src), M, K, q, planes, rowsum,
+                                       scale, s)
+           : apt::launch_pack(static_cast<const int8_t*>(a_src), M, K, q, planes, rowsum, s);
+  if (e != hipSuccess) return hip_status(e);
+  return apt::gemm_launch(M, N, K, p, q, planes, w_packed, rowsum, w_rowsum, c_int32,
+                          fp16 ? scale : a_scale, w_scale, c_fp16, nullptr, nullptr, c, ws,
+                          L.route_bytes, stream);
 }
 
 apt_status_t apt_gemm_decode(int M, int N, int K, int p, int q, const void* a_src, int a_kind,

@@ -120,10 +120,29 @@ hipError_t launch_gemm_xor_act(const GemmArgs& g, const void* a_src, bool fp16_s
                                uint16_t* a_scale_out, const apt_config_t& cfg, hipStream_t stream);
 bool xor_act_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg, bool fp16_src);
 
+// Activations given unpacked (int8 codes, or fp16 values quantized per row)
+// to a route that builds its operand bytes itself: the int8-format MFMA route
+// writes its fragments, row sums (and fp16 scales) straight from them
+// (act_frag.hip).
+struct ActSource {
+  const void* data;    // [M][K] int8 codes or fp16 bits
+  bool fp16;
+  int32_t* rowsum;     // device [M]: receives the row sums
+  uint16_t* scale;     // device [M]: receives the fp16 source's scales
+  uint16_t* scale_out; // device [M] or NULL: a copy of them for the caller
+};
+hipError_t launch_act_frag(const void* src, bool fp16, int M, int K, int q, int nsteps, void* frag,
+                           int32_t* rowsum, uint16_t* scale, uint16_t* scale_out, int* counters,
+                           int ncounters, hipStream_t s);
+
 // Reassembled int8 MFMA route (gemm_int8.hip).  The workspace holds the
-// activations expanded into MFMA fragments (int8_workspace_bytes).
+// activations expanded into MFMA fragments (int8_workspace_bytes): from the
+// packed planes (src NULL), or, with the int8 operand format only, from an
+// unpacked source (g.a_rowsum and g.a_scale must then name src's outputs).
 hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
-                            hipStream_t stream);
+                            hipStream_t stream, const ActSource* src = nullptr);
+// Operand format of the activations in a config of the MFMA routes (0: int8).
+int int8_operand_format(const apt_config_t& cfg, int q);
 constexpr int kMaxGrid = 4096;  // persistent workgroups of the int8 route, at most
 bool int8_config_ok(const apt_config_t& cfg, int N);
 bool int8_sizes_ok(int M, int N, int K, int p, int q, const apt_config_t& cfg);

@@ -156,8 +156,10 @@ size_t int8_workspace_bytes(int M, int N, int K, int q, const apt_config_t& cfg)
   return bytes;
 }
 
+int int8_operand_format(const apt_config_t& cfg, int q) { return int8::operand_format(cfg, q); }
+
 hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* workspace,
-                            hipStream_t stream) {
+                            hipStream_t stream, const ActSource* src) {
   using namespace int8;
   Plan pl[2];
   const int nl = make_plans(g.M, g.N, g.K, cfg, pl);
@@ -199,7 +201,11 @@ hipError_t launch_gemm_int8(const GemmArgs& g, const apt_config_t& cfg, void* wo
   v4i* frag = static_cast<v4i*>(workspace);
   const Int8Params& p0 = prm[0];
   hipError_t e = hipErrorInvalidValue;
-  switch (g.q) {
+  if (src != nullptr) {
+    if (fmt != 0) return hipErrorInvalidValue;
+    e = launch_act_frag(src->data, src->fp16, g.M, g.K, g.q, p0.nsteps, frag, src->rowsum,
+                        src->scale, src->scale_out, counters, ncounters, stream);
+  } else switch (g.q) {
     case 1: e = launch_expand_for_q<1>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
     case 2: e = launch_expand_for_q<2>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;
     case 3: e = launch_expand_for_q<3>(fmt, g.a_packed, g.M, p0.nchunks, p0.nsteps, p0.mblocks, frag, counters, ncounters, stream); break;

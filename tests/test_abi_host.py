@@ -15,7 +15,8 @@ def test_exports_every_declared_symbol():
                           "apt_quantize_pack_activations_fp16", "apt_select_config", "apt_gemm_workspace_bytes", "apt_gemm",
                           "apt_gemm_affine", "apt_search_workspace_bytes", "apt_search_config",
                           "apt_config_table_clear", "apt_config_table_size", "apt_last_hip_error",
-                          "apt_gemm_noalloc", "apt_gemm_decode",
+                          "apt_gemm_noalloc", "apt_gemm_decode", "apt_gemm_act",
+                          "apt_gemm_act_workspace_bytes",
                           "apt_status_string"}
     L = apt.lib()
     for n in names:
@@ -327,6 +328,59 @@ XOR = apt.APT_ROUTE_XOR
 def test_gemm_decode_validation(kw, want):
     """Rejected before any HIP call (the pointers are never dereferenced)."""
     assert gemm_decode(**kw) == want
+
+
+def gemm_act(M=4, N=4, K=64, p=2, q=2, x=A, kind=apt.APT_ACT_CODES, w=W, rw=RW, c32=C, sa=S,
+             sw=S + 128, c16=None, so=None, cfg=None, ws=None, ws_bytes=0):
+    return apt.apt_gemm_act(M, N, K, p, q, x, kind, w, rw, c32, sa, sw, c16, so, cfg, ws, ws_bytes,
+                            None)
+
+
+INT8_CFG = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(M=0), apt.APT_ERR_INVALID_ARG), (dict(N=0), apt.APT_ERR_INVALID_ARG),
+    (dict(K=0), apt.APT_ERR_INVALID_ARG), (dict(p=0), apt.APT_ERR_INVALID_ARG),
+    (dict(q=9), apt.APT_ERR_INVALID_ARG), (dict(kind=7), apt.APT_ERR_INVALID_ARG),
+    (dict(x=None), apt.APT_ERR_INVALID_ARG), (dict(w=None), apt.APT_ERR_INVALID_ARG),
+    (dict(w=W + 8), apt.APT_ERR_INVALID_ARG),
+    (dict(kind=apt.APT_ACT_FP16, x=A + 1, sa=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c32=None), apt.APT_ERR_INVALID_ARG),
+    (dict(c16=C, sw=None), apt.APT_ERR_INVALID_ARG), (dict(c16=C, sa=None), apt.APT_ERR_INVALID_ARG),
+    (dict(kind=apt.APT_ACT_FP16), apt.APT_ERR_INVALID_ARG),        # a_scale with an fp16 source
+    (dict(so=S + 64), apt.APT_ERR_INVALID_ARG),                    # scale output with codes
+    (dict(K=33026, p=8, q=8), apt.APT_ERR_UNSUPPORTED),
+    (dict(cfg=apt.apt_config_t.make(apt.APT_ROUTE_XOR, mt=3)), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, cfg=INT8_CFG, rw=None), apt.APT_ERR_INVALID_ARG),  # MFMA routes need the weight row sums
+    (dict(M=64, cfg=INT8_CFG), apt.APT_ERR_WORKSPACE),
+    (dict(M=64, cfg=INT8_CFG, ws=S + 4, ws_bytes=1 << 30), apt.APT_ERR_INVALID_ARG),
+    (dict(M=64, K=(1 << 30) + 128, p=1, q=1, cfg=INT8_CFG), apt.APT_ERR_UNSUPPORTED),
+])
+def test_gemm_act_validation(kw, want):
+    """Rejected before any HIP call (the pointers are never dereferenced)."""
+    assert gemm_act(**kw) == want
+
+
+def test_gemm_act_workspace_bytes():
+    """Fused XOR decode: none; int8 MFMA: the route's workspace plus row sums
+    and scales; other routes: also the packed activations."""
+    ws = apt.apt_gemm_act_workspace_bytes
+    assert ws(1, 4096, 4096, 2, 2, apt.APT_ACT_CODES) == 0
+    assert ws(1, 4096, 4096, 2, 2, apt.APT_ACT_FP16) == 0
+    M, N, K = 1024, 4096, 4096
+    route = apt.apt_gemm_workspace_bytes(M, N, K, 2, 4, INT8_CFG)
+    r256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    assert ws(M, N, K, 2, 4, apt.APT_ACT_CODES, INT8_CFG) == r256(route) + r256(4 * M) + r256(2 * M)
+    xor = apt.apt_config_t.make(apt.APT_ROUTE_XOR)
+    assert ws(64, N, K, 2, 4, apt.APT_ACT_CODES, xor) == (
+        r256(apt.apt_packed_bytes(64, K, 4)) + r256(4 * 64) + r256(2 * 64))
+    fp4 = apt.apt_config_t.make(apt.APT_ROUTE_FP4_MFMA, 128, 128, 128, 2, 2)
+    route = apt.apt_gemm_workspace_bytes(M, N, K, 2, 2, fp4)
+    assert ws(M, N, K, 2, 2, apt.APT_ACT_FP16, fp4) == (
+        r256(route) + r256(apt.apt_packed_bytes(M, K, 2)) + r256(4 * M) + r256(2 * M))
+    assert ws(0, N, K, 2, 2, apt.APT_ACT_CODES) == 0
+    assert ws(4, N, K, 2, 2, 5) == 0
 
 
 def test_config_struct_layout():
