@@ -19,10 +19,13 @@
 // K are padding (u = 0), the k-steps of the chunk that makes the chunk count
 // even are all-zero bytes, and rows past M up to the block are padding rows.
 //
-// One workgroup per row (so the fp16 row maximum and the row sum are one
-// workgroup reduction), one 32-element word per thread and pass.  Rows are
-// dealt to workgroups so that the 32 rows of a block run on one XCD: their
-// 16-byte pieces of each 512-byte fragment half then meet in that XCD's L2.
+// A workgroup takes 8 consecutive rows and walks their K: lane l of a wave
+// takes row l mod 8 and word l / 8 of each group of 8 words, so that one
+// store instruction writes the 16-byte pieces of 8 rows that make one whole
+// 128-byte line of a fragment, and one load instruction reads 8 rows' 256
+// contiguous bytes.  The fp16 row maximum and the row sum are reductions over
+// the lanes of a row (three lane swaps, then LDS across waves).  The loads of
+// up to kHeldIters word groups per lane are issued before any is used.
 #include <algorithm>
 #include <type_traits>
 
@@ -35,71 +38,92 @@ namespace {
 using namespace rowcode;
 
 constexpr int kWave = 64;
-constexpr int kMaxThreads = 256;
+constexpr int kMaxWaves = 16;
+constexpr int kRows = 8;                      // rows per workgroup
+constexpr int kWordLanes = kWave / kRows;     // words per wave and iteration
 constexpr int kWordElems = 32;
-constexpr int kXcds = 8;
 constexpr int kBlockRows = 32;
-// words per thread whose source stays in registers between the fp16 passes
-constexpr int kHeldWords = 4;
+// word groups per lane whose source stays in registers (issued up front)
+constexpr int kHeldIters = 4;
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 template <bool kHalf, bool kVec, int B>
-__global__ __launch_bounds__(kMaxThreads) void act_frag_kernel(
+__global__ __launch_bounds__(kWave* kMaxWaves) void act_frag_kernel(
     const uint8_t* __restrict__ src, int M, int K, int nchunks, int nsteps, int mblocks,
     v4i* __restrict__ frag, int32_t* __restrict__ rowsum, uint16_t* __restrict__ scale,
     uint16_t* __restrict__ scale_out, int* __restrict__ counters, int ncounters) {
   using Src = typename std::conditional<kHalf, HalfRow<kVec, B>, CodeRow<kVec, B>>::type;
-  __shared__ uint32_t lds_red[kMaxThreads / kWave];
+  constexpr int kD = Src::kDwords;
+  __shared__ uint32_t lds_red[kMaxWaves][kRows];
   // The stream-K arrival counters of this call start cleared (the GEMM
   // launch follows in stream order).
   for (int i = blockIdx.x * (int)blockDim.x + threadIdx.x; i < ncounters; i += gridDim.x * blockDim.x)
     counters[i] = 0;
-  const int x = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
-  const int row = (j / kBlockRows) * (kXcds * kBlockRows) + x * kBlockRows + j % kBlockRows;
-  if (row >= mblocks * kBlockRows) return;  // uniform: the whole workgroup
-  const bool real = row < M;
-  const int T = blockDim.x;
   const int nw = blockDim.x / kWave;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int r = lane % kRows, wl = lane / kRows;
+  const int row = blockIdx.x * kRows + r;  // < mblocks * 32 (the grid covers the blocks exactly)
+  const bool real = row < M;
   const int words = nchunks * kWordsPerPlane;  // words holding elements (up to K_pad)
+  const int step = kWordLanes * nw;            // words per iteration of the workgroup
+  const int iters = (words + step - 1) / step;
+  // one resource over the whole [M][K] source: offsets past its end (rows
+  // past M) read zeros; elements past K of a row are masked below
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(src + (int64_t)(real ? row : 0) * K * Src::kElemBytes), 0,
-      real ? (uint32_t)K * Src::kElemBytes : 0u, kRawBufferFlags);
-  auto load = [&](int w, uint32_t (&d)[2][Src::kDwords]) __attribute__((always_inline)) {
-    Src::load(rsrc, w * kWordElems, d[0]);
-    Src::load(rsrc, w * kWordElems + kLaneElems, d[1]);
+      const_cast<uint8_t*>(src), 0, (uint32_t)((int64_t)M * K * Src::kElemBytes), kRawBufferFlags);
+  const int64_t row_off = (int64_t)row * K;  // elements
+  auto word_of = [&](int it) { return it * step + wave * kWordLanes + wl; };
+  // the 32 elements of word w of this lane's row, elements past K as zero bits
+  auto load = [&](int w, uint32_t (&d)[2][kD]) __attribute__((always_inline)) {
+    const int k0 = w * kWordElems;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int kh = k0 + h * kLaneElems;
+      // (whole-source byte offsets stay below 2^31: the host checks)
+      Src::load(rsrc, (int)(row_off + (kh < K ? kh : 0)), d[h]);
+      const int n_valid = real ? K - kh : 0;
+#pragma unroll
+      for (int t = 0; t < kD; ++t) {
+        constexpr int per = kLaneElems / kD;  // elements per dword: 4 codes or 2 halves
+        const int nv = n_valid - per * t;
+        const uint32_t keep = nv >= per ? 0xFFFFFFFFu : (nv <= 0 ? 0u : ((1u << (8 * Src::kElemBytes * nv)) - 1u));
+        d[h][t] &= keep;
+      }
+    }
   };
 
-  uint32_t held[kHeldWords][2][Src::kDwords];
+  uint32_t held[kHeldIters][2][kD];
+#pragma unroll
+  for (int i = 0; i < kHeldIters; ++i)
+    if (i < iters && word_of(i) < words) load(word_of(i), held[i]);
   float rh = 0.0f, s2 = 0.0f;
   if constexpr (kHalf) {
     // Pass 1: the row's largest magnitude, then its scale.
     ushort2_t mm = {0, 0};
 #pragma unroll
-    for (int i = 0; i < kHeldWords; ++i) {
-      const int w = threadIdx.x + i * T;
-      if (w < words) {
-        load(w, held[i]);
+    for (int i = 0; i < kHeldIters; ++i)
+      if (i < iters && word_of(i) < words) {
         mm = Src::fold_max(mm, held[i][0]);
         mm = Src::fold_max(mm, held[i][1]);
       }
-    }
-    for (int w = threadIdx.x + kHeldWords * T; w < words; w += T) {
-      uint32_t d[2][Src::kDwords];
+    for (int it = kHeldIters; it < iters; ++it) {
+      const int w = word_of(it);
+      if (w >= words) continue;
+      uint32_t d[2][kD];
       load(w, d);
       mm = Src::fold_max(mm, d[0]);
       mm = Src::fold_max(mm, d[1]);
     }
     uint32_t m = max((uint32_t)mm.x, (uint32_t)mm.y);
-    for (int off = kWave / 2; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
-    if (lane == 0) lds_red[wave] = m;
+    for (int off = kRows; off < kWave; off <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+    if (wl == 0) lds_red[wave][r] = m;
     __syncthreads();
     m = 0u;
-    for (int w = 0; w < nw; ++w) m = max(m, lds_red[w]);
+    for (int v = 0; v < nw; ++v) m = max(m, lds_red[v][r]);
     __syncthreads();  // lds_red is reused for the row sum
     const uint16_t s16 = row_scale<B>(m, rh, s2);
-    if (threadIdx.x == 0 && real) {
+    if (wave == 0 && wl == 0 && real) {
       scale[row] = s16;
       if (scale_out != nullptr) scale_out[row] = s16;
     }
@@ -108,7 +132,7 @@ __global__ __launch_bounds__(kMaxThreads) void act_frag_kernel(
   // Pass 2: operand bytes of each word, in the fragment order.
   const int mb = row / kBlockRows, l = row % kBlockRows;
   uint32_t usum = 0u;
-  auto emit = [&](int w, const uint32_t (&d)[2][Src::kDwords]) __attribute__((always_inline)) {
+  auto emit = [&](int w, const uint32_t (&d)[2][kD]) __attribute__((always_inline)) {
     uint32_t c[8];  // byte b of c[i]: u of element 4 i + b of the word
     Src::words(d[0], rh, s2, c);
     Src::words(d[1], rh, s2, c + 4);
@@ -123,7 +147,7 @@ __global__ __launch_bounds__(kMaxThreads) void act_frag_kernel(
     // o[t], byte j = element 8 j + t = byte t mod 4 of c[2 j + t / 4]
     uint32_t o[8];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {      // h = t / 4: the odd or even c
+    for (int h = 0; h < 2; ++h) {          // h = t / 4: the odd or even c
 #pragma unroll
       for (int tp = 0; tp < 4; tp += 2) {  // t mod 4 in pairs
         // [c0.b, c2.b, c0.b', c2.b'] and [c4.b, c6.b, c4.b', c6.b'] with b = tp, b' = tp + 1
@@ -138,39 +162,31 @@ __global__ __launch_bounds__(kMaxThreads) void act_frag_kernel(
     f[l] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
     f[l + 32] = v4i{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
   };
-  if constexpr (kHalf) {
 #pragma unroll
-    for (int i = 0; i < kHeldWords; ++i) {
-      const int w = threadIdx.x + i * T;
-      if (w < words) emit(w, held[i]);
-    }
-    for (int w = threadIdx.x + kHeldWords * T; w < words; w += T) {
-      uint32_t d[2][Src::kDwords];
-      load(w, d);
-      emit(w, d);
-    }
-  } else {
-    for (int w = threadIdx.x; w < words; w += T) {
-      uint32_t d[2][Src::kDwords];
-      load(w, d);
-      emit(w, d);
-    }
+  for (int i = 0; i < kHeldIters; ++i)
+    if (i < iters && word_of(i) < words) emit(word_of(i), held[i]);
+  for (int it = kHeldIters; it < iters; ++it) {
+    const int w = word_of(it);
+    if (w >= words) continue;
+    uint32_t d[2][kD];
+    load(w, d);
+    emit(w, d);
   }
   // the chunk that makes the count even: all-zero bytes
-  for (int w = words + threadIdx.x; w < nsteps; w += T) {
+  for (int w = words + wave * kWordLanes + wl; w < nsteps; w += step) {
     v4i* f = frag + ((int64_t)mb * nsteps + w) * kWave;
     f[l] = v4i{0, 0, 0, 0};
     f[l + 32] = v4i{0, 0, 0, 0};
   }
 
-  for (int off = kWave / 2; off > 0; off >>= 1) usum += __shfl_xor(usum, off);
+  for (int off = kRows; off < kWave; off <<= 1) usum += __shfl_xor(usum, off);
   if (nw > 1) {
-    if (lane == 0) lds_red[wave] = usum;
+    if (wl == 0) lds_red[wave][r] = usum;
     __syncthreads();
     usum = 0u;
-    for (int w = 0; w < nw; ++w) usum += lds_red[w];
+    for (int v = 0; v < nw; ++v) usum += lds_red[v][r];
   }
-  if (threadIdx.x == 0 && real)
+  if (wave == 0 && wl == 0 && real)
     // sum_k (2 u - (2^b - 1)) over the K real elements
     rowsum[row] = (int32_t)(2u * usum - ((1u << B) - 1u) * (uint32_t)K);
 }
@@ -180,13 +196,11 @@ hipError_t launch_one(const void* src, int M, int K, int nchunks, int nsteps, vo
                       int32_t* rowsum, uint16_t* scale, uint16_t* scale_out, int* counters,
                       int ncounters, hipStream_t s) {
   const int mblocks = (M + kBlockRows - 1) / kBlockRows;
-  // workgroups: the row count rounded up to whole groups of 8 XCDs x 32 rows
-  const int groups = (mblocks + kXcds - 1) / kXcds;
-  const dim3 grid((unsigned)(groups * kXcds * kBlockRows));
-  // threads: one word each, in whole waves, at most kMaxThreads
+  const dim3 grid((unsigned)(mblocks * (kBlockRows / kRows)));
+  // waves: enough for the words of a row at 8 per wave, at most kMaxWaves
   const int words = nchunks * kWordsPerPlane;
-  const int threads = std::min(kMaxThreads, (words + kWave - 1) / kWave * kWave);
-  return launch_kernel(act_frag_kernel<kHalf, kVec, B>, grid, dim3(threads), 0, s,
+  const int waves = std::min(kMaxWaves, (words + kWordLanes - 1) / kWordLanes);
+  return launch_kernel(act_frag_kernel<kHalf, kVec, B>, grid, dim3(waves * kWave), 0, s,
                        static_cast<const uint8_t*>(src), M, K, nchunks, nsteps, mblocks,
                        static_cast<v4i*>(frag), rowsum, scale, scale_out, counters, ncounters);
 }

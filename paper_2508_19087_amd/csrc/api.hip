@@ -234,7 +234,9 @@ ActLayout act_layout(int M, int N, int K, int p, int q, bool fp16, const apt_con
     L.plan = ActPlan::kFusedXor;
     return L;
   }
-  const bool frags = c.route == APT_ROUTE_INT8_MFMA && int8_operand_format(c, q) == 0;
+  // (the fragment writer addresses the whole source with 31-bit byte offsets)
+  const bool frags = c.route == APT_ROUTE_INT8_MFMA && int8_operand_format(c, q) == 0 &&
+                     (int64_t)M * K * (fp16 ? 2 : 1) < ((int64_t)1 << 31);
   L.plan = frags ? ActPlan::kFragments : ActPlan::kPack;
   L.route_bytes = align256(gemm_workspace_need(M, N, K, q, c));
   size_t off = L.route_bytes;

@@ -379,6 +379,15 @@ def test_gemm_act_workspace_bytes():
     route = apt.apt_gemm_workspace_bytes(M, N, K, 2, 2, fp4)
     assert ws(M, N, K, 2, 2, apt.APT_ACT_FP16, fp4) == (
         r256(route) + r256(apt.apt_packed_bytes(M, K, 2)) + r256(4 * M) + r256(2 * M))
+    # past 2^31 source bytes the rows go through the packer (planes in the workspace)
+    big_m, big_k = 1 << 16, 1 << 15
+    route = apt.apt_gemm_workspace_bytes(big_m, 256, big_k, 1, 1, INT8_CFG)
+    assert route > 0
+    assert ws(big_m, 256, big_k - 1, 1, 1, apt.APT_ACT_CODES, INT8_CFG) == (
+        r256(apt.apt_gemm_workspace_bytes(big_m, 256, big_k - 1, 1, 1, INT8_CFG)) + r256(4 * big_m)
+        + r256(2 * big_m))
+    assert ws(big_m, 256, big_k, 1, 1, apt.APT_ACT_CODES, INT8_CFG) == (
+        r256(route) + r256(apt.apt_packed_bytes(big_m, big_k, 1)) + r256(4 * big_m) + r256(2 * big_m))
     assert ws(0, N, K, 2, 2, apt.APT_ACT_CODES) == 0
     assert ws(4, N, K, 2, 2, 5) == 0
 
