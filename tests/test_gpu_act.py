@@ -186,3 +186,32 @@ def test_act_binding_and_workspace():
                           None, c.data_ptr(), None, None, None, None, cfg,
                           ws.data_ptr(), nb, _stream())
     assert st == apt.APT_ERR_INVALID_ARG   # the MFMA routes need the weights' row sums
+
+
+def test_act_special_fp16_rows():
+    """Zero rows (scale 0), signed zeros, subnormal-only rows, fp16 extremes
+    and exact ties of the quantizer, through the fragment writer (int8 route)
+    and the packer path (XOR route, M > 8): int32 against the oracle's codes,
+    scales bit-exact."""
+    import torch
+    K, q, p, N = 320, 3, 2, 64
+    L = 2 ** q - 1
+    x = np.zeros((12, K), np.float16)
+    x[1, ::2] = np.float16(-0.0)
+    x[2] = (np.arange(K) % 7 - 3).astype(np.float16) * np.float16(2.0 ** -24)
+    x[3, :4] = [65504.0, -65504.0, 1.0, -1.0]
+    s = 2.0 ** -3
+    ties = np.arange(-L + 1, L, 2, dtype=np.float64)
+    x[4, :len(ties)] = (ties * s).astype(np.float16)
+    x[4, len(ties)] = np.float16(L * s)
+    x[5:] = synth.fp16_activations(synth.rng(99), 7, K)
+    w_codes = synth.uniform_codes(synth.rng(100), N, K, p)
+    w = apt.pack(dev(w_codes), p)
+    codes, s16 = ref.quantize_fp16(x, q)
+    want = ref.gemm(codes, w_codes, p, q)
+    for cfg in (apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 3),
+                apt.apt_config_t.make(apt.APT_ROUTE_XOR)):
+        c32, _, sc = apt.gemm_act(dev(x), q, w, cfg=cfg)
+        torch.cuda.synchronize()
+        assert np.array_equal(sc.cpu().numpy().view(np.uint16), s16.view(np.uint16)), cfg.route
+        assert_int32_equal(c32.cpu().numpy(), want, "special rows route %d" % cfg.route)
