@@ -375,8 +375,9 @@ __host__ __device__ constexpr int pad_of(int b) { return b == 8 ? -128 : 0; }
 // w < G' takes pairs [w S / G', (w+1) S / G') of them (S = sk_pairs), i.e. the
 // end of one tile, possibly whole tiles, and the start of another
 // (stream-K).  The host keeps G' at most twice the stream-K tile count, so a
-// tile has about two parts: every further part costs a partial tile written
-// and read back.  A workgroup walks its stream-K pairs
+// tile has about two parts (every further part costs a partial tile written
+// and read back), or G' equal to it, so that each leftover tile is one
+// workgroup's whole part (see sk_parts).  A workgroup walks its stream-K pairs
 // first and its whole tiles after, as one continuous chunk stream: the
 // software pipeline runs across tile boundaries, and at the end of each part
 // of a tile the accumulators are flushed:

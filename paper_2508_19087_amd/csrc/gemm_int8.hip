@@ -69,6 +69,21 @@ struct Plan {
   size_t partial_bytes, counter_bytes;
 };
 
+// Parts per stream-K tile.  When the leftover tiles are more than half of
+// the compute units the grid covers but no more than all of them, each stays
+// whole and simply extends one workgroup's chunk stream, one per compute unit:
+// that saves the launch and pipeline start of a second round without any
+// partial traffic (MI355X, interleaved runs: W4A4 2048x11008x4096, 176
+// leftover 256x128 tiles on 512 workgroups, 85.4 us whole against 88.0 us
+// for one workgroup per tile and 98.0 us in two parts; W2A4 1024x11008x4096,
+// 176 leftover 128x128 tiles, 51.5 against 54.0 us).  Otherwise about two
+// parts per tile: more parts only add partial traffic.
+int64_t sk_parts(const TileShape& sh, int grid, int sk_tiles) {
+  const int per_cu = sh.wm * sh.wn <= 4 ? 2 : 1;  // resident workgroups per compute unit
+  const int64_t units = std::max(1, grid / per_cu);
+  return 2 * (int64_t)sk_tiles > units && sk_tiles <= units ? 1 : 2;
+}
+
 Plan make_plan(int M, int K, int shape, int n_begin, int n_cols, int grid) {
   Plan pl;
   pl.shape = shape;
@@ -82,10 +97,13 @@ Plan make_plan(int M, int K, int shape, int n_begin, int n_cols, int grid) {
   pl.dp_tiles = pl.tiles / pl.grid;
   pl.sk_tiles = pl.tiles - pl.dp_tiles * pl.grid;
   pl.sk_pairs = pl.sk_tiles * pairs;
-  // about two parts per stream-K tile: more parts only add partial traffic
-  pl.sk_grid = (int)std::min<int64_t>(pl.grid, std::max<int64_t>(1, 2 * (int64_t)pl.sk_tiles));
-  pl.partial_bytes = pl.sk_tiles ? 2 * (size_t)pl.grid * sh.bm * sh.bn * 4 : 0;
-  pl.counter_bytes = (size_t)pl.sk_tiles * 4;
+  pl.sk_grid = (int)std::min<int64_t>(pl.grid, std::max<int64_t>(1, sk_parts(sh, pl.grid, pl.sk_tiles) *
+                                                                    (int64_t)pl.sk_tiles));
+  // one workgroup per leftover tile (sk_grid == sk_tiles): every part is a
+  // whole tile, so no partial tile or counter is ever used
+  const bool shared = pl.sk_tiles > 0 && pl.sk_grid != pl.sk_tiles;
+  pl.partial_bytes = shared ? 2 * (size_t)pl.grid * sh.bm * sh.bn * 4 : 0;
+  pl.counter_bytes = shared ? (size_t)pl.sk_tiles * 4 : 0;
   return pl;
 }
 

@@ -105,19 +105,34 @@ double model_loop_us(const Int8Shape& s, int f, int M, int N, int K, int grid, i
     return (double)wg_pairs * (wgs <= cus ? s.t[f].pair_alone_us : s.t[f].pair_us);
   };
   if (grid == 0) {
+    // a second round of workgroups starts its pipeline again (the loads of
+    // its first chunks and the ring fill, about two pairs alone: W4A4
+    // 2048x11008x4096 88.6 us against 85.0 us with the leftover tiles
+    // chained onto the first round's workgroups)
     const int64_t full = tiles / slots, rem = tiles % slots;
-    return (double)full * round_us(slots, pairs) + (rem ? round_us(rem, pairs) : 0.0);
+    return (double)full * round_us(slots, pairs) +
+           (rem ? round_us(rem, pairs) + (full ? 2.0 * s.t[f].pair_alone_us : 0.0) : 0.0);
   }
   const int64_t g = std::min<int64_t>(grid, tiles * pairs);
   const int64_t dp = tiles / g, sk_tiles = tiles - dp * g;
   const int64_t sk_pairs = sk_tiles * pairs;
-  // stream-K pairs go to min(g, 2 * sk_tiles) workgroups (the launch's rule)
-  const int64_t sk_g = sk_tiles ? std::min<int64_t>(g, 2 * sk_tiles) : 0;
+  // stream-K tiles whole when they are more than half of the compute units
+  // the grid covers and no more than all of them, else in about two parts
+  // (the launch's rule)
+  const int64_t units = std::max<int64_t>(1, g / s.per_cu);
+  const int64_t k = 2 * sk_tiles > units && sk_tiles <= units ? 1 : 2;
+  const int64_t sk_g = sk_tiles ? std::min<int64_t>(g, k * sk_tiles) : 0;
+  if (k == 1 && dp >= 1 && s.per_cu == 2 && g == slots) {
+    // whole leftover tiles extend the chunk streams of sk_g <= cus
+    // workgroups, at most one per compute unit (which holds workgroups w and
+    // w + cus), which runs its extra pairs alone after the shared rounds
+    return (double)dp * pairs * s.t[f].pair_us + (double)pairs * s.t[f].pair_alone_us;
+  }
   const int64_t per_wg = dp * pairs + (sk_g ? (sk_pairs + sk_g - 1) / sk_g : 0);
   const int64_t active = dp ? g : sk_g;
   const int64_t rounds = (active + slots - 1) / slots;
   double us = (double)rounds * round_us(std::min(active, slots), per_wg);
-  if (sk_tiles > 0) {
+  if (sk_tiles > 0 && k > 1) {
     // every shared tile: (parts - 1) partials written and read back; a tile
     // has sk_g / sk_tiles parts, one more where part bounds fall inside it
     const double parts = (double)sk_g / (double)sk_tiles + 0.5;
@@ -168,14 +183,17 @@ int split_columns(const Int8Shape& s, int M, int N, int cus) {
 // The shipped lookup table (Sec. V-B keeps the search results for common LLM
 // shapes): the configs the best-kernel search module picked on MI355X for the
 // workload shapes with M > 8 (bench.py --search), keyed by the M bucket
-// ceil(log2 M), N, K, p and q.  Smaller M always takes the XOR route.
+// ceil(log2 M), N, K, p and q.  Smaller M always takes the XOR route.  The
+// two 11008 x 4096 entries run one persistent round with the leftover tiles
+// chained whole onto its workgroups (measured 3-5% faster than one workgroup
+// per tile; see sk_parts in gemm_int8.hip).
 struct ShippedEntry {
   int mlog, N, K, p, q;
   apt_config_t cfg;
 };
 constexpr ShippedEntry kShipped[] = {
     { 4,   512,   512, 1, 2, {1, 0, 0, 0, 0, 0, 0, 0, 8, 0, 0, 0, 0, {0, 0, 0}}},  // w1a2_16x512x512
-    {11, 11008,  4096, 4, 4, {3, 256, 128, 128, 4, 1, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w4a4_prefill_2048x11008x4096
+    {11, 11008,  4096, 4, 4, {3, 256, 128, 128, 4, 1, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w4a4_prefill_2048x11008x4096
     { 9,  4096, 11008, 1, 1, {4, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w1a1_512x4096x11008
     { 9,  4096, 11008, 1, 4, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w1a4_512x4096x11008
     { 9,  4096, 11008, 2, 8, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w2a8_512x4096x11008
@@ -183,7 +201,7 @@ constexpr ShippedEntry kShipped[] = {
     { 9,  4096, 11008, 3, 8, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w3a8_512x4096x11008
     { 9,  4096, 11008, 4, 8, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // sweep_w4a8_512x4096x11008
     {10,  4096,  4096, 2, 4, {3, 128, 128, 128, 2, 2, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_q_m1024
-    {10, 11008,  4096, 2, 4, {3, 128, 128, 128, 2, 2, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_gate_m1024
+    {10, 11008,  4096, 2, 4, {3, 128, 128, 128, 2, 2, 512, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_gate_m1024
     {10,  4096, 11008, 2, 4, {3, 128, 128, 128, 2, 2, 0, 3, 0, 0, 0, 0, 0, {0, 0, 0}}},  // w2a4_down_m1024
 };
 

@@ -70,11 +70,17 @@ def _int8_workspace(M, N, K, c, q=4):
     launches = [(c.bm, c.bn, N, c.grid)]
     if c.split_n:
         launches = [(c.bm, c.bn, c.split_n, c.grid), (c.tail_bm, c.tail_bn, N - c.split_n, c.tail_grid)]
+    waves = {(256, 256): 8, (512, 128): 8, (128, 128): 4}
     for bm, bn, cols, g in launches:
         tiles = -(-M // bm) * -(-cols // bn)
         grid = tiles if g == 0 else min(g, tiles * nce // 2)
         sk_tiles = tiles - tiles // grid * grid
-        if sk_tiles:
+        # leftover tiles more than half of the compute units the grid covers and
+        # at most all of them stay whole, one per workgroup: no partials
+        w = waves.get((bm, bn), 4 if (bm, bn, c.waves_m * c.waves_n) == (256, 128, 4) else 8)
+        units = max(1, grid // (2 if w <= 4 else 1))
+        whole = 2 * sk_tiles > units and sk_tiles <= units
+        if sk_tiles and not whole:
             ws += up(2 * grid * bm * bn * 4) + up(sk_tiles * 4)
     return ws
 
@@ -88,11 +94,18 @@ def test_workspace_stream_k():
     assert apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c) == 2048 * 4096
     c.grid = 344  # divides the tile count: no stream-K part
     assert apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c) == 2048 * 4096
-    # a tail launch over [8192, 11008) with 128x128 tiles on 256 workgroups
-    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 0, 3, 0, 8192, 128, 128, 256)
+    # a tail launch over [8192, 11008) with 128x128 tiles on 512 workgroups
+    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2, 0, 3, 0, 8192, 128, 128, 512)
     ws = apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c)
-    assert ws == 2048 * 4096 + 512 * 128 * 128 * 4 + 512  # 352 tail tiles: 96 shared
+    assert ws == 2048 * 4096 + 1024 * 128 * 128 * 4 + 1536  # 352 tail tiles, all shared
     assert ws == _int8_workspace(2048, 11008, 4096, c)
+    # on 256 workgroups (128 compute units) the 96 leftover tail tiles stay whole
+    c.tail_grid = 256
+    assert apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c) == 2048 * 4096
+    assert _int8_workspace(2048, 11008, 4096, c) == 2048 * 4096
+    # the prefill on one round of 512 workgroups: 176 leftover 256x128 tiles, whole
+    c = apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 128, 128, 4, 1, 512, 3)
+    assert apt.apt_gemm_workspace_bytes(2048, 11008, 4096, 4, 4, c) == 2048 * 4096
 
 
 @pytest.mark.parametrize("shape", _shapes())
@@ -168,8 +181,9 @@ def gemm(M=4, N=4, K=64, p=2, q=2, a=A, w=W, ra=RA, rw=RW, c32=C, sa=None, sw=No
      apt.APT_ERR_INVALID_ARG),
     (dict(M=64, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 4097, 3)),
      apt.APT_ERR_INVALID_ARG),
+    # (2 tiles on 4 workgroups: split in two parts each, with partial tiles)
     (dict(M=64, N=512, K=1024, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 256, 256, 128, 4, 2,
-                                                         3, 3), ws=WS,
+                                                         4, 3), ws=WS,
           ws_bytes=64 * 1024), apt.APT_ERR_WORKSPACE),
     # tail launch: split_n a multiple of bn inside (0, N), a configured tail tile
     (dict(M=64, N=300, cfg=apt.apt_config_t.make(apt.APT_ROUTE_INT8_MFMA, 128, 128, 128, 2, 2, 0, 3, 0,
@@ -495,7 +509,7 @@ def test_shipped_table_configs_and_approximate_match():
             assert apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, c) > 0
     prefill = apt.select_config(2048, 11008, 4096, 4, 4)
     assert (prefill.route, prefill.bm, prefill.bn, prefill.waves_m, prefill.waves_n, prefill.grid) == \
-        (apt.APT_ROUTE_INT8_MFMA, 256, 128, 4, 1, 0)
+        (apt.APT_ROUTE_INT8_MFMA, 256, 128, 4, 1, 512)
     near = apt.select_config(1900, 11000, 4200, 4, 4)
     assert near.as_dict() == prefill.as_dict()
     down = apt.select_config(512, 4096, 11008, 3, 3)
