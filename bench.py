@@ -1639,6 +1639,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--settle", type=float, default=0.3,
+                    help="seconds of untimed steps before the warm-up steps, so that the GPU's "
+                         "clocks have risen to their loaded level (0 to skip)")
     ap.add_argument("--no-decode-cold", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--roofline-calls", type=int, default=50,
@@ -1763,6 +1766,18 @@ def main():
     wl.overlap = not args.serial_step
     wl.unfused_decode = args.unfused_decode
     wl.packed_prefill = args.packed_prefill
+    # Settle: the GPU raises its clocks over the first tenths of a second of
+    # load (measured: 108 us per step after 10 warm-up steps, 93 us after
+    # 1000), so steps run untimed for `settle` seconds before the W warm-up
+    # steps, and the K timed steps see the clocks a loaded GPU runs at.
+    settle_steps = 0
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < args.settle:
+        for _ in range(50):
+            wl.step()
+        settle_steps += 50
+        torch.cuda.synchronize()
+    settle_s = time.perf_counter() - t_settle
     for _ in range(args.warmup):
         wl.step()
     torch.cuda.synchronize()
@@ -1812,6 +1827,8 @@ def main():
                                            "MFMA fragments)"),
                    "prefill_config": cfg},
         "roofline": roofline,
+        "settle": {"seconds": round(settle_s, 3), "steps": settle_steps,
+                   "note": "untimed steps before the warm-up steps, while the GPU raises its clocks"},
     }
     log("bench: fp16 activation quantizer")
     result["quantize_fp16"] = quantize_fp16_rates()
