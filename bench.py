@@ -1425,14 +1425,38 @@ def workload_problems():
     return probs
 
 
-def workloads_run(calls: int = 20):
+def settle_gpu(seconds: float):
+    """Untimed load before a measurement mode: back-to-back W4A4
+    1024x4096x4096 calls for `seconds`, so that the GPU's clocks have risen to
+    the level they hold under load before anything is timed (the bench step
+    does the same with its own steps)."""
+    if seconds <= 0:
+        return
+    import torch
+
+    import paper_2508_19087_amd as apt
+    gen = torch.Generator().manual_seed(11)
+    w = apt.pack(torch.randint(-8, 8, (4096, 4096), dtype=torch.int8, generator=gen).cuda(), 4)
+    a = apt.pack(torch.randint(-8, 8, (1024, 4096), dtype=torch.int8, generator=gen).cuda(), 4,
+                 activations=True)
+    ws = torch.empty(max(apt.apt_gemm_workspace_bytes(1024, 4096, 4096, 4, 4), 256), dtype=torch.uint8,
+                     device="cuda")
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            apt.gemm(a, w, workspace=ws)
+        torch.cuda.synchronize()
+
+
+def workloads_run(calls: int = 20, settle_s: float = 0.02):
     """For rocprofv3 --kernel-trace: every workload configuration packed
-    first, then, workload by workload, one torch fill of a marker buffer (a
-    kernel that separates the workloads in the trace) and `calls` back-to-back
-    apt_gemm calls in the selected config (int32 output, plus the fp16
-    epilogue where the workload has scales); then the same for the activation
-    packers of the decode workloads (code and fp16 sources).  Prints the plan
-    as JSON."""
+    first, then, workload by workload, untimed calls for `settle_s` seconds
+    (loaded clocks), one torch fill of a marker buffer (a kernel that
+    separates the workloads in the trace) and `calls` back-to-back apt_gemm
+    calls in the selected config (int32 output, plus the fp16 epilogue where
+    the workload has scales); then the same for the activation packers of
+    the decode workloads (code and fp16 sources) and for apt_gemm_decode.
+    Prints the plan as JSON."""
     import numpy as np
     import torch
 
@@ -1448,25 +1472,43 @@ def workloads_run(calls: int = 20):
     marker = torch.empty(1, dtype=torch.int32, device="cuda")
     torch.cuda.synchronize()
     plan = []
+
+    def group(entry, one_call):
+        # untimed calls of the same kind first, for `settle_s`, so that the
+        # timed ones run at loaded clocks (a segment of their own, marked
+        # "settle" in the plan and left out of the summary); then `calls`
+        # back-to-back calls after a marker fill
+        marker.fill_(-1)
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < settle_s:
+            for _ in range(10):
+                one_call()
+            torch.cuda.synchronize()
+        plan.append({"settle": True})
+        marker.fill_(len(plan))
+        for _ in range(calls):
+            one_call()
+        torch.cuda.synchronize()
+        plan.append(entry)
+
     for i, (prob, a, w, sa, sw) in enumerate(items):
         cfg = apt.select_config(prob.M, prob.N, prob.K, prob.p, prob.q)
         ws_bytes = apt.apt_gemm_workspace_bytes(prob.M, prob.N, prob.K, prob.p, prob.q, cfg)
         ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
         c32 = torch.empty((prob.M, prob.N), dtype=torch.int32, device="cuda")
         c16 = torch.empty((prob.M, prob.N), dtype=torch.float16, device="cuda") if sa is not None else None
-        marker.fill_(i)
         sp = torch.cuda.current_stream().cuda_stream
-        for _ in range(calls):
+
+        def one_call():
             apt.check(apt.apt_gemm(prob.M, prob.N, prob.K, prob.p, prob.q, a.data.data_ptr(),
                                    w.data.data_ptr(), a.rowsum.data_ptr(), w.rowsum.data_ptr(),
                                    c32.data_ptr(), sa.data_ptr() if sa is not None else None,
                                    sw.data_ptr() if sw is not None else None,
                                    c16.data_ptr() if c16 is not None else None, cfg,
                                    ws.data_ptr(), ws_bytes, sp), "apt_gemm")
-        torch.cuda.synchronize()
-        plan.append({"workload": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
-                     "q": prob.q, "ops": prob.ops, "fp16": c16 is not None, "calls": calls,
-                     "config": cfg.as_dict()})
+        group({"workload": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
+               "q": prob.q, "ops": prob.ops, "fp16": c16 is not None, "calls": calls,
+               "config": cfg.as_dict()}, one_call)
         del ws, c32, c16
     # the activation packers of the decode workloads (M <= 8, K = 4096): the
     # code source and the fp16 quantizer, `calls` back-to-back calls each
@@ -1483,8 +1525,7 @@ def workloads_run(calls: int = 20):
         sc = torch.empty(prob.M, dtype=torch.float16, device="cuda")
         sp = torch.cuda.current_stream().cuda_stream
         for kind in ("codes", "fp16"):
-            marker.fill_(len(plan))
-            for _ in range(calls):
+            def one_call():
                 if kind == "codes":
                     st = apt.apt_quantize_pack_activations(codes.data_ptr(), prob.M, prob.K, prob.q,
                                                            buf.data_ptr(), rs.data_ptr(), sp)
@@ -1493,11 +1534,10 @@ def workloads_run(calls: int = 20):
                                                                 buf.data_ptr(), rs.data_ptr(),
                                                                 sc.data_ptr(), sp)
                 apt.check(st, "pack")
-            torch.cuda.synchronize()
-            plan.append({"workload": "pack_%s_m%d_k%d_q%d" % (kind, prob.M, prob.K, prob.q),
-                         "M": prob.M, "K": prob.K, "q": prob.q, "calls": calls, "pack": kind,
-                         "bytes": prob.M * prob.K * (1 if kind == "codes" else 2)
-                         + apt.apt_packed_bytes(prob.M, prob.K, prob.q) + 4 * prob.M})
+            group({"workload": "pack_%s_m%d_k%d_q%d" % (kind, prob.M, prob.K, prob.q),
+                   "M": prob.M, "K": prob.K, "q": prob.q, "calls": calls, "pack": kind,
+                   "bytes": prob.M * prob.K * (1 if kind == "codes" else 2)
+                   + apt.apt_packed_bytes(prob.M, prob.K, prob.q) + 4 * prob.M}, one_call)
     # the decode workloads through apt_gemm_decode (one launch from the token's
     # codes or fp16 values, int32 and fp16 outputs)
     for i, (prob, a, w, sa, sw) in enumerate(items):
@@ -1511,8 +1551,7 @@ def workloads_run(calls: int = 20):
         so = torch.empty(prob.M, dtype=torch.float16, device="cuda")
         sp = torch.cuda.current_stream().cuda_stream
         for kind in ("codes", "fp16"):
-            marker.fill_(len(plan))
-            for _ in range(calls):
+            def one_call():
                 if kind == "codes":
                     st = apt.apt_gemm_decode(prob.M, prob.N, prob.K, prob.p, prob.q, codes.data_ptr(),
                                              apt.APT_ACT_CODES, w.data.data_ptr(), c32.data_ptr(),
@@ -1522,9 +1561,8 @@ def workloads_run(calls: int = 20):
                                              apt.APT_ACT_FP16, w.data.data_ptr(), c32.data_ptr(), None,
                                              sw.data_ptr(), c16.data_ptr(), so.data_ptr(), None, sp)
                 apt.check(st, "apt_gemm_decode")
-            torch.cuda.synchronize()
-            plan.append({"workload": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
-                         "q": prob.q, "ops": prob.ops, "calls": calls, "decode": kind})
+            group({"workload": prob.name, "M": prob.M, "N": prob.N, "K": prob.K, "p": prob.p,
+                   "q": prob.q, "ops": prob.ops, "calls": calls, "decode": kind}, one_call)
     print(json.dumps(plan), flush=True)
 
 
@@ -1545,11 +1583,15 @@ def write_workload_stats(trace_csv: str, plan_json: str, command: str):
         elif cur is not None and "rocclr" not in name:  # (host-to-device copies are not timed)
             cur.append((name, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0))
     assert len(segs) == len(plan), (len(segs), len(plan))
+    keep = [i for i, pl in enumerate(plan) if not pl.get("settle")]
+    plan, segs = [plan[i] for i in keep], [segs[i] for i in keep]
     lines = ["# Kernel durations of every workload configuration in its selected config (rocprofv3",
              "# kernel trace; per kernel: median and mean duration over the calls after the first,",
              "# in microseconds; 'per call' sums the kernels one apt_gemm call launches, 'TOPS' is",
              "# 2 M N K over that sum).  Weights and activations are packed before the timed calls,",
              "# except in the apt_gemm_decode lines, which take the tokens' codes or fp16 values.",
+             "# Each workload's timed calls follow 20 ms of untimed calls of the same kind (loaded",
+             "# clocks; the run starts with 0.3 s of untimed W4A4 1024x4096x4096 calls).",
              "# command (repository root on the MI355X box): " + command,
              ""]
     for pl, seg in zip(plan, segs):
@@ -1640,8 +1682,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--settle", type=float, default=0.3,
-                    help="seconds of untimed steps before the warm-up steps, so that the GPU's "
-                         "clocks have risen to their loaded level (0 to skip)")
+                    help="seconds of untimed steps before the warm-up steps (other timing modes: "
+                         "of untimed GEMM calls), so that the GPU's clocks have risen to their "
+                         "loaded level (0 to skip)")
     ap.add_argument("--no-decode-cold", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--roofline-calls", type=int, default=50,
@@ -1716,6 +1759,12 @@ def main():
     if args.counters_run:
         counters_run(packed_prefill=args.packed_prefill)
         return
+    if any((args.workloads, args.vendor_int8, args.format_sweep, args.calibrate, args.routes,
+            args.search, args.decode_shapes, args.decode_sweep, args.epilogues, args.paper_shapes,
+            args.xor_crossover, args.decode_chain)):
+        # these timing modes start at loaded clocks (the bench step settles
+        # with its own steps)
+        settle_gpu(args.settle)
     if args.workloads:
         workloads_run()
         return

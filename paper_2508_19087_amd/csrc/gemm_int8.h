@@ -730,16 +730,46 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     }
   };
 
+  // Stream-K partial tiles: two slots per workgroup, each in accumulator
+  // order (lane-contiguous 16-byte vectors), with device-coherent (sc1)
+  // accesses.
+  constexpr int kAccVecs = FN * FM * 4;  // v4i per lane
+  constexpr uint32_t kSlotBytes = (uint32_t)BM * BN * 4;
+  const __amdgpu_buffer_rsrc_t p_rsrc = make_rsrc(prm.partial, prm.partial_bytes);
+  const uint32_t p_lane = (uint32_t)((wave * kAccVecs * kWave + lane) * 16);
+  auto partial_off = [&](int b, int a, int j) __attribute__((always_inline)) -> uint32_t {
+    return p_lane + (uint32_t)(((b * FM + a) * 4 + j) * kWave * 16);
+  };
+
   // Final values of tile (m0, n0): each 32x32 accumulator block goes through
   // the wave's LDS slot and comes back row by row, so that every store
   // instruction writes 8 whole 128-byte output rows; the affine correction
-  // and the optional fp16 scaling are applied on the way out.
-  auto epilogue = [&](int m0, int n0) __attribute__((always_inline)) {
+  // and the optional fp16 scaling are applied on the way out.  A tile shared
+  // by workgroups [pv_first, pv_last] first adds, block by block, the
+  // partials of every sharing workgroup except this one (the first one's
+  // in its second slot, the others' in their first): the four loads of a
+  // block leave together, where one load per round trip is all the
+  // registers of the main loop leave room for over a whole tile.
+  auto epilogue = [&](int m0, int n0, int pv_first, int pv_last) __attribute__((always_inline)) {
     const int er = lane / 8, ec = (lane % 8) * 4;  // read-back row (+8 i) and first column
 #pragma unroll
     for (int a = 0; a < FM; ++a) {
 #pragma unroll
       for (int b = 0; b < FN; ++b) {
+        for (int v = pv_first; v <= pv_last; ++v) {
+          if (v == st.w) continue;
+          const uint32_t so = (uint32_t)(v == pv_first ? 2 * v + 1 : 2 * v) * kSlotBytes;
+          v4i pv[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            pv[j] = __builtin_bit_cast(
+                v4i, __builtin_amdgcn_raw_buffer_load_b128(p_rsrc, partial_off(b, a, j), so, 16 /* sc1 */));
+          __builtin_amdgcn_sched_barrier(0);  // all four loads leave before the first add waits
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[b][a][4 * j + i] += pv[j][i];
+        }
         // acc[b][a][4 gi + j] = D[n = 8 gi + 4 (lane / 32) + j][m = lane mod 32]
 #pragma unroll
         for (int gi = 0; gi < 4; ++gi) {
@@ -805,11 +835,7 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
     }
   };
 
-  // ---- stream-K partial tiles: accumulator order, device-coherent accesses
-  constexpr int kAccVecs = FN * FM * 4;  // v4i per lane
-  constexpr uint32_t kSlotBytes = (uint32_t)BM * BN * 4;
-  const __amdgpu_buffer_rsrc_t p_rsrc = make_rsrc(prm.partial, prm.partial_bytes);
-  const uint32_t p_lane = (uint32_t)((wave * kAccVecs * kWave + lane) * 16);
+  // ---- stream-K partial tiles
   auto store_partial = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < FN; ++b)
@@ -819,23 +845,8 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
         for (int j = 0; j < 4; ++j) {
           const v4i v = {acc[b][a][4 * j], acc[b][a][4 * j + 1], acc[b][a][4 * j + 2],
                          acc[b][a][4 * j + 3]};
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), p_rsrc,
-                                                 p_lane + ((b * FM + a) * 4 + j) * kWave * 16,
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), p_rsrc, partial_off(b, a, j),
                                                  slot * kSlotBytes, 16 /* sc1 */);
-        }
-  };
-  auto add_partial = [&](int slot) __attribute__((always_inline)) {
-#pragma unroll
-    for (int b = 0; b < FN; ++b)
-#pragma unroll
-      for (int a = 0; a < FM; ++a)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const v4i v = __builtin_bit_cast(
-              v4i, __builtin_amdgcn_raw_buffer_load_b128(
-                       p_rsrc, p_lane + ((b * FM + a) * 4 + j) * kWave * 16, slot * kSlotBytes, 16));
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc[b][a][4 * j + i] += v[i];
         }
   };
   // Publishes this workgroup's partial of stream-K tile u in `slot` and
@@ -876,9 +887,11 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
           acc[b][a] = __builtin_convertvector(__builtin_bit_cast(v16f, acc[b][a]), v16i);
     }
     bool finish = true;
+    int w_first = 0, w_last = -1;  // the workgroups sharing the tile (none: whole)
     if (__builtin_expect(c.pbeg != 0 || c.pend != st.pairs, 0)) {
       const int e = c.tile == sh_tile[0] ? 0 : 1;
-      const int w_first = sh_first[e], w_last = sh_last[e];
+      w_first = sh_first[e];
+      w_last = sh_last[e];
       const int parts = w_last - w_first + 1;
       int* counter = prm.counters + (c.tile - st.sk_base);
       if (c.pbeg == 0) {  // owner: the first pairs of the tile, at the end of its range
@@ -891,11 +904,8 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
       } else {            // producer: later pairs, at the start of its range
         finish = arrive(2 * st.w, counter, parts);
       }
-      if (finish)
-        for (int v = w_first; v <= w_last; ++v)
-          if (v != st.w) add_partial(v == w_first ? 2 * v + 1 : 2 * v);
     }
-    if (finish) epilogue(c.m0, c.n0);
+    if (finish) epilogue(c.m0, c.n0, w_first, w_last);
   };
 
   // ---- pipeline over the chunk stream.  Chunk 2p+e of the stream is chunk
