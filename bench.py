@@ -11,7 +11,12 @@ One step is one pass of the whole path over one batch of synthetic input:
                       converts them straight into the int8 MFMA operand
                       fragments (--packed-prefill: the packer, then apt_gemm).
 Weights are packed once before timing (they are static).  Every call goes
-through the C ABI with the config chosen by the library's selector.
+through the C ABI with the config chosen by the library's selector.  The
+decode chain runs on a second stream beside the prefill, and consecutive
+steps' prefills alternate between two streams with their own buffers (two
+independent batches in flight; --one-batch: every prefill on one stream, a
+figure the JSON line also reports; --serial-step: the whole step on one
+stream).
 
 Printed JSON line: whole-step effective TOPS (2 M N K summed over the three
 GEMMs), the roofline of the dominant kernel (the prefill GEMM, int8 MFMA
@@ -101,6 +106,20 @@ class Workload:
                 it["c16"] = torch.empty((prob.M, prob.N), dtype=torch.float16, device="cuda")
             self.items.append(it)
         self.ops = sum(it["prob"].ops for it in self.items)
+        # Two prefill batches in flight: consecutive steps' prefill calls
+        # alternate between the main stream and a third one (default priority),
+        # each with its own output, workspace and activation buffers, so the
+        # next batch's fragment writer and first tiles start on the compute
+        # units the current GEMM's last round leaves idle.  Stream order keeps
+        # each buffer set's calls in sequence.
+        self.batches = 2
+        self.alt = torch.cuda.Stream()
+        self.alt_sp = self.alt.cuda_stream
+        second = dict(self.items[2])
+        for key in ("c32", "ws", "a_buf", "a_rs"):
+            second[key] = torch.empty_like(self.items[2][key])
+        self.pre_sets = [self.items[2], second]
+        self.count = 0
         torch.cuda.synchronize()
 
     def pack_act(self, it, sp=None):
@@ -153,10 +172,10 @@ class Workload:
                                    it["ws"].data_ptr(), it["ws_act_bytes"], sp)
         self.apt.check(st, "apt_gemm_act")
 
-    def prefill(self, sp=None):
+    def prefill(self, sp=None, it=None):
         """The prefill problem as the step runs it: apt_gemm_act from the codes,
         or with `packed_prefill` the packer and then apt_gemm."""
-        it = self.items[2]
+        it = it if it is not None else self.items[2]
         if self.packed_prefill:
             self.pack_act(it, sp)
             self.gemm(it, sp=sp)
@@ -164,11 +183,13 @@ class Workload:
             self.gemm_act(it, sp)
 
     def step(self):
-        """One pass of the path: the two decode GEMMs from their tokens' codes
-        (converted and decomposed into planes inside the GEMV, or with
-        `unfused_decode` packed by the packer first), then the prefill GEMM
-        from its codes (see prefill).  With `overlap`, the decode problems run
-        on the side stream and the prefill on the main one."""
+        """One pass of the path over one batch: the two decode GEMMs from their
+        tokens' codes (converted and decomposed into planes inside the GEMV,
+        or with `unfused_decode` packed by the packer first), then the
+        prefill GEMM from its codes (see prefill).  With `overlap`, the decode
+        problems run on the side stream and the prefill on the main one, or,
+        with two batches in flight, on the main and the third stream in turn
+        (buffer set = step parity); without it, everything on the main one."""
         sp = self.side_sp if self.overlap else self.sp
         for it in self.items[:2]:
             if self.unfused_decode:
@@ -176,7 +197,12 @@ class Workload:
                 self.gemm(it, sp=sp)
             else:
                 self.decode(it, sp=sp)
-        self.prefill()
+        if self.overlap and self.batches == 2:
+            k = self.count % 2
+            self.count += 1
+            self.prefill(sp=(self.sp, self.alt_sp)[k], it=self.pre_sets[k])
+        else:
+            self.prefill()
 
 
 def prefill_call(wl):
@@ -1720,6 +1746,10 @@ def main():
     ap.add_argument("--serial-step", action="store_true",
                     help="run the whole step on one stream (the decode GEMMs before the prefill) "
                          "instead of the decode chain on a second stream beside the prefill")
+    ap.add_argument("--one-batch", action="store_true",
+                    help="one prefill batch in flight: every step's prefill on the main stream "
+                         "(the decode chain still on the second stream), instead of consecutive "
+                         "steps' prefills alternating between two streams")
     ap.add_argument("--vendor-int8", action="store_true",
                     help="print the vendor library's dense int8 GEMM (torch._int_mm) on the prefill "
                          "shape with int8 operands, as context, and exit")
@@ -1813,6 +1843,7 @@ def main():
         print(json.dumps(res, indent=1), flush=True)
         return
     wl.overlap = not args.serial_step
+    wl.batches = 1 if (args.one_batch or args.serial_step) else 2
     wl.unfused_decode = args.unfused_decode
     wl.packed_prefill = args.packed_prefill
     # Settle: the GPU raises its clocks over the first tenths of a second of
@@ -1838,6 +1869,19 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     step_s = (t1 - t0) / args.steps
+    one_batch_s = None
+    if wl.batches == 2:
+        # the same steps with one prefill batch in flight, for comparison
+        wl.batches = 1
+        for _ in range(5):
+            wl.step()
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        for _ in range(args.steps):
+            wl.step()
+        torch.cuda.synchronize()
+        one_batch_s = (time.perf_counter() - t2) / args.steps
+        wl.batches = 2
     # The dominant kernel alone: back-to-back prefill GEMM calls between two
     # events on the stream they run on (an event per call would put a bubble
     # of several microseconds in the stream each time).
@@ -1868,7 +1912,11 @@ def main():
                                "+ W4A4 prefill M=2048 N=11008 K=4096 (int32); activations converted "
                                "and decomposed every step, weights packed once",
                    "schedule": ("decode chain on a second stream beside the prefill chain"
+                                + ("; consecutive steps' prefills alternate between the main and a "
+                                   "third stream (two batches in flight, separate buffers)"
+                                   if wl.batches == 2 else "")
                                 if wl.overlap else "one stream"),
+                   "batches_in_flight": wl.batches if wl.overlap else 1,
                    "decode_activations": ("packer + apt_gemm" if wl.unfused_decode else
                                           "apt_gemm_decode (converted inside the GEMV)"),
                    "prefill_activations": ("packer + apt_gemm" if wl.packed_prefill else
@@ -1879,6 +1927,11 @@ def main():
         "settle": {"seconds": round(settle_s, 3), "steps": settle_steps,
                    "note": "untimed steps before the warm-up steps, while the GPU raises its clocks"},
     }
+    if one_batch_s is not None:
+        result["one_batch_in_flight"] = {
+            "ms_per_step": round(one_batch_s * 1e3, 4), "value": round(wl.ops / one_batch_s / 1e12, 3),
+            "note": "the same K steps right after the timed ones with every prefill on the main "
+                    "stream (one batch in flight; bench.py --one-batch times this as the headline)"}
     log("bench: fp16 activation quantizer")
     result["quantize_fp16"] = quantize_fp16_rates()
     if not args.no_decode_cold:
