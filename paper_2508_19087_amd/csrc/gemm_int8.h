@@ -108,6 +108,7 @@ __device__ __forceinline__ void store16(int32_t* p, v4i v) {
 
 // An empty instruction that reads x: code computing x cannot be moved past it.
 __device__ __forceinline__ void keep_here(const v16i& x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void keep_here(const v4i& x, uint32_t y) { asm volatile("" ::"v"(x), "v"(y)); }
 
 // Buffer resource over [base, base + bytes) for raw buffer loads: a
 // wave-uniform base in SGPRs plus a per-lane 32-bit offset and a uniform
@@ -784,12 +785,24 @@ __device__ __forceinline__ void gemm_int8_body(const Int8Params& prm, uint8_t* l
         const bool full = vec_ok && ncol + 3 < g.N;
         const v4u wt = *reinterpret_cast<const v4u*>(lds_wt + nl);
         const v4f ws = *reinterpret_cast<const v4f*>(lds_ws + nl);
+        // the block's four rows and their row terms are read together, before
+        // any of the (uniform) edge and format branches below, which would
+        // otherwise take one LDS round trip each
+        v4i dv[4];
+        uint32_t atv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dv[i] = *reinterpret_cast<const v4i*>(epi_slot + (er + 8 * i) * kEpiStride + ec * 4);
+          atv[i] = lds_at[wm * WTM + a * 32 + er + 8 * i];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) keep_here(dv[i], atv[i]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int ml = wm * WTM + a * 32 + er + 8 * i;  // row in the tile
           const int m = m0 + ml;
-          const v4i d = *reinterpret_cast<const v4i*>(epi_slot + (er + 8 * i) * kEpiStride + ec * 4);
-          const uint32_t at = lds_at[ml];
+          const v4i d = dv[i];
+          const uint32_t at = atv[i];
           int32_t cv[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) cv[j] = (int32_t)(kMul * (uint32_t)d[j] + at + wt[j]);
