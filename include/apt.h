@@ -28,6 +28,10 @@
  *   - No call launches anything when validation fails.
  *   - The only mutable state the library holds is the configuration table that
  *     apt_search_config fills; a lock guards it, and calls are thread-safe.
+ *     Everything else a call uses lives in its arguments, so calls on
+ *     different streams may run at the same time as long as they share no
+ *     output or workspace (apt_gemm_noalloc, which uses the library's one
+ *     fixed workspace, is the exception).
  *   - Codes outside the signed b-bit range are reduced modulo 2^b (only the low
  *     b bits of each int8 code are used).
  *
