@@ -198,8 +198,11 @@ hipError_t launch_one(const void* src, int M, int K, int nchunks, int nsteps, vo
   const int mblocks = (M + kBlockRows - 1) / kBlockRows;
   const dim3 grid((unsigned)(mblocks * (kBlockRows / kRows)));
   // waves: enough for the words of a row at 8 per wave, at most kMaxWaves
+  // for the fp16 source (its conversion needs them) and 8 for codes (smaller
+  // workgroups find room sooner beside another call's GEMM)
   const int words = nchunks * kWordsPerPlane;
-  const int waves = std::min(kMaxWaves, (words + kWordLanes - 1) / kWordLanes);
+  const int cap = kHalf ? kMaxWaves : 8;
+  const int waves = std::min(cap, (words + kWordLanes - 1) / kWordLanes);
   return launch_kernel(act_frag_kernel<kHalf, kVec, B>, grid, dim3(waves * kWave), 0, s,
                        static_cast<const uint8_t*>(src), M, K, nchunks, nsteps, mblocks,
                        static_cast<v4i*>(frag), rowsum, scale, scale_out, counters, ncounters);
